@@ -1,0 +1,252 @@
+"""Plain CPU oracle for deep ACDC / AFDF cascades.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this module.  The product path
+(the HIP library and its Python binding) never calls it, and it shares no code,
+tables or constants with that path.
+
+Everything is computed in float64 (complex128 for the AFDF variant) with dense
+O(N^2) matrices built directly from their definitions.  There is no fast
+transform, no blocking and no fusion: each function follows the paper's
+statement of the layer in the order the paper gives it.
+
+Paper: Moczulski, Denil, Appleyard, de Freitas, "ACDC: A Structured Efficient
+Linear Layer", ICLR 2016 (arXiv:1511.05946).
+
+Conventions (row vectors throughout, as in the paper's Sec. 1 eq. (1) y = xW):
+
+* ``x``            [B, N] layer-cascade input
+* ``A``, ``D``     [K, N] diagonals a_k, d_k of layer k (A_k = diag(a_k))
+* ``perm``         [K, N] int; ``perm[k]`` *gathers* the input of layer k:
+                   u_k[n] = z_{k-1}[perm[k][n]]
+* ``flags``        bit 0 PERM, bit 1 RELU (after layers 0..K-2), bit 2 COMPLEX
+
+Readings of the paper used here (each listed in the design doc):
+
+* DCT index range: n, k in [0, N) and eps_0 = 1/sqrt(2) only (Sec. 4, the
+  c_nk definition; the "k = N" clause is a DCT-I leftover -- only this reading
+  makes the matrix orthogonal, which Sec. 4 states).
+* Orientation: n is the spatial index, so ``h2 = h1 @ C`` is the DCT-II and
+  ``@ C.T`` (= C^{-1}) the DCT-III (Sec. 4 derivative block: h2 = h1 C).
+* Batch reduction of dL/da, dL/dd: sum over rows (Sec. 4 gives per-example
+  derivatives).
+* ReLU derivative at 0 is 0 (strict v > 0).
+* AFDF: F[n, k] = exp(-2 pi i n k / N), F^{-1} its exact inverse conj(F)/N
+  (Sec. 3); complex gradients follow the PyTorch convention
+  grad = dL/dRe + i dL/dIm, i.e. g_x = g_y W^H.
+
+Parity pins: see tests/test_oracle.py.  Every function here is pinned there
+against something other than itself (a library DCT/FFT special case, closed
+forms of the layer, a brute-force dense product, finite differences, and
+torch autograd).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+FLAG_PERM = 1
+FLAG_RELU = 2
+FLAG_COMPLEX = 4
+
+_CHUNK = 512  # rows per dense product, only to bound memory
+
+
+def dct_matrix(N: int) -> np.ndarray:
+    """Orthonormal DCT-II matrix C[n, k] (Sec. 4, definition of c_nk).
+
+    c_nk = sqrt(2/N) * eps_k * cos(pi (2n+1) k / (2N)),  n, k in [0, N),
+    eps_0 = 1/sqrt(2), eps_k = 1 otherwise.  Row vector x maps to x @ C.
+    """
+    n = np.arange(N, dtype=np.float64)[:, None]
+    k = np.arange(N, dtype=np.float64)[None, :]
+    eps = np.where(k == 0, 1.0 / np.sqrt(2.0), 1.0)
+    return np.sqrt(2.0 / N) * eps * np.cos(np.pi * (2.0 * n + 1.0) * k / (2.0 * N))
+
+
+def dft_matrix(N: int) -> np.ndarray:
+    """Unnormalised DFT matrix F[n, k] = exp(-2 pi i n k / N) (Sec. 3, AFDF).
+
+    The exponent is reduced mod N in integers before scaling so the angle is
+    exact for large N.
+    """
+    n = np.arange(N, dtype=np.int64)[:, None]
+    k = np.arange(N, dtype=np.int64)[None, :]
+    return np.exp(-2j * np.pi * ((n * k) % N).astype(np.float64) / N)
+
+
+def _transforms(N: int, complex_: bool):
+    """Return (T, Tinv) with Tinv the exact inverse of T.
+
+    ACDC (Sec. 4): T = C, Tinv = C^T (C orthogonal).
+    AFDF (Sec. 3): T = F, Tinv = conj(F) / N.
+    """
+    if complex_:
+        F = dft_matrix(N)
+        return F, np.conj(F) / N
+    C = dct_matrix(N)
+    return C, C.T.copy()
+
+
+def _check(x, A, D, perm, flags):
+    x = np.asarray(x)
+    A = np.asarray(A)
+    D = np.asarray(D)
+    if x.ndim != 2 or A.ndim != 2 or D.shape != A.shape or A.shape[1] != x.shape[1]:
+        raise ValueError("shapes: x [B,N], A and D [K,N]")
+    if (flags & FLAG_COMPLEX) and (flags & FLAG_RELU):
+        raise ValueError("ReLU is not defined for the complex variant")
+    if flags & FLAG_PERM:
+        perm = np.asarray(perm)
+        if perm.shape != A.shape:
+            raise ValueError("perm must be [K,N]")
+        for k in range(perm.shape[0]):
+            if not np.array_equal(np.sort(perm[k]), np.arange(A.shape[1])):
+                raise ValueError(f"perm[{k}] is not a permutation")
+    dt = np.complex128 if flags & FLAG_COMPLEX else np.float64
+    return x.astype(dt), A.astype(dt), D.astype(dt), perm
+
+
+def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False):
+    """Cascade forward y = x prod_k [P_k] A_k T D_k T^{-1}  (eq. for AFDF_K in
+    Sec. 3, made real in Sec. 4 as ACDC_K; permutations and ReLU interleaved as
+    in Sec. 6.2).
+
+    Per layer k (row vectors, Sec. 4 notation):
+        u_k = z[:, perm[k]]          (if PERM)
+        h1  = u_k * a_k              (x A)
+        h2  = h1 @ T                 (x A C)
+        h3  = h2 * d_k               (x A C D)
+        v_k = h3 @ Tinv              (x A C D C^{-1})
+        z   = max(v_k, 0)            (if RELU and k < K-1) else v_k
+
+    Returns y, or (y, cache) with cache = dict(u=[...], h2=[...], v=[...]) of
+    per-layer float64 arrays when ``keep`` is true.
+    """
+    x, A, D, perm = _check(x, A, D, perm, flags)
+    K, N = A.shape
+    T, Tinv = _transforms(N, bool(flags & FLAG_COMPLEX))
+    relu = bool(flags & FLAG_RELU)
+    y = np.empty_like(x)
+    cache = {"u": [np.empty_like(x) for _ in range(K)],
+             "h2": [np.empty_like(x) for _ in range(K)],
+             "v": [np.empty_like(x) for _ in range(K)]} if keep else None
+    for r0 in range(0, x.shape[0], _CHUNK):
+        z = x[r0:r0 + _CHUNK]
+        for k in range(K):
+            u = z[:, perm[k]] if flags & FLAG_PERM else z
+            h1 = u * A[k]
+            h2 = h1 @ T
+            h3 = h2 * D[k]
+            v = h3 @ Tinv
+            z = np.maximum(v, 0.0) if (relu and k < K - 1) else v
+            if keep:
+                cache["u"][k][r0:r0 + _CHUNK] = u
+                cache["h2"][k][r0:r0 + _CHUNK] = h2
+                cache["v"][k][r0:r0 + _CHUNK] = v
+        y[r0:r0 + _CHUNK] = z
+    return (y, cache) if keep else y
+
+
+def backward(x, grad_y, A, D, perm=None, flags: int = 0):
+    """Analytic backward of the cascade (Sec. 4 derivative block, applied
+    layer by layer in reverse; ReLU and permutation steps of Sec. 6.2).
+
+    Real ACDC, per layer k from K-1 down to 0, with g = dL/dz_k:
+        g    = g * (v_k > 0)                  (if RELU and k < K-1)
+        gh3  = g @ C                          (dL/dh3 = C dL/dy in the paper's
+                                               column form; row form g C)
+        dd_k = sum_rows h2_k * gh3            (dL/dd = h2 . C dL/dy)
+        gh1  = (gh3 * d_k) @ C^T              (C^{-1} d . C dL/dy)
+        da_k = sum_rows u_k * gh1             (dL/da = x . C^{-1} d . C dL/dy)
+        gu   = gh1 * a_k                      (dL/dx = a . C^{-1} d . C dL/dy)
+        g[:, perm[k]] = gu                    (inverse of the gather)
+
+    Complex AFDF (PyTorch convention g_x = g_y W^H):
+        gh3 = g @ F / N, dd_k = sum conj(h2_k) gh3, gh1 = (gh3 conj(d_k)) @ conj(F),
+        da_k = sum conj(u_k) gh1, gu = gh1 conj(a_k).
+
+    Returns (grad_x [B,N], grad_A [K,N], grad_D [K,N]); the parameter
+    gradients are sums over the batch.
+    """
+    x, A, D, perm = _check(x, A, D, perm, flags)
+    cplx = bool(flags & FLAG_COMPLEX)
+    gy = np.asarray(grad_y).astype(np.complex128 if cplx else np.float64)
+    if gy.shape != x.shape:
+        raise ValueError("grad_y must match x")
+    K, N = A.shape
+    T, Tinv = _transforms(N, cplx)
+    # Backward transforms: row form of the transposed (conjugate-transposed
+    # for AFDF) forward matrices.
+    Tinv_H = np.conj(Tinv).T  # C for ACDC, F / N for AFDF
+    T_H = np.conj(T).T        # C^T for ACDC, conj(F) for AFDF
+    relu = bool(flags & FLAG_RELU)
+    grad_x = np.empty_like(x)
+    grad_A = np.zeros_like(A)
+    grad_D = np.zeros_like(D)
+    for r0 in range(0, x.shape[0], _CHUNK):
+        xs = x[r0:r0 + _CHUNK]
+        _, cache = forward(xs, A, D, perm, flags, keep=True)
+        g = gy[r0:r0 + _CHUNK]
+        for k in range(K - 1, -1, -1):
+            if relu and k < K - 1:
+                g = g * (cache["v"][k] > 0.0)
+            gh3 = g @ Tinv_H
+            h2 = cache["h2"][k]
+            grad_D[k] += np.sum((np.conj(h2) if cplx else h2) * gh3, axis=0)
+            gh1 = (gh3 * (np.conj(D[k]) if cplx else D[k])) @ T_H
+            u = cache["u"][k]
+            grad_A[k] += np.sum((np.conj(u) if cplx else u) * gh1, axis=0)
+            gu = gh1 * (np.conj(A[k]) if cplx else A[k])
+            if flags & FLAG_PERM:
+                g = np.empty_like(gu)
+                g[:, perm[k]] = gu
+            else:
+                g = gu
+        grad_x[r0:r0 + _CHUNK] = g
+    return grad_x, grad_A, grad_D
+
+
+def layer_matrix(a, d, complex_: bool = False) -> np.ndarray:
+    """Dense matrix of one layer, A T D T^{-1} (Sec. 4 / Sec. 3); N small."""
+    N = len(a)
+    T, Tinv = _transforms(N, complex_)
+    dt = np.complex128 if complex_ else np.float64
+    return np.diag(np.asarray(a, dt)) @ T @ np.diag(np.asarray(d, dt)) @ Tinv
+
+
+def dense_operator(A, D, perm=None, flags: int = 0) -> np.ndarray:
+    """Dense product W of a cascade without ReLU (eq. for AFDF_K, Sec. 3), so
+    that y = x @ W.  Each gather u = z[:, p] is the permutation matrix with
+    P[p[n], n] = 1.  Intended for N <= 64."""
+    if flags & FLAG_RELU:
+        raise ValueError("a cascade with ReLU is not a single matrix")
+    A = np.asarray(A)
+    K, N = A.shape
+    cplx = bool(flags & FLAG_COMPLEX)
+    W = np.eye(N, dtype=np.complex128 if cplx else np.float64)
+    for k in range(K):
+        if flags & FLAG_PERM:
+            P = np.zeros((N, N))
+            P[np.asarray(perm[k]), np.arange(N)] = 1.0
+            W = W @ P
+        W = W @ layer_matrix(A[k], D[k], cplx)
+    return W
+
+
+def flops_per_row_layer(N: int, complex_: bool = False) -> float:
+    """Algorithmic flop count of one forward row-layer.
+
+    ACDC: 4N + 5 N log2 N (Sec. 5, FFTW counting convention).
+    AFDF: two complex N-point FFTs at 5 N log2 N each plus two complex
+    diagonal products at 6N each.
+    """
+    lg = np.log2(N)
+    if complex_:
+        return 10.0 * N * lg + 12.0 * N
+    return 4.0 * N + 5.0 * N * lg
+
+
+def arithmetic_intensity(N: int) -> float:
+    """Batched single-layer arithmetic intensity (4 + 5 log2 N) / 8 (Sec. 5)."""
+    return (4.0 + 5.0 * np.log2(N)) / 8.0

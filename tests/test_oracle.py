@@ -1,0 +1,391 @@
+"""Pins for the CPU oracle (no GPU).
+
+Each test checks the oracle against something other than itself: a library
+special case (scipy's orthonormal DCT-II, numpy's FFT), a closed form of the
+layer, a brute-force dense product built from the library transforms, finite
+differences, or torch autograd over an independently built graph.  The last
+group plants plausible mistakes in the oracle and checks that some pin fails.
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.fft
+
+from oracle import acdc_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+P, R, CX = O.FLAG_PERM, O.FLAG_RELU, O.FLAG_COMPLEX
+
+
+def rand_case(rng, B, N, K, flags, relu_input=False):
+    cplx = bool(flags & CX)
+    if cplx:
+        x = rng.standard_normal((B, N)) + 1j * rng.standard_normal((B, N))
+        A = rng.normal(1, .1, (K, N)) + 1j * rng.normal(0, .1, (K, N))
+        D = rng.normal(1, .1, (K, N)) + 1j * rng.normal(0, .1, (K, N))
+        gy = rng.standard_normal((B, N)) + 1j * rng.standard_normal((B, N))
+    else:
+        x = rng.standard_normal((B, N))
+        if relu_input:
+            x = np.maximum(x, 0)
+        A = rng.normal(1, .1, (K, N))
+        D = rng.normal(1, .1, (K, N))
+        gy = rng.standard_normal((B, N))
+    perm = np.stack([rng.permutation(N) for _ in range(K)])
+    return x, A, D, perm, gy
+
+
+def lib_forward(x, A, D, perm, flags):
+    """The cascade written with library transforms only (scipy DCT-II/III
+    'ortho', numpy FFT): the special case the oracle must reduce to."""
+    z = np.asarray(x)
+    K = A.shape[0]
+    for k in range(K):
+        u = z[:, perm[k]] if flags & P else z
+        if flags & CX:
+            v = np.fft.ifft(np.fft.fft(u * A[k], axis=1) * D[k], axis=1)
+        else:
+            v = scipy.fft.idct(scipy.fft.dct(u * A[k], type=2, norm="ortho", axis=1) * D[k],
+                               type=2, norm="ortho", axis=1)
+        z = np.maximum(v, 0) if (flags & R and k < K - 1) else v
+    return z
+
+
+# ---------------------------------------------------------------- the DCT matrix
+
+@pytest.mark.parametrize("N", [1, 2, 3, 5, 8, 16, 64, 100, 256, 1024])
+def test_dct_is_scipy_orthonormal_dct2(N):
+    rng = np.random.default_rng(N)
+    x = rng.standard_normal((7, N))
+    C = O.dct_matrix(N)
+    np.testing.assert_allclose(x @ C, scipy.fft.dct(x, type=2, norm="ortho", axis=1),
+                               rtol=0, atol=1e-12 * np.sqrt(N))
+
+
+@pytest.mark.parametrize("N", [2, 8, 48, 256, 1024])
+def test_dct_orthonormal_and_inverse(N):
+    C = O.dct_matrix(N)
+    np.testing.assert_allclose(C.T @ C, np.eye(N), atol=1e-12)
+    np.testing.assert_allclose(C @ C.T, np.eye(N), atol=1e-12)
+    x = np.random.default_rng(1).standard_normal((3, N))
+    np.testing.assert_allclose(np.linalg.norm(x @ C, axis=1), np.linalg.norm(x, axis=1), rtol=1e-12)
+
+
+@pytest.mark.parametrize("N", [4, 9, 64])
+def test_dct_of_constant_is_dc_only(N):
+    # 1 @ C = sqrt(N) e_0 for the orthonormal DCT-II.
+    e0 = np.zeros(N)
+    e0[0] = np.sqrt(N)
+    np.testing.assert_allclose(np.ones(N) @ O.dct_matrix(N), e0, atol=1e-12)
+
+
+def test_dct_small_closed_form_values():
+    # N = 2: C = [[1/sqrt2, 1/sqrt2], [1/sqrt2, -1/sqrt2]] (cos(pi/4), cos(3pi/4)).
+    s = 1 / np.sqrt(2)
+    np.testing.assert_allclose(O.dct_matrix(2), [[s, s], [s, -s]], atol=1e-15)
+
+
+@pytest.mark.parametrize("N", [1, 4, 7, 32])
+def test_dft_matrix_is_numpy_fft(N):
+    rng = np.random.default_rng(N)
+    x = rng.standard_normal((3, N)) + 1j * rng.standard_normal((3, N))
+    np.testing.assert_allclose(x @ O.dft_matrix(N), np.fft.fft(x, axis=1), atol=1e-11 * N)
+
+
+# ---------------------------------------------------------- closed forms (Sec. 4)
+
+def test_identity_layer():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((5, 32))
+    y = O.forward(x, np.ones((3, 32)), np.ones((3, 32)))
+    np.testing.assert_allclose(y, x, atol=1e-12)
+
+
+def test_constant_D_scales_by_A():
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((4, 24))
+    a = rng.normal(1, .1, (1, 24))
+    y = O.forward(x, a, np.full((1, 24), 2.5))
+    np.testing.assert_allclose(y, 2.5 * x * a, atol=1e-12)
+
+
+def test_dc_only_D_gives_row_mean():
+    # D = e_0: h3 keeps only the DC coefficient, so every output is mean(x * a).
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((6, 20))
+    a = rng.normal(1, .1, (1, 20))
+    d = np.zeros((1, 20))
+    d[0, 0] = 1.0
+    y = O.forward(x, a, d)
+    np.testing.assert_allclose(y, np.repeat((x * a).mean(1, keepdims=True), 20, 1), atol=1e-12)
+
+
+def test_identity_perm_equals_no_perm():
+    rng = np.random.default_rng(5)
+    x, A, D, _, _ = rand_case(rng, 4, 16, 3, 0)
+    ident = np.tile(np.arange(16), (3, 1))
+    np.testing.assert_array_equal(O.forward(x, A, D, ident, P | R), O.forward(x, A, D, None, R))
+
+
+@pytest.mark.parametrize("flags", [0, P, R, P | R, CX, CX | P])
+@pytest.mark.parametrize("N,K", [(8, 1), (16, 3), (48, 4), (64, 2), (256, 5)])
+def test_forward_equals_library_transforms(flags, N, K):
+    rng = np.random.default_rng(N * 31 + K)
+    x, A, D, perm, _ = rand_case(rng, 9, N, K, flags, relu_input=bool(flags & R))
+    np.testing.assert_allclose(O.forward(x, A, D, perm, flags), lib_forward(x, A, D, perm, flags),
+                               atol=1e-11, rtol=1e-11)
+
+
+# -------------------------------------------------- brute-force dense products
+
+def lib_dense(A, D, perm, flags):
+    """W built column by column from the library transforms, with explicit
+    Python loops for the permutation and diagonal products."""
+    K, N = A.shape
+    cplx = bool(flags & CX)
+    W = np.eye(N, dtype=complex if cplx else float)
+    for k in range(K):
+        if flags & P:
+            Pm = np.zeros((N, N))
+            for n in range(N):
+                Pm[perm[k][n], n] = 1.0  # u[n] = z[perm[n]]  <=>  u = z @ Pm
+            W = W @ Pm
+        L = np.zeros((N, N), dtype=W.dtype)
+        for i in range(N):
+            e = np.zeros(N, dtype=W.dtype)
+            e[i] = 1.0
+            L[i] = lib_forward(e[None, :], A[k:k + 1], D[k:k + 1], None, flags & CX)[0]
+        W = W @ L
+    return W
+
+
+@pytest.mark.parametrize("flags", [0, P, CX, CX | P])
+@pytest.mark.parametrize("N,K", [(4, 1), (6, 2), (16, 3), (64, 4)])
+def test_dense_operator_bruteforce(flags, N, K):
+    rng = np.random.default_rng(7 + N + K)
+    x, A, D, perm, _ = rand_case(rng, 5, N, K, flags)
+    W = O.dense_operator(A, D, perm, flags)
+    np.testing.assert_allclose(W, lib_dense(A, D, perm, flags), atol=1e-11)
+    np.testing.assert_allclose(x @ W, O.forward(x, A, D, perm, flags), atol=1e-11)
+
+
+def test_cascade_order_first_layer_acts_first():
+    # y = x L_0 L_1: swapping the layers must change the result.
+    rng = np.random.default_rng(8)
+    x, A, D, perm, _ = rand_case(rng, 3, 16, 2, 0)
+    y = O.forward(x, A, D)
+    L0, L1 = O.layer_matrix(A[0], D[0]), O.layer_matrix(A[1], D[1])
+    np.testing.assert_allclose(y, x @ L0 @ L1, atol=1e-12)
+    assert np.abs(y - x @ L1 @ L0).max() > 1e-3
+
+
+def test_dct_orientation_matters():
+    # C D C^T != C^T D C: the reading h2 = h1 C is observable.
+    rng = np.random.default_rng(9)
+    C = O.dct_matrix(16)
+    d = rng.normal(1, .3, 16)
+    assert np.abs(C @ np.diag(d) @ C.T - C.T @ np.diag(d) @ C).max() > 1e-2
+
+
+def test_layer_invariant_to_column_scaling_of_C():
+    # Reading of the garbled eps_k range: any per-frequency rescaling S of C with
+    # the exact inverse leaves y unchanged, so it cannot affect outputs.
+    rng = np.random.default_rng(10)
+    C = O.dct_matrix(12)
+    S = np.diag(rng.uniform(.5, 2, 12))
+    Cs = C @ S
+    a, d = rng.normal(1, .1, 12), rng.normal(1, .1, 12)
+    np.testing.assert_allclose(np.diag(a) @ Cs @ np.diag(d) @ np.linalg.inv(Cs),
+                               O.layer_matrix(a, d), atol=1e-12)
+
+
+# ------------------------------------------------------ AFDF closed forms (Sec. 3)
+
+def test_afdf_single_layer_is_circular_convolution():
+    # Remark in Sec. 3: F^{-1} diag F is circulant; x A F D F^{-1} = (x a) (*) ifft(d).
+    rng = np.random.default_rng(11)
+    N = 12
+    x, A, D, _, _ = rand_case(rng, 3, N, 1, CX)
+    c = np.fft.ifft(D[0])
+    h = x * A[0]
+    ref = np.zeros_like(h)
+    for n in range(N):
+        for m in range(N):
+            ref[:, n] += h[:, m] * c[(n - m) % N]
+    np.testing.assert_allclose(O.forward(x, A, D, None, CX), ref, atol=1e-12)
+
+
+def test_afdf_optical_presentation():
+    # Sec. 3 optical presentation: y F = (x A_1 F) D_1 R_2 D_2 ... R_K D_K with
+    # R_k = F^{-1} A_k F.
+    rng = np.random.default_rng(12)
+    N, K = 10, 3
+    x, A, D, _, _ = rand_case(rng, 2, N, K, CX)
+    F = np.fft.fft(np.eye(N), axis=1)
+    Finv = np.linalg.inv(F)
+    M = np.diag(D[0])
+    for k in range(1, K):
+        M = M @ (Finv @ np.diag(A[k]) @ F) @ np.diag(D[k])
+    lhs = O.forward(x, A, D, None, CX) @ F
+    np.testing.assert_allclose(lhs, (x * A[0]) @ F @ M, atol=1e-10)
+
+
+# ------------------------------------------------------------------- backward
+
+def fd_grads(x, A, D, perm, flags, gy, eps=1e-6):
+    def loss(x_, A_, D_):
+        return float(np.sum(gy * O.forward(x_, A_, D_, perm, flags)))
+
+    out = []
+    for arr_id in range(3):
+        arrs = [x.copy(), A.copy(), D.copy()]
+        g = np.zeros_like(arrs[arr_id])
+        for idx in np.ndindex(*g.shape):
+            p = [a.copy() for a in arrs]
+            m = [a.copy() for a in arrs]
+            p[arr_id][idx] += eps
+            m[arr_id][idx] -= eps
+            g[idx] = (loss(*p) - loss(*m)) / (2 * eps)
+        out.append(g)
+    return out
+
+
+@pytest.mark.parametrize("flags", [0, P, R, P | R])
+@pytest.mark.parametrize("N,K", [(4, 1), (8, 2), (16, 3)])
+def test_backward_finite_differences(flags, N, K):
+    rng = np.random.default_rng(100 + N * 3 + K + flags)
+    x, A, D, perm, gy = rand_case(rng, 3, N, K, flags)
+    if flags & R:
+        _, cache = O.forward(x, A, D, perm, flags, keep=True)
+        margin = min(np.abs(cache["v"][k]).min() for k in range(K - 1)) if K > 1 else 1.0
+        assert margin > 1e-4, "re-seed: ReLU kink too close for finite differences"
+    gx, gA, gD = O.backward(x, gy, A, D, perm, flags)
+    fx, fA, fD = fd_grads(x, A, D, perm, flags, gy)
+    for a, b in ((gx, fx), (gA, fA), (gD, fD)):
+        np.testing.assert_allclose(a, b, atol=1e-7, rtol=1e-6)
+
+
+def _torch_graph(xt, At, Dt, perm, flags, Ct=None):
+    import torch
+    z = xt
+    K = At.shape[0]
+    for k in range(K):
+        u = z[:, torch.as_tensor(perm[k])] if flags & P else z
+        h1 = u * At[k]
+        if flags & CX:
+            v = torch.fft.ifft(torch.fft.fft(h1, dim=1) * Dt[k], dim=1)
+        else:
+            v = ((h1 @ Ct) * Dt[k]) @ Ct.T
+        z = torch.relu(v) if (flags & R and k < K - 1) else v
+    return z
+
+
+@pytest.mark.parametrize("flags", [0, P, R, P | R, CX, CX | P])
+def test_backward_matches_torch_autograd(flags):
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(200 + flags)
+    N, K, B = 32, 4, 6
+    x, A, D, perm, gy = rand_case(rng, B, N, K, flags)
+    dt = torch.complex128 if flags & CX else torch.float64
+    xt = torch.tensor(x, dtype=dt, requires_grad=True)
+    At = torch.tensor(A, dtype=dt, requires_grad=True)
+    Dt = torch.tensor(D, dtype=dt, requires_grad=True)
+    Ct = torch.tensor(scipy.fft.dct(np.eye(N), type=2, norm="ortho", axis=1), dtype=torch.float64)
+    y = _torch_graph(xt, At, Dt, perm, flags, Ct)
+    y.backward(torch.tensor(gy, dtype=dt))
+    gx, gA, gD = O.backward(x, gy, A, D, perm, flags)
+    np.testing.assert_allclose(gx, xt.grad.numpy(), atol=1e-11)
+    np.testing.assert_allclose(gA, At.grad.numpy(), atol=1e-10)
+    np.testing.assert_allclose(gD, Dt.grad.numpy(), atol=1e-10)
+
+
+def test_backward_batch_split_additivity():
+    rng = np.random.default_rng(300)
+    x, A, D, perm, gy = rand_case(rng, 10, 16, 3, P | R)
+    gx, gA, gD = O.backward(x, gy, A, D, perm, P | R)
+    gx1, gA1, gD1 = O.backward(x[:4], gy[:4], A, D, perm, P | R)
+    gx2, gA2, gD2 = O.backward(x[4:], gy[4:], A, D, perm, P | R)
+    np.testing.assert_allclose(gx, np.concatenate([gx1, gx2]), atol=1e-13)
+    np.testing.assert_allclose(gA, gA1 + gA2, atol=1e-12)
+    np.testing.assert_allclose(gD, gD1 + gD2, atol=1e-12)
+
+
+# ------------------------------------------------------ paper's printed numbers
+
+def test_cost_model_matches_paper_printed_numbers():
+    g = json.load(open(os.path.join(GOLDEN, "paper_cost_model.json")))
+    lo, hi = g["ai_range_N"]
+    # printed to one decimal (9.25 appears as 9.3, so allow half a unit)
+    assert abs(O.arithmetic_intensity(lo) - g["ai_range_printed"][0]) <= 0.05 + 1e-12
+    assert abs(O.arithmetic_intensity(hi) - g["ai_range_printed"][1]) <= 0.05 + 1e-12
+    assert round(g["titan_x_peak_gflops"] / g["titan_x_peak_gbps"]) == g["titan_x_ridge_flop_per_byte_approx"]
+    N = 4096
+    assert O.flops_per_row_layer(N) == 4 * N + 5 * N * 12
+
+
+# ----------------------------------------- planted mistakes must be caught (CPU)
+
+def _pins_pass():
+    """A compact subset of the pins above, run against the (possibly patched)
+    oracle.  Returns False as soon as one fails."""
+    rng = np.random.default_rng(400)
+    try:
+        for flags in (P | R, CX | P):
+            x, A, D, perm, gy = rand_case(rng, 4, 8, 2, flags)
+            np.testing.assert_allclose(O.forward(x, A, D, perm, flags),
+                                       lib_forward(x, A, D, perm, flags), atol=1e-10)
+        test_backward_matches_torch_autograd(P | R)
+        test_backward_matches_torch_autograd(CX | P)
+    except AssertionError:
+        return False
+    return True
+
+
+def test_planted_mistakes_are_caught(monkeypatch):
+    assert _pins_pass()
+    good_dct = O.dct_matrix
+
+    # 1) transposed DCT (C^T D C instead of C D C^T)
+    monkeypatch.setattr(O, "dct_matrix", lambda N: good_dct(N).T.copy())
+    assert not _pins_pass()
+    monkeypatch.setattr(O, "dct_matrix", good_dct)
+
+    # 2) wrong normalisation eps_0 = 1 (breaks orthogonality)
+    def bad_eps(N):
+        C = good_dct(N).copy()
+        C[:, 0] *= np.sqrt(2)
+        return C
+    monkeypatch.setattr(O, "dct_matrix", bad_eps)
+    assert not _pins_pass()
+    monkeypatch.setattr(O, "dct_matrix", good_dct)
+
+    # 3) DFT sign flipped
+    good_dft = O.dft_matrix
+    monkeypatch.setattr(O, "dft_matrix", lambda N: np.conj(good_dft(N)))
+    assert not _pins_pass()
+    monkeypatch.setattr(O, "dft_matrix", good_dft)
+
+    # 4) scatter instead of gather for the permutation
+    good_fwd = O.forward
+
+    def scatter_fwd(x, A, D, perm=None, flags=0, keep=False):
+        inv = None if perm is None else np.argsort(np.asarray(perm), axis=1)
+        return good_fwd(x, A, D, inv, flags, keep)
+    monkeypatch.setattr(O, "forward", scatter_fwd)
+    assert not _pins_pass()
+    monkeypatch.setattr(O, "forward", good_fwd)
+
+    # 5) a dropped conjugate / sign in the backward (perturb the analytic
+    #    backward by computing it on conj(D) for the complex path)
+    good_bwd = O.backward
+
+    def bad_bwd(x, gy, A, D, perm=None, flags=0):
+        return good_bwd(x, gy, A, np.conj(D) if flags & CX else D, perm, flags)
+    monkeypatch.setattr(O, "backward", bad_bwd)
+    assert not _pins_pass()
+    monkeypatch.setattr(O, "backward", good_bwd)
+
+    assert _pins_pass()
