@@ -1,0 +1,175 @@
+"""Benchmark: ACDC cascade forward + backward on one MI355X.
+
+A step is one training pass of the whole cascade over one batch: the forward
+kernel (which also stores the layer inputs) followed by the backward kernel and
+the fixed-order reduction of dL/da, dL/dd.  Inputs are synthetic and seeded
+(paper_1511_05946_amd.workloads) and already resident in HBM when timing
+starts.
+
+Prints ONE JSON line (plus diagnostics on stderr):
+  value      rows*layers/s = batch*K / (seconds per step)
+  roofline   the dominant kernel (backward cascade) against the fp32 vector
+             peak: algorithmic flops per launch / measured launch time
+  cpu_baseline  the fp64 oracle on a bounded sample of the same workload
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "ACDC rows·layers/sec (fwd+bwd) at N=4096,K=12; % of HBM/fp32 roofline"
+UNIT = "rows·layers/s"
+PEAK_FP32_TFLOPS = 157.3     # MI355X fp32 vector peak (256 CU x 2.4 GHz x 256 flop/clk)
+PEAK_HBM_GBPS = 8000.0
+
+
+def flops_row_layer(N: int, complex_: bool) -> float:
+    # Sec. 5 count: 4N + 5N log2 N per row-layer (FFTW convention); AFDF: two
+    # complex N-point FFTs and two complex diagonals.
+    lg = math.log2(N)
+    return (10 * N * lg + 12 * N) if complex_ else (4 * N + 5 * N * lg)
+
+
+def cpu_baseline(w, seed: int, budget_s: float = 12.0, max_rows: int = 512):
+    """Time the oracle (forward + analytic backward, fp64) on growing row
+    chunks of the workload until the budget is used."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import acdc_oracle as O
+    from paper_1511_05946_amd.workloads import make_inputs
+
+    x, A, D, perm, gy = make_inputs(w.N, w.K, min(w.batch, max_rows), w.flags, seed)
+    rows = 0
+    t_total = 0.0
+    chunk = 16 if w.N >= 4096 else 64
+    while rows < x.shape[0] and t_total < budget_s:
+        sl = slice(rows, min(rows + chunk, x.shape[0]))
+        t0 = time.perf_counter()
+        O.forward(x[sl], A, D, perm, w.flags)
+        O.backward(x[sl], gy[sl], A, D, perm, w.flags)
+        t_total += time.perf_counter() - t0
+        rows = sl.stop
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": rows * w.K / t_total, "unit": UNIT, "cores": int(threads), "kind": "oracle",
+            "sample": f"{rows} of {w.batch} rows, full N={w.N}, K={w.K}, fwd + bwd, "
+                      f"O(N^2) fp64 dense-matrix oracle, {t_total:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--recompute", action="store_true",
+                    help="backward recomputes the layer inputs instead of using the forward's")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the cascade shards over rows with one all-reduce of dL/da, dL/dd, "
+              "which is not built here.", file=sys.stderr)
+        sys.exit(2)
+
+    import ctypes
+
+    import torch
+
+    import paper_1511_05946_amd.acdc as acdc
+    from paper_1511_05946_amd._lib import lib
+    from paper_1511_05946_amd.workloads import HEADLINE, WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload or HEADLINE]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    x, A, D, perm, gy = make_inputs(w.N, w.K, w.batch, w.flags, args.seed)
+    t = lambda a: torch.from_numpy(a).to(dev)
+    xt, At, Dt, pt, gyt = t(x), t(A), t(D), t(perm), t(gy)
+    fl = w.flags & ~acdc.FLAG_COMPLEX
+    acdc.prepare(w.N, w.flags)
+    y = torch.empty_like(xt)
+    saved = torch.empty(acdc.saved_shape(xt, w.K), dtype=xt.dtype, device=dev)
+
+    def step():
+        if args.recompute:
+            acdc.forward(xt, At, Dt, pt, fl, out=y)
+            return acdc.backward(xt, gyt, At, Dt, pt, fl, saved=None)
+        acdc.forward(xt, At, Dt, pt, fl, out=y, saved=saved)
+        return acdc.backward(xt, gyt, At, Dt, pt, fl, saved=saved)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    L = lib()
+    L.acdc_profile_enable(1)
+    ms = (ctypes.c_double * 3)()
+    cnt = (ctypes.c_int64 * 3)()
+    L.acdc_profile_read(ms, cnt)  # clear
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    rc = L.acdc_profile_read(ms, cnt)
+    L.acdc_profile_enable(0)
+    if rc != 0:
+        raise RuntimeError(f"acdc_profile_read failed: {rc}")
+
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    value = w.batch * w.K / (ms_step * 1e-3)
+    kern = {name: {"avg_ms": ms[i] / max(cnt[i], 1), "launches": int(cnt[i])}
+            for i, name in enumerate(("forward", "backward", "reduce"))}
+    fwd_launches_per_step = cnt[0] / args.steps
+    f_rl = flops_row_layer(w.N, w.complex)
+    # dominant kernel: the backward cascade; its algorithmic work is one pass
+    # of the layer transform per row-layer, like the forward (Sec. 5).
+    bwd_ms = kern["backward"]["avg_ms"]
+    bwd_flops = w.batch * w.K * f_rl
+    achieved = bwd_flops / (bwd_ms * 1e-3) / 1e12
+    fwd_ms = kern["forward"]["avg_ms"]
+    fwd_achieved = w.batch * w.K * f_rl / (fwd_ms * 1e-3) / 1e12
+    roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": None,
+            "kernel": "k_real_bwd" if not w.complex else "k_cplx_bwd",
+            "kernel_avg_ms": round(bwd_ms, 4),
+            "algorithmic_flops_per_launch": bwd_flops}
+    # fraction of the whole-step roofline (fwd+bwd algorithmic flops at peak)
+    step_flops = 2 * w.batch * w.K * f_rl
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": UNIT, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "c64" if w.complex else "f32",
+        "data": "synthetic (seeded; x ~ relu(N(0,1)), A,D ~ N(1,0.1^2), random permutations)",
+        "config": {"workload": w.name, "N": w.N, "K": w.K, "batch": w.batch,
+                   "flags": w.flags, "parallelism": "single GPU",
+                   "backward": "recompute" if args.recompute else "saved layer inputs"},
+        "roofline": roof,
+        "step_roofline_frac": round(step_flops / (ms_step * 1e-3) / 1e12 / PEAK_FP32_TFLOPS, 4),
+        "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]} for k, v in kern.items()},
+        "forward_tflops": round(fwd_achieved, 3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.seed)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    print(f"[bench] fwd kernel {fwd_ms:.3f} ms ({fwd_launches_per_step:.0f}/step), bwd kernel {bwd_ms:.3f} ms, "
+          f"reduce {kern['reduce']['avg_ms']:.3f} ms, step {ms_step:.3f} ms", file=sys.stderr)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,136 @@
+/*
+ * acdc.h -- C ABI of the MI355X (gfx950) ACDC / AFDF cascade library.
+ *
+ * Operation (Moczulski et al., "ACDC: A Structured Efficient Linear Layer",
+ * arXiv:1511.05946).  One layer maps a row vector x of width N to
+ *
+ *     y = x A C D C^{-1}                      (Sec. 4, ACDC; A = diag(a), D = diag(d))
+ *
+ * with C the orthonormal DCT-II, c_nk = sqrt(2/N) eps_k cos(pi (2n+1) k / 2N),
+ * n the spatial index, eps_0 = 1/sqrt(2), eps_k = 1 otherwise (Sec. 4), so
+ * x C is the DCT-II of x and (.) C^{-1} = (.) C^T the DCT-III.  With
+ * ACDC_FLAG_COMPLEX the layer is the complex AFDF of Sec. 3,
+ *
+ *     y = x A F D F^{-1},   F[n,k] = exp(-2 pi i n k / N),  F^{-1} = conj(F)/N.
+ *
+ * A cascade applies K layers in order, layer 0 first (the order-K product of
+ * Sec. 3, made real in Sec. 4), optionally gathering each layer's input
+ * through a fixed permutation and applying ReLU between layers (Sec. 6.2):
+ *
+ *     u_k = z_{k-1}[perm[k]]      (if ACDC_FLAG_PERM; z_{-1} = x)
+ *     v_k = u_k A_k C D_k C^{-1}
+ *     z_k = max(v_k, 0)           (if ACDC_FLAG_RELU and k < K-1), else v_k
+ *     y   = z_{K-1}
+ *
+ * The backward pass gives dL/dx, dL/da_k, dL/dd_k (Sec. 4 derivative block)
+ * with the parameter gradients summed over the batch.  Complex gradients use
+ * the convention grad = dL/dRe + i dL/dIm (so dL/dx = dL/dy W^H).
+ *
+ * Memory.  Every pointer is a device pointer on the current HIP device unless
+ * stated otherwise.  Arrays are contiguous, row-major, 16-byte aligned:
+ *   x, y, grad_y, grad_x   [batch][N]   float (ACDC) or interleaved complex64
+ *                                       (AFDF: 2N floats per row)
+ *   A, D, grad_A, grad_D   [K][N]       same element type as x
+ *   perm                   [K][N]       int32, each row a permutation of 0..N-1
+ *   saved                  [K-1][batch][N] layer inputs u_1..u_{K-1}
+ * The caller owns every buffer, including the workspaces; the library only
+ * owns a small per-(device, N) table of constants built on first use (or by
+ * acdc_prepare) and kept until the process ends.
+ *
+ * Errors.  Each call validates its arguments on the host before any HIP call
+ * and returns a status; on error nothing is launched and no output is
+ * touched.  Outputs must not alias inputs.  Launch failures return
+ * ACDC_ERR_HIP (the HIP error code is kept per thread, see
+ * acdc_last_hip_error); faults during execution surface asynchronously, as
+ * for any HIP kernel.
+ *
+ * Streams.  Work is enqueued on `stream` (0 = the default stream) without any
+ * host synchronisation, except that the very first use of a width N on a
+ * device uploads its constant table synchronously.  Results are bitwise
+ * reproducible for identical inputs on the same device.
+ *
+ * Supported widths (acdc_supported): ACDC N in {8, 16, ..., 16384} and 9216;
+ * AFDF N in {8, 16, ..., 8192}.  Batch sizes from 0 upward; K >= 1.
+ */
+#ifndef ACDC_H_
+#define ACDC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same type as hipStream_t, declared here so this header needs no HIP headers. */
+typedef struct ihipStream_t* acdc_stream_t;
+
+enum acdc_flags {
+  ACDC_FLAG_PERM = 1u,    /* gather each layer's input through perm[k] */
+  ACDC_FLAG_RELU = 2u,    /* ReLU after layers 0..K-2 (not with COMPLEX) */
+  ACDC_FLAG_COMPLEX = 4u  /* complex AFDF layers on interleaved complex64 */
+};
+
+enum acdc_status {
+  ACDC_OK = 0,
+  ACDC_ERR_INVALID_ARG = -1, /* null/misaligned/aliased pointer, bad size or flag */
+  ACDC_ERR_UNSUPPORTED = -2, /* width N not built, or COMPLEX|RELU */
+  ACDC_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required */
+  ACDC_ERR_HIP = -4          /* a HIP runtime call failed */
+};
+
+/* 1 if (N, flags) is supported by this build, else 0.  Host only. */
+int acdc_supported(int32_t N, uint32_t flags);
+
+/* Build and upload the constant table for (N, flags) on the current device,
+ * so that later calls enqueue without host synchronisation.  Optional. */
+int acdc_prepare(int32_t N, uint32_t flags);
+
+/* Bytes of the optional activation buffer `saved` ([K-1][batch][N] elements). */
+size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
+
+/* Bytes of workspace acdc_forward needs (a re-layout of D).  Host only. */
+size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
+
+/* Bytes of workspace acdc_backward needs: per-workgroup partial sums of the
+ * parameter gradients, the re-layout of D, and -- when have_saved is 0 -- room
+ * to recompute the layer inputs (the paper's recompute policy, Sec. 5). */
+size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags, int have_saved);
+
+/* Forward cascade: y = cascade(x).  If `saved` is non-null it also stores the
+ * layer inputs u_1..u_{K-1} there (acdc_saved_bytes), for acdc_backward. */
+int acdc_forward(const float* x, float* y, const float* A, const float* D, const int32_t* perm,
+                 int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, void* workspace,
+                 size_t workspace_bytes, acdc_stream_t stream);
+
+/* Backward cascade.  Given x and grad_y = dL/dy, writes grad_x = dL/dx and
+ * grad_A, grad_D = dL/da_k, dL/dd_k summed over the batch (overwritten, not
+ * accumulated).  `saved` is the buffer filled by acdc_forward for the same x,
+ * A, D, perm, or null, in which case the layer inputs are recomputed into the
+ * workspace first.  batch == 0 writes zero parameter gradients. */
+int acdc_backward(const float* x, const float* grad_y, const float* A, const float* D,
+                  const int32_t* perm, const float* saved, float* grad_x, float* grad_A, float* grad_D,
+                  int64_t batch, int32_t N, int32_t K, uint32_t flags, void* workspace,
+                  size_t workspace_bytes, acdc_stream_t stream);
+
+/* Kernel timing for benchmarks (not for the callers' hot path).  While
+ * enabled, each launch of the forward-cascade kernel (kind 0), the
+ * backward-cascade kernel (kind 1) and the batch-reduction kernel (kind 2) is
+ * bracketed by HIP events on its stream.  acdc_profile_read waits for the
+ * recorded events, writes the summed durations in milliseconds to ms[0..2]
+ * and the launch counts to launches[0..2] (host arrays of 3), and clears
+ * the record.  Events are created once and reused. */
+int acdc_profile_enable(int enable);
+int acdc_profile_read(double* ms, int64_t* launches);
+
+/* Static description of a status code. */
+const char* acdc_status_string(int status);
+
+/* hipError_t behind the calling thread's most recent ACDC_ERR_HIP (0 if none). */
+int acdc_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ACDC_H_ */

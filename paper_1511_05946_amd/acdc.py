@@ -1,0 +1,155 @@
+"""Python binding of the ACDC / AFDF cascade library.
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of libacdc.so.  Tensors are torch tensors on a ROCm device; the work
+is enqueued on the current torch stream of that device.
+
+Layer (Sec. 4 of arXiv:1511.05946): y = x A C D C^{-1} on row vectors, C the
+orthonormal DCT-II; the complex AFDF layer of Sec. 3 uses the DFT.  A cascade
+chains K layers with optional fixed permutations and ReLU between them.
+"""
+
+from __future__ import annotations
+
+import torch
+
+from ._lib import lib, status_string
+
+FLAG_PERM = 1
+FLAG_RELU = 2
+FLAG_COMPLEX = 4
+
+
+class ACDCError(RuntimeError):
+    pass
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        extra = ""
+        if rc == -4:
+            extra = f" (hipError {lib().acdc_last_hip_error()})"
+        raise ACDCError(f"{what}: {status_string(rc)}{extra}")
+
+
+def _flags(flags: int, x: torch.Tensor) -> int:
+    if x.is_complex():
+        flags |= FLAG_COMPLEX
+    return flags
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+def _dims(x: torch.Tensor, A: torch.Tensor):
+    if x.dim() != 2 or A.dim() != 2:
+        raise ValueError("x must be [batch, N] and A, D [K, N]")
+    return x.shape[0], x.shape[1], A.shape[0]
+
+
+def _validate(tensors, complex_: bool, device):
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if t.device != device:
+            raise ValueError(f"{name} is on {t.device}, expected {device}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if name == "perm":
+            if t.dtype != torch.int32:
+                raise ValueError("perm must be int32")
+        elif complex_ and t.dtype != torch.complex64:
+            raise ValueError(f"{name} must be complex64")
+        elif not complex_ and t.dtype != torch.float32:
+            raise ValueError(f"{name} must be float32")
+
+
+def _stream(device):
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def supported(N: int, flags: int = 0) -> bool:
+    return bool(lib().acdc_supported(int(N), int(flags)))
+
+
+def prepare(N: int, flags: int = 0, device=None):
+    with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
+        _check(lib().acdc_prepare(int(N), int(flags)), "acdc_prepare")
+
+
+def saved_shape(x: torch.Tensor, K: int):
+    return (max(K - 1, 0), x.shape[0], x.shape[1])
+
+
+def forward(x, A, D, perm=None, flags: int = 0, save: bool = False, out=None, saved=None):
+    """y = cascade(x).  Returns (y, saved) where saved holds the layer inputs
+    u_1..u_{K-1} when ``save`` (or a preallocated ``saved``) is given."""
+    flags = _flags(flags, x)
+    cplx = bool(flags & FLAG_COMPLEX)
+    B, N, K = _dims(x, A)
+    if out is None:
+        out = torch.empty_like(x)
+    if save and saved is None:
+        saved = torch.empty(saved_shape(x, K), dtype=x.dtype, device=x.device)
+    _validate({"x": x, "A": A, "D": D, "y": out, "saved": saved,
+               "perm": perm if flags & FLAG_PERM else None}, cplx, x.device)
+    L = lib()
+    ws_bytes = L.acdc_forward_workspace_bytes(B, N, K, flags)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=x.device)
+    with torch.cuda.device(x.device):
+        rc = L.acdc_forward(_ptr(x), _ptr(out), _ptr(A), _ptr(D),
+                            _ptr(perm) if flags & FLAG_PERM else None, B, N, K, flags,
+                            _ptr(saved) if (saved is not None and K > 1) else None,
+                            _ptr(ws), ws_bytes, _stream(x.device))
+    _check(rc, "acdc_forward")
+    return out, saved
+
+
+def backward(x, grad_y, A, D, perm=None, flags: int = 0, saved=None):
+    """(grad_x, grad_A, grad_D); parameter gradients are summed over the batch.
+    Without ``saved`` the layer inputs are recomputed inside the call."""
+    flags = _flags(flags, x)
+    cplx = bool(flags & FLAG_COMPLEX)
+    B, N, K = _dims(x, A)
+    gx = torch.empty_like(x)
+    gA = torch.empty_like(A)
+    gD = torch.empty_like(D)
+    _validate({"x": x, "grad_y": grad_y, "A": A, "D": D, "saved": saved,
+               "perm": perm if flags & FLAG_PERM else None}, cplx, x.device)
+    L = lib()
+    have_saved = 1 if (saved is not None or K == 1) else 0
+    ws_bytes = L.acdc_backward_workspace_bytes(B, N, K, flags, have_saved)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=x.device)
+    with torch.cuda.device(x.device):
+        rc = L.acdc_backward(_ptr(x), _ptr(grad_y), _ptr(A), _ptr(D),
+                             _ptr(perm) if flags & FLAG_PERM else None,
+                             _ptr(saved) if (saved is not None and K > 1) else None,
+                             _ptr(gx), _ptr(gA), _ptr(gD), B, N, K, flags, _ptr(ws), ws_bytes,
+                             _stream(x.device))
+    _check(rc, "acdc_backward")
+    return gx, gA, gD
+
+
+class ACDCCascade(torch.autograd.Function):
+    """autograd wrapper: stores the layer inputs in the forward pass."""
+
+    @staticmethod
+    def forward(ctx, x, A, D, perm, flags):
+        y, saved = forward(x.contiguous(), A.contiguous(), D.contiguous(), perm, flags, save=True)
+        ctx.save_for_backward(x, A, D, perm if perm is not None else torch.empty(0), saved)
+        ctx.flags = flags
+        ctx.has_perm = perm is not None
+        return y
+
+    @staticmethod
+    def backward(ctx, gy):
+        x, A, D, perm, saved = ctx.saved_tensors
+        gx, gA, gD = backward(x, gy.contiguous(), A, D, perm if ctx.has_perm else None, ctx.flags, saved)
+        return gx, gA, gD, None, None
+
+
+def acdc_cascade(x, A, D, perm=None, flags: int = 0):
+    return ACDCCascade.apply(x, A, D, perm, flags)

@@ -1,0 +1,523 @@
+// HIP kernels for gfx950 and the C ABI declared in include/acdc.h.
+//
+// Kernels (one instantiation per supported width):
+//   k_real_dq      D re-laid out into the per-thread quartet order (tiny)
+//   k_real_fwd     forward cascade, ROWS rows per workgroup, all K layers
+//                  fused, rows kept in registers + one LDS slab per row
+//   k_real_bwd     backward cascade with the reduction of dL/da, dL/dd over
+//                  the workgroup's rows into one partial per workgroup
+//   k_real_reduce  fixed-order sum of the partials over workgroups
+//   k_cplx_*       the same for the complex AFDF layers
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <map>
+#include <mutex>
+#include <tuple>
+#include <vector>
+
+#include "acdc.h"
+#include "acdc_registry.hpp"
+
+namespace acdc {
+
+// LDS synchronisation for a row spread over T threads.  A row that fits in
+// one wavefront only needs its LDS accesses kept in program order (LDS
+// operations of a wavefront execute in order); wider rows use the workgroup
+// barrier.
+template <int T>
+struct DevCtx {
+  __device__ __forceinline__ void sync_row() {
+    if constexpr (T > 64) {
+      __syncthreads();
+    } else {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+  }
+  __device__ __forceinline__ void sync_all() { __syncthreads(); }
+};
+
+template <class PL>
+__global__ __launch_bounds__(256) void k_real_dq(const float* __restrict__ D, float4* __restrict__ Dq, int K,
+                                                 const char* __restrict__ tab) {
+  constexpr int E = PL::NSL * PL::T;
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long long)K * E) return;
+  const int k = int(i / E), e = int(i % E);
+  Dq[i] = real_dq_entry<PL>(D + (long long)k * PL::N, tab, e);
+}
+
+template <class PL>
+__global__ __launch_bounds__(Launch<PL>::FWD_THREADS)
+__attribute__((amdgpu_waves_per_eu(Launch<PL>::FWD_WPE))) void k_real_fwd(RealArgs a) {
+  using L = Launch<PL>;
+  __shared__ float lds[L::FWD_ROWS * L::FWD_SLAB];
+  DevCtx<PL::T> ctx;
+  const int tid = threadIdx.x, r = tid / PL::T, t = tid % PL::T;
+  real_forward_row<PL>(ctx, a, t, (long long)blockIdx.x * L::FWD_ROWS + r, lds + r * L::FWD_SLAB);
+}
+
+template <class PL>
+__global__ __launch_bounds__(Launch<PL>::BWD_THREADS)
+__attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealArgs a) {
+  using L = Launch<PL>;
+  __shared__ float lds[L::BWD_ROWS * L::BWD_SLAB];
+  DevCtx<PL::T> ctx;
+  const int tid = threadIdx.x, r = tid / PL::T, t = tid % PL::T;
+  real_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS + r, tid,
+                                     (long long)blockIdx.x, lds, lds + r * L::BWD_SLAB);
+}
+
+template <class PL>
+__global__ __launch_bounds__(256) void k_real_reduce(const float* __restrict__ partial, long long ntiles, int K,
+                                                     float* __restrict__ gA, float* __restrict__ gD,
+                                                     const char* __restrict__ tab) {
+  constexpr long long PS = PL::N + PL::QF;
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long long)K * PS) return;
+  real_reduce_entry<PL>(partial, ntiles, K, int(i / PS), int(i % PS), gA, gD, tab);
+}
+
+template <class PL>
+__global__ __launch_bounds__(Launch<PL>::FWD_THREADS)
+__attribute__((amdgpu_waves_per_eu(Launch<PL>::FWD_WPE))) void k_cplx_fwd(CplxArgs a) {
+  using L = Launch<PL>;
+  __shared__ float lds[L::FWD_ROWS * L::FWD_SLAB];
+  DevCtx<PL::T> ctx;
+  const int tid = threadIdx.x, r = tid / PL::T, t = tid % PL::T;
+  cplx_forward_row<PL>(ctx, a, t, (long long)blockIdx.x * L::FWD_ROWS + r, lds + r * L::FWD_SLAB);
+}
+
+template <class PL>
+__global__ __launch_bounds__(Launch<PL>::BWD_THREADS)
+__attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_cplx_bwd(CplxArgs a) {
+  using L = Launch<PL>;
+  __shared__ float lds[L::BWD_ROWS * L::BWD_SLAB];
+  DevCtx<PL::T> ctx;
+  const int tid = threadIdx.x, r = tid / PL::T, t = tid % PL::T;
+  cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS + r, tid,
+                                     (long long)blockIdx.x, lds, lds + r * L::BWD_SLAB);
+}
+
+template <class PL>
+__global__ __launch_bounds__(256) void k_cplx_reduce(const float* __restrict__ partial, long long ntiles, int K,
+                                                     float* __restrict__ gA, float* __restrict__ gD) {
+  constexpr long long PS = 4LL * PL::N;
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long long)K * PS) return;
+  const int k = int(i / PS), e = int(i % PS);
+  const float s = tile_sum(partial, ntiles, (long long)K * PS, (long long)k * PS + e);
+  if (e < 2 * PL::N) gA[(long long)k * 2 * PL::N + e] = s;
+  else gD[(long long)k * 2 * PL::N + (e - 2 * PL::N)] = s;
+}
+
+// ------------------------------------------------------------------ host side
+
+namespace {
+
+thread_local int g_last_hip = 0;
+std::mutex g_mu;
+std::map<std::tuple<int, int, int>, void*> g_tables;  // (device, N, complex) -> device table
+
+size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+int hip_fail(hipError_t e) {
+  g_last_hip = int(e);
+  return ACDC_ERR_HIP;
+}
+
+// ----------------------------------------------------------- kernel timing
+// While enabled, every main kernel launch is bracketed by HIP events on its
+// stream (kind 0: forward cascade, 1: backward cascade, 2: batch reduction).
+struct ProfRec {
+  hipEvent_t a, b;
+  int kind;
+};
+bool g_prof_on = false;
+std::mutex g_prof_mu;
+std::vector<ProfRec> g_prof_recs;
+std::vector<hipEvent_t> g_prof_pool;
+
+hipEvent_t prof_event() {
+  if (!g_prof_pool.empty()) {
+    hipEvent_t e = g_prof_pool.back();
+    g_prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+struct ProfScope {
+  int kind;
+  hipStream_t s;
+  hipEvent_t a = nullptr, b = nullptr;
+  ProfScope(int k, hipStream_t st) : kind(k), s(st) {
+    if (!g_prof_on) return;
+    std::lock_guard<std::mutex> lock(g_prof_mu);
+    a = prof_event();
+    b = prof_event();
+    if (a && b) (void)hipEventRecord(a, s);
+  }
+  ~ProfScope() {
+    if (!a || !b) return;
+    (void)hipEventRecord(b, s);
+    std::lock_guard<std::mutex> lock(g_prof_mu);
+    g_prof_recs.push_back(ProfRec{a, b, kind});
+  }
+};
+
+bool supported(int N, unsigned flags) {
+  bool ok = false;
+  auto probe = [&]<class PL>() { ok = true; };
+  if (flags & kFlagComplex) dispatch_complex(N, probe);
+  else dispatch_real(N, probe);
+  return ok;
+}
+
+// Constant table of (N, complex) on the current device; built and uploaded
+// on first use.
+int get_table(int N, bool cplx, const char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e);
+  std::lock_guard<std::mutex> lock(g_mu);
+  auto key = std::make_tuple(dev, N, cplx ? 1 : 0);
+  auto it = g_tables.find(key);
+  if (it != g_tables.end()) {
+    *out = static_cast<const char*>(it->second);
+    return ACDC_OK;
+  }
+  std::vector<unsigned char> host;
+  bool built = false, ok = false;
+  auto build = [&]<class PL>() {
+    built = true;
+    if constexpr (PL::kComplex) ok = build_complex_tables<PL>(host);
+    else ok = build_real_tables<PL>(host);
+  };
+  if (cplx) dispatch_complex(N, build);
+  else dispatch_real(N, build);
+  if (!built) return ACDC_ERR_UNSUPPORTED;
+  if (!ok) return ACDC_ERR_UNSUPPORTED;
+  void* d = nullptr;
+  e = hipMalloc(&d, host.size());
+  if (e != hipSuccess) return hip_fail(e);
+  e = hipMemcpy(d, host.data(), host.size(), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(d);
+    return hip_fail(e);
+  }
+  g_tables[key] = d;
+  *out = static_cast<const char*>(d);
+  return ACDC_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_common(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
+  if (flags & ~7u) return ACDC_ERR_INVALID_ARG;
+  if ((flags & kFlagComplex) && (flags & kFlagRelu)) return ACDC_ERR_UNSUPPORTED;
+  if (batch < 0 || K < 1 || K > 65535 || N < 1) return ACDC_ERR_INVALID_ARG;
+  if (!supported(N, flags)) return ACDC_ERR_UNSUPPORTED;
+  if (batch > (int64_t(1) << 40) / N) return ACDC_ERR_INVALID_ARG;
+  return ACDC_OK;
+}
+
+int check_ptrs(std::initializer_list<const void*> must, std::initializer_list<const void*> may) {
+  for (const void* p : must)
+    if (p == nullptr || !aligned16(p)) return ACDC_ERR_INVALID_ARG;
+  for (const void* p : may)
+    if (p != nullptr && !aligned16(p)) return ACDC_ERR_INVALID_ARG;
+  return ACDC_OK;
+}
+
+bool distinct(std::initializer_list<const void*> outs, std::initializer_list<const void*> all) {
+  for (const void* o : outs) {
+    if (o == nullptr) continue;
+    int seen = 0;
+    for (const void* p : all)
+      if (p == o) ++seen;
+    if (seen != 1) return false;
+  }
+  return true;
+}
+
+template <class PL>
+long long fwd_blocks(int64_t batch) {
+  return (batch + Launch<PL>::FWD_ROWS - 1) / Launch<PL>::FWD_ROWS;
+}
+template <class PL>
+long long bwd_tiles(int64_t batch) {
+  return (batch + Launch<PL>::BWD_ROWS - 1) / Launch<PL>::BWD_ROWS;
+}
+
+size_t elem_floats(uint32_t flags) { return (flags & kFlagComplex) ? 2 : 1; }
+
+struct WsLayout {
+  size_t dq = 0, partial = 0, stash = 0, total = 0;
+  size_t off_dq = 0, off_partial = 0, off_stash = 0;
+};
+
+WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved) {
+  WsLayout w;
+  auto f = [&]<class PL>() {
+    const long long tiles = bwd_tiles<PL>(batch);
+    if constexpr (PL::kComplex) {
+      w.partial = align256(size_t(tiles) * K * 4 * PL::N * sizeof(float));
+    } else {
+      w.dq = align256(size_t(K) * PL::NSL * PL::T * sizeof(float4));
+      w.partial = align256(size_t(tiles) * K * (PL::N + PL::QF) * sizeof(float));
+    }
+  };
+  if (flags & kFlagComplex) dispatch_complex(N, f);
+  else dispatch_real(N, f);
+  if (!have_saved && K > 1) w.stash = align256(size_t(K - 1) * size_t(batch) * N * elem_floats(flags) * 4);
+  w.off_dq = 0;
+  w.off_partial = w.dq;
+  w.off_stash = w.dq + w.partial;
+  w.total = w.dq + w.partial + w.stash;
+  return w;
+}
+
+size_t fwd_ws(int32_t N, int32_t K, uint32_t flags) {
+  size_t b = 0;
+  if (!(flags & kFlagComplex))
+    dispatch_real(N, [&]<class PL>() { b = align256(size_t(K) * PL::NSL * PL::T * sizeof(float4)); });
+  return b;
+}
+
+template <class PL>
+int launch_real_dq(const float* D, float4* Dq, int K, const char* tab, hipStream_t s) {
+  const long long n = (long long)K * PL::NSL * PL::T;
+  hipLaunchKernelGGL(k_real_dq<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, D, Dq, K, tab);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? ACDC_OK : hip_fail(e);
+}
+
+template <class PL>
+int launch_real_fwd(const RealArgs& a, hipStream_t s) {
+  ProfScope prof(0, s);
+  hipLaunchKernelGGL(k_real_fwd<PL>, dim3(unsigned(fwd_blocks<PL>(a.batch))), dim3(Launch<PL>::FWD_THREADS), 0,
+                     s, a);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? ACDC_OK : hip_fail(e);
+}
+
+template <class PL>
+int launch_cplx_fwd(const CplxArgs& a, hipStream_t s) {
+  ProfScope prof(0, s);
+  hipLaunchKernelGGL(k_cplx_fwd<PL>, dim3(unsigned(fwd_blocks<PL>(a.batch))), dim3(Launch<PL>::FWD_THREADS), 0,
+                     s, a);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? ACDC_OK : hip_fail(e);
+}
+
+}  // namespace
+}  // namespace acdc
+
+using namespace acdc;
+
+extern "C" int acdc_supported(int32_t N, uint32_t flags) {
+  if (flags & ~7u) return 0;
+  if ((flags & kFlagComplex) && (flags & kFlagRelu)) return 0;
+  return supported(N, flags) ? 1 : 0;
+}
+
+extern "C" int acdc_prepare(int32_t N, uint32_t flags) {
+  if (!acdc_supported(N, flags)) return ACDC_ERR_UNSUPPORTED;
+  const char* tab = nullptr;
+  return get_table(N, (flags & kFlagComplex) != 0, &tab);
+}
+
+extern "C" size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
+  if (check_common(batch, N, K, flags) != ACDC_OK) return 0;
+  return size_t(K - 1) * size_t(batch) * size_t(N) * elem_floats(flags) * sizeof(float);
+}
+
+extern "C" size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
+  if (check_common(batch, N, K, flags) != ACDC_OK) return 0;
+  return fwd_ws(N, K, flags);
+}
+
+extern "C" size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags,
+                                                int have_saved) {
+  if (check_common(batch, N, K, flags) != ACDC_OK) return 0;
+  return bwd_layout(batch, N, K, flags, have_saved != 0).total;
+}
+
+extern "C" int acdc_forward(const float* x, float* y, const float* A, const float* D, const int32_t* perm,
+                            int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, void* workspace,
+                            size_t workspace_bytes, acdc_stream_t stream) {
+  int rc = check_common(batch, N, K, flags);
+  if (rc != ACDC_OK) return rc;
+  const bool perm_on = (flags & kFlagPerm) != 0;
+  if (batch == 0) return ACDC_OK;
+  rc = check_ptrs({x, y, A, D}, {perm_on ? (const void*)perm : nullptr, saved, workspace});
+  if (rc != ACDC_OK) return rc;
+  if (perm_on && perm == nullptr) return ACDC_ERR_INVALID_ARG;
+  if (!distinct({y, saved}, {x, y, A, D, perm, saved, workspace})) return ACDC_ERR_INVALID_ARG;
+  const size_t need = fwd_ws(N, K, flags);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return ACDC_ERR_WORKSPACE;
+  const bool cplx = (flags & kFlagComplex) != 0;
+  const char* tab = nullptr;
+  rc = get_table(N, cplx, &tab);
+  if (rc != ACDC_OK) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (cplx) {
+    dispatch_complex(N, [&]<class PL>() {
+      CplxArgs a{x, y, A, D, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
+      rc = launch_cplx_fwd<PL>(a, s);
+    });
+  } else {
+    dispatch_real(N, [&]<class PL>() {
+      float4* Dq = static_cast<float4*>(workspace);
+      rc = launch_real_dq<PL>(D, Dq, K, tab, s);
+      if (rc != ACDC_OK) return;
+      RealArgs a{x, y, A, Dq, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
+      rc = launch_real_fwd<PL>(a, s);
+    });
+  }
+  return rc;
+}
+
+extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A, const float* D,
+                             const int32_t* perm, const float* saved, float* grad_x, float* grad_A,
+                             float* grad_D, int64_t batch, int32_t N, int32_t K, uint32_t flags,
+                             void* workspace, size_t workspace_bytes, acdc_stream_t stream) {
+  int rc = check_common(batch, N, K, flags);
+  if (rc != ACDC_OK) return rc;
+  const bool perm_on = (flags & kFlagPerm) != 0;
+  rc = check_ptrs({A, D, grad_A, grad_D}, {perm_on ? (const void*)perm : nullptr, saved, workspace});
+  if (rc != ACDC_OK) return rc;
+  if (batch > 0) {
+    rc = check_ptrs({x, grad_y, grad_x}, {});
+    if (rc != ACDC_OK) return rc;
+    if (perm_on && perm == nullptr) return ACDC_ERR_INVALID_ARG;
+  }
+  if (!distinct({grad_x, grad_A, grad_D}, {x, grad_y, A, D, perm, saved, grad_x, grad_A, grad_D, workspace}))
+    return ACDC_ERR_INVALID_ARG;
+  const bool have_saved = saved != nullptr || K == 1;
+  const WsLayout w = bwd_layout(batch, N, K, flags, have_saved);
+  if (w.total > 0 && (workspace == nullptr || workspace_bytes < w.total)) return ACDC_ERR_WORKSPACE;
+  const bool cplx = (flags & kFlagComplex) != 0;
+  const char* tab = nullptr;
+  rc = get_table(N, cplx, &tab);
+  if (rc != ACDC_OK) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  float* partial = reinterpret_cast<float*>(ws + w.off_partial);
+  float* stash = have_saved ? const_cast<float*>(saved) : reinterpret_cast<float*>(ws + w.off_stash);
+  if (cplx) {
+    dispatch_complex(N, [&]<class PL>() {
+      using L = Launch<PL>;
+      const long long tiles = bwd_tiles<PL>(batch);
+      if (batch > 0) {
+        if (!have_saved) {
+          CplxArgs f{x, nullptr, A, D, perm, stash, nullptr, nullptr, nullptr, tab, batch, K, flags};
+          rc = launch_cplx_fwd<PL>(f, s);
+          if (rc != ACDC_OK) return;
+        }
+        CplxArgs a{x, nullptr, A, D, perm, stash, grad_y, grad_x, partial, tab, batch, K, flags};
+        hipError_t e;
+        {
+          ProfScope prof(1, s);
+          hipLaunchKernelGGL(k_cplx_bwd<PL>, dim3(unsigned(tiles)), dim3(L::BWD_THREADS), 0, s, a);
+          e = hipGetLastError();
+        }
+        if (e != hipSuccess) {
+          rc = hip_fail(e);
+          return;
+        }
+      }
+      const long long n = (long long)K * 4 * PL::N;
+      hipError_t e;
+      {
+        ProfScope prof(2, s);
+        hipLaunchKernelGGL(k_cplx_reduce<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, partial, tiles, K,
+                         grad_A, grad_D);
+        e = hipGetLastError();
+      }
+      rc = e == hipSuccess ? ACDC_OK : hip_fail(e);
+    });
+  } else {
+    dispatch_real(N, [&]<class PL>() {
+      using L = Launch<PL>;
+      const long long tiles = bwd_tiles<PL>(batch);
+      if (batch > 0) {
+        float4* Dq = reinterpret_cast<float4*>(ws + w.off_dq);
+        rc = launch_real_dq<PL>(D, Dq, K, tab, s);
+        if (rc != ACDC_OK) return;
+        if (!have_saved) {
+          RealArgs f{x, nullptr, A, Dq, perm, stash, nullptr, nullptr, nullptr, tab, batch, K, flags};
+          rc = launch_real_fwd<PL>(f, s);
+          if (rc != ACDC_OK) return;
+        }
+        RealArgs a{x, nullptr, A, Dq, perm, stash, grad_y, grad_x, partial, tab, batch, K, flags};
+        hipError_t e;
+        {
+          ProfScope prof(1, s);
+          hipLaunchKernelGGL(k_real_bwd<PL>, dim3(unsigned(tiles)), dim3(L::BWD_THREADS), 0, s, a);
+          e = hipGetLastError();
+        }
+        if (e != hipSuccess) {
+          rc = hip_fail(e);
+          return;
+        }
+      }
+      const long long n = (long long)K * (PL::N + PL::QF);
+      hipError_t e;
+      {
+        ProfScope prof(2, s);
+        hipLaunchKernelGGL(k_real_reduce<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, partial, tiles, K,
+                         grad_A, grad_D, tab);
+        e = hipGetLastError();
+      }
+      rc = e == hipSuccess ? ACDC_OK : hip_fail(e);
+    });
+  }
+  return rc;
+}
+
+extern "C" int acdc_profile_enable(int enable) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  g_prof_on = enable != 0;
+  return ACDC_OK;
+}
+
+extern "C" int acdc_profile_read(double* ms, int64_t* launches) {
+  if (ms == nullptr || launches == nullptr) return ACDC_ERR_INVALID_ARG;
+  for (int i = 0; i < 3; ++i) {
+    ms[i] = 0.0;
+    launches[i] = 0;
+  }
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  int rc = ACDC_OK;
+  for (const ProfRec& r : g_prof_recs) {
+    float t = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, r.a, r.b);
+    if (e != hipSuccess) rc = hip_fail(e);
+    ms[r.kind] += t;
+    launches[r.kind] += 1;
+    g_prof_pool.push_back(r.a);
+    g_prof_pool.push_back(r.b);
+  }
+  g_prof_recs.clear();
+  return rc;
+}
+
+extern "C" const char* acdc_status_string(int status) {
+  switch (status) {
+    case ACDC_OK: return "ok";
+    case ACDC_ERR_INVALID_ARG: return "invalid argument";
+    case ACDC_ERR_UNSUPPORTED: return "unsupported width or flag combination";
+    case ACDC_ERR_WORKSPACE: return "workspace missing or too small";
+    case ACDC_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+extern "C" int acdc_last_hip_error(void) { return g_last_hip; }

@@ -1,0 +1,126 @@
+// Compile-time plans: how one row of width N is spread over threads and how
+// its transforms are factored into Stockham passes.
+//
+// Real ACDC rows (DCT-II via Makhoul's reordering, Sec. 5 multi-call recipe
+// and its Makhoul reference): a row of N reals is packed as M = N/2 complex
+// values z[m] = v[2m] + i v[2m+1] and transformed by an M-point complex FFT.
+// T threads share a row; each holds P = M/T complex values in registers.
+// The FFT runs as NPASS Stockham passes with radices RAD[0..NPASS-1]; the
+// inverse FFT runs the radices in reverse order so that its output lands in
+// exactly the register layout the forward FFT reads.
+//
+// Complex AFDF rows (Sec. 3): N complex values, N-point FFT, same idea
+// without the real-to-complex packing.
+#pragma once
+
+#include <cstdint>
+
+namespace acdc {
+
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
+template <int N_, int T_, int R0_, int R1_, int R2_ = 1, int R3_ = 1>
+struct RealPlan {
+  static constexpr bool kComplex = false;
+  static constexpr int N = N_;
+  static constexpr int M = N_ / 2;  // complex points per row
+  static constexpr int T = T_;      // threads per row
+  static constexpr int P = M / T_;  // complex registers per thread
+  static constexpr int NPASS = (R2_ == 1) ? 2 : ((R3_ == 1) ? 3 : 4);
+  __host__ __device__ static constexpr int rad(int p) {
+    return p == 0 ? R0_ : p == 1 ? R1_ : p == 2 ? R2_ : R3_;
+  }
+  // radix of pass p of the forward (INV=false) or inverse (INV=true) FFT
+  __host__ __device__ static constexpr int radix(int p, bool inv) {
+    return inv ? rad(NPASS - 1 - p) : rad(p);
+  }
+  // Stockham stride Ns before pass p: product of the earlier radices
+  __host__ __device__ static constexpr int ns(int p, bool inv) {
+    int s = 1;
+    for (int q = 0; q < p; ++q) s *= radix(q, inv);
+    return s;
+  }
+  static constexpr int R0 = R0_;
+  static constexpr int RL = rad(NPASS - 1);
+  static constexpr int B0 = P / R0;              // butterflies per thread, first pass
+  static constexpr int BL = P / RL;              // butterflies per thread, last pass
+  static constexpr int NB = M / RL;              // butterflies of the last pass
+  static constexpr int NSL = (BL / 2) * RL + 1;  // quartet slots per thread (+1 spare)
+  static constexpr int QF = NSL * T * 4;         // floats of one row's quartet image
+  static constexpr int SLAB = cmax(N, QF);       // LDS floats per row
+  // twiddle table (float2) offsets: forward passes 1.., then inverse passes 1..
+  __host__ __device__ static constexpr int tw_count(int p, bool inv) {
+    return p == 0 ? 0 : ns(p, inv) * (radix(p, inv) - 1);
+  }
+  __host__ __device__ static constexpr int tw_off(int p, bool inv) {
+    int o = 0;
+    for (int d = 0; d < 2; ++d)
+      for (int q = 0; q < NPASS; ++q) {
+        if (d == (inv ? 1 : 0) && q == p) return o;
+        o += tw_count(q, d == 1);
+      }
+    return o;
+  }
+  static constexpr int TW_FLOAT2 = tw_off(NPASS, true);
+  // table block layout in bytes: [fft twiddles][mk0 float4 NSL*T][mk1 float4 NSL*T]
+  //                             [qidx int4 NSL*T][qmask int NSL*T]
+  static constexpr int OFF_MK0 = ((TW_FLOAT2 * 8 + 255) / 256) * 256;
+  static constexpr int OFF_MK1 = OFF_MK0 + NSL * T * 16;
+  static constexpr int OFF_QIDX = OFF_MK1 + NSL * T * 16;
+  static constexpr int OFF_QMASK = OFF_QIDX + NSL * T * 16;
+  static constexpr int TABLE_BYTES = ((OFF_QMASK + NSL * T * 4 + 255) / 256) * 256;
+
+  static_assert(N % 4 == 0, "N must be a multiple of 4");
+  static_assert(M % T == 0, "threads must divide the row");
+  static_assert(T <= 64 ? (64 % T == 0) : (T % 64 == 0), "rows tile whole waves");
+  static_assert(R0_ * R1_ * R2_ * R3_ == M, "radices must multiply to N/2");
+  static_assert(P % R0_ == 0 && P % R1_ == 0 && P % R2_ == 0 && P % R3_ == 0,
+                "each radix must divide the per-thread register count");
+  static_assert(B0 % 2 == 0, "first pass pairs mirrored butterflies");
+  static_assert(BL % 2 == 0 && RL % 2 == 0, "last pass pairs negated butterflies");
+  static_assert(R0 % 2 == 0, "first pass radix must be even");
+};
+
+template <int N_, int T_, int R0_, int R1_, int R2_ = 1, int R3_ = 1>
+struct ComplexPlan {
+  static constexpr bool kComplex = true;
+  static constexpr int N = N_;  // complex points per row
+  static constexpr int M = N_;
+  static constexpr int T = T_;
+  static constexpr int P = N_ / T_;
+  static constexpr int NPASS = (R1_ == 1) ? 1 : ((R2_ == 1) ? 2 : ((R3_ == 1) ? 3 : 4));
+  __host__ __device__ static constexpr int rad(int p) {
+    return p == 0 ? R0_ : p == 1 ? R1_ : p == 2 ? R2_ : R3_;
+  }
+  __host__ __device__ static constexpr int radix(int p, bool inv) {
+    return inv ? rad(NPASS - 1 - p) : rad(p);
+  }
+  __host__ __device__ static constexpr int ns(int p, bool inv) {
+    int s = 1;
+    for (int q = 0; q < p; ++q) s *= radix(q, inv);
+    return s;
+  }
+  static constexpr int SLAB = 2 * N_;  // LDS floats per row
+  __host__ __device__ static constexpr int tw_count(int p, bool inv) {
+    return p == 0 ? 0 : ns(p, inv) * (radix(p, inv) - 1);
+  }
+  __host__ __device__ static constexpr int tw_off(int p, bool inv) {
+    int o = 0;
+    for (int d = 0; d < 2; ++d)
+      for (int q = 0; q < NPASS; ++q) {
+        if (d == (inv ? 1 : 0) && q == p) return o;
+        o += tw_count(q, d == 1);
+      }
+    return o;
+  }
+  static constexpr int TW_FLOAT2 = tw_off(NPASS, true);
+  static constexpr int TABLE_BYTES = ((TW_FLOAT2 * 8 + 255) / 256) * 256 + 256;
+
+  static_assert(N_ % T_ == 0, "threads must divide the row");
+  static_assert(T <= 64 ? (64 % T == 0) : (T % 64 == 0), "rows tile whole waves");
+  static_assert(R0_ * R1_ * R2_ * R3_ == N_, "radices must multiply to N");
+  static_assert(P % R0_ == 0 && P % R1_ == 0 && P % R2_ == 0 && P % R3_ == 0,
+                "each radix must divide the per-thread register count");
+};
+
+}  // namespace acdc

@@ -1,0 +1,141 @@
+// The supported row widths and their plans, plus the per-element helpers
+// shared by the GPU kernels and the CPU emulation (parameter re-layout and
+// the fixed-order batch reduction).
+#pragma once
+
+#include "acdc_complex.hpp"
+#include "acdc_real.hpp"
+#include "acdc_tables.hpp"
+
+namespace acdc {
+
+// Real ACDC plans: N -> (threads per row, Stockham radices of the N/2-point FFT).
+using RP8 = RealPlan<8, 1, 2, 2>;
+using RP16 = RealPlan<16, 1, 2, 4>;
+using RP32 = RealPlan<32, 2, 4, 4>;
+using RP64 = RealPlan<64, 2, 4, 8>;
+using RP128 = RealPlan<128, 4, 8, 8>;
+using RP256 = RealPlan<256, 4, 16, 8>;
+using RP512 = RealPlan<512, 8, 16, 16>;
+using RP1024 = RealPlan<1024, 16, 16, 2, 16>;
+using RP2048 = RealPlan<2048, 32, 16, 4, 16>;
+using RP4096 = RealPlan<4096, 64, 16, 8, 16>;
+using RP8192 = RealPlan<8192, 128, 16, 16, 16>;
+using RP9216 = RealPlan<9216, 192, 12, 8, 4, 12>;
+using RP16384 = RealPlan<16384, 256, 16, 32, 16>;
+
+// Complex AFDF plans: N -> (threads per row, radices of the N-point FFT).
+using CP8 = ComplexPlan<8, 1, 2, 4>;
+using CP16 = ComplexPlan<16, 1, 4, 4>;
+using CP32 = ComplexPlan<32, 2, 4, 8>;
+using CP64 = ComplexPlan<64, 4, 8, 8>;
+using CP128 = ComplexPlan<128, 8, 16, 8>;
+using CP256 = ComplexPlan<256, 8, 16, 16>;
+using CP512 = ComplexPlan<512, 16, 32, 16>;
+using CP1024 = ComplexPlan<1024, 32, 32, 32>;
+using CP2048 = ComplexPlan<2048, 64, 32, 2, 32>;
+using CP4096 = ComplexPlan<4096, 128, 32, 4, 32>;
+using CP8192 = ComplexPlan<8192, 256, 32, 8, 32>;
+
+// Rows per workgroup.  Forward rows are independent; backward rows of one
+// workgroup are reduced together into one partial of dL/da, dL/dd.
+template <class PL>
+struct Launch {
+  static constexpr int FWD_ROWS = PL::T >= 128 ? 1 : 128 / PL::T;
+  static constexpr int BWD_ROWS = PL::T == 192 ? 4 : (PL::T >= 512 ? 1 : 512 / PL::T);
+  static constexpr int FWD_THREADS = FWD_ROWS * PL::T;
+  static constexpr int BWD_THREADS = BWD_ROWS * PL::T;
+  static constexpr int FWD_SLAB = PL::kComplex ? PL::SLAB : PL::N;  // floats per row
+  static constexpr int BWD_SLAB = PL::SLAB;
+  static constexpr int FWD_LDS_BYTES = FWD_ROWS * FWD_SLAB * 4;
+  static constexpr int BWD_LDS_BYTES = BWD_ROWS * BWD_SLAB * 4;
+  // Occupancy the register allocator must reach (512 / WPE registers per lane).
+  static constexpr int FWD_WPE = 2;
+  static constexpr int BWD_WPE = 2;
+  static_assert(FWD_LDS_BYTES <= 160 * 1024 && BWD_LDS_BYTES <= 160 * 1024, "LDS budget");
+  static_assert(BWD_THREADS <= 1024 && FWD_THREADS <= 1024, "workgroup size");
+};
+
+// Calls f.template operator()<Plan>() for the real plan of width N.
+template <class F>
+inline bool dispatch_real(int N, F&& f) {
+  switch (N) {
+    case 8: f.template operator()<RP8>(); return true;
+    case 16: f.template operator()<RP16>(); return true;
+    case 32: f.template operator()<RP32>(); return true;
+    case 64: f.template operator()<RP64>(); return true;
+    case 128: f.template operator()<RP128>(); return true;
+    case 256: f.template operator()<RP256>(); return true;
+    case 512: f.template operator()<RP512>(); return true;
+    case 1024: f.template operator()<RP1024>(); return true;
+    case 2048: f.template operator()<RP2048>(); return true;
+    case 4096: f.template operator()<RP4096>(); return true;
+    case 8192: f.template operator()<RP8192>(); return true;
+    case 9216: f.template operator()<RP9216>(); return true;
+    case 16384: f.template operator()<RP16384>(); return true;
+    default: return false;
+  }
+}
+
+template <class F>
+inline bool dispatch_complex(int N, F&& f) {
+  switch (N) {
+    case 8: f.template operator()<CP8>(); return true;
+    case 16: f.template operator()<CP16>(); return true;
+    case 32: f.template operator()<CP32>(); return true;
+    case 64: f.template operator()<CP64>(); return true;
+    case 128: f.template operator()<CP128>(); return true;
+    case 256: f.template operator()<CP256>(); return true;
+    case 512: f.template operator()<CP512>(); return true;
+    case 1024: f.template operator()<CP1024>(); return true;
+    case 2048: f.template operator()<CP2048>(); return true;
+    case 4096: f.template operator()<CP4096>(); return true;
+    case 8192: f.template operator()<CP8192>(); return true;
+    default: return false;
+  }
+}
+
+// d of layer k at the four quartet indices of slot entry e = slot*T + t.
+template <class PL>
+__host__ __device__ __forceinline__ float4 real_dq_entry(const float* Dk, const char* tab, int e) {
+  const int4 idx = reinterpret_cast<const int4*>(tab + PL::OFF_QIDX)[e];
+  const int m = reinterpret_cast<const int*>(tab + PL::OFF_QMASK)[e] & 0xF;
+  return make_float4((m & 1) ? Dk[idx.x] : 0.f, (m & 2) ? Dk[idx.y] : 0.f, (m & 4) ? Dk[idx.z] : 0.f,
+                     (m & 8) ? Dk[idx.w] : 0.f);
+}
+
+// Fixed-order sum over tiles of partial element e of layer k (blocks of 32
+// tiles summed first, then the block sums in order).
+__host__ __device__ __forceinline__ float tile_sum(const float* partial, long long ntiles, long long stride,
+                                                   long long off) {
+  float total = 0.f;
+  for (long long t0 = 0; t0 < ntiles; t0 += 32) {
+    const long long t1 = (t0 + 32 < ntiles) ? t0 + 32 : ntiles;
+    float s = 0.f;
+    for (long long t = t0; t < t1; ++t) s += partial[t * stride + off];
+    total += s;
+  }
+  return total;
+}
+
+// Real path: element e in [0, N + QF) of layer k of the reduced gradient.
+template <class PL>
+__host__ __device__ __forceinline__ void real_reduce_entry(const float* partial, long long ntiles, int K,
+                                                           int k, int e, float* gA, float* gD,
+                                                           const char* tab) {
+  constexpr long long PS = PL::N + PL::QF;
+  const float s = tile_sum(partial, ntiles, (long long)K * PS, (long long)k * PS + e);
+  if (e < PL::N) {
+    gA[(long long)k * PL::N + e] = s;
+  } else {
+    const int eq = e - PL::N, st = eq >> 2, c = eq & 3;
+    const int sm = (reinterpret_cast<const int*>(tab + PL::OFF_QMASK)[st] >> 4) & 0xF;
+    if (sm & (1 << c)) {
+      const int4 idx = reinterpret_cast<const int4*>(tab + PL::OFF_QIDX)[st];
+      const int n = c == 0 ? idx.x : c == 1 ? idx.y : c == 2 ? idx.z : idx.w;
+      gD[(long long)k * PL::N + n] = s;
+    }
+  }
+}
+
+}  // namespace acdc

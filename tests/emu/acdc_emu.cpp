@@ -1,0 +1,187 @@
+// CPU emulation of the HIP kernels' row bodies (test infrastructure).
+//
+// The same __host__ __device__ templates that the GPU kernels instantiate are
+// run here with one OS thread per GPU thread and a std::barrier standing in
+// for every LDS synchronisation, on host memory.  This checks the index
+// algebra, the plan tables and the reduction order on the CPU; the GPU tests
+// then check the real kernels.  Built by tests/emu/build_emu.py.
+#include <barrier>
+#include <cstdio>
+#include <thread>
+#include <vector>
+
+#include "../../paper_1511_05946_amd/csrc/acdc_registry.hpp"
+
+using namespace acdc;
+
+namespace {
+
+struct HostCtx {
+  std::barrier<>* bar;
+  void sync_row() { bar->arrive_and_wait(); }
+  void sync_all() { bar->arrive_and_wait(); }
+};
+
+template <class F>
+void run_wg(int threads, F&& body) {
+  std::barrier<> bar(threads);
+  std::vector<std::thread> th;
+  th.reserve(threads);
+  for (int tid = 0; tid < threads; ++tid)
+    th.emplace_back([&, tid] {
+      HostCtx ctx{&bar};
+      body(ctx, tid);
+    });
+  for (auto& x : th) x.join();
+}
+
+template <class PL>
+void real_fwd(const float* x, float* y, const float* A, const float* D, const int* perm, long long batch,
+              int K, unsigned flags, float* saved, const std::vector<unsigned char>& tab) {
+  using L = Launch<PL>;
+  std::vector<float4> dq((size_t)K * PL::NSL * PL::T);
+  for (int k = 0; k < K; ++k)
+    for (int e = 0; e < PL::NSL * PL::T; ++e)
+      dq[(size_t)k * PL::NSL * PL::T + e] =
+          real_dq_entry<PL>(D + (size_t)k * PL::N, (const char*)tab.data(), e);
+  RealArgs a{x, y, A, dq.data(), perm, saved, nullptr, nullptr, nullptr, (const char*)tab.data(), batch, K,
+             flags};
+  const long long nwg = (batch + L::FWD_ROWS - 1) / L::FWD_ROWS;
+  std::vector<float> lds((size_t)L::FWD_ROWS * L::FWD_SLAB);
+  for (long long wg = 0; wg < nwg; ++wg)
+    run_wg(L::FWD_THREADS, [&](HostCtx& ctx, int tid) {
+      const int r = tid / PL::T, t = tid % PL::T;
+      real_forward_row<PL>(ctx, a, t, wg * L::FWD_ROWS + r, lds.data() + (size_t)r * L::FWD_SLAB);
+    });
+}
+
+template <class PL>
+void real_bwd(const float* x, const float* gy, const float* A, const float* D, const int* perm,
+              const float* saved_in, float* gx, float* gA, float* gD, long long batch, int K, unsigned flags,
+              const std::vector<unsigned char>& tab) {
+  using L = Launch<PL>;
+  std::vector<float> saved_buf;
+  const float* saved = saved_in;
+  if (saved == nullptr && K > 1) {
+    saved_buf.resize((size_t)(K - 1) * batch * PL::N);
+    real_fwd<PL>(x, nullptr, A, D, perm, batch, K, flags, saved_buf.data(), tab);
+    saved = saved_buf.data();
+  }
+  std::vector<float4> dq((size_t)K * PL::NSL * PL::T);
+  for (int k = 0; k < K; ++k)
+    for (int e = 0; e < PL::NSL * PL::T; ++e)
+      dq[(size_t)k * PL::NSL * PL::T + e] =
+          real_dq_entry<PL>(D + (size_t)k * PL::N, (const char*)tab.data(), e);
+  const long long ntiles = (batch + L::BWD_ROWS - 1) / L::BWD_ROWS;
+  const long long PS = PL::N + PL::QF;
+  std::vector<float> partial((size_t)ntiles * K * PS);
+  RealArgs a{x, nullptr, A, dq.data(), perm, const_cast<float*>(saved), gy, gx, partial.data(),
+             (const char*)tab.data(), batch, K, flags};
+  std::vector<float> lds((size_t)L::BWD_ROWS * L::BWD_SLAB);
+  for (long long wg = 0; wg < ntiles; ++wg)
+    run_wg(L::BWD_THREADS, [&](HostCtx& ctx, int tid) {
+      const int r = tid / PL::T, t = tid % PL::T;
+      real_backward_row<PL, L::BWD_ROWS>(ctx, a, t, wg * L::BWD_ROWS + r, tid, wg, lds.data(),
+                                         lds.data() + (size_t)r * L::BWD_SLAB);
+    });
+  for (int k = 0; k < K; ++k)
+    for (int e = 0; e < PS; ++e)
+      real_reduce_entry<PL>(partial.data(), ntiles, K, k, e, gA, gD, (const char*)tab.data());
+}
+
+template <class PL>
+void cplx_fwd(const float* x, float* y, const float* A, const float* D, const int* perm, long long batch,
+              int K, unsigned flags, float* saved, const std::vector<unsigned char>& tab) {
+  using L = Launch<PL>;
+  CplxArgs a{x, y, A, D, perm, saved, nullptr, nullptr, nullptr, (const char*)tab.data(), batch, K, flags};
+  const long long nwg = (batch + L::FWD_ROWS - 1) / L::FWD_ROWS;
+  std::vector<float> lds((size_t)L::FWD_ROWS * L::FWD_SLAB);
+  for (long long wg = 0; wg < nwg; ++wg)
+    run_wg(L::FWD_THREADS, [&](HostCtx& ctx, int tid) {
+      const int r = tid / PL::T, t = tid % PL::T;
+      cplx_forward_row<PL>(ctx, a, t, wg * L::FWD_ROWS + r, lds.data() + (size_t)r * L::FWD_SLAB);
+    });
+}
+
+template <class PL>
+void cplx_bwd(const float* x, const float* gy, const float* A, const float* D, const int* perm,
+              const float* saved_in, float* gx, float* gA, float* gD, long long batch, int K, unsigned flags,
+              const std::vector<unsigned char>& tab) {
+  using L = Launch<PL>;
+  std::vector<float> saved_buf;
+  const float* saved = saved_in;
+  if (saved == nullptr && K > 1) {
+    saved_buf.resize((size_t)(K - 1) * batch * 2 * PL::N);
+    cplx_fwd<PL>(x, nullptr, A, D, perm, batch, K, flags, saved_buf.data(), tab);
+    saved = saved_buf.data();
+  }
+  const long long ntiles = (batch + L::BWD_ROWS - 1) / L::BWD_ROWS;
+  const long long PS = 4LL * PL::N;
+  std::vector<float> partial((size_t)ntiles * K * PS);
+  CplxArgs a{x, nullptr, A, D, perm, const_cast<float*>(saved), gy, gx, partial.data(),
+             (const char*)tab.data(), batch, K, flags};
+  std::vector<float> lds((size_t)L::BWD_ROWS * L::BWD_SLAB);
+  for (long long wg = 0; wg < ntiles; ++wg)
+    run_wg(L::BWD_THREADS, [&](HostCtx& ctx, int tid) {
+      const int r = tid / PL::T, t = tid % PL::T;
+      cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, t, wg * L::BWD_ROWS + r, tid, wg, lds.data(),
+                                         lds.data() + (size_t)r * L::BWD_SLAB);
+    });
+  for (int k = 0; k < K; ++k)
+    for (long long e = 0; e < PS; ++e) {
+      const float s = tile_sum(partial.data(), ntiles, (long long)K * PS, (long long)k * PS + e);
+      if (e < 2 * PL::N) gA[(size_t)k * 2 * PL::N + e] = s;
+      else gD[(size_t)k * 2 * PL::N + (e - 2 * PL::N)] = s;
+    }
+}
+
+}  // namespace
+
+extern "C" int acdc_emu_forward(const float* x, float* y, const float* A, const float* D, const int* perm,
+                                long long batch, int N, int K, unsigned flags, float* saved) {
+  int rc = -2;
+  if (flags & kFlagComplex) {
+    dispatch_complex(N, [&]<class PL>() {
+      std::vector<unsigned char> tab;
+      build_complex_tables<PL>(tab);
+      cplx_fwd<PL>(x, y, A, D, perm, batch, K, flags, saved, tab);
+      rc = 0;
+    });
+  } else {
+    dispatch_real(N, [&]<class PL>() {
+      std::vector<unsigned char> tab;
+      if (!build_real_tables<PL>(tab)) {
+        rc = -5;
+        return;
+      }
+      real_fwd<PL>(x, y, A, D, perm, batch, K, flags, saved, tab);
+      rc = 0;
+    });
+  }
+  return rc;
+}
+
+extern "C" int acdc_emu_backward(const float* x, const float* gy, const float* A, const float* D,
+                                 const int* perm, const float* saved, float* gx, float* gA, float* gD,
+                                 long long batch, int N, int K, unsigned flags) {
+  int rc = -2;
+  if (flags & kFlagComplex) {
+    dispatch_complex(N, [&]<class PL>() {
+      std::vector<unsigned char> tab;
+      build_complex_tables<PL>(tab);
+      cplx_bwd<PL>(x, gy, A, D, perm, saved, gx, gA, gD, batch, K, flags, tab);
+      rc = 0;
+    });
+  } else {
+    dispatch_real(N, [&]<class PL>() {
+      std::vector<unsigned char> tab;
+      if (!build_real_tables<PL>(tab)) {
+        rc = -5;
+        return;
+      }
+      real_bwd<PL>(x, gy, A, D, perm, saved, gx, gA, gD, batch, K, flags, tab);
+      rc = 0;
+    });
+  }
+  return rc;
+}

@@ -1,0 +1,82 @@
+"""CPU emulation of the kernel row bodies (no GPU).
+
+The HIP kernels' __host__ __device__ bodies, the plan tables and the
+fixed-order reductions run on the CPU (one thread per GPU lane, barriers for
+LDS syncs) and are compared with the fp64 oracle at the same tolerance as
+the GPU parity tests.  This pins the index algebra of every plan before any
+GPU run; the GPU tests then pin the compiled kernels."""
+
+import ctypes
+import os
+import shutil
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import acdc_oracle as O
+from paper_1511_05946_amd.workloads import make_inputs
+from tests.helpers import TOL_COMPLEX, TOL_REAL, rel_err, relu_safe_rows
+
+sys.path.insert(0, os.path.join(os.path.dirname(__file__), "emu"))
+
+
+@pytest.fixture(scope="module")
+def emu():
+    if shutil.which("hipcc") is None and not os.path.exists("/opt/rocm/bin/hipcc"):
+        pytest.skip("hipcc not available")
+    import build_emu
+    L = ctypes.CDLL(build_emu.build())
+    P = ctypes.c_void_p
+    L.acdc_emu_forward.argtypes = [P, P, P, P, P, ctypes.c_longlong, ctypes.c_int, ctypes.c_int,
+                                   ctypes.c_uint, P]
+    L.acdc_emu_backward.argtypes = [P, P, P, P, P, P, P, P, P, ctypes.c_longlong, ctypes.c_int,
+                                    ctypes.c_int, ctypes.c_uint]
+    return L
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data
+
+
+def check(L, N, K, B, flags, seed=0, with_saved=False):
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, seed)
+    tol = TOL_COMPLEX if flags & O.FLAG_COMPLEX else TOL_REAL
+    y = np.zeros_like(x)
+    saved = np.zeros((max(K - 1, 0), B, N), x.dtype) if with_saved else None
+    assert L.acdc_emu_forward(_p(x), _p(y), _p(A), _p(D), _p(perm), B, N, K, flags, _p(saved)) == 0
+    yr, cache = O.forward(x, A, D, perm, flags, keep=True)
+    assert rel_err(y, yr) < tol
+    if with_saved and K > 1:
+        for k in range(1, K):
+            assert rel_err(saved[k - 1], cache["u"][k]) < tol
+    keep = relu_safe_rows(cache["v"], K) if flags & O.FLAG_RELU else np.ones(B, bool)
+    x, gy = np.ascontiguousarray(x[keep]), np.ascontiguousarray(gy[keep])
+    Bk = x.shape[0]
+    gx, gA, gD = np.zeros_like(x), np.zeros_like(A), np.zeros_like(D)
+    sv = np.ascontiguousarray(saved[:, keep]) if (with_saved and K > 1) else None
+    assert L.acdc_emu_backward(_p(x), _p(gy), _p(A), _p(D), _p(perm), _p(sv), _p(gx), _p(gA), _p(gD),
+                               Bk, N, K, flags) == 0
+    rx, rA, rD = O.backward(x, gy, A, D, perm, flags)
+    assert rel_err(gx, rx) < tol
+    assert rel_err(gA, rA) < tol
+    assert rel_err(gD, rD) < tol
+
+
+@pytest.mark.parametrize("N", [8, 16, 32, 64, 128, 256, 512, 1024])
+@pytest.mark.parametrize("flags", [0, O.FLAG_PERM | O.FLAG_RELU])
+def test_real_small(emu, N, flags):
+    check(emu, N, 3, 9, flags, seed=N)
+
+
+@pytest.mark.parametrize("N", [8, 16, 64, 256, 1024])
+def test_complex_small(emu, N):
+    check(emu, N, 2, 5, O.FLAG_COMPLEX | O.FLAG_PERM, seed=N)
+
+
+def test_real_4096_with_saved(emu):
+    check(emu, 4096, 3, 3, O.FLAG_PERM | O.FLAG_RELU, seed=1, with_saved=True)
+
+
+def test_real_9216_three_waves_per_row(emu):
+    check(emu, 9216, 2, 2, O.FLAG_PERM | O.FLAG_RELU, seed=2)

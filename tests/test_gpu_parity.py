@@ -1,0 +1,223 @@
+"""GPU parity: the HIP kernels (through the C ABI) against the fp64 oracle.
+
+Every comparison uses the max relative error per output with the group rms
+as floor (rows of y / grad_x, layers of grad_A / grad_D): <= 1e-4 for fp32,
+<= 2e-4 for complex64.  Backward parity for ReLU cascades runs on the rows
+whose ReLU decisions are farther than 1e-5 * rms from zero in the oracle
+forward (a flipped decision legitimately changes that row's gradient).
+"""
+
+import numpy as np
+import pytest
+
+from oracle import acdc_oracle as O
+from paper_1511_05946_amd.workloads import WORKLOADS, make_inputs
+from tests.helpers import TOL_COMPLEX, TOL_REAL, rel_err, relu_safe_rows
+
+pytestmark = pytest.mark.gpu
+
+P, R, CX = O.FLAG_PERM, O.FLAG_RELU, O.FLAG_COMPLEX
+
+
+@pytest.fixture(scope="module")
+def acdc():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1511_05946_amd.acdc as mod
+    return mod
+
+
+def dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+
+def host(t):
+    import torch
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def run_case(acdc, N, K, B, flags, seed=0, save=True, check_bwd=True, rows=None):
+    print(f"[case] N={N} K={K} B={B} flags={flags} seed={seed} save={save}", flush=True)
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, seed)
+    tol = TOL_COMPLEX if flags & CX else TOL_REAL
+    xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
+    y, saved = acdc.forward(xt, At, Dt, pt, flags & ~CX, save=save)
+    yg = host(y)
+    sel = np.arange(B) if rows is None else rows
+    yr, cache = O.forward(x[sel], A, D, perm, flags, keep=True)
+    e = rel_err(yg[sel], yr)
+    assert e < tol, f"forward rel err {e:.3e}"
+    if save and K > 1:
+        sg = host(saved)
+        for k in range(1, K):
+            assert rel_err(sg[k - 1][sel], cache["u"][k]) < tol
+    if not check_bwd:
+        return
+    keep = relu_safe_rows(cache["v"], K) if flags & R else np.ones(len(sel), bool)
+    idx = sel[keep]
+    print(f"[case]   backward on {len(idx)}/{len(sel)} rows", flush=True)
+    xs, gys = x[idx], gy[idx]
+    xst = dev(xs)
+    sv = None
+    if save and K > 1:
+        _, sv = acdc.forward(xst, At, Dt, pt, flags & ~CX, save=True)
+    gx, gA, gD = acdc.backward(xst, dev(gys), At, Dt, pt, flags & ~CX, saved=sv)
+    rx, rA, rD = O.backward(xs, gys, A, D, perm, flags)
+    for name, g, r in (("grad_x", gx, rx), ("grad_A", gA, rA), ("grad_D", gD, rD)):
+        e = rel_err(host(g), r)
+        assert e < tol, f"{name} rel err {e:.3e}"
+
+
+@pytest.mark.parametrize("N", [8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096])
+@pytest.mark.parametrize("flags", [0, P, P | R])
+def test_real_widths(acdc, N, flags):
+    run_case(acdc, N, 3, 67, flags, seed=N + flags)          # 67: a ragged last workgroup
+
+
+@pytest.mark.parametrize("N", [8192, 9216, 16384])
+def test_real_wide_rows(acdc, N):
+    run_case(acdc, N, 2, 5, P | R, seed=N)
+
+
+@pytest.mark.parametrize("N", [8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096, 8192])
+def test_complex_widths(acdc, N):
+    run_case(acdc, N, 3, 11, CX | P, seed=N)
+
+
+@pytest.mark.parametrize("save", [True, False])
+def test_single_layer_and_single_row(acdc, save):
+    run_case(acdc, 256, 1, 1, 0, save=save)
+    run_case(acdc, 4096, 1, 1, R, save=save)
+    run_case(acdc, 1024, 4, 1, P | R, save=save)
+
+
+@pytest.mark.parametrize("name", list(WORKLOADS))
+def test_workloads_small_batch(acdc, name):
+    w = WORKLOADS[name]
+    B = {"acdc_n256_k1": 64, "acdc_n1024_k12_perm": 96, "acdc_n4096_k12_perm_relu": 48,
+         "acdc_n9216_k16_perm_relu": 12, "afdf_n4096_k8_perm": 24}[name]
+    run_case(acdc, w.N, w.K, B, w.flags, seed=0)
+
+
+@pytest.mark.parametrize("name", list(WORKLOADS))
+def test_workloads_full_size_sampled(acdc, name):
+    """Full batch in the benchmark's launch configuration; the oracle checks
+    a sample of rows (rows are independent in the forward pass and in grad_x),
+    and the batch-summed parameter gradients are checked by batch-split
+    additivity of the GPU results."""
+    import torch
+    w = WORKLOADS[name]
+    rng = np.random.default_rng(5)
+    nsamp = 6 if w.N >= 9216 else 12
+    rows = np.sort(rng.choice(w.batch, nsamp, replace=False))
+    run_case(acdc, w.N, w.K, w.batch, w.flags, seed=0, rows=rows, check_bwd=False)
+    # grad_x rows and additivity of grad_A/grad_D on the full batch
+    x, A, D, perm, gy = make_inputs(w.N, w.K, w.batch, w.flags, 0)
+    fl = w.flags & ~CX
+    xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
+    _, sv = acdc.forward(xt, At, Dt, pt, fl, save=True)
+    gx, gA, gD = acdc.backward(xt, gyt, At, Dt, pt, fl, saved=sv)
+    h = w.batch // 2
+    gA1 = acdc.backward(xt[:h].contiguous(), gyt[:h].contiguous(), At, Dt, pt, fl)[1]
+    gD1 = acdc.backward(xt[:h].contiguous(), gyt[:h].contiguous(), At, Dt, pt, fl)[2]
+    _, gA2, gD2 = acdc.backward(xt[h:].contiguous(), gyt[h:].contiguous(), At, Dt, pt, fl)
+    tol = TOL_COMPLEX if w.complex else TOL_REAL
+    assert rel_err(host(gA), host(gA1 + gA2)) < tol
+    assert rel_err(host(gD), host(gD1 + gD2)) < tol
+    _, cache = O.forward(x[rows], A, D, perm, w.flags, keep=True)
+    keep = relu_safe_rows(cache["v"], w.K) if w.flags & R else np.ones(len(rows), bool)
+    rx, _, _ = O.backward(x[rows][keep], gy[rows][keep], A, D, perm, w.flags)
+    assert rel_err(host(gx)[rows][keep], rx) < tol
+    torch.cuda.synchronize()
+
+
+def test_determinism_and_saved_equals_recompute(acdc):
+    N, K, B, flags = 1024, 6, 300, P | R
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, 3)
+    xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
+    y1, s1 = acdc.forward(xt, At, Dt, pt, flags, save=True)
+    y2, s2 = acdc.forward(xt, At, Dt, pt, flags, save=True)
+    assert np.array_equal(host(y1), host(y2))
+    assert np.array_equal(host(s1), host(s2))
+    a = acdc.backward(xt, gyt, At, Dt, pt, flags, saved=s1)
+    b = acdc.backward(xt, gyt, At, Dt, pt, flags, saved=s2)
+    c = acdc.backward(xt, gyt, At, Dt, pt, flags, saved=None)
+    for u, v, w_ in zip(a, b, c):
+        assert np.array_equal(host(u), host(v))
+        assert np.array_equal(host(u), host(w_))
+
+
+def test_identity_perm_equals_flag_off(acdc):
+    N, K, B = 512, 3, 40
+    x, A, D, _, gy = make_inputs(N, K, B, 0, 4)
+    ident = np.tile(np.arange(N, dtype=np.int32), (K, 1))
+    xt, At, Dt, it, gyt = dev(x), dev(A), dev(D), dev(ident), dev(gy)
+    y0, _ = acdc.forward(xt, At, Dt, None, R)
+    y1, _ = acdc.forward(xt, At, Dt, it, P | R)
+    assert np.array_equal(host(y0), host(y1))
+    g0 = acdc.backward(xt, gyt, At, Dt, None, R)
+    g1 = acdc.backward(xt, gyt, At, Dt, it, P | R)
+    for u, v in zip(g0, g1):
+        assert np.array_equal(host(u), host(v))
+
+
+def test_closed_forms(acdc):
+    import torch
+    N, B = 4096, 8
+    rng = np.random.default_rng(6)
+    x = rng.standard_normal((B, N)).astype(np.float32)
+    ones = np.ones((2, N), np.float32)
+    y, _ = acdc.forward(dev(x), dev(ones), dev(ones), None, 0)
+    assert rel_err(host(y), x) < TOL_REAL                      # A = D = 1: identity
+    a = rng.normal(1, .1, (1, N)).astype(np.float32)
+    d = np.zeros((1, N), np.float32)
+    d[0, 0] = 1.0
+    y, _ = acdc.forward(dev(x), dev(a), dev(d), None, 0)      # D = e0: row mean of x*a
+    ref = np.repeat((x.astype(np.float64) * a).mean(1, keepdims=True), N, 1)
+    assert rel_err(host(y), ref) < TOL_REAL
+    torch.cuda.synchronize()
+
+
+def test_outputs_fully_written(acdc):
+    import torch
+    N, K, B, flags = 2048, 3, 37, P | R
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, 7)
+    xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
+    y = torch.full_like(xt, float("nan"))
+    saved = torch.full((K - 1, B, N), float("nan"), device="cuda")
+    acdc.forward(xt, At, Dt, pt, flags, out=y, saved=saved)
+    assert np.isfinite(host(y)).all() and np.isfinite(host(saved)).all()
+    gx, gA, gD = acdc.backward(xt, gyt, At, Dt, pt, flags, saved=saved)
+    assert np.isfinite(host(gx)).all() and np.isfinite(host(gA)).all() and np.isfinite(host(gD)).all()
+
+
+def test_empty_batch(acdc):
+    import torch
+    N, K = 256, 2
+    A = torch.ones((K, N), device="cuda")
+    x = torch.empty((0, N), device="cuda")
+    y, _ = acdc.forward(x, A, A.clone(), None, 0)
+    assert y.shape == (0, N)
+    gx, gA, gD = acdc.backward(x, x.clone(), A, A.clone(), None, 0)
+    assert gx.shape == (0, N)
+    assert not host(gA).any() and not host(gD).any()
+
+
+def test_autograd_wrapper(acdc):
+    import torch
+    N, K, B, flags = 256, 4, 16, P | R
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, 8)
+    xt = dev(x).requires_grad_(True)
+    At = dev(A).requires_grad_(True)
+    Dt = dev(D).requires_grad_(True)
+    y = acdc.acdc_cascade(xt, At, Dt, dev(perm), flags)
+    y.backward(dev(gy))
+    _, cache = O.forward(x, A, D, perm, flags, keep=True)
+    assert relu_safe_rows(cache["v"], K).all()
+    rx, rA, rD = O.backward(x, gy, A, D, perm, flags)
+    assert rel_err(host(xt.grad), rx) < TOL_REAL
+    assert rel_err(host(At.grad), rA) < TOL_REAL
+    assert rel_err(host(Dt.grad), rD) < TOL_REAL
