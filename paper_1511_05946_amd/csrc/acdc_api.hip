@@ -55,8 +55,11 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::FWD_WPE))) void k_real_fwd(RealAr
   using L = Launch<PL>;
   __shared__ float lds[L::FWD_ROWS * L::FWD_SLAB];
   DevCtx<PL::T> ctx;
-  const int tid = threadIdx.x, r = tid / PL::T, t = tid % PL::T;
-  real_forward_row<PL>(ctx, a, t, (long long)blockIdx.x * L::FWD_ROWS + r, lds + r * L::FWD_SLAB);
+  const int tid = threadIdx.x;
+  const unsigned t = unsigned(tid) % PL::T;
+  int r = tid / PL::T;
+  if constexpr (PL::T >= 64) r = __builtin_amdgcn_readfirstlane(r);  // one row per whole wave
+  real_forward_row<PL>(ctx, a, t, (long long)blockIdx.x * L::FWD_ROWS, unsigned(r), lds + r * L::FWD_SLAB);
 }
 
 template <class PL>
@@ -65,8 +68,11 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealAr
   using L = Launch<PL>;
   __shared__ float lds[L::BWD_ROWS * L::BWD_SLAB];
   DevCtx<PL::T> ctx;
-  const int tid = threadIdx.x, r = tid / PL::T, t = tid % PL::T;
-  real_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS + r, tid,
+  const int tid = threadIdx.x;
+  const unsigned t = unsigned(tid) % PL::T;
+  int r = tid / PL::T;
+  if constexpr (PL::T >= 64) r = __builtin_amdgcn_readfirstlane(r);  // one row per whole wave
+  real_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS, unsigned(r), tid,
                                      (long long)blockIdx.x, lds, lds + r * L::BWD_SLAB);
 }
 
@@ -74,10 +80,10 @@ template <class PL>
 __global__ __launch_bounds__(256) void k_real_reduce(const float* __restrict__ partial, long long ntiles, int K,
                                                      float* __restrict__ gA, float* __restrict__ gD,
                                                      const char* __restrict__ tab) {
-  constexpr long long PS = PL::N + PL::QF;
+  constexpr long long PS4 = (PL::N + PL::QF) / 4;
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (long long)K * PS) return;
-  real_reduce_entry<PL>(partial, ntiles, K, int(i / PS), int(i % PS), gA, gD, tab);
+  if (i >= (long long)K * PS4) return;
+  real_reduce_entry4<PL>(partial, ntiles, K, int(i / PS4), int(i % PS4), gA, gD, tab);
 }
 
 template <class PL>
@@ -86,8 +92,11 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::FWD_WPE))) void k_cplx_fwd(CplxAr
   using L = Launch<PL>;
   __shared__ float lds[L::FWD_ROWS * L::FWD_SLAB];
   DevCtx<PL::T> ctx;
-  const int tid = threadIdx.x, r = tid / PL::T, t = tid % PL::T;
-  cplx_forward_row<PL>(ctx, a, t, (long long)blockIdx.x * L::FWD_ROWS + r, lds + r * L::FWD_SLAB);
+  const int tid = threadIdx.x;
+  const unsigned t = unsigned(tid) % PL::T;
+  int r = tid / PL::T;
+  if constexpr (PL::T >= 64) r = __builtin_amdgcn_readfirstlane(r);  // one row per whole wave
+  cplx_forward_row<PL>(ctx, a, t, (long long)blockIdx.x * L::FWD_ROWS, unsigned(r), lds + r * L::FWD_SLAB);
 }
 
 template <class PL>
@@ -96,21 +105,20 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_cplx_bwd(CplxAr
   using L = Launch<PL>;
   __shared__ float lds[L::BWD_ROWS * L::BWD_SLAB];
   DevCtx<PL::T> ctx;
-  const int tid = threadIdx.x, r = tid / PL::T, t = tid % PL::T;
-  cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS + r, tid,
+  const int tid = threadIdx.x;
+  const unsigned t = unsigned(tid) % PL::T;
+  int r = tid / PL::T;
+  if constexpr (PL::T >= 64) r = __builtin_amdgcn_readfirstlane(r);  // one row per whole wave
+  cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS, unsigned(r), tid,
                                      (long long)blockIdx.x, lds, lds + r * L::BWD_SLAB);
 }
 
 template <class PL>
 __global__ __launch_bounds__(256) void k_cplx_reduce(const float* __restrict__ partial, long long ntiles, int K,
                                                      float* __restrict__ gA, float* __restrict__ gD) {
-  constexpr long long PS = 4LL * PL::N;
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (long long)K * PS) return;
-  const int k = int(i / PS), e = int(i % PS);
-  const float s = tile_sum(partial, ntiles, (long long)K * PS, (long long)k * PS + e);
-  if (e < 2 * PL::N) gA[(long long)k * 2 * PL::N + e] = s;
-  else gD[(long long)k * 2 * PL::N + (e - 2 * PL::N)] = s;
+  if (i >= (long long)K * PL::N) return;
+  cplx_reduce_entry4<PL>(partial, ntiles, K, int(i / PL::N), int(i % PL::N), gA, gD);
 }
 
 // ------------------------------------------------------------------ host side
@@ -432,7 +440,7 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
           return;
         }
       }
-      const long long n = (long long)K * 4 * PL::N;
+      const long long n = (long long)K * PL::N;
       hipError_t e;
       {
         ProfScope prof(2, s);
@@ -467,7 +475,7 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
           return;
         }
       }
-      const long long n = (long long)K * (PL::N + PL::QF);
+      const long long n = (long long)K * (PL::N + PL::QF) / 4;
       hipError_t e;
       {
         ProfScope prof(2, s);

@@ -13,6 +13,7 @@
 #pragma once
 
 #include "acdc_dft.hpp"
+#include "acdc_mem.hpp"
 #include "acdc_plans.hpp"
 #include "acdc_stockham.hpp"
 
@@ -24,71 +25,80 @@ struct CplxOps {
   static constexpr int R0 = PL::rad(0), RL = PL::rad(PL::NPASS - 1);
   static constexpr int B0 = P / R0, BL = P / RL;
 
-  // f(element, v[s]) over the spatial layout
+  // f(lane_part, const_part, v[s]) with element = t + const_part over the
+  // spatial (resp. frequency) layout.
   template <class F>
-  __host__ __device__ __forceinline__ static void for_spatial(float2 (&v)[P], int t, F&& f) {
+  __host__ __device__ __forceinline__ static void for_spatial(float2 (&v)[P], unsigned t, F&& f) {
 #pragma unroll
     for (int beta = 0; beta < B0; ++beta)
 #pragma unroll
-      for (int i = 0; i < R0; ++i) f(t + T * (beta + i * B0), v[beta * R0 + i]);
+      for (int i = 0; i < R0; ++i) f(t, unsigned(T * (beta + i * B0)), v[beta * R0 + i]);
   }
   template <class F>
-  __host__ __device__ __forceinline__ static void for_spatial2(float2 (&v)[P], float2 (&w)[P], int t, F&& f) {
+  __host__ __device__ __forceinline__ static void for_spatial2(float2 (&v)[P], float2 (&w)[P], unsigned t, F&& f) {
 #pragma unroll
     for (int beta = 0; beta < B0; ++beta)
 #pragma unroll
-      for (int i = 0; i < R0; ++i) f(t + T * (beta + i * B0), v[beta * R0 + i], w[beta * R0 + i]);
+      for (int i = 0; i < R0; ++i) f(t, unsigned(T * (beta + i * B0)), v[beta * R0 + i], w[beta * R0 + i]);
   }
   template <class F>
-  __host__ __device__ __forceinline__ static void for_freq(float2 (&v)[P], int t, F&& f) {
+  __host__ __device__ __forceinline__ static void for_freq(float2 (&v)[P], unsigned t, F&& f) {
 #pragma unroll
     for (int beta = 0; beta < BL; ++beta)
 #pragma unroll
-      for (int m = 0; m < RL; ++m) f(t + T * (beta + m * BL), v[beta * RL + m]);
+      for (int m = 0; m < RL; ++m) f(t, unsigned(T * (beta + m * BL)), v[beta * RL + m]);
   }
 
-  __host__ __device__ __forceinline__ static void load(const float* row, float2 (&v)[P], int t, bool valid) {
-    const float2* r = reinterpret_cast<const float2*>(row);
-    for_spatial(v, t, [&](int e, float2& z) { z = valid ? r[e] : make_float2(0.f, 0.f); });
+  // g views the workgroup's first row; roff = this row's offset (complex elements)
+  // Rows past the batch end read the block's first row and are zeroed.
+  __host__ __device__ __forceinline__ static void load(GView g, unsigned roff, float2 (&v)[P], unsigned t,
+                                                       bool valid) {
+    const unsigned ro = valid ? roff : 0u;
+    const float zf = valid ? 1.0f : 0.0f;
+    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) {
+      const float2 h = g.ld2((l + ro) * 8u, c * 8u);
+      z = make_float2(h.x * zf, h.y * zf);
+    });
   }
-  __host__ __device__ __forceinline__ static void store(float* row, float2 (&v)[P], int t) {
-    float2* r = reinterpret_cast<float2*>(row);
-    for_spatial(v, t, [&](int e, float2& z) { r[e] = z; });
+  __host__ __device__ __forceinline__ static void store(GView g, unsigned roff, float2 (&v)[P], unsigned t) {
+    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { g.st2(z, (l + roff) * 8u, c * 8u); });
   }
   template <bool CONJ>
-  __host__ __device__ __forceinline__ static void scale(float2 (&v)[P], const float* a, int t) {
-    const float2* ar = reinterpret_cast<const float2*>(a);
-    for_spatial(v, t, [&](int e, float2& z) { z = CONJ ? cmulc(z, ar[e]) : cmul(z, ar[e]); });
+  __host__ __device__ __forceinline__ static void scale(float2 (&v)[P], GView a, unsigned t) {
+    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) {
+      const float2 w = a.ld2(l * 8u, c * 8u);
+      z = CONJ ? cmulc(z, w) : cmul(z, w);
+    });
   }
   template <bool CONJ>
-  __host__ __device__ __forceinline__ static void scale_freq(float2 (&v)[P], const float* d, float f, int t) {
-    const float2* dr = reinterpret_cast<const float2*>(d);
-    for_freq(v, t, [&](int e, float2& z) {
-      const float2 w = make_float2(dr[e].x * f, dr[e].y * f);
+  __host__ __device__ __forceinline__ static void scale_freq(float2 (&v)[P], GView d, float f, unsigned t) {
+    for_freq(v, t, [&](unsigned l, unsigned c, float2& z) {
+      const float2 dv = d.ld2(l * 8u, c * 8u);
+      const float2 w = make_float2(dv.x * f, dv.y * f);
       z = CONJ ? cmulc(z, w) : cmul(z, w);
     });
   }
 
   template <class Ctx>
-  __host__ __device__ __forceinline__ static void gather(Ctx& ctx, float2 (&v)[P], int t, float2* slab,
-                                                         const int* perm) {
+  __host__ __device__ __forceinline__ static void gather(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
+                                                         GView perm) {
     ctx.sync_row();
-    for_spatial(v, t, [&](int e, float2& z) { slab[e] = z; });
+    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { slab[l + c] = z; });
     ctx.sync_row();
-    for_spatial(v, t, [&](int e, float2& z) { z = slab[perm[e]]; });
+    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { z = slab[perm.ldi1(l * 4u, c * 4u)]; });
   }
   template <class Ctx>
-  __host__ __device__ __forceinline__ static void scatter(Ctx& ctx, float2 (&v)[P], int t, float2* slab,
-                                                          const int* perm) {
+  __host__ __device__ __forceinline__ static void scatter(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
+                                                          GView perm) {
     ctx.sync_row();
-    for_spatial(v, t, [&](int e, float2& z) { slab[perm[e]] = z; });
+    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { slab[perm.ldi1(l * 4u, c * 4u)] = z; });
     ctx.sync_row();
-    for_spatial(v, t, [&](int e, float2& z) { z = slab[e]; });
+    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { z = slab[l + c]; });
   }
 
   template <bool INV, class Ctx>
-  __host__ __device__ __forceinline__ static void fft(Ctx& ctx, float2 (&v)[P], int t, float2* slab,
-                                                      const float2* tw) {
+  __host__ __device__ __forceinline__ static void fft(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
+                                                      GView tw) {
     stockham_fft<PL, INV, 0, 0>(ctx, v, t, slab, tw);
   }
 };
@@ -110,71 +120,78 @@ struct CplxArgs {
 };
 
 template <class PL, class Ctx>
-__host__ __device__ void cplx_forward_row(Ctx& ctx, const CplxArgs& a, int t, long long row, float* slab) {
+__host__ __device__ void cplx_forward_row(Ctx& ctx, const CplxArgs& a, unsigned t, long long row0, unsigned rr,
+                                          float* slab) {
   using O = CplxOps<PL>;
   constexpr int N = PL::N, P = PL::P;
   constexpr long long RS = 2LL * N;  // floats per row
+  const long long row = row0 + rr;
   const bool valid = row < a.batch;
-  const float2* tw = reinterpret_cast<const float2*>(a.tab);
+  const unsigned roff = rr * unsigned(N);
+  const GView tab = GView::of(a.tab);
   float2* slab2 = reinterpret_cast<float2*>(slab);
   const float invN = 1.0f / float(N);
   float2 v[P];
-  O::load(a.x + row * RS, v, t, valid);
+  O::load(GView::of(a.x + row0 * RS), roff, v, t, valid);
   for (int k = 0; k < a.K; ++k) {
-    if (a.flags & 1u) O::gather(ctx, v, t, slab2, a.perm + (long long)k * N);
-    if (a.saved != nullptr && k > 0 && valid) O::store(a.saved + ((long long)(k - 1) * a.batch + row) * RS, v, t);
-    O::template scale<false>(v, a.A + k * RS, t);
-    O::template fft<false>(ctx, v, t, slab2, tw);
-    O::template scale_freq<false>(v, a.D + k * RS, invN, t);
-    O::template fft<true>(ctx, v, t, slab2, tw);
+    if (a.flags & 1u) O::gather(ctx, v, t, slab2, GView::of(a.perm + (long long)k * N));
+    if (a.saved != nullptr && k > 0 && valid)
+      O::store(GView::of(a.saved + ((long long)(k - 1) * a.batch + row0) * RS), roff, v, t);
+    O::template scale<false>(v, GView::of(a.A + k * RS), t);
+    O::template fft<false>(ctx, v, t, slab2, tab);
+    O::template scale_freq<false>(v, GView::of(a.D + k * RS), invN, t);
+    O::template fft<true>(ctx, v, t, slab2, tab);
   }
-  if (a.y != nullptr && valid) O::store(a.y + row * RS, v, t);
+  if (a.y != nullptr && valid) O::store(GView::of(a.y + row0 * RS), roff, v, t);
 }
 
 template <class PL, int ROWS, class Ctx>
-__host__ __device__ void cplx_backward_row(Ctx& ctx, const CplxArgs& a, int t, long long row, int tid,
-                                           long long tile, float* lds, float* slab) {
+__host__ __device__ void cplx_backward_row(Ctx& ctx, const CplxArgs& a, unsigned t, long long row0, unsigned rr,
+                                           int tid, long long tile, float* lds, float* slab) {
   using O = CplxOps<PL>;
   constexpr int N = PL::N, P = PL::P, T = PL::T;
   constexpr int THREADS = ROWS * T;
   constexpr long long RS = 2LL * N;
   constexpr long long PS = 4LL * N;
+  const long long row = row0 + rr;
   const bool valid = row < a.batch;
-  const float2* tw = reinterpret_cast<const float2*>(a.tab);
+  const unsigned roff = rr * unsigned(N);
+  const GView tab = GView::of(a.tab);
   float2* slab2 = reinterpret_cast<float2*>(slab);
   const float invN = 1.0f / float(N);
   float2 g[P];
-  O::load(a.gy + row * RS, g, t, valid);
+  O::load(GView::of(a.gy + row0 * RS), roff, g, t, valid);
   for (int k = a.K - 1; k >= 0; --k) {
-    const float* urow = (k == 0) ? a.x + row * RS : a.saved + ((long long)(k - 1) * a.batch + row) * RS;
+    const GView ug = GView::of(k == 0 ? a.x + row0 * RS : a.saved + ((long long)(k - 1) * a.batch + row0) * RS);
+    const GView ak = GView::of(a.A + k * RS);
     float* part = a.partial + (tile * a.K + k) * PS;
     float2 h[P];
-    O::load(urow, h, t, valid);
-    O::template scale<false>(h, a.A + k * RS, t);
-    O::template fft<false>(ctx, h, t, slab2, tw);          // h2
-    O::template fft<false>(ctx, g, t, slab2, tw);
+    O::load(ug, roff, h, t, valid);
+    O::template scale<false>(h, ak, t);
+    O::template fft<false>(ctx, h, t, slab2, tab);          // h2
+    O::template fft<false>(ctx, g, t, slab2, tab);
 #pragma unroll
     for (int s = 0; s < P; ++s) g[s] = make_float2(g[s].x * invN, g[s].y * invN);  // gh3
     ctx.sync_row();
 #pragma unroll
     for (int s = 0; s < P; ++s) h[s] = cmulc(g[s], h[s]);   // conj(h2) * gh3 in frequency layout
-    O::for_freq(h, t, [&](int e, float2& z) { slab2[e] = z; });
+    O::for_freq(h, t, [&](unsigned l, unsigned c, float2& z) { slab2[l + c] = z; });
     ctx.sync_all();
-    sum_rows<ROWS, PL::SLAB, THREADS>(lds, part + RS, int(RS), tid);
+    sum_rows<ROWS, PL::SLAB, THREADS>(lds, GView::of(part + RS), int(RS), tid);
     ctx.sync_all();
-    O::template scale_freq<true>(g, a.D + k * RS, 1.0f, t);  // gh3 * conj(d)
-    O::template fft<true>(ctx, g, t, slab2, tw);             // gh1 (unnormalised inverse)
+    O::template scale_freq<true>(g, GView::of(a.D + k * RS), 1.0f, t);  // gh3 * conj(d)
+    O::template fft<true>(ctx, g, t, slab2, tab);                        // gh1 (unnormalised inverse)
     float2 u[P];
-    O::load(urow, u, t, valid);
+    O::load(ug, roff, u, t, valid);
     ctx.sync_row();
-    O::for_spatial2(u, g, t, [&](int e, float2& uu, float2& gg) { slab2[e] = cmulc(gg, uu); });
+    O::for_spatial2(u, g, t, [&](unsigned l, unsigned c, float2& uu, float2& gg) { slab2[l + c] = cmulc(gg, uu); });
     ctx.sync_all();
-    sum_rows<ROWS, PL::SLAB, THREADS>(lds, part, int(RS), tid);
+    sum_rows<ROWS, PL::SLAB, THREADS>(lds, GView::of(part), int(RS), tid);
     ctx.sync_all();
-    O::template scale<true>(g, a.A + k * RS, t);            // gu = gh1 * conj(a)
-    if (a.flags & 1u) O::scatter(ctx, g, t, slab2, a.perm + (long long)k * N);
+    O::template scale<true>(g, ak, t);            // gu = gh1 * conj(a)
+    if (a.flags & 1u) O::scatter(ctx, g, t, slab2, GView::of(a.perm + (long long)k * N));
   }
-  if (valid) O::store(a.gx + row * RS, g, t);
+  if (valid) O::store(GView::of(a.gx + row0 * RS), roff, g, t);
 }
 
 }  // namespace acdc

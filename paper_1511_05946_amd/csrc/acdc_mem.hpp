@@ -1,0 +1,95 @@
+// Global-memory views for the kernel bodies.
+//
+// On gfx950 a view is a buffer resource (4 SGPRs) and every access is
+//   buffer_load/store  vdata, voffset (VGPR), rsrc, soffset (SGPR/const) offen
+// so a thread keeps one 32-bit offset per access pattern and all per-chunk,
+// per-slot and per-layer strides ride in the scalar offset.  This keeps
+// loop-invariant 64-bit addresses out of the vector register file.  Views
+// cover < 4 GiB from their base; callers rebase per row block / per layer.
+//
+// In the CPU emulation a view is a plain pointer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+
+namespace acdc {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+
+struct GView {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __amdgpu_buffer_rsrc_t r;
+#endif
+  char* p;  // stores: uniform base + 32-bit offset (global_store with an SGPR base)
+
+  __host__ __device__ __forceinline__ static GView of(const void* base) {
+    GView g;
+#if defined(__HIP_DEVICE_COMPILE__)
+    // raw buffer: stride 0, num_records = 4 GiB - 1, gfx9 dword3 (32-bit data)
+    g.r = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)0xffffffff, 0x00020000);
+#endif
+    g.p = static_cast<char*>(const_cast<void*>(base));
+    return g;
+  }
+
+  __host__ __device__ __forceinline__ float4 ld4(unsigned voff, unsigned soff) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const f32x4 v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+    return make_float4(v[0], v[1], v[2], v[3]);
+#else
+    float4 v;
+    std::memcpy(&v, p + voff + soff, 16);
+    return v;
+#endif
+  }
+  __host__ __device__ __forceinline__ int4 ldi4(unsigned voff, unsigned soff) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const i32x4 v = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+    return make_int4(v[0], v[1], v[2], v[3]);
+#else
+    int4 v;
+    std::memcpy(&v, p + voff + soff, 16);
+    return v;
+#endif
+  }
+  __host__ __device__ __forceinline__ float2 ld2(unsigned voff, unsigned soff) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const f32x2 v = __builtin_bit_cast(f32x2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+    return make_float2(v[0], v[1]);
+#else
+    float2 v;
+    std::memcpy(&v, p + voff + soff, 8);
+    return v;
+#endif
+  }
+  __host__ __device__ __forceinline__ int ldi1(unsigned voff, unsigned soff) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return (int)__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+#else
+    int v;
+    std::memcpy(&v, p + voff + soff, 4);
+    return v;
+#endif
+  }
+  // Stores go through a plain global pointer: buffer stores fed from the
+  // register arrays defeat register promotion of those arrays in this
+  // compiler, so only loads use the buffer path.
+  __host__ __device__ __forceinline__ void st4(float4 v, unsigned voff, unsigned soff) const {
+    *reinterpret_cast<float4*>(p + (voff + soff)) = v;
+  }
+  __host__ __device__ __forceinline__ void st4(float a, float b, float c, float d, unsigned voff,
+                                               unsigned soff) const {
+    *reinterpret_cast<float4*>(p + (voff + soff)) = make_float4(a, b, c, d);
+  }
+  __host__ __device__ __forceinline__ void st2(float2 v, unsigned voff, unsigned soff) const {
+    *reinterpret_cast<float2*>(p + (voff + soff)) = v;
+  }
+};
+
+}  // namespace acdc

@@ -26,6 +26,7 @@
 #pragma once
 
 #include "acdc_dft.hpp"
+#include "acdc_mem.hpp"
 #include "acdc_plans.hpp"
 #include "acdc_stockham.hpp"
 
@@ -44,54 +45,67 @@ struct RealOps {
   static constexpr int NSL = PL::NSL;
 
   // ---------------------------------------------------------------- chunks
-  // Visit the float4 chunks h[4c..4c+3] owned by thread t: f(c, lo, hi) with
+  // Thread t owns the float4 chunks h[4c..4c+3] with
+  //   side a: c = t + (T*q + i*T*B0)
+  //   side b: c = (CB - t) + (T*(B0/2-1) - T*q + i*T*B0),  CB = T*B0 - 1 - T*(B0/2-1)
+  // for q < B0/2, i < R0/2: a per-thread part plus a compile-time part.
+  static constexpr unsigned CB = T * B0 - 1 - T * (B0 / 2 - 1);
+  struct Lane {
+    unsigned a, b;
+  };
+  __host__ __device__ __forceinline__ static Lane lane(unsigned t) { return Lane{t, CB - t}; }
+
+  // Visit the chunks of a thread: f(lane_chunk, const_chunk, lo, hi) with
   // lo = (h0, h2), hi = (h3, h1) references into the spatial layout.
   template <class F>
-  __host__ __device__ __forceinline__ static void for_chunks(float2 (&v)[P], int t, F&& f) {
+  __host__ __device__ __forceinline__ static void for_chunks(float2 (&v)[P], Lane L, F&& f) {
 #pragma unroll
     for (int q = 0; q < B0 / 2; ++q) {
 #pragma unroll
       for (int i = 0; i < R0 / 2; ++i) {
-        const int p = t + T * q;
-        f(p + i * T * B0, v[2 * q * R0 + i], v[(2 * q + 1) * R0 + R0 - 1 - i]);
-        f(T * B0 - 1 - p + i * T * B0, v[(2 * q + 1) * R0 + i], v[2 * q * R0 + R0 - 1 - i]);
+        f(L.a, unsigned(T * q + i * T * B0), v[2 * q * R0 + i], v[(2 * q + 1) * R0 + R0 - 1 - i]);
+        f(L.b, unsigned(T * (B0 / 2 - 1) - T * q + i * T * B0), v[(2 * q + 1) * R0 + i],
+          v[2 * q * R0 + R0 - 1 - i]);
       }
     }
   }
   template <class F>
-  __host__ __device__ __forceinline__ static void for_chunks2(float2 (&v)[P], float2 (&w)[P], int t,
-                                                              F&& f) {
+  __host__ __device__ __forceinline__ static void for_chunks2(float2 (&v)[P], float2 (&w)[P], Lane L, F&& f) {
 #pragma unroll
     for (int q = 0; q < B0 / 2; ++q) {
 #pragma unroll
       for (int i = 0; i < R0 / 2; ++i) {
-        const int p = t + T * q;
-        f(p + i * T * B0, v[2 * q * R0 + i], v[(2 * q + 1) * R0 + R0 - 1 - i],
+        f(L.a, unsigned(T * q + i * T * B0), v[2 * q * R0 + i], v[(2 * q + 1) * R0 + R0 - 1 - i],
           w[2 * q * R0 + i], w[(2 * q + 1) * R0 + R0 - 1 - i]);
-        f(T * B0 - 1 - p + i * T * B0, v[(2 * q + 1) * R0 + i], v[2 * q * R0 + R0 - 1 - i],
-          w[(2 * q + 1) * R0 + i], w[2 * q * R0 + R0 - 1 - i]);
+        f(L.b, unsigned(T * (B0 / 2 - 1) - T * q + i * T * B0), v[(2 * q + 1) * R0 + i],
+          v[2 * q * R0 + R0 - 1 - i], w[(2 * q + 1) * R0 + i], w[2 * q * R0 + R0 - 1 - i]);
       }
     }
   }
 
-  __host__ __device__ __forceinline__ static void load(const float* row, float2 (&v)[P], int t,
+  // Row loads/stores: g views the workgroup's first row, roff = this row's
+  // offset from it in float4 chunks.
+  // Rows past the batch end (valid == false) read the block's first row,
+  // which always exists, and are zeroed: no branches around the loads.
+  __host__ __device__ __forceinline__ static void load(GView g, unsigned roff, float2 (&v)[P], Lane L,
                                                        bool valid) {
-    for_chunks(v, t, [&](int c, float2& lo, float2& hi) {
-      float4 h = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (valid) h = reinterpret_cast<const float4*>(row)[c];
-      lo = make_float2(h.x, h.z);
-      hi = make_float2(h.w, h.y);
+    const unsigned ro = valid ? roff : 0u;
+    const float z = valid ? 1.0f : 0.0f;
+    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
+      const float4 h = g.ld4((lc + ro) * 16u, cc * 16u);
+      lo = make_float2(h.x * z, h.z * z);
+      hi = make_float2(h.w * z, h.y * z);
     });
   }
-  __host__ __device__ __forceinline__ static void store(float* row, float2 (&v)[P], int t) {
-    for_chunks(v, t, [&](int c, float2& lo, float2& hi) {
-      reinterpret_cast<float4*>(row)[c] = make_float4(lo.x, hi.y, lo.y, hi.x);
+  __host__ __device__ __forceinline__ static void store(GView g, unsigned roff, float2 (&v)[P], Lane L) {
+    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
+      g.st4(make_float4(lo.x, hi.y, lo.y, hi.x), (lc + roff) * 16u, cc * 16u);
     });
   }
-  // v *= a (spatial diagonal)
-  __host__ __device__ __forceinline__ static void scale(float2 (&v)[P], const float* a, int t) {
-    for_chunks(v, t, [&](int c, float2& lo, float2& hi) {
-      const float4 s = reinterpret_cast<const float4*>(a)[c];
+  // v *= a (spatial diagonal of one layer)
+  __host__ __device__ __forceinline__ static void scale(float2 (&v)[P], GView a, Lane L) {
+    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
+      const float4 s = a.ld4(lc * 16u, cc * 16u);
       lo = make_float2(lo.x * s.x, lo.y * s.z);
       hi = make_float2(hi.x * s.w, hi.y * s.y);
     });
@@ -103,34 +117,34 @@ struct RealOps {
 
   // u[n] = z[perm[n]]: write z to LDS in natural order, read it back gathered.
   template <class Ctx>
-  __host__ __device__ __forceinline__ static void gather(Ctx& ctx, float2 (&v)[P], int t, float* slab,
-                                                         const int* perm) {
+  __host__ __device__ __forceinline__ static void gather(Ctx& ctx, float2 (&v)[P], Lane L, float* slab,
+                                                         GView perm) {
     ctx.sync_row();
-    for_chunks(v, t, [&](int c, float2& lo, float2& hi) {
-      reinterpret_cast<float4*>(slab)[c] = make_float4(lo.x, hi.y, lo.y, hi.x);
+    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
+      reinterpret_cast<float4*>(slab)[lc + cc] = make_float4(lo.x, hi.y, lo.y, hi.x);
     });
     ctx.sync_row();
-    for_chunks(v, t, [&](int c, float2& lo, float2& hi) {
-      const int4 pi = reinterpret_cast<const int4*>(perm)[c];
+    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
+      const int4 pi = perm.ldi4(lc * 16u, cc * 16u);
       lo = make_float2(slab[pi.x], slab[pi.z]);
       hi = make_float2(slab[pi.w], slab[pi.y]);
     });
   }
   // g_z[perm[n]] = g_u[n]: the adjoint of gather.
   template <class Ctx>
-  __host__ __device__ __forceinline__ static void scatter(Ctx& ctx, float2 (&v)[P], int t, float* slab,
-                                                          const int* perm) {
+  __host__ __device__ __forceinline__ static void scatter(Ctx& ctx, float2 (&v)[P], Lane L, float* slab,
+                                                          GView perm) {
     ctx.sync_row();
-    for_chunks(v, t, [&](int c, float2& lo, float2& hi) {
-      const int4 pi = reinterpret_cast<const int4*>(perm)[c];
+    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
+      const int4 pi = perm.ldi4(lc * 16u, cc * 16u);
       slab[pi.x] = lo.x;
       slab[pi.y] = hi.y;
       slab[pi.z] = lo.y;
       slab[pi.w] = hi.x;
     });
     ctx.sync_row();
-    for_chunks(v, t, [&](int c, float2& lo, float2& hi) {
-      const float4 h = reinterpret_cast<const float4*>(slab)[c];
+    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
+      const float4 h = reinterpret_cast<const float4*>(slab)[lc + cc];
       lo = make_float2(h.x, h.z);
       hi = make_float2(h.w, h.y);
     });
@@ -140,8 +154,8 @@ struct RealOps {
   // Forward: mirrored first pass (chunk-local input), negated last pass
   // (Makhoul partners together); the inverse runs the mirror image.
   template <bool INV, class Ctx>
-  __host__ __device__ __forceinline__ static void fft(Ctx& ctx, float2 (&v)[P], int t, float2* slab,
-                                                      const float2* tw) {
+  __host__ __device__ __forceinline__ static void fft(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
+                                                      GView tw) {
     if constexpr (INV) stockham_fft<PL, true, 2, 1>(ctx, v, t, slab, tw);
     else stockham_fft<PL, false, 1, 2>(ctx, v, t, slab, tw);
   }
@@ -178,8 +192,17 @@ struct RealOps {
     zm = make_float2(S.x - tt.x, tt.y - S.y);       // conj(S - tt)
   }
 
-  __host__ __device__ __forceinline__ static void post(float2 (&v)[P], float (&X)[NSL][4], int t,
-                                                       const float4* mk0, const float4* mk1) {
+  // Makhoul twiddles of quartet slot `slot` for thread t (t16 = 16*t).
+  __host__ __device__ __forceinline__ static float4 mk0(GView tab, unsigned t16, int slot) {
+    return tab.ld4(t16, unsigned(PL::OFF_MK0 + slot * T * 16));
+  }
+  __host__ __device__ __forceinline__ static float4 mk1(GView tab, unsigned t16, int slot) {
+    return tab.ld4(t16, unsigned(PL::OFF_MK1 + slot * T * 16));
+  }
+
+  __host__ __device__ __forceinline__ static void post(float2 (&v)[P], float (&X)[NSL][4], unsigned t,
+                                                       GView tab) {
+    const unsigned t16 = t * 16u;
     const bool sp = (t == 0);
 #pragma unroll
     for (int q = 0; q < BL / 2; ++q) {
@@ -196,26 +219,27 @@ struct RealOps {
             zm = sel2(sp, v[RL + 3 * RL / 2 - 1 - i], zm);
           }
         }
-        post_one(zk, zm, mk0[slot * T + t], mk1[slot * T + t], X[slot]);
+        post_one(zk, zm, mk0(tab, t16, slot), mk1(tab, t16, slot), X[slot]);
       }
     }
-    post_one(v[RL / 2], v[RL / 2], mk0[(NSL - 1) * T + t], mk1[(NSL - 1) * T + t], X[NSL - 1]);
+    post_one(v[RL / 2], v[RL / 2], mk0(tab, t16, NSL - 1), mk1(tab, t16, NSL - 1), X[NSL - 1]);
   }
 
-  __host__ __device__ __forceinline__ static void pre(float (&X)[NSL][4], float2 (&v)[P], int t,
-                                                      const float4* mk0, const float4* mk1) {
+  __host__ __device__ __forceinline__ static void pre(float (&X)[NSL][4], float2 (&v)[P], unsigned t,
+                                                      GView tab) {
+    const unsigned t16 = t * 16u;
     const bool sp = (t == 0);
     float2 ok[NSL], om[NSL];
 #pragma unroll
-    for (int s = 0; s < NSL; ++s) pre_one(X[s], mk0[s * T + t], mk1[s * T + t], ok[s], om[s]);
+    for (int s = 0; s < NSL; ++s) pre_one(X[s], mk0(tab, t16, s), mk1(tab, t16, s), ok[s], om[s]);
     place(ok, om, v, sp);
   }
 
   // Forward middle of a layer, fused per quartet slot so that no full DCT
   // image is held: Z (frequency layout) -> DCT-II quartet -> * d -> DCT-III
   // pre-twiddle -> Z' (frequency layout), written back into v.
-  __host__ __device__ __forceinline__ static void mid(float2 (&v)[P], int t, const float4* mk0, const float4* mk1,
-                                                      const float4* dq) {
+  __host__ __device__ __forceinline__ static void mid(float2 (&v)[P], unsigned t, GView tab, GView dq) {
+    const unsigned t16 = t * 16u;
     const bool sp = (t == 0);
     float2 ok[NSL], om[NSL];
 #pragma unroll
@@ -233,7 +257,7 @@ struct RealOps {
             zm = sel2(sp, v[RL + 3 * RL / 2 - 1 - i], zm);
           }
         }
-        const float4 m0 = mk0[slot * T + t], m1 = mk1[slot * T + t], d = dq[slot * T + t];
+        const float4 m0 = mk0(tab, t16, slot), m1 = mk1(tab, t16, slot), d = dq.ld4(t16, unsigned(slot * T * 16));
         float X[4];
         post_one(zk, zm, m0, m1, X);
         X[0] *= d.x;
@@ -245,7 +269,7 @@ struct RealOps {
     }
     {
       const int slot = NSL - 1;
-      const float4 m0 = mk0[slot * T + t], m1 = mk1[slot * T + t], d = dq[slot * T + t];
+      const float4 m0 = mk0(tab, t16, slot), m1 = mk1(tab, t16, slot), d = dq.ld4(t16, unsigned(slot * T * 16));
       float X[4];
       post_one(v[RL / 2], v[RL / 2], m0, m1, X);
       X[0] *= d.x;
@@ -286,10 +310,10 @@ struct RealOps {
 
   // X *= d in quartet layout (dq already holds d at the four indices, with
   // zeros where an index does not exist).
-  __host__ __device__ __forceinline__ static void scale_q(float (&X)[NSL][4], const float4* dq, int t) {
+  __host__ __device__ __forceinline__ static void scale_q(float (&X)[NSL][4], GView dq, unsigned t) {
 #pragma unroll
     for (int s = 0; s < NSL; ++s) {
-      const float4 d = dq[s * T + t];
+      const float4 d = dq.ld4(t * 16u, unsigned(s * T * 16));
       X[s][0] *= d.x;
       X[s][1] *= d.y;
       X[s][2] *= d.z;
@@ -318,60 +342,64 @@ struct RealArgs {
 };
 
 template <class PL, class Ctx>
-__host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, int t, long long row, float* slab) {
+__host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned t, long long row0, unsigned rr,
+                                          float* slab) {
   using O = RealOps<PL>;
   constexpr int N = PL::N, P = PL::P, NSL = PL::NSL, T = PL::T;
+  const long long row = row0 + rr;
   const bool valid = row < a.batch;
-  const float2* tw = reinterpret_cast<const float2*>(a.tab);
-  const float4* mk0 = reinterpret_cast<const float4*>(a.tab + PL::OFF_MK0);
-  const float4* mk1 = reinterpret_cast<const float4*>(a.tab + PL::OFF_MK1);
+  const unsigned roff = rr * unsigned(N / 4);
+  const GView tab = GView::of(a.tab);
+  const typename O::Lane L = O::lane(t);
   float2* slab2 = reinterpret_cast<float2*>(slab);
   float2 v[P];
-  O::load(a.x + row * N, v, t, valid);
+  O::load(GView::of(a.x + row0 * N), roff, v, L, valid);
   for (int k = 0; k < a.K; ++k) {
-    if (a.flags & kFlagPerm) O::gather(ctx, v, t, slab, a.perm + (long long)k * N);
+    if (a.flags & kFlagPerm) O::gather(ctx, v, L, slab, GView::of(a.perm + (long long)k * N));
     if (a.saved != nullptr && k > 0 && valid)
-      O::store(a.saved + ((long long)(k - 1) * a.batch + row) * N, v, t);
-    O::scale(v, a.A + (long long)k * N, t);
-    O::template fft<false>(ctx, v, t, slab2, tw);
-    O::mid(v, t, mk0, mk1, a.Dq + (long long)k * NSL * T);
-    O::template fft<true>(ctx, v, t, slab2, tw);
+      O::store(GView::of(a.saved + ((long long)(k - 1) * a.batch + row0) * N), roff, v, L);
+    O::scale(v, GView::of(a.A + (long long)k * N), L);
+    O::template fft<false>(ctx, v, t, slab2, tab);
+    O::mid(v, t, tab, GView::of(a.Dq + (long long)k * NSL * T));
+    O::template fft<true>(ctx, v, t, slab2, tab);
     if ((a.flags & kFlagRelu) && k < a.K - 1) O::relu(v);
   }
-  if (a.y != nullptr && valid) O::store(a.y + row * N, v, t);
+  if (a.y != nullptr && valid) O::store(GView::of(a.y + row0 * N), roff, v, L);
 }
 
 template <class PL, int ROWS, class Ctx>
-__host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, int t, long long row, int tid,
-                                           long long tile, float* lds, float* slab) {
+__host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned t, long long row0, unsigned rr,
+                                           int tid, long long tile, float* lds, float* slab) {
   using O = RealOps<PL>;
   constexpr int N = PL::N, P = PL::P, NSL = PL::NSL, T = PL::T, QF = PL::QF;
   constexpr int THREADS = ROWS * T;
   constexpr long long PS = N + QF;
+  const long long row = row0 + rr;
   const bool valid = row < a.batch;
-  const float2* tw = reinterpret_cast<const float2*>(a.tab);
-  const float4* mk0 = reinterpret_cast<const float4*>(a.tab + PL::OFF_MK0);
-  const float4* mk1 = reinterpret_cast<const float4*>(a.tab + PL::OFF_MK1);
+  const unsigned roff = rr * unsigned(N / 4);
+  const GView tab = GView::of(a.tab);
+  const typename O::Lane L = O::lane(t);
   float2* slab2 = reinterpret_cast<float2*>(slab);
   float2 g[P];
-  O::load(a.gy + row * N, g, t, valid);
+  O::load(GView::of(a.gy + row0 * N), roff, g, L, valid);
   for (int k = a.K - 1; k >= 0; --k) {
-    const float* urow = (k == 0) ? a.x + row * N : a.saved + ((long long)(k - 1) * a.batch + row) * N;
-    const float* ak = a.A + (long long)k * N;
+    const GView ug = GView::of(k == 0 ? a.x + row0 * N : a.saved + ((long long)(k - 1) * a.batch + row0) * N);
+    const GView ak = GView::of(a.A + (long long)k * N);
+    const GView dq = GView::of(a.Dq + (long long)k * NSL * T);
     float* part = a.partial + (tile * a.K + k) * PS;
     // h2 = DCT(u * a) (recomputed from the stored layer input)
     float H[NSL][4];
     {
       float2 v[P];
-      O::load(urow, v, t, valid);
-      O::scale(v, ak, t);
-      O::template fft<false>(ctx, v, t, slab2, tw);
-      O::post(v, H, t, mk0, mk1);
+      O::load(ug, roff, v, L, valid);
+      O::scale(v, ak, L);
+      O::template fft<false>(ctx, v, t, slab2, tab);
+      O::post(v, H, t, tab);
     }
     // gh3 = DCT(g)
     float G[NSL][4];
-    O::template fft<false>(ctx, g, t, slab2, tw);
-    O::post(g, G, t, mk0, mk1);
+    O::template fft<false>(ctx, g, t, slab2, tab);
+    O::post(g, G, t, tab);
     // dL/dd partial: sum over the workgroup's rows of h2 * gh3 (quartet layout)
     ctx.sync_row();
 #pragma unroll
@@ -379,34 +407,34 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, int t, l
       reinterpret_cast<float4*>(slab)[s * T + t] =
           make_float4(H[s][0] * G[s][0], H[s][1] * G[s][1], H[s][2] * G[s][2], H[s][3] * G[s][3]);
     ctx.sync_all();
-    sum_rows<ROWS, PL::SLAB, THREADS>(lds, part + N, QF, tid);
+    sum_rows<ROWS, PL::SLAB, THREADS>(lds, GView::of(part + N), QF, tid);
     ctx.sync_all();
     // gh1 = DCT-III(gh3 * d)
-    O::scale_q(G, a.Dq + (long long)k * NSL * T, t);
-    O::pre(G, g, t, mk0, mk1);
-    O::template fft<true>(ctx, g, t, slab2, tw);
+    O::scale_q(G, dq, t);
+    O::pre(G, g, t, tab);
+    O::template fft<true>(ctx, g, t, slab2, tab);
     // dL/da partial: sum of u * gh1 (spatial, natural order)
     float2 u[P];
-    O::load(urow, u, t, valid);
+    O::load(ug, roff, u, L, valid);
     ctx.sync_row();
-    O::for_chunks2(u, g, t, [&](int c, float2& ulo, float2& uhi, float2& glo, float2& ghi) {
-      reinterpret_cast<float4*>(slab)[c] =
+    O::for_chunks2(u, g, L, [&](unsigned lc, unsigned cc, float2& ulo, float2& uhi, float2& glo, float2& ghi) {
+      reinterpret_cast<float4*>(slab)[lc + cc] =
           make_float4(ulo.x * glo.x, uhi.y * ghi.y, ulo.y * glo.y, uhi.x * ghi.x);
     });
     ctx.sync_all();
-    sum_rows<ROWS, PL::SLAB, THREADS>(lds, part, N, tid);
+    sum_rows<ROWS, PL::SLAB, THREADS>(lds, GView::of(part), N, tid);
     ctx.sync_all();
     // dL/du = gh1 * a, through the ReLU of the previous layer, then un-permute
-    O::scale(g, ak, t);
+    O::scale(g, ak, L);
     if ((a.flags & kFlagRelu) && k > 0) {
-      O::for_chunks2(u, g, t, [&](int, float2& ulo, float2& uhi, float2& glo, float2& ghi) {
+      O::for_chunks2(u, g, L, [&](unsigned, unsigned, float2& ulo, float2& uhi, float2& glo, float2& ghi) {
         glo = make_float2(ulo.x > 0.f ? glo.x : 0.f, ulo.y > 0.f ? glo.y : 0.f);
         ghi = make_float2(uhi.x > 0.f ? ghi.x : 0.f, uhi.y > 0.f ? ghi.y : 0.f);
       });
     }
-    if (a.flags & kFlagPerm) O::scatter(ctx, g, t, slab, a.perm + (long long)k * N);
+    if (a.flags & kFlagPerm) O::scatter(ctx, g, L, slab, GView::of(a.perm + (long long)k * N));
   }
-  if (valid) O::store(a.gx + row * N, g, t);
+  if (valid) O::store(GView::of(a.gx + row0 * N), roff, g, L);
 }
 
 }  // namespace acdc

@@ -104,38 +104,62 @@ __host__ __device__ __forceinline__ float4 real_dq_entry(const float* Dk, const 
                      (m & 8) ? Dk[idx.w] : 0.f);
 }
 
-// Fixed-order sum over tiles of partial element e of layer k (blocks of 32
-// tiles summed first, then the block sums in order).
-__host__ __device__ __forceinline__ float tile_sum(const float* partial, long long ntiles, long long stride,
-                                                   long long off) {
-  float total = 0.f;
+// Fixed-order sum over tiles of partial float4 e4 (stride in float4s):
+// blocks of 32 tiles are summed in tile order, then the block sums in order.
+__host__ __device__ __forceinline__ float4 tile_sum4(const float4* partial, long long ntiles, long long stride,
+                                                     long long off) {
+  float4 total = make_float4(0.f, 0.f, 0.f, 0.f);
   for (long long t0 = 0; t0 < ntiles; t0 += 32) {
     const long long t1 = (t0 + 32 < ntiles) ? t0 + 32 : ntiles;
-    float s = 0.f;
-    for (long long t = t0; t < t1; ++t) s += partial[t * stride + off];
-    total += s;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+    for (long long t = t0; t < t1; ++t) {
+      const float4 u = partial[t * stride + off];
+      s.x += u.x;
+      s.y += u.y;
+      s.z += u.z;
+      s.w += u.w;
+    }
+    total.x += s.x;
+    total.y += s.y;
+    total.z += s.z;
+    total.w += s.w;
   }
   return total;
 }
 
-// Real path: element e in [0, N + QF) of layer k of the reduced gradient.
+// Real path: float4 e4 in [0, (N + QF)/4) of layer k of the reduced
+// gradient.  The first N/4 are dL/da in natural order; the rest are the
+// dL/dd quartets of slot entries e = e4 - N/4, scattered to their indices.
 template <class PL>
-__host__ __device__ __forceinline__ void real_reduce_entry(const float* partial, long long ntiles, int K,
-                                                           int k, int e, float* gA, float* gD,
-                                                           const char* tab) {
-  constexpr long long PS = PL::N + PL::QF;
-  const float s = tile_sum(partial, ntiles, (long long)K * PS, (long long)k * PS + e);
-  if (e < PL::N) {
-    gA[(long long)k * PL::N + e] = s;
+__host__ __device__ __forceinline__ void real_reduce_entry4(const float* partial, long long ntiles, int K, int k,
+                                                            int e4, float* gA, float* gD, const char* tab) {
+  constexpr long long PS4 = (PL::N + PL::QF) / 4;
+  const float4 s = tile_sum4(reinterpret_cast<const float4*>(partial), ntiles, (long long)K * PS4,
+                             (long long)k * PS4 + e4);
+  if (e4 < PL::N / 4) {
+    reinterpret_cast<float4*>(gA + (long long)k * PL::N)[e4] = s;
   } else {
-    const int eq = e - PL::N, st = eq >> 2, c = eq & 3;
+    const int st = e4 - PL::N / 4;
     const int sm = (reinterpret_cast<const int*>(tab + PL::OFF_QMASK)[st] >> 4) & 0xF;
-    if (sm & (1 << c)) {
-      const int4 idx = reinterpret_cast<const int4*>(tab + PL::OFF_QIDX)[st];
-      const int n = c == 0 ? idx.x : c == 1 ? idx.y : c == 2 ? idx.z : idx.w;
-      gD[(long long)k * PL::N + n] = s;
-    }
+    const int4 idx = reinterpret_cast<const int4*>(tab + PL::OFF_QIDX)[st];
+    float* gd = gD + (long long)k * PL::N;
+    if (sm & 1) gd[idx.x] = s.x;
+    if (sm & 2) gd[idx.y] = s.y;
+    if (sm & 4) gd[idx.z] = s.z;
+    if (sm & 8) gd[idx.w] = s.w;
   }
+}
+
+// Complex path: float4 e4 in [0, N) of layer k (dL/da then dL/dd, natural).
+template <class PL>
+__host__ __device__ __forceinline__ void cplx_reduce_entry4(const float* partial, long long ntiles, int K, int k,
+                                                            int e4, float* gA, float* gD) {
+  constexpr long long PS4 = PL::N;  // 4N floats per layer
+  const float4 s = tile_sum4(reinterpret_cast<const float4*>(partial), ntiles, (long long)K * PS4,
+                             (long long)k * PS4 + e4);
+  if (e4 < PL::N / 2) reinterpret_cast<float4*>(gA + (long long)k * 2 * PL::N)[e4] = s;
+  else reinterpret_cast<float4*>(gD + (long long)k * 2 * PL::N)[e4 - PL::N / 2] = s;
 }
 
 }  // namespace acdc

@@ -15,25 +15,26 @@
 #pragma once
 
 #include "acdc_dft.hpp"
+#include "acdc_mem.hpp"
 
 namespace acdc {
 
 template <class PL, int KIND, int B>
-__host__ __device__ __forceinline__ int bfly(int t, int beta) {
+__host__ __device__ __forceinline__ unsigned bfly(unsigned t, int beta) {
   if constexpr (KIND == 0) {
     return t + PL::T * beta;
   } else if constexpr (KIND == 1) {
-    const int p = t + PL::T * (beta >> 1);
+    const unsigned p = t + PL::T * (beta >> 1);
     return (beta & 1) ? PL::T * B - 1 - p : p;
   } else {
-    const int p = t + PL::T * (beta >> 1);
+    const unsigned p = t + PL::T * (beta >> 1);
     return (beta & 1) ? (p == 0 ? PL::NB / 2 : PL::NB - p) : p;
   }
 }
 
 template <class PL, bool INV, int PASS, int KF, int KL, class Ctx>
-__host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL::P], int t, float2* slab,
-                                                      const float2* tw) {
+__host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL::P], unsigned t, float2* slab,
+                                                      GView tw) {
   constexpr int P = PL::P;
   constexpr int r = PL::radix(PASS, INV);
   constexpr int Ns = PL::ns(PASS, INV);
@@ -42,7 +43,7 @@ __host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL:
   constexpr bool first = (PASS == 0);
   constexpr bool last = (PASS == PL::NPASS - 1);
   constexpr int KIND = first ? KF : (last ? KL : 0);
-  int j[b];
+  unsigned j[b];
 #pragma unroll
   for (int beta = 0; beta < b; ++beta) j[beta] = bfly<PL, KIND, b>(t, beta);
   if constexpr (!first) {
@@ -52,13 +53,14 @@ __host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL:
       for (int i = 0; i < r; ++i) v[beta * r + i] = slab[j[beta] + i * stride];
   }
   if constexpr (Ns > 1) {
-    const float2* twp = tw + PL::tw_off(PASS, INV);
+    // twiddles W_{Ns r}^{i k}, k = j mod Ns, from table row k of this pass
+    constexpr unsigned off = unsigned(PL::tw_off(PASS, INV)) * 8u;
 #pragma unroll
     for (int beta = 0; beta < b; ++beta) {
-      const int k = j[beta] % Ns;
-      const float2* w = twp + k * (r - 1);
+      const unsigned k = j[beta] % Ns;
+      const unsigned vo = k * unsigned(r - 1) * 8u;
 #pragma unroll
-      for (int i = 1; i < r; ++i) v[beta * r + i] = ctw<INV>(v[beta * r + i], w[i - 1]);
+      for (int i = 1; i < r; ++i) v[beta * r + i] = ctw<INV>(v[beta * r + i], tw.ld2(vo, off + (i - 1) * 8u));
     }
   }
 #pragma unroll
@@ -67,8 +69,8 @@ __host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL:
     ctx.sync_row();
 #pragma unroll
     for (int beta = 0; beta < b; ++beta) {
-      const int k = j[beta] % Ns;
-      const int base = (j[beta] - k) * r + k;
+      const unsigned k = j[beta] % Ns;
+      const unsigned base = (j[beta] - k) * r + k;
 #pragma unroll
       for (int m = 0; m < r; ++m) slab[base + m * Ns] = v[beta * r + m];
     }
@@ -77,8 +79,8 @@ __host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL:
 }
 
 template <class PL, bool INV, int KF, int KL, class Ctx>
-__host__ __device__ __forceinline__ void stockham_fft(Ctx& ctx, float2 (&v)[PL::P], int t, float2* slab,
-                                                     const float2* tw) {
+__host__ __device__ __forceinline__ void stockham_fft(Ctx& ctx, float2 (&v)[PL::P], unsigned t, float2* slab,
+                                                     GView tw) {
   stockham_pass<PL, INV, 0, KF, KL>(ctx, v, t, slab, tw);
   if constexpr (PL::NPASS > 1) stockham_pass<PL, INV, 1, KF, KL>(ctx, v, t, slab, tw);
   if constexpr (PL::NPASS > 2) stockham_pass<PL, INV, 2, KF, KL>(ctx, v, t, slab, tw);
@@ -88,9 +90,9 @@ __host__ __device__ __forceinline__ void stockham_fft(Ctx& ctx, float2 (&v)[PL::
 // Sum the per-row images [rows][SLAB] of a workgroup in fixed row order and
 // write nfl floats to out (float4 granularity).  Called by every thread.
 template <int ROWS, int SLAB, int THREADS>
-__host__ __device__ __forceinline__ void sum_rows(const float* lds, float* out, int nfl, int tid) {
-  const int n4 = nfl / 4;
-  for (int e = tid; e < n4; e += THREADS) {
+__host__ __device__ __forceinline__ void sum_rows(const float* lds, GView out, int nfl, int tid) {
+  const unsigned n4 = unsigned(nfl) / 4;
+  for (unsigned e = unsigned(tid); e < n4; e += THREADS) {
     float4 s = reinterpret_cast<const float4*>(lds)[e];
 #pragma unroll
     for (int r = 1; r < ROWS; ++r) {
@@ -100,7 +102,7 @@ __host__ __device__ __forceinline__ void sum_rows(const float* lds, float* out, 
       s.z += u.z;
       s.w += u.w;
     }
-    reinterpret_cast<float4*>(out)[e] = s;
+    out.st4(s, e * 16u, 0u);
   }
 }
 

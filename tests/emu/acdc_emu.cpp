@@ -51,7 +51,7 @@ void real_fwd(const float* x, float* y, const float* A, const float* D, const in
   for (long long wg = 0; wg < nwg; ++wg)
     run_wg(L::FWD_THREADS, [&](HostCtx& ctx, int tid) {
       const int r = tid / PL::T, t = tid % PL::T;
-      real_forward_row<PL>(ctx, a, t, wg * L::FWD_ROWS + r, lds.data() + (size_t)r * L::FWD_SLAB);
+      real_forward_row<PL>(ctx, a, unsigned(t), wg * L::FWD_ROWS, unsigned(r), lds.data() + (size_t)r * L::FWD_SLAB);
     });
 }
 
@@ -81,12 +81,12 @@ void real_bwd(const float* x, const float* gy, const float* A, const float* D, c
   for (long long wg = 0; wg < ntiles; ++wg)
     run_wg(L::BWD_THREADS, [&](HostCtx& ctx, int tid) {
       const int r = tid / PL::T, t = tid % PL::T;
-      real_backward_row<PL, L::BWD_ROWS>(ctx, a, t, wg * L::BWD_ROWS + r, tid, wg, lds.data(),
+      real_backward_row<PL, L::BWD_ROWS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, lds.data(),
                                          lds.data() + (size_t)r * L::BWD_SLAB);
     });
   for (int k = 0; k < K; ++k)
-    for (int e = 0; e < PS; ++e)
-      real_reduce_entry<PL>(partial.data(), ntiles, K, k, e, gA, gD, (const char*)tab.data());
+    for (int e4 = 0; e4 < PS / 4; ++e4)
+      real_reduce_entry4<PL>(partial.data(), ntiles, K, k, e4, gA, gD, (const char*)tab.data());
 }
 
 template <class PL>
@@ -99,7 +99,7 @@ void cplx_fwd(const float* x, float* y, const float* A, const float* D, const in
   for (long long wg = 0; wg < nwg; ++wg)
     run_wg(L::FWD_THREADS, [&](HostCtx& ctx, int tid) {
       const int r = tid / PL::T, t = tid % PL::T;
-      cplx_forward_row<PL>(ctx, a, t, wg * L::FWD_ROWS + r, lds.data() + (size_t)r * L::FWD_SLAB);
+      cplx_forward_row<PL>(ctx, a, unsigned(t), wg * L::FWD_ROWS, unsigned(r), lds.data() + (size_t)r * L::FWD_SLAB);
     });
 }
 
@@ -124,15 +124,11 @@ void cplx_bwd(const float* x, const float* gy, const float* A, const float* D, c
   for (long long wg = 0; wg < ntiles; ++wg)
     run_wg(L::BWD_THREADS, [&](HostCtx& ctx, int tid) {
       const int r = tid / PL::T, t = tid % PL::T;
-      cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, t, wg * L::BWD_ROWS + r, tid, wg, lds.data(),
+      cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, lds.data(),
                                          lds.data() + (size_t)r * L::BWD_SLAB);
     });
   for (int k = 0; k < K; ++k)
-    for (long long e = 0; e < PS; ++e) {
-      const float s = tile_sum(partial.data(), ntiles, (long long)K * PS, (long long)k * PS + e);
-      if (e < 2 * PL::N) gA[(size_t)k * 2 * PL::N + e] = s;
-      else gD[(size_t)k * 2 * PL::N + (e - 2 * PL::N)] = s;
-    }
+    for (int e4 = 0; e4 < PL::N; ++e4) cplx_reduce_entry4<PL>(partial.data(), ntiles, K, k, e4, gA, gD);
 }
 
 }  // namespace
