@@ -75,6 +75,9 @@ def main():
                     help="backward recomputes the layer inputs instead of using the forward's")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 256 MiB device copy (known bytes) so that profiler "
+                         "byte counters can be scaled against it")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -94,6 +97,15 @@ def main():
     w = WORKLOADS[args.workload or HEADLINE]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copy calibration: 3 copies of {src.numel() * 4} bytes read + written",
+              file=sys.stderr)
+        del src, dst
     x, A, D, perm, gy = make_inputs(w.N, w.K, w.batch, w.flags, args.seed)
     t = lambda a: torch.from_numpy(a).to(dev)
     xt, At, Dt, pt, gyt = t(x), t(A), t(D), t(perm), t(gy)

@@ -27,16 +27,23 @@ namespace acdc {
 // barrier.
 template <int T>
 struct DevCtx {
+  // Barriers order LDS only ("local" fences): global loads issued ahead of
+  // a barrier stay in flight across it.
+  __device__ __forceinline__ static void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  }
   __device__ __forceinline__ void sync_row() {
     if constexpr (T > 64) {
-      __syncthreads();
+      lds_barrier();
     } else {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
   }
-  __device__ __forceinline__ void sync_all() { __syncthreads(); }
+  __device__ __forceinline__ void sync_all() { lds_barrier(); }
 };
 
 template <class PL>

@@ -177,7 +177,7 @@ __host__ __device__ void cplx_backward_row(Ctx& ctx, const CplxArgs& a, unsigned
     for (int s = 0; s < P; ++s) h[s] = cmulc(g[s], h[s]);   // conj(h2) * gh3 in frequency layout
     O::for_freq(h, t, [&](unsigned l, unsigned c, float2& z) { slab2[l + c] = z; });
     ctx.sync_all();
-    sum_rows<ROWS, PL::SLAB, THREADS>(lds, GView::of(part + RS), int(RS), tid);
+    sum_rows<ROWS, PL::SLAB, THREADS, 2 * N>(lds, GView::of(part + RS), tid);
     ctx.sync_all();
     O::template scale_freq<true>(g, GView::of(a.D + k * RS), 1.0f, t);  // gh3 * conj(d)
     O::template fft<true>(ctx, g, t, slab2, tab);                        // gh1 (unnormalised inverse)
@@ -186,7 +186,7 @@ __host__ __device__ void cplx_backward_row(Ctx& ctx, const CplxArgs& a, unsigned
     ctx.sync_row();
     O::for_spatial2(u, g, t, [&](unsigned l, unsigned c, float2& uu, float2& gg) { slab2[l + c] = cmulc(gg, uu); });
     ctx.sync_all();
-    sum_rows<ROWS, PL::SLAB, THREADS>(lds, GView::of(part), int(RS), tid);
+    sum_rows<ROWS, PL::SLAB, THREADS, 2 * N>(lds, GView::of(part), tid);
     ctx.sync_all();
     O::template scale<true>(g, ak, t);            // gu = gh1 * conj(a)
     if (a.flags & 1u) O::scatter(ctx, g, t, slab2, GView::of(a.perm + (long long)k * N));

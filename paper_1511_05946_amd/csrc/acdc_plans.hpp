@@ -15,9 +15,26 @@
 
 #include <cstdint>
 
+#ifndef ACDC_TAB_PF
+#define ACDC_TAB_PF 3  // quartet slots whose tables are loaded ahead
+#endif
+#ifndef ACDC_LDS_PAD
+#define ACDC_LDS_PAD 1
+#endif
+
 namespace acdc {
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
+constexpr double csqrt(double x) {
+  double r = x > 1 ? x : 1.0;
+  for (int i = 0; i < 64; ++i) r = 0.5 * (r + x / r);
+  return r;
+}
+constexpr int ilog2(int v) {
+  int l = 0;
+  while ((1 << (l + 1)) <= v) ++l;
+  return l;
+}
 
 template <int N_, int T_, int R0_, int R1_, int R2_ = 1, int R3_ = 1>
 struct RealPlan {
@@ -45,9 +62,15 @@ struct RealPlan {
   static constexpr int B0 = P / R0;              // butterflies per thread, first pass
   static constexpr int BL = P / RL;              // butterflies per thread, last pass
   static constexpr int NB = M / RL;              // butterflies of the last pass
-  static constexpr int NSL = (BL / 2) * RL + 1;  // quartet slots per thread (+1 spare)
+  static constexpr int NSL = (BL / 2) * RL;      // quartet slots per thread
   static constexpr int QF = NSL * T * 4;         // floats of one row's quartet image
-  static constexpr int SLAB = cmax(N, QF);       // LDS floats per row
+  // FFT data in LDS: complex element a lives at a + (a >> PADSH), one pad
+  // slot per 2^PADSH elements, so the stride-r writes of the first pass and
+  // the stride-1 reads of the next spread over all banks.
+  static constexpr int PADSH =
+      !ACDC_LDS_PAD ? 30 : (ilog2(R0_) >= 2 && (1 << ilog2(R0_)) == R0_ ? ilog2(R0_) : 4);
+  static constexpr int FFT_FLOATS = 2 * (M + (M >> PADSH));
+  static constexpr int SLAB = cmax(cmax(N, QF), FFT_FLOATS);  // LDS floats per row
   // twiddle table (float2) offsets: forward passes 1.., then inverse passes 1..
   __host__ __device__ static constexpr int tw_count(int p, bool inv) {
     return p == 0 ? 0 : ns(p, inv) * (radix(p, inv) - 1);
@@ -100,7 +123,10 @@ struct ComplexPlan {
     for (int q = 0; q < p; ++q) s *= radix(q, inv);
     return s;
   }
-  static constexpr int SLAB = 2 * N_;  // LDS floats per row
+  static constexpr int PADSH =
+      !ACDC_LDS_PAD ? 30 : (ilog2(R0_) >= 2 && (1 << ilog2(R0_)) == R0_ ? ilog2(R0_) : 4);
+  static constexpr int FFT_FLOATS = 2 * (N_ + (N_ >> PADSH));
+  static constexpr int SLAB = FFT_FLOATS;  // LDS floats per row
   __host__ __device__ static constexpr int tw_count(int p, bool inv) {
     return p == 0 ? 0 : ns(p, inv) * (radix(p, inv) - 1);
   }

@@ -45,69 +45,91 @@ struct RealOps {
   static constexpr int NSL = PL::NSL;
 
   // ---------------------------------------------------------------- chunks
-  // Thread t owns the float4 chunks h[4c..4c+3] with
-  //   side a: c = t + (T*q + i*T*B0)
-  //   side b: c = (CB - t) + (T*(B0/2-1) - T*q + i*T*B0),  CB = T*B0 - 1 - T*(B0/2-1)
-  // for q < B0/2, i < R0/2: a per-thread part plus a compile-time part.
+  // Thread t owns NCH float4 chunks h[4c..4c+3] of the row.  Chunk ordinal
+  // n = 2*(q*(R0/2) + i) + side, q < B0/2, i < R0/2, is at
+  //   side a (n even): c = t + (T*q + i*T*B0)
+  //   side b (n odd):  c = (CB - t) + (T*(B0/2-1) - T*q + i*T*B0),  CB = T*B0 - 1 - T*(B0/2-1)
+  // a per-thread part plus a compile-time part; its complex values are
+  // lo = (h0, h2) and hi = (h3, h1) of the spatial layout.
+  static constexpr int NCH = P / 2;
+  static_assert(NCH == B0 * (R0 / 2), "chunks cover the thread's registers");
   static constexpr unsigned CB = T * B0 - 1 - T * (B0 / 2 - 1);
   struct Lane {
     unsigned a, b;
   };
   __host__ __device__ __forceinline__ static Lane lane(unsigned t) { return Lane{t, CB - t}; }
+  __host__ __device__ static constexpr int ch_q(int n) { return (n >> 1) / (R0 / 2); }
+  __host__ __device__ static constexpr int ch_i(int n) { return (n >> 1) % (R0 / 2); }
+  __host__ __device__ static constexpr unsigned ch_cc(int n) {
+    return (n & 1) ? unsigned(T * (B0 / 2 - 1) - T * ch_q(n) + ch_i(n) * T * B0)
+                   : unsigned(T * ch_q(n) + ch_i(n) * T * B0);
+  }
+  __host__ __device__ static constexpr int ch_lo(int n) {
+    return (n & 1) ? (2 * ch_q(n) + 1) * R0 + ch_i(n) : 2 * ch_q(n) * R0 + ch_i(n);
+  }
+  __host__ __device__ static constexpr int ch_hi(int n) {
+    return (n & 1) ? 2 * ch_q(n) * R0 + R0 - 1 - ch_i(n) : (2 * ch_q(n) + 1) * R0 + R0 - 1 - ch_i(n);
+  }
+  __host__ __device__ __forceinline__ static unsigned ch_lc(Lane L, int n) { return (n & 1) ? L.b : L.a; }
 
-  // Visit the chunks of a thread: f(lane_chunk, const_chunk, lo, hi) with
-  // lo = (h0, h2), hi = (h3, h1) references into the spatial layout.
+  // f(lane_chunk, const_chunk, lo, hi) for every chunk, in ordinal order.
   template <class F>
   __host__ __device__ __forceinline__ static void for_chunks(float2 (&v)[P], Lane L, F&& f) {
 #pragma unroll
-    for (int q = 0; q < B0 / 2; ++q) {
-#pragma unroll
-      for (int i = 0; i < R0 / 2; ++i) {
-        f(L.a, unsigned(T * q + i * T * B0), v[2 * q * R0 + i], v[(2 * q + 1) * R0 + R0 - 1 - i]);
-        f(L.b, unsigned(T * (B0 / 2 - 1) - T * q + i * T * B0), v[(2 * q + 1) * R0 + i],
-          v[2 * q * R0 + R0 - 1 - i]);
-      }
-    }
+    for (int n = 0; n < NCH; ++n) f(ch_lc(L, n), ch_cc(n), v[ch_lo(n)], v[ch_hi(n)]);
   }
   template <class F>
   __host__ __device__ __forceinline__ static void for_chunks2(float2 (&v)[P], float2 (&w)[P], Lane L, F&& f) {
 #pragma unroll
-    for (int q = 0; q < B0 / 2; ++q) {
-#pragma unroll
-      for (int i = 0; i < R0 / 2; ++i) {
-        f(L.a, unsigned(T * q + i * T * B0), v[2 * q * R0 + i], v[(2 * q + 1) * R0 + R0 - 1 - i],
-          w[2 * q * R0 + i], w[(2 * q + 1) * R0 + R0 - 1 - i]);
-        f(L.b, unsigned(T * (B0 / 2 - 1) - T * q + i * T * B0), v[(2 * q + 1) * R0 + i],
-          v[2 * q * R0 + R0 - 1 - i], w[(2 * q + 1) * R0 + i], w[2 * q * R0 + R0 - 1 - i]);
-      }
-    }
+    for (int n = 0; n < NCH; ++n) f(ch_lc(L, n), ch_cc(n), v[ch_lo(n)], v[ch_hi(n)], w[ch_lo(n)], w[ch_hi(n)]);
   }
 
   // Row loads/stores: g views the workgroup's first row, roff = this row's
   // offset from it in float4 chunks.
   // Rows past the batch end (valid == false) read the block's first row,
   // which always exists, and are zeroed: no branches around the loads.
+  __host__ __device__ __forceinline__ static void load_raw(float4 (&h)[NCH], GView g, unsigned roff, Lane L,
+                                                           bool valid) {
+    const unsigned ro = valid ? roff : 0u;
+#pragma unroll
+    for (int n = 0; n < NCH; ++n) h[n] = g.ld4((ch_lc(L, n) + ro) * 16u, ch_cc(n) * 16u);
+  }
+  __host__ __device__ __forceinline__ static void unpack(const float4 (&h)[NCH], float2 (&v)[P], bool valid) {
+    const float z = valid ? 1.0f : 0.0f;
+    int n = 0;
+    for_chunks(v, Lane{0, 0}, [&](unsigned, unsigned, float2& lo, float2& hi) {
+      lo = make_float2(h[n].x * z, h[n].z * z);
+      hi = make_float2(h[n].w * z, h[n].y * z);
+      ++n;
+    });
+  }
   __host__ __device__ __forceinline__ static void load(GView g, unsigned roff, float2 (&v)[P], Lane L,
                                                        bool valid) {
-    const unsigned ro = valid ? roff : 0u;
-    const float z = valid ? 1.0f : 0.0f;
-    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
-      const float4 h = g.ld4((lc + ro) * 16u, cc * 16u);
-      lo = make_float2(h.x * z, h.z * z);
-      hi = make_float2(h.w * z, h.y * z);
-    });
+    float4 h[NCH];
+    load_raw(h, g, roff, L, valid);
+    unpack(h, v, valid);
   }
   __host__ __device__ __forceinline__ static void store(GView g, unsigned roff, float2 (&v)[P], Lane L) {
     for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
       g.st4(make_float4(lo.x, hi.y, lo.y, hi.x), (lc + roff) * 16u, cc * 16u);
     });
   }
-  // v *= a (spatial diagonal of one layer)
-  __host__ __device__ __forceinline__ static void scale(float2 (&v)[P], GView a, Lane L) {
-    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
-      const float4 s = a.ld4(lc * 16u, cc * 16u);
-      lo = make_float2(lo.x * s.x, lo.y * s.z);
-      hi = make_float2(hi.x * s.w, hi.y * s.y);
+  // Per-thread chunks of a row-independent vector (a spatial diagonal).
+  __host__ __device__ __forceinline__ static void load_vec(float4 (&s)[NCH], GView g, Lane L) {
+#pragma unroll
+    for (int n = 0; n < NCH; ++n) s[n] = g.ld4(ch_lc(L, n) * 16u, ch_cc(n) * 16u);
+  }
+  __host__ __device__ __forceinline__ static void load_idx(int4 (&s)[NCH], GView g, Lane L) {
+#pragma unroll
+    for (int n = 0; n < NCH; ++n) s[n] = g.ldi4(ch_lc(L, n) * 16u, ch_cc(n) * 16u);
+  }
+  // v *= a (spatial diagonal of one layer, chunks from load_vec)
+  __host__ __device__ __forceinline__ static void scale(float2 (&v)[P], const float4 (&s)[NCH]) {
+    int n = 0;
+    for_chunks(v, Lane{0, 0}, [&](unsigned, unsigned, float2& lo, float2& hi) {
+      lo = make_float2(lo.x * s[n].x, lo.y * s[n].z);
+      hi = make_float2(hi.x * s[n].w, hi.y * s[n].y);
+      ++n;
     });
   }
   __host__ __device__ __forceinline__ static void relu(float2 (&v)[P]) {
@@ -115,34 +137,42 @@ struct RealOps {
     for (int s = 0; s < P; ++s) v[s] = make_float2(v[s].x > 0.f ? v[s].x : 0.f, v[s].y > 0.f ? v[s].y : 0.f);
   }
 
-  // u[n] = z[perm[n]]: write z to LDS in natural order, read it back gathered.
-  template <class Ctx>
+  // u[n] = z[perm[n]]: write z to LDS in natural order, read it back gathered
+  // through the thread's index chunks (from load_idx).  `hook` runs between
+  // the LDS write and the gathered reads.
+  template <class Ctx, class Hook>
   __host__ __device__ __forceinline__ static void gather(Ctx& ctx, float2 (&v)[P], Lane L, float* slab,
-                                                         GView perm) {
+                                                         const int4 (&idx)[NCH], Hook&& hook) {
     ctx.sync_row();
     for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
       reinterpret_cast<float4*>(slab)[lc + cc] = make_float4(lo.x, hi.y, lo.y, hi.x);
     });
     ctx.sync_row();
-    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
-      const int4 pi = perm.ldi4(lc * 16u, cc * 16u);
+    hook();
+    ACDC_SCHED_FENCE();
+    int n = 0;
+    for_chunks(v, L, [&](unsigned, unsigned, float2& lo, float2& hi) {
+      const int4 pi = idx[n++];
       lo = make_float2(slab[pi.x], slab[pi.z]);
       hi = make_float2(slab[pi.w], slab[pi.y]);
     });
   }
   // g_z[perm[n]] = g_u[n]: the adjoint of gather.
-  template <class Ctx>
+  template <class Ctx, class Hook>
   __host__ __device__ __forceinline__ static void scatter(Ctx& ctx, float2 (&v)[P], Lane L, float* slab,
-                                                          GView perm) {
+                                                          const int4 (&idx)[NCH], Hook&& hook) {
     ctx.sync_row();
-    for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
-      const int4 pi = perm.ldi4(lc * 16u, cc * 16u);
+    int n = 0;
+    for_chunks(v, L, [&](unsigned, unsigned, float2& lo, float2& hi) {
+      const int4 pi = idx[n++];
       slab[pi.x] = lo.x;
       slab[pi.y] = hi.y;
       slab[pi.z] = lo.y;
       slab[pi.w] = hi.x;
     });
     ctx.sync_row();
+    hook();
+    ACDC_SCHED_FENCE();
     for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
       const float4 h = reinterpret_cast<const float4*>(slab)[lc + cc];
       lo = make_float2(h.x, h.z);
@@ -153,11 +183,11 @@ struct RealOps {
   // ------------------------------------------------------------ FFT passes
   // Forward: mirrored first pass (chunk-local input), negated last pass
   // (Makhoul partners together); the inverse runs the mirror image.
-  template <bool INV, class Ctx>
+  template <bool INV, class Ctx, class Tail>
   __host__ __device__ __forceinline__ static void fft(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
-                                                      GView tw) {
-    if constexpr (INV) stockham_fft<PL, true, 2, 1>(ctx, v, t, slab, tw);
-    else stockham_fft<PL, false, 1, 2>(ctx, v, t, slab, tw);
+                                                      GView tw, Tail&& tail) {
+    if constexpr (INV) stockham_fft<PL, true, 2, 1>(ctx, v, t, slab, tw, tail);
+    else stockham_fft<PL, false, 1, 2>(ctx, v, t, slab, tw, tail);
   }
 
   // ------------------------------------------------------ Makhoul quartets
@@ -179,10 +209,8 @@ struct RealOps {
   }
   // Inverse of post_one for the DCT-III (with the 1/M of the inverse FFT
   // folded into qap and conj(qb)).
-  __host__ __device__ __forceinline__ static void pre_one(const float (&Y)[4], float4 m0, float4 m1,
+  __host__ __device__ __forceinline__ static void pre_one(const float (&Y)[4], float2 w, float2 qb, float2 qap,
                                                           float2& zk, float2& zm) {
-    const float2 w = make_float2(m0.x, m0.y);
-    const float2 qb = make_float2(m1.x, m1.y), qap = make_float2(m1.z, m1.w);
     const float2 Ap = cmul(make_float2(Y[0], -Y[1]), qap);
     const float2 Bp = cmulc(make_float2(Y[2] + Y[3], Y[3] - Y[2]), qb);
     const float2 S = cadd(Ap, Bp), Dd = csub(Ap, Bp);
@@ -192,133 +220,125 @@ struct RealOps {
     zm = make_float2(S.x - tt.x, tt.y - S.y);       // conj(S - tt)
   }
 
-  // Makhoul twiddles of quartet slot `slot` for thread t (t16 = 16*t).
-  __host__ __device__ __forceinline__ static float4 mk0(GView tab, unsigned t16, int slot) {
-    return tab.ld4(t16, unsigned(PL::OFF_MK0 + slot * T * 16));
+  // Thread 0's first butterfly pair is (0, NB/2): both are self-negating,
+  // so its partners are not at the generic register positions.  Permuting
+  // those 2*RL registers by pi (new[rho] = old[pi(rho)]) puts every Makhoul
+  // pair at (i, 2*RL-1-i); slot 0 then holds the two self-paired values
+  // (Z[0], Z[M/2]), handled by special twiddles.
+  __host__ __device__ static constexpr int perm_pi(int rho) {
+    return rho < RL / 2       ? rho
+           : rho < RL         ? RL + rho - RL / 2
+           : rho < 3 * RL / 2 ? rho + RL / 2
+           : rho < 2 * RL - 1 ? rho - RL + 1
+                              : RL / 2;
   }
-  __host__ __device__ __forceinline__ static float4 mk1(GView tab, unsigned t16, int slot) {
-    return tab.ld4(t16, unsigned(PL::OFF_MK1 + slot * T * 16));
+  __host__ __device__ static constexpr int perm_pi_inv(int o) {
+    int r = 0;
+    for (int rho = 0; rho < 2 * RL; ++rho)
+      if (perm_pi(rho) == o) r = rho;
+    return r;
+  }
+  __host__ __device__ __forceinline__ static void permute0(float2 (&v)[P], bool sp) {
+    float2 nv[2 * RL];
+#pragma unroll
+    for (int rho = 0; rho < 2 * RL; ++rho) nv[rho] = perm_pi(rho) == rho ? v[rho] : sel2(sp, v[perm_pi(rho)], v[rho]);
+#pragma unroll
+    for (int rho = 0; rho < 2 * RL; ++rho) v[rho] = nv[rho];
+  }
+  __host__ __device__ __forceinline__ static void unpermute0(float2 (&v)[P], bool sp) {
+    float2 nv[2 * RL];
+#pragma unroll
+    for (int o = 0; o < 2 * RL; ++o) nv[o] = perm_pi_inv(o) == o ? v[o] : sel2(sp, v[perm_pi_inv(o)], v[o]);
+#pragma unroll
+    for (int o = 0; o < 2 * RL; ++o) v[o] = nv[o];
+  }
+  // The DCT-III pre-twiddle of thread 0's slot 0 needs its own qb:
+  // exp(i pi/8) / (2 sqrt(N)).
+  static constexpr float kQbRe = float(0.9238795325112867561 / (2.0 * csqrt(double(N))));
+  static constexpr float kQbIm = float(0.3826834323650897717 / (2.0 * csqrt(double(N))));
+  __host__ __device__ __forceinline__ static float2 pre_qb(float4 m1, int q, int i, bool sp) {
+    const float2 qb = make_float2(m1.x, m1.y);
+    if (q == 0 && i == 0) return sel2(sp, make_float2(kQbRe, kQbIm), qb);
+    return qb;
   }
 
-  __host__ __device__ __forceinline__ static void post(float2 (&v)[P], float (&X)[NSL][4], unsigned t,
-                                                       GView tab) {
+  // Makhoul twiddles (m0, m1) and the quartet-layout diagonal d of every
+  // slot.  Loops over the slots load slot s + PF while slot s computes; the
+  // first PF slots are loaded ahead, in the tail of the preceding FFT.
+  static constexpr int PF = NSL < ACDC_TAB_PF ? NSL : ACDC_TAB_PF;
+  struct SlotTabs {
+    float4 m0[NSL], m1[NSL], d[NSL];
+  };
+  __host__ __device__ __forceinline__ static void load_slot(SlotTabs& tb, int slot, unsigned t, GView tab,
+                                                            GView dq) {
     const unsigned t16 = t * 16u;
-    const bool sp = (t == 0);
+    tb.m0[slot] = tab.ld4(t16, unsigned(PL::OFF_MK0 + slot * T * 16));
+    tb.m1[slot] = tab.ld4(t16, unsigned(PL::OFF_MK1 + slot * T * 16));
+    tb.d[slot] = dq.ld4(t16, unsigned(slot * T * 16));
+  }
+  __host__ __device__ __forceinline__ static void load_head(SlotTabs& tb, unsigned t, GView tab, GView dq) {
 #pragma unroll
-    for (int q = 0; q < BL / 2; ++q) {
+    for (int s = 0; s < PF; ++s) load_slot(tb, s, t, tab, dq);
+  }
+
+  // Forward middle of a layer, in place per quartet slot: Z (frequency
+  // layout) -> DCT-II quartet -> * d -> DCT-III pre-twiddle -> Z'.
+  __host__ __device__ __forceinline__ static void mid(float2 (&v)[P], unsigned t, GView tab, GView dq,
+                                                      SlotTabs& tb) {
+    const bool sp = (t == 0);
+    permute0(v, sp);
+#pragma unroll
+    for (int q = 0; q < BL / 2; ++q)
 #pragma unroll
       for (int i = 0; i < RL; ++i) {
         const int slot = q * RL + i;
-        float2 zk = v[2 * q * RL + i];
-        float2 zm = v[(2 * q + 1) * RL + RL - 1 - i];
-        if (q == 0) {
-          if (i < RL / 2) {
-            zm = sel2(sp, v[(RL - i) % RL], zm);
-          } else {
-            zk = sel2(sp, v[RL + i - RL / 2], zk);
-            zm = sel2(sp, v[RL + 3 * RL / 2 - 1 - i], zm);
-          }
-        }
-        post_one(zk, zm, mk0(tab, t16, slot), mk1(tab, t16, slot), X[slot]);
-      }
-    }
-    post_one(v[RL / 2], v[RL / 2], mk0(tab, t16, NSL - 1), mk1(tab, t16, NSL - 1), X[NSL - 1]);
-  }
-
-  __host__ __device__ __forceinline__ static void pre(float (&X)[NSL][4], float2 (&v)[P], unsigned t,
-                                                      GView tab) {
-    const unsigned t16 = t * 16u;
-    const bool sp = (t == 0);
-    float2 ok[NSL], om[NSL];
-#pragma unroll
-    for (int s = 0; s < NSL; ++s) pre_one(X[s], mk0(tab, t16, s), mk1(tab, t16, s), ok[s], om[s]);
-    place(ok, om, v, sp);
-  }
-
-  // Forward middle of a layer, fused per quartet slot so that no full DCT
-  // image is held: Z (frequency layout) -> DCT-II quartet -> * d -> DCT-III
-  // pre-twiddle -> Z' (frequency layout), written back into v.
-  __host__ __device__ __forceinline__ static void mid(float2 (&v)[P], unsigned t, GView tab, GView dq) {
-    const unsigned t16 = t * 16u;
-    const bool sp = (t == 0);
-    float2 ok[NSL], om[NSL];
-#pragma unroll
-    for (int q = 0; q < BL / 2; ++q) {
-#pragma unroll
-      for (int i = 0; i < RL; ++i) {
-        const int slot = q * RL + i;
-        float2 zk = v[2 * q * RL + i];
-        float2 zm = v[(2 * q + 1) * RL + RL - 1 - i];
-        if (q == 0) {
-          if (i < RL / 2) {
-            zm = sel2(sp, v[(RL - i) % RL], zm);
-          } else {
-            zk = sel2(sp, v[RL + i - RL / 2], zk);
-            zm = sel2(sp, v[RL + 3 * RL / 2 - 1 - i], zm);
-          }
-        }
-        const float4 m0 = mk0(tab, t16, slot), m1 = mk1(tab, t16, slot), d = dq.ld4(t16, unsigned(slot * T * 16));
+        if (slot + PF < NSL) load_slot(tb, slot + PF, t, tab, dq);
+        ACDC_SCHED_FENCE();
+        const float4 m0 = tb.m0[slot], m1 = tb.m1[slot], d = tb.d[slot];
+        float2& zk = v[2 * q * RL + i];
+        float2& zm = v[2 * q * RL + 2 * RL - 1 - i];
         float X[4];
         post_one(zk, zm, m0, m1, X);
         X[0] *= d.x;
         X[1] *= d.y;
         X[2] *= d.z;
         X[3] *= d.w;
-        pre_one(X, m0, m1, ok[slot], om[slot]);
+        pre_one(X, make_float2(m0.x, m0.y), pre_qb(m1, q, i, sp), make_float2(m1.z, m1.w), zk, zm);
       }
-    }
-    {
-      const int slot = NSL - 1;
-      const float4 m0 = mk0(tab, t16, slot), m1 = mk1(tab, t16, slot), d = dq.ld4(t16, unsigned(slot * T * 16));
-      float X[4];
-      post_one(v[RL / 2], v[RL / 2], m0, m1, X);
-      X[0] *= d.x;
-      X[1] *= d.y;
-      X[2] *= d.z;
-      X[3] *= d.w;
-      pre_one(X, m0, m1, ok[slot], om[slot]);
-    }
-    place(ok, om, v, sp);
+    unpermute0(v, sp);
   }
 
-  // Write the pre-twiddled pairs back to the frequency layout (thread 0's
-  // first pair uses the special quartet order, see post()).
-  __host__ __device__ __forceinline__ static void place(float2 (&ok)[NSL], float2 (&om)[NSL], float2 (&v)[P],
-                                                        bool sp) {
+  // Backward middle of a layer.  From H-side spectrum v (of u*a) and the
+  // upstream spectrum g, per slot: H = DCT-II(v), G = DCT-II(g); the image
+  // H*G (the dL/dd term of this row, quartet layout) goes to the slab; then
+  // g <- DCT-III pre-twiddle of G*d.  v is consumed.
+  __host__ __device__ __forceinline__ static void mid_bwd(float2 (&v)[P], float2 (&g)[P], unsigned t, GView tab,
+                                                          GView dq, SlotTabs& tb, float* slab) {
+    const bool sp = (t == 0);
+    permute0(v, sp);
+    permute0(g, sp);
 #pragma unroll
-    for (int q = 1; q < BL / 2; ++q) {
+    for (int q = 0; q < BL / 2; ++q)
 #pragma unroll
       for (int i = 0; i < RL; ++i) {
-        v[2 * q * RL + i] = ok[q * RL + i];
-        v[(2 * q + 1) * RL + RL - 1 - i] = om[q * RL + i];
+        const int slot = q * RL + i;
+        if (slot + PF < NSL) load_slot(tb, slot + PF, t, tab, dq);
+        ACDC_SCHED_FENCE();
+        const float4 m0 = tb.m0[slot], m1 = tb.m1[slot], d = tb.d[slot];
+        float2& gk = g[2 * q * RL + i];
+        float2& gm = g[2 * q * RL + 2 * RL - 1 - i];
+        float H[4], G[4];
+        post_one(v[2 * q * RL + i], v[2 * q * RL + 2 * RL - 1 - i], m0, m1, H);
+        post_one(gk, gm, m0, m1, G);
+        reinterpret_cast<float4*>(slab)[slot * T + t] =
+            make_float4(H[0] * G[0], H[1] * G[1], H[2] * G[2], H[3] * G[3]);
+        G[0] *= d.x;
+        G[1] *= d.y;
+        G[2] *= d.z;
+        G[3] *= d.w;
+        pre_one(G, make_float2(m0.x, m0.y), pre_qb(m1, q, i, sp), make_float2(m1.z, m1.w), gk, gm);
       }
-    }
-#pragma unroll
-    for (int rho = 0; rho < 2 * RL; ++rho) {
-      const float2 gen = rho < RL ? ok[rho] : om[2 * RL - 1 - rho];
-      float2 spc;
-      if (rho < RL) {
-        const int e = rho;
-        spc = e < RL / 2 ? ok[e] : (e == RL / 2 ? ok[NSL - 1] : om[RL - e]);
-      } else {
-        const int e = rho - RL;
-        spc = e < RL / 2 ? ok[e + RL / 2] : om[3 * RL / 2 - 1 - e];
-      }
-      v[rho] = sel2(sp, spc, gen);
-    }
-  }
-
-  // X *= d in quartet layout (dq already holds d at the four indices, with
-  // zeros where an index does not exist).
-  __host__ __device__ __forceinline__ static void scale_q(float (&X)[NSL][4], GView dq, unsigned t) {
-#pragma unroll
-    for (int s = 0; s < NSL; ++s) {
-      const float4 d = dq.ld4(t * 16u, unsigned(s * T * 16));
-      X[s][0] *= d.x;
-      X[s][1] *= d.y;
-      X[s][2] *= d.z;
-      X[s][3] *= d.w;
-    }
+    unpermute0(g, sp);
   }
 };
 
@@ -345,23 +365,34 @@ template <class PL, class Ctx>
 __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned t, long long row0, unsigned rr,
                                           float* slab) {
   using O = RealOps<PL>;
-  constexpr int N = PL::N, P = PL::P, NSL = PL::NSL, T = PL::T;
+  constexpr int N = PL::N, P = PL::P, NSL = PL::NSL, T = PL::T, NCH = O::NCH;
   const long long row = row0 + rr;
   const bool valid = row < a.batch;
+  const bool permute = (a.flags & kFlagPerm) != 0;
   const unsigned roff = rr * unsigned(N / 4);
   const GView tab = GView::of(a.tab);
   const typename O::Lane L = O::lane(t);
   float2* slab2 = reinterpret_cast<float2*>(slab);
   float2 v[P];
+  int4 idx[NCH];
+  float4 av[NCH];
   O::load(GView::of(a.x + row0 * N), roff, v, L, valid);
   for (int k = 0; k < a.K; ++k) {
-    if (a.flags & kFlagPerm) O::gather(ctx, v, L, slab, GView::of(a.perm + (long long)k * N));
+    const GView ak = GView::of(a.A + (long long)k * N);
+    const GView dq = GView::of(a.Dq + (long long)k * NSL * T);
+    if (permute) {
+      O::load_idx(idx, GView::of(a.perm + (long long)k * N), L);
+      O::gather(ctx, v, L, slab, idx, [&] { O::load_vec(av, ak, L); });
+    } else {
+      O::load_vec(av, ak, L);
+    }
     if (a.saved != nullptr && k > 0 && valid)
       O::store(GView::of(a.saved + ((long long)(k - 1) * a.batch + row0) * N), roff, v, L);
-    O::scale(v, GView::of(a.A + (long long)k * N), L);
-    O::template fft<false>(ctx, v, t, slab2, tab);
-    O::mid(v, t, tab, GView::of(a.Dq + (long long)k * NSL * T));
-    O::template fft<true>(ctx, v, t, slab2, tab);
+    O::scale(v, av);
+    typename O::SlotTabs tb;
+    O::template fft<false>(ctx, v, t, slab2, tab, [&] { O::load_head(tb, t, tab, dq); });
+    O::mid(v, t, tab, dq, tb);
+    O::template fft<true>(ctx, v, t, slab2, tab, [] {});
     if ((a.flags & kFlagRelu) && k < a.K - 1) O::relu(v);
   }
   if (a.y != nullptr && valid) O::store(GView::of(a.y + row0 * N), roff, v, L);
@@ -371,68 +402,79 @@ template <class PL, int ROWS, class Ctx>
 __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned t, long long row0, unsigned rr,
                                            int tid, long long tile, float* lds, float* slab) {
   using O = RealOps<PL>;
-  constexpr int N = PL::N, P = PL::P, NSL = PL::NSL, T = PL::T, QF = PL::QF;
+  constexpr int N = PL::N, P = PL::P, NSL = PL::NSL, T = PL::T, QF = PL::QF, NCH = O::NCH;
   constexpr int THREADS = ROWS * T;
   constexpr long long PS = N + QF;
   const long long row = row0 + rr;
   const bool valid = row < a.batch;
+  const bool permute = (a.flags & kFlagPerm) != 0;
   const unsigned roff = rr * unsigned(N / 4);
   const GView tab = GView::of(a.tab);
   const typename O::Lane L = O::lane(t);
   float2* slab2 = reinterpret_cast<float2*>(slab);
+  // layer input u_k: the block input for k = 0, else the stored layer input
+  const float* const x0 = a.x + row0 * N;
+  const float* const s0 = a.saved + (row0 - a.batch) * N;
+  auto u_view = [&](int k) { return GView::of(k == 0 ? x0 : s0 + (long long)k * a.batch * N); };
   float2 g[P];
+  float4 uv[NCH], av[NCH];
+  int4 idx[NCH];
   O::load(GView::of(a.gy + row0 * N), roff, g, L, valid);
+  O::load_raw(uv, u_view(a.K - 1), roff, L, valid);
   for (int k = a.K - 1; k >= 0; --k) {
-    const GView ug = GView::of(k == 0 ? a.x + row0 * N : a.saved + ((long long)(k - 1) * a.batch + row0) * N);
     const GView ak = GView::of(a.A + (long long)k * N);
     const GView dq = GView::of(a.Dq + (long long)k * NSL * T);
     float* part = a.partial + (tile * a.K + k) * PS;
-    // h2 = DCT(u * a) (recomputed from the stored layer input)
-    float H[NSL][4];
+    // h2 = DCT(u * a), gh3 = DCT(g); dL/dd image h2 * gh3; g <- pre(gh3 * d)
     {
       float2 v[P];
-      O::load(ug, roff, v, L, valid);
-      O::scale(v, ak, L);
-      O::template fft<false>(ctx, v, t, slab2, tab);
-      O::post(v, H, t, tab);
+      O::load_vec(av, ak, L);
+      O::unpack(uv, v, valid);
+      O::scale(v, av);
+      typename O::SlotTabs tb;
+      O::template fft<false>(ctx, v, t, slab2, tab, [] {});
+      O::template fft<false>(ctx, g, t, slab2, tab, [&] { O::load_head(tb, t, tab, dq); });
+      ctx.sync_row();
+      O::mid_bwd(v, g, t, tab, dq, tb, slab);
     }
-    // gh3 = DCT(g)
-    float G[NSL][4];
-    O::template fft<false>(ctx, g, t, slab2, tab);
-    O::post(g, G, t, tab);
-    // dL/dd partial: sum over the workgroup's rows of h2 * gh3 (quartet layout)
-    ctx.sync_row();
-#pragma unroll
-    for (int s = 0; s < NSL; ++s)
-      reinterpret_cast<float4*>(slab)[s * T + t] =
-          make_float4(H[s][0] * G[s][0], H[s][1] * G[s][1], H[s][2] * G[s][2], H[s][3] * G[s][3]);
     ctx.sync_all();
-    sum_rows<ROWS, PL::SLAB, THREADS>(lds, GView::of(part + N), QF, tid);
+    sum_rows<ROWS, PL::SLAB, THREADS, QF>(lds, GView::of(part + N), tid);
     ctx.sync_all();
-    // gh1 = DCT-III(gh3 * d)
-    O::scale_q(G, dq, t);
-    O::pre(G, g, t, tab);
-    O::template fft<true>(ctx, g, t, slab2, tab);
-    // dL/da partial: sum of u * gh1 (spatial, natural order)
-    float2 u[P];
-    O::load(ug, roff, u, L, valid);
-    ctx.sync_row();
-    O::for_chunks2(u, g, L, [&](unsigned lc, unsigned cc, float2& ulo, float2& uhi, float2& glo, float2& ghi) {
-      reinterpret_cast<float4*>(slab)[lc + cc] =
-          make_float4(ulo.x * glo.x, uhi.y * ghi.y, ulo.y * glo.y, uhi.x * ghi.x);
-    });
-    ctx.sync_all();
-    sum_rows<ROWS, PL::SLAB, THREADS>(lds, GView::of(part), N, tid);
-    ctx.sync_all();
-    // dL/du = gh1 * a, through the ReLU of the previous layer, then un-permute
-    O::scale(g, ak, L);
-    if ((a.flags & kFlagRelu) && k > 0) {
-      O::for_chunks2(u, g, L, [&](unsigned, unsigned, float2& ulo, float2& uhi, float2& glo, float2& ghi) {
-        glo = make_float2(ulo.x > 0.f ? glo.x : 0.f, ulo.y > 0.f ? glo.y : 0.f);
-        ghi = make_float2(uhi.x > 0.f ? ghi.x : 0.f, uhi.y > 0.f ? ghi.y : 0.f);
+    // gh1 = DCT-III(gh3 * d); u_k is reloaded meanwhile
+    O::template fft<true>(ctx, g, t, slab2, tab, [&] { O::load_raw(uv, u_view(k), roff, L, valid); });
+    {
+      // Through the ReLU of the previous layer: u_k = 0 exactly where the
+      // mask is off, so masking gh1 first leaves u * gh1 unchanged.  Then
+      // the dL/da image u * gh1 (spatial, natural order) goes to the slab.
+      const bool mask = (a.flags & kFlagRelu) && k > 0;
+      const float z = valid ? 1.0f : 0.0f;
+      ctx.sync_row();
+      int n = 0;
+      O::for_chunks(g, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
+        const float4 u = make_float4(uv[n].x * z, uv[n].y * z, uv[n].z * z, uv[n].w * z);
+        ++n;
+        if (mask) {
+          lo = make_float2(u.x > 0.f ? lo.x : 0.f, u.z > 0.f ? lo.y : 0.f);
+          hi = make_float2(u.w > 0.f ? hi.x : 0.f, u.y > 0.f ? hi.y : 0.f);
+        }
+        reinterpret_cast<float4*>(slab)[lc + cc] = make_float4(u.x * lo.x, u.y * hi.y, u.z * lo.y, u.w * hi.x);
       });
     }
-    if (a.flags & kFlagPerm) O::scatter(ctx, g, L, slab, GView::of(a.perm + (long long)k * N));
+    O::load_vec(av, ak, L);
+    ACDC_SCHED_FENCE();
+    ctx.sync_all();
+    sum_rows<ROWS, PL::SLAB, THREADS, N>(lds, GView::of(part), tid);
+    ctx.sync_all();
+    // dL/du = gh1 * a, then un-permute; the next layer's u loads meanwhile
+    O::scale(g, av);
+    const int kn = k > 0 ? k - 1 : 0;
+    auto next = [&] { O::load_raw(uv, u_view(kn), roff, L, valid); };
+    if (permute) {
+      O::load_idx(idx, GView::of(a.perm + (long long)k * N), L);
+      O::scatter(ctx, g, L, slab, idx, next);
+    } else {
+      next();
+    }
   }
   if (valid) O::store(GView::of(a.gx + row0 * N), roff, g, L);
 }

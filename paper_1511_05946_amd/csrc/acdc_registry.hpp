@@ -39,13 +39,20 @@ using CP8192 = ComplexPlan<8192, 256, 32, 8, 32>;
 
 // Rows per workgroup.  Forward rows are independent; backward rows of one
 // workgroup are reduced together into one partial of dL/da, dL/dd.
+#ifndef ACDC_FWD_THREADS
+#define ACDC_FWD_THREADS 64
+#endif
+#ifndef ACDC_BWD_THREADS
+#define ACDC_BWD_THREADS 512
+#endif
 template <class PL>
 struct Launch {
-  static constexpr int FWD_ROWS = PL::T >= 128 ? 1 : 128 / PL::T;
-  static constexpr int BWD_ROWS = PL::T == 192 ? 4 : (PL::T >= 512 ? 1 : 512 / PL::T);
+  static constexpr int FWD_ROWS = PL::T >= ACDC_FWD_THREADS ? 1 : ACDC_FWD_THREADS / PL::T;
+  static constexpr int BWD_ROWS =
+      PL::T == 192 ? 2 : (PL::T >= ACDC_BWD_THREADS ? 1 : ACDC_BWD_THREADS / PL::T);
   static constexpr int FWD_THREADS = FWD_ROWS * PL::T;
   static constexpr int BWD_THREADS = BWD_ROWS * PL::T;
-  static constexpr int FWD_SLAB = PL::kComplex ? PL::SLAB : PL::N;  // floats per row
+  static constexpr int FWD_SLAB = PL::kComplex ? PL::SLAB : cmax(PL::N, PL::FFT_FLOATS);  // floats per row
   static constexpr int BWD_SLAB = PL::SLAB;
   static constexpr int FWD_LDS_BYTES = FWD_ROWS * FWD_SLAB * 4;
   static constexpr int BWD_LDS_BYTES = BWD_ROWS * BWD_SLAB * 4;
@@ -56,23 +63,38 @@ struct Launch {
   static_assert(BWD_THREADS <= 1024 && FWD_THREADS <= 1024, "workgroup size");
 };
 
+// ACDC_ONLY_N=<width> instantiates a single real plan (quick development
+// builds); every other width then reports unsupported.
+template <class PLn, class F>
+inline bool run_plan(F& f) {
+#ifdef ACDC_ONLY_N
+  if constexpr (PLn::N != ACDC_ONLY_N || PLn::kComplex) {
+    return false;
+  } else
+#endif
+  {
+    f.template operator()<PLn>();
+    return true;
+  }
+}
+
 // Calls f.template operator()<Plan>() for the real plan of width N.
 template <class F>
 inline bool dispatch_real(int N, F&& f) {
   switch (N) {
-    case 8: f.template operator()<RP8>(); return true;
-    case 16: f.template operator()<RP16>(); return true;
-    case 32: f.template operator()<RP32>(); return true;
-    case 64: f.template operator()<RP64>(); return true;
-    case 128: f.template operator()<RP128>(); return true;
-    case 256: f.template operator()<RP256>(); return true;
-    case 512: f.template operator()<RP512>(); return true;
-    case 1024: f.template operator()<RP1024>(); return true;
-    case 2048: f.template operator()<RP2048>(); return true;
-    case 4096: f.template operator()<RP4096>(); return true;
-    case 8192: f.template operator()<RP8192>(); return true;
-    case 9216: f.template operator()<RP9216>(); return true;
-    case 16384: f.template operator()<RP16384>(); return true;
+    case 8: return run_plan<RP8>(f);
+    case 16: return run_plan<RP16>(f);
+    case 32: return run_plan<RP32>(f);
+    case 64: return run_plan<RP64>(f);
+    case 128: return run_plan<RP128>(f);
+    case 256: return run_plan<RP256>(f);
+    case 512: return run_plan<RP512>(f);
+    case 1024: return run_plan<RP1024>(f);
+    case 2048: return run_plan<RP2048>(f);
+    case 4096: return run_plan<RP4096>(f);
+    case 8192: return run_plan<RP8192>(f);
+    case 9216: return run_plan<RP9216>(f);
+    case 16384: return run_plan<RP16384>(f);
     default: return false;
   }
 }
@@ -80,17 +102,17 @@ inline bool dispatch_real(int N, F&& f) {
 template <class F>
 inline bool dispatch_complex(int N, F&& f) {
   switch (N) {
-    case 8: f.template operator()<CP8>(); return true;
-    case 16: f.template operator()<CP16>(); return true;
-    case 32: f.template operator()<CP32>(); return true;
-    case 64: f.template operator()<CP64>(); return true;
-    case 128: f.template operator()<CP128>(); return true;
-    case 256: f.template operator()<CP256>(); return true;
-    case 512: f.template operator()<CP512>(); return true;
-    case 1024: f.template operator()<CP1024>(); return true;
-    case 2048: f.template operator()<CP2048>(); return true;
-    case 4096: f.template operator()<CP4096>(); return true;
-    case 8192: f.template operator()<CP8192>(); return true;
+    case 8: return run_plan<CP8>(f);
+    case 16: return run_plan<CP16>(f);
+    case 32: return run_plan<CP32>(f);
+    case 64: return run_plan<CP64>(f);
+    case 128: return run_plan<CP128>(f);
+    case 256: return run_plan<CP256>(f);
+    case 512: return run_plan<CP512>(f);
+    case 1024: return run_plan<CP1024>(f);
+    case 2048: return run_plan<CP2048>(f);
+    case 4096: return run_plan<CP4096>(f);
+    case 8192: return run_plan<CP8192>(f);
     default: return false;
   }
 }

@@ -32,9 +32,37 @@ __host__ __device__ __forceinline__ unsigned bfly(unsigned t, int beta) {
   }
 }
 
-template <class PL, bool INV, int PASS, int KF, int KL, class Ctx>
+// Twiddles of one pass for the butterflies of thread t, held in registers.
+// A pass's twiddles are loaded while the previous pass still computes, so
+// the table latency hides behind its DFTs, LDS exchange and barrier.
+template <class PL, bool INV, int PASS, int KF, int KL>
+struct PassTw {
+  static constexpr bool kLive = PASS > 0 && PASS < PL::NPASS && PL::ns(PASS, INV) > 1;
+  static constexpr int r = kLive ? PL::radix(PASS, INV) : 2;
+  static constexpr int b = PL::P / r;
+  static constexpr int NW = kLive ? b * (r - 1) : 1;
+  float2 w[NW];
+  __host__ __device__ __forceinline__ void load(unsigned t, GView tw) {
+    if constexpr (kLive) {
+      constexpr int Ns = PL::ns(PASS, INV);
+      constexpr int KIND = (PASS == PL::NPASS - 1) ? KL : 0;
+      constexpr unsigned off = unsigned(PL::tw_off(PASS, INV)) * 8u;
+#pragma unroll
+      for (int beta = 0; beta < b; ++beta) {
+        const unsigned vo = (bfly<PL, KIND, b>(t, beta) % Ns) * unsigned(r - 1) * 8u;
+#pragma unroll
+        for (int i = 1; i < r; ++i) w[beta * (r - 1) + i - 1] = tw.ld2(vo, off + (i - 1) * 8u);
+      }
+    }
+  }
+};
+
+// One pass.  `next` is called once this pass no longer needs its own
+// twiddles (it issues the next pass's loads); a scheduling fence keeps those
+// loads ahead of this pass's arithmetic.
+template <class PL, bool INV, int PASS, int KF, int KL, class Ctx, class Next>
 __host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL::P], unsigned t, float2* slab,
-                                                      GView tw) {
+                                                      const PassTw<PL, INV, PASS, KF, KL>& tw, Next&& next) {
   constexpr int P = PL::P;
   constexpr int r = PL::radix(PASS, INV);
   constexpr int Ns = PL::ns(PASS, INV);
@@ -46,23 +74,37 @@ __host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL:
   unsigned j[b];
 #pragma unroll
   for (int beta = 0; beta < b; ++beta) j[beta] = bfly<PL, KIND, b>(t, beta);
+  constexpr unsigned S = PL::PADSH;
   if constexpr (!first) {
+    // inputs j + i*stride; stride is a multiple of 2^S, so the padded index
+    // is pad(j) + i*(stride + stride/2^S)
+    if constexpr (stride % (1 << S) == 0) {
+      constexpr unsigned sp = stride + (stride >> S);
+#pragma unroll
+      for (int beta = 0; beta < b; ++beta) {
+        const unsigned pj = j[beta] + (j[beta] >> S);
+#pragma unroll
+        for (int i = 0; i < r; ++i) v[beta * r + i] = slab[pj + i * sp];
+      }
+    } else {
+#pragma unroll
+      for (int beta = 0; beta < b; ++beta)
+#pragma unroll
+        for (int i = 0; i < r; ++i) {
+          const unsigned a = j[beta] + i * stride;
+          v[beta * r + i] = slab[a + (a >> S)];
+        }
+    }
+  }
+  if constexpr (PassTw<PL, INV, PASS, KF, KL>::kLive) {
+    // input i of butterfly j times W_{Ns r}^{i (j mod Ns)}
 #pragma unroll
     for (int beta = 0; beta < b; ++beta)
 #pragma unroll
-      for (int i = 0; i < r; ++i) v[beta * r + i] = slab[j[beta] + i * stride];
+      for (int i = 1; i < r; ++i) v[beta * r + i] = ctw<INV>(v[beta * r + i], tw.w[beta * (r - 1) + i - 1]);
   }
-  if constexpr (Ns > 1) {
-    // twiddles W_{Ns r}^{i k}, k = j mod Ns, from table row k of this pass
-    constexpr unsigned off = unsigned(PL::tw_off(PASS, INV)) * 8u;
-#pragma unroll
-    for (int beta = 0; beta < b; ++beta) {
-      const unsigned k = j[beta] % Ns;
-      const unsigned vo = k * unsigned(r - 1) * 8u;
-#pragma unroll
-      for (int i = 1; i < r; ++i) v[beta * r + i] = ctw<INV>(v[beta * r + i], tw.ld2(vo, off + (i - 1) * 8u));
-    }
-  }
+  next();
+  ACDC_SCHED_FENCE();
 #pragma unroll
   for (int beta = 0; beta < b; ++beta) Dft<r, INV>::run(&v[beta * r]);
   if constexpr (!last) {
@@ -71,38 +113,79 @@ __host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL:
     for (int beta = 0; beta < b; ++beta) {
       const unsigned k = j[beta] % Ns;
       const unsigned base = (j[beta] - k) * r + k;
+      if constexpr (Ns % (1 << S) == 0 || (Ns == 1 && (1 << S) % r == 0)) {
+        // no carry into the pad bits: pad(base + m Ns) = pad(base) + m (Ns + Ns/2^S)
+        constexpr unsigned nsp = Ns + (Ns >> S);
+        const unsigned pb = base + (base >> S);
 #pragma unroll
-      for (int m = 0; m < r; ++m) slab[base + m * Ns] = v[beta * r + m];
+        for (int m = 0; m < r; ++m) slab[pb + m * nsp] = v[beta * r + m];
+      } else {
+#pragma unroll
+        for (int m = 0; m < r; ++m) {
+          const unsigned a = base + m * Ns;
+          slab[a + (a >> S)] = v[beta * r + m];
+        }
+      }
     }
     ctx.sync_row();
   }
 }
 
+// Whole transform.  `tail` runs in the last pass right after its twiddle
+// multiply: callers use it to issue the loads of what follows the FFT.
+template <class PL, bool INV, int KF, int KL, class Ctx, class Tail>
+__host__ __device__ __forceinline__ void stockham_fft(Ctx& ctx, float2 (&v)[PL::P], unsigned t, float2* slab,
+                                                     GView tab, Tail&& tail) {
+  constexpr int NP = PL::NPASS;
+  PassTw<PL, INV, 0, KF, KL> w0;
+  PassTw<PL, INV, 1, KF, KL> w1;
+  if constexpr (NP == 1) {
+    stockham_pass<PL, INV, 0, KF, KL>(ctx, v, t, slab, w0, tail);
+  } else {
+    stockham_pass<PL, INV, 0, KF, KL>(ctx, v, t, slab, w0, [&] { w1.load(t, tab); });
+    PassTw<PL, INV, 2, KF, KL> w2;
+    if constexpr (NP == 2) {
+      stockham_pass<PL, INV, 1, KF, KL>(ctx, v, t, slab, w1, tail);
+    } else {
+      stockham_pass<PL, INV, 1, KF, KL>(ctx, v, t, slab, w1, [&] { w2.load(t, tab); });
+      PassTw<PL, INV, 3, KF, KL> w3;
+      if constexpr (NP == 3) {
+        stockham_pass<PL, INV, 2, KF, KL>(ctx, v, t, slab, w2, tail);
+      } else {
+        stockham_pass<PL, INV, 2, KF, KL>(ctx, v, t, slab, w2, [&] { w3.load(t, tab); });
+        stockham_pass<PL, INV, 3, KF, KL>(ctx, v, t, slab, w3, tail);
+      }
+    }
+  }
+}
+
 template <class PL, bool INV, int KF, int KL, class Ctx>
 __host__ __device__ __forceinline__ void stockham_fft(Ctx& ctx, float2 (&v)[PL::P], unsigned t, float2* slab,
-                                                     GView tw) {
-  stockham_pass<PL, INV, 0, KF, KL>(ctx, v, t, slab, tw);
-  if constexpr (PL::NPASS > 1) stockham_pass<PL, INV, 1, KF, KL>(ctx, v, t, slab, tw);
-  if constexpr (PL::NPASS > 2) stockham_pass<PL, INV, 2, KF, KL>(ctx, v, t, slab, tw);
-  if constexpr (PL::NPASS > 3) stockham_pass<PL, INV, 3, KF, KL>(ctx, v, t, slab, tw);
+                                                     GView tab) {
+  stockham_fft<PL, INV, KF, KL>(ctx, v, t, slab, tab, [] {});
 }
 
 // Sum the per-row images [rows][SLAB] of a workgroup in fixed row order and
-// write nfl floats to out (float4 granularity).  Called by every thread.
-template <int ROWS, int SLAB, int THREADS>
-__host__ __device__ __forceinline__ void sum_rows(const float* lds, GView out, int nfl, int tid) {
-  const unsigned n4 = unsigned(nfl) / 4;
-  for (unsigned e = unsigned(tid); e < n4; e += THREADS) {
-    float4 s = reinterpret_cast<const float4*>(lds)[e];
+// write the first NFL floats to out (float4 granularity).  Called by every
+// thread; the trip count is a compile-time constant.
+template <int ROWS, int SLAB, int THREADS, int NFL>
+__host__ __device__ __forceinline__ void sum_rows(const float* lds, GView out, int tid) {
+  constexpr int N4 = NFL / 4;
 #pragma unroll
-    for (int r = 1; r < ROWS; ++r) {
-      const float4 u = reinterpret_cast<const float4*>(lds + r * SLAB)[e];
-      s.x += u.x;
-      s.y += u.y;
-      s.z += u.z;
-      s.w += u.w;
+  for (int e0 = 0; e0 < N4; e0 += THREADS) {
+    const unsigned e = unsigned(e0 + tid);
+    if (N4 % THREADS == 0 || e < unsigned(N4)) {
+      float4 s = reinterpret_cast<const float4*>(lds)[e];
+#pragma unroll
+      for (int r = 1; r < ROWS; ++r) {
+        const float4 u = reinterpret_cast<const float4*>(lds + r * SLAB)[e];
+        s.x += u.x;
+        s.y += u.y;
+        s.z += u.z;
+        s.w += u.w;
+      }
+      out.st4(s, e * 16u, 0u);
     }
-    out.st4(s, e * 16u, 0u);
   }
 }
 

@@ -40,17 +40,17 @@ inline void fill_fft_twiddles(float2* tw) {
   }
 }
 
-// Spectrum index k handled by quartet slot `slot` of thread t, or -1 for the
-// spare slot of every thread but thread 0.
+// Spectrum index k handled by quartet slot `slot` of thread t, or -2 for
+// slot 0 of thread 0, which carries the two self-paired values Z[0] and
+// Z[M/2] and yields X[0], X[M], X[3M/2], X[M/2].
 template <class PL>
 inline int real_slot_k(int t, int slot) {
-  constexpr int RL = PL::RL, BL = PL::BL, NB = PL::NB, T = PL::T;
-  if (slot == PL::NSL - 1) return t == 0 ? PL::M / 2 : -1;
+  constexpr int RL = PL::RL, NB = PL::NB, T = PL::T;
   const int q = slot / RL, i = slot % RL;
   const int p = t + T * q;
   if (p != 0) return p + i * NB;
+  if (i == 0) return -2;
   return i < RL / 2 ? i * NB : NB / 2 + (i - RL / 2) * NB;
-  (void)BL;
 }
 
 // Returns false if the quartet slots do not cover every DCT index exactly once.
@@ -69,32 +69,35 @@ inline bool build_real_tables(std::vector<unsigned char>& buf) {
     for (int t = 0; t < T; ++t) {
       const int e = slot * T + t;
       const int k = real_slot_k<PL>(t, slot);
-      if (k < 0) {
-        mk0[e] = make_float4(0, 0, 0, 0);
-        mk1[e] = make_float4(0, 0, 0, 0);
-        qidx[e] = make_int4(0, 0, 0, 0);
-        qmask[e] = 0;
-        continue;
+      int idx[4];
+      if (k == -2) {
+        // w = i turns the generic quartet into P1 = 2 Z[0], P2 = 2 conj(Z[M/2]).
+        const HostC q8 = w_pow(1, 16);  // exp(-i pi/8)
+        const double c8 = q8.re, s8 = -q8.im;
+        mk0[e] = make_float4(0.f, 1.f, float(s0 / 2), float(-s0 / 2));
+        mk1[e] = make_float4(float(s * (c8 + s8) / 4), float(s * (c8 - s8) / 4), float(s0 / 2), float(s0 / 2));
+        idx[0] = 0;
+        idx[1] = M;
+        idx[2] = 3 * M / 2;
+        idx[3] = M / 2;
+      } else {
+        const double sk = (k == 0) ? s0 : s;
+        const HostC w = w_pow(k, N);        // W_N^k
+        const HostC q = w_pow(k, 4LL * N);  // W_4N^k
+        const double fa = sk / 2, fb = s / (2 * std::sqrt(2.0)), fp = 1.0 / (2.0 * M * sk);
+        mk0[e] = make_float4(float(w.re), float(w.im), float(fa * q.re), float(fa * q.im));
+        mk1[e] = make_float4(float(fb * q.re), float(fb * q.im), float(fp * q.re), float(-fp * q.im));
+        idx[0] = k;
+        idx[1] = N - k;
+        idx[2] = M - k;
+        idx[3] = M + k;
       }
-      const double sk = (k == 0) ? s0 : s;
-      const HostC w = w_pow(k, N);        // W_N^k
-      const HostC q = w_pow(k, 4LL * N);  // W_4N^k
-      const double fa = sk / 2, fb = s / (2 * std::sqrt(2.0)), fp = 1.0 / (2.0 * M * sk);
-      mk0[e] = make_float4(float(w.re), float(w.im), float(fa * q.re), float(fa * q.im));
-      mk1[e] = make_float4(float(fb * q.re), float(fb * q.im), float(fp * q.re), float(-fp * q.im));
-      int idx[4] = {k, N - k, M - k, M + k};
-      int dmask = 0, smask = 0;
       for (int c = 0; c < 4; ++c) {
-        if (idx[c] < N) dmask |= 1 << c;
-        else idx[c] = 0;
+        if (idx[c] < 0 || idx[c] >= N) return false;
+        cover[idx[c]]++;
       }
-      if (k == 0) smask = 0x5;              // X[0], X[M]
-      else if (2 * k == M) smask = 0x3;     // X[M/2], X[3M/2]
-      else smask = 0xF;
-      for (int c = 0; c < 4; ++c)
-        if (smask & (1 << c)) cover[idx[c]]++;
       qidx[e] = make_int4(idx[0], idx[1], idx[2], idx[3]);
-      qmask[e] = dmask | (smask << 4);
+      qmask[e] = 0xF | (0xF << 4);
     }
   for (int n = 0; n < N; ++n)
     if (cover[n] != 1) return false;
