@@ -2,6 +2,7 @@
 //
 // Kernels (one instantiation per supported width):
 //   k_real_dq      D re-laid out into the per-thread quartet order (tiny)
+//   k_real_mq      per-layer quartet coefficients of the forward middle (tiny)
 //   k_real_fwd     forward cascade, ROWS rows per workgroup, all K layers
 //                  fused, rows kept in registers + one LDS slab per row
 //   k_real_bwd     backward cascade with the reduction of dL/da, dL/dd over
@@ -54,6 +55,22 @@ __global__ __launch_bounds__(256) void k_real_dq(const float* __restrict__ D, fl
   if (i >= (long long)K * E) return;
   const int k = int(i / E), e = int(i % E);
   Dq[i] = real_dq_entry<PL>(D + (long long)k * PL::N, tab, e);
+}
+
+template <class PL>
+__global__ __launch_bounds__(256) void k_real_mq(const float* __restrict__ D, float4* __restrict__ Mq, int K,
+                                                 const char* __restrict__ tab) {
+  constexpr int E = PL::NSL * PL::T;
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long long)K * E) return;
+  const int k = int(i / E), e = int(i % E);
+  float4 row[2];
+  real_mq_entry<PL>(D + (long long)k * PL::N, tab, e, row);
+  // layout [k][slot][r][t]
+  const int slot = e / PL::T, t = e % PL::T;
+  float4* out = Mq + (long long)k * E * 2 + (long long)slot * 2 * PL::T + t;
+  out[0] = row[0];
+  out[PL::T] = row[1];
 }
 
 template <class PL>
@@ -272,9 +289,14 @@ long long bwd_tiles(int64_t batch) {
 size_t elem_floats(uint32_t flags) { return (flags & kFlagComplex) ? 2 : 1; }
 
 struct WsLayout {
-  size_t dq = 0, partial = 0, stash = 0, total = 0;
-  size_t off_dq = 0, off_partial = 0, off_stash = 0;
+  size_t dq = 0, mq = 0, partial = 0, stash = 0, total = 0;
+  size_t off_dq = 0, off_mq = 0, off_partial = 0, off_stash = 0;
 };
+
+template <class PL>
+size_t mq_bytes(int32_t K) {
+  return align256(size_t(K) * PL::NSL * 2 * PL::T * sizeof(float4));
+}
 
 WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved) {
   WsLayout w;
@@ -285,22 +307,24 @@ WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool ha
     } else {
       w.dq = align256(size_t(K) * PL::NSL * PL::T * sizeof(float4));
       w.partial = align256(size_t(tiles) * K * (PL::N + PL::QF) * sizeof(float));
+      if (!have_saved && K > 1 && batch > 0) w.mq = mq_bytes<PL>(K);  // the recomputing forward
     }
   };
   if (flags & kFlagComplex) dispatch_complex(N, f);
   else dispatch_real(N, f);
   if (!have_saved && K > 1) w.stash = align256(size_t(K - 1) * size_t(batch) * N * elem_floats(flags) * 4);
   w.off_dq = 0;
-  w.off_partial = w.dq;
-  w.off_stash = w.dq + w.partial;
-  w.total = w.dq + w.partial + w.stash;
+  w.off_mq = w.dq;
+  w.off_partial = w.off_mq + w.mq;
+  w.off_stash = w.off_partial + w.partial;
+  w.total = w.off_stash + w.stash;
   return w;
 }
 
 size_t fwd_ws(int32_t N, int32_t K, uint32_t flags) {
   size_t b = 0;
   if (!(flags & kFlagComplex))
-    dispatch_real(N, [&]<class PL>() { b = align256(size_t(K) * PL::NSL * PL::T * sizeof(float4)); });
+    dispatch_real(N, [&]<class PL>() { b = mq_bytes<PL>(K); });
   return b;
 }
 
@@ -308,6 +332,14 @@ template <class PL>
 int launch_real_dq(const float* D, float4* Dq, int K, const char* tab, hipStream_t s) {
   const long long n = (long long)K * PL::NSL * PL::T;
   hipLaunchKernelGGL(k_real_dq<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, D, Dq, K, tab);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? ACDC_OK : hip_fail(e);
+}
+
+template <class PL>
+int launch_real_mq(const float* D, float4* Mq, int K, const char* tab, hipStream_t s) {
+  const long long n = (long long)K * PL::NSL * PL::T;
+  hipLaunchKernelGGL(k_real_mq<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, D, Mq, K, tab);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? ACDC_OK : hip_fail(e);
 }
@@ -388,10 +420,10 @@ extern "C" int acdc_forward(const float* x, float* y, const float* A, const floa
     });
   } else {
     dispatch_real(N, [&]<class PL>() {
-      float4* Dq = static_cast<float4*>(workspace);
-      rc = launch_real_dq<PL>(D, Dq, K, tab, s);
+      float4* Mq = static_cast<float4*>(workspace);
+      rc = launch_real_mq<PL>(D, Mq, K, tab, s);
       if (rc != ACDC_OK) return;
-      RealArgs a{x, y, A, Dq, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
+      RealArgs a{x, y, A, nullptr, Mq, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
       rc = launch_real_fwd<PL>(a, s);
     });
   }
@@ -466,11 +498,14 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
         rc = launch_real_dq<PL>(D, Dq, K, tab, s);
         if (rc != ACDC_OK) return;
         if (!have_saved) {
-          RealArgs f{x, nullptr, A, Dq, perm, stash, nullptr, nullptr, nullptr, tab, batch, K, flags};
+          float4* Mq = reinterpret_cast<float4*>(ws + w.off_mq);
+          rc = launch_real_mq<PL>(D, Mq, K, tab, s);
+          if (rc != ACDC_OK) return;
+          RealArgs f{x, nullptr, A, nullptr, Mq, perm, stash, nullptr, nullptr, nullptr, tab, batch, K, flags};
           rc = launch_real_fwd<PL>(f, s);
           if (rc != ACDC_OK) return;
         }
-        RealArgs a{x, nullptr, A, Dq, perm, stash, grad_y, grad_x, partial, tab, batch, K, flags};
+        RealArgs a{x, nullptr, A, Dq, nullptr, perm, stash, grad_y, grad_x, partial, tab, batch, K, flags};
         hipError_t e;
         {
           ProfScope prof(1, s);

@@ -18,6 +18,9 @@
 #ifndef ACDC_TAB_PF
 #define ACDC_TAB_PF 3  // quartet slots whose tables are loaded ahead
 #endif
+#ifndef ACDC_MQ_PF
+#define ACDC_MQ_PF 3  // quartet-coefficient slots loaded ahead in the forward middle
+#endif
 #ifndef ACDC_LDS_PAD
 #define ACDC_LDS_PAD 1
 #endif

@@ -308,6 +308,51 @@ struct RealOps {
     unpermute0(v, sp);
   }
 
+  // Forward middle with the per-layer quartet coefficients of
+  // real_mq_entry (32 operations per slot instead of post_one, * d,
+  // pre_one).  Layout of one layer: [slot][2][T] float4, lane-contiguous;
+  // slot s + PFM loads while slot s computes.
+  static constexpr int PFM = NSL < ACDC_MQ_PF ? NSL : ACDC_MQ_PF;
+  struct MqTabs {
+    float4 m[NSL][2];
+  };
+  __host__ __device__ __forceinline__ static void load_mslot(MqTabs& tb, int slot, unsigned t, GView mq) {
+#pragma unroll
+    for (int r = 0; r < 2; ++r) tb.m[slot][r] = mq.ld4(t * 16u, unsigned((slot * 2 + r) * T * 16));
+  }
+  __host__ __device__ __forceinline__ static void load_mhead(MqTabs& tb, unsigned t, GView mq) {
+#pragma unroll
+    for (int s = 0; s < PFM; ++s) load_mslot(tb, s, t, mq);
+  }
+  __host__ __device__ __forceinline__ static void mid_one(float2& zk, float2& zm, float4 c0, float4 c1) {
+    const float2 w = make_float2(c1.z, c1.w);
+    const float2 E = make_float2(zk.x + zm.x, zk.y - zm.y);   // Z[k] + conj Z[M-k]
+    const float2 Od = make_float2(zk.y + zm.y, zm.x - zk.x);  // (Z[k] - conj Z[M-k]) / i
+    const float2 wO = cmul(Od, w);
+    const float2 s1 = cadd(E, wO), s2 = csub(E, wO);
+    // symmetric 2x2 maps: L1 = [[c0.x, c0.y], [c0.y, c0.z]], L2 = [[c0.w, c1.x], [c1.x, c1.y]]
+    const float2 p1 = make_float2(__builtin_fmaf(c0.y, s1.y, c0.x * s1.x), __builtin_fmaf(c0.z, s1.y, c0.y * s1.x));
+    const float2 p2 = make_float2(__builtin_fmaf(c1.x, s2.y, c0.w * s2.x), __builtin_fmaf(c1.y, s2.y, c1.x * s2.x));
+    const float2 S = cadd(p1, p2), Dd = csub(p1, p2);
+    const float2 cw = cmulc(Dd, w);  // conj(w) * Dd; tt = i * cw
+    zk = make_float2(S.x - cw.y, S.y + cw.x);
+    zm = make_float2(S.x + cw.y, cw.x - S.y);
+  }
+  __host__ __device__ __forceinline__ static void mid_mq(float2 (&v)[P], unsigned t, GView mq, MqTabs& tb) {
+    const bool sp = (t == 0);
+    permute0(v, sp);
+#pragma unroll
+    for (int q = 0; q < BL / 2; ++q)
+#pragma unroll
+      for (int i = 0; i < RL; ++i) {
+        const int slot = q * RL + i;
+        if (slot + PFM < NSL) load_mslot(tb, slot + PFM, t, mq);
+        ACDC_SCHED_FENCE();
+        mid_one(v[2 * q * RL + i], v[2 * q * RL + 2 * RL - 1 - i], tb.m[slot][0], tb.m[slot][1]);
+      }
+    unpermute0(v, sp);
+  }
+
   // Backward middle of a layer.  From H-side spectrum v (of u*a) and the
   // upstream spectrum g, per slot: H = DCT-II(v), G = DCT-II(g); the image
   // H*G (the dL/dd term of this row, quartet layout) goes to the slab; then
@@ -349,7 +394,8 @@ struct RealArgs {
   const float* x;
   float* y;            // forward output (may be null: stash-only forward)
   const float* A;
-  const float4* Dq;    // [K][NSL*T] d in quartet layout
+  const float4* Dq;    // [K][NSL*T] d in quartet layout (backward)
+  const float4* Mq;    // [K][NSL][2][T] forward quartet coefficients
   const int* perm;     // [K][N] (PERM only)
   float* saved;        // [K-1][batch][N] layer inputs u_1..u_{K-1} (may be null)
   const float* gy;     // backward: upstream gradient
@@ -379,7 +425,7 @@ __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned 
   O::load(GView::of(a.x + row0 * N), roff, v, L, valid);
   for (int k = 0; k < a.K; ++k) {
     const GView ak = GView::of(a.A + (long long)k * N);
-    const GView dq = GView::of(a.Dq + (long long)k * NSL * T);
+    const GView mq = GView::of(a.Mq + (long long)k * NSL * 2 * T);
     if (permute) {
       O::load_idx(idx, GView::of(a.perm + (long long)k * N), L);
       O::gather(ctx, v, L, slab, idx, [&] { O::load_vec(av, ak, L); });
@@ -389,9 +435,9 @@ __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned 
     if (a.saved != nullptr && k > 0 && valid)
       O::store(GView::of(a.saved + ((long long)(k - 1) * a.batch + row0) * N), roff, v, L);
     O::scale(v, av);
-    typename O::SlotTabs tb;
-    O::template fft<false>(ctx, v, t, slab2, tab, [&] { O::load_head(tb, t, tab, dq); });
-    O::mid(v, t, tab, dq, tb);
+    typename O::MqTabs tb;
+    O::template fft<false>(ctx, v, t, slab2, tab, [&] { O::load_mhead(tb, t, mq); });
+    O::mid_mq(v, t, mq, tb);
     O::template fft<true>(ctx, v, t, slab2, tab, [] {});
     if ((a.flags & kFlagRelu) && k < a.K - 1) O::relu(v);
   }

@@ -126,6 +126,61 @@ __host__ __device__ __forceinline__ float4 real_dq_entry(const float* Dk, const 
                      (m & 8) ? Dk[idx.w] : 0.f);
 }
 
+// Forward quartet operator of layer k at slot entry e = slot*T + t.
+//
+// The middle of a forward layer takes one quartet's spectrum pair
+// (Z[k], Z[M-k]) through the DCT-II post-twiddle, the D diagonal and the
+// DCT-III pre-twiddle (RealOps::post_one / pre_one).  Writing
+//   E = Z[k] + conj Z[M-k],  O = (Z[k] - conj Z[M-k]) / i,
+//   s1 = E + w O,  s2 = E - w O          (w = W_N^k, the real-FFT split)
+// the post-twiddle, the four d values and the pre-twiddle act on s1 and s2
+// separately, each as a 2x2 real matrix:
+//   s1 -> qap * diag(d0, d1) * (qa s1)          (X[k], X[N-k] pair)
+//   s2 -> conj(qb') * H^T diag(d2, d3) H * (qb s2)   (X[M-k], X[M+k] pair)
+// with H = [[1,-1],[1,1]].  Both matrices are symmetric because qap and
+// qb' point along conj(qa) and qb (also for thread 0's self-paired slot),
+// so a slot needs w and 3 + 3 coefficients:
+//   out[0] = (L1_00, L1_01, L1_11, L2_00),  out[1] = (L2_01, L2_11, w.x, w.y).
+// Coefficients are formed in double from the fp32 twiddle tables and
+// rounded once.
+struct QuartetD {
+  double x, y;
+};
+__host__ __device__ inline QuartetD qd_mul(QuartetD a, QuartetD w) {
+  return QuartetD{a.x * w.x - a.y * w.y, a.x * w.y + a.y * w.x};
+}
+__host__ __device__ inline QuartetD qd_mulc(QuartetD a, QuartetD w) {  // a * conj(w)
+  return QuartetD{a.x * w.x + a.y * w.y, a.y * w.x - a.x * w.y};
+}
+template <class PL>
+__host__ __device__ inline void real_mq_entry(const float* Dk, const char* tab, int e, float4 (&out)[2]) {
+  const float4 m0 = reinterpret_cast<const float4*>(tab + PL::OFF_MK0)[e];
+  const float4 m1 = reinterpret_cast<const float4*>(tab + PL::OFF_MK1)[e];
+  const float4 d = real_dq_entry<PL>(Dk, tab, e);
+  const QuartetD qa{m0.z, m0.w}, qb{m1.x, m1.y}, qap{m1.z, m1.w};
+  // thread 0's slot 0 carries the self-paired values; its pre-twiddle uses
+  // exp(i pi/8) / (2 sqrt(N)) (RealOps::pre_qb)
+  const QuartetD qbp = e == 0 ? QuartetD{RealOps<PL>::kQbRe, RealOps<PL>::kQbIm} : qb;
+  double L1[2][2], L2[2][2];
+  for (int j = 0; j < 2; ++j) {
+    const QuartetD s{double(j == 0), double(j == 1)};
+    // s1 path: u1 = qa s1, (Y0, -Y1) = (d0 Re u1, d1 Im u1), Ap = (.) qap
+    const QuartetD u1 = qd_mul(s, qa);
+    const QuartetD ap = qd_mul(QuartetD{d.x * u1.x, d.y * u1.y}, qap);
+    L1[0][j] = ap.x;
+    L1[1][j] = ap.y;
+    // s2 path: u2 = qb s2, X2 = u2.x - u2.y, X3 = u2.x + u2.y, Y = d X,
+    // Bp = (Y2 + Y3, Y3 - Y2) conj(qb')
+    const QuartetD u2 = qd_mul(s, qb);
+    const double y2 = d.z * (u2.x - u2.y), y3 = d.w * (u2.x + u2.y);
+    const QuartetD bp = qd_mulc(QuartetD{y2 + y3, y3 - y2}, qbp);
+    L2[0][j] = bp.x;
+    L2[1][j] = bp.y;
+  }
+  out[0] = make_float4(float(L1[0][0]), float(0.5 * (L1[0][1] + L1[1][0])), float(L1[1][1]), float(L2[0][0]));
+  out[1] = make_float4(float(0.5 * (L2[0][1] + L2[1][0])), float(L2[1][1]), m0.x, m0.y);
+}
+
 // Fixed-order sum over tiles of partial float4 e4 (stride in float4s):
 // blocks of 32 tiles are summed in tile order, then the block sums in order.
 __host__ __device__ __forceinline__ float4 tile_sum4(const float4* partial, long long ntiles, long long stride,

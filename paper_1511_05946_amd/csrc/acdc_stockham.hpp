@@ -33,6 +33,8 @@ __host__ __device__ __forceinline__ unsigned bfly(unsigned t, int beta) {
 }
 
 // Twiddles of one pass for the butterflies of thread t, held in registers.
+// Input i of butterfly j takes W_{Ns r}^{i k}, k = j mod Ns, stored at
+// [i-1][k] of the pass's table block.
 // A pass's twiddles are loaded while the previous pass still computes, so
 // the table latency hides behind its DFTs, LDS exchange and barrier.
 template <class PL, bool INV, int PASS, int KF, int KL>
@@ -49,9 +51,11 @@ struct PassTw {
       constexpr unsigned off = unsigned(PL::tw_off(PASS, INV)) * 8u;
 #pragma unroll
       for (int beta = 0; beta < b; ++beta) {
-        const unsigned vo = (bfly<PL, KIND, b>(t, beta) % Ns) * unsigned(r - 1) * 8u;
+        // table layout [i-1][k], k = j mod Ns: lanes with consecutive j
+        // read consecutive float2, so one load touches few cache lines
+        const unsigned vo = (bfly<PL, KIND, b>(t, beta) % Ns) * 8u;
 #pragma unroll
-        for (int i = 1; i < r; ++i) w[beta * (r - 1) + i - 1] = tw.ld2(vo, off + (i - 1) * 8u);
+        for (int i = 1; i < r; ++i) w[beta * (r - 1) + i - 1] = tw.ld2(vo, off + unsigned((i - 1) * Ns) * 8u);
       }
     }
   }

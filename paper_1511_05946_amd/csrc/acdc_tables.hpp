@@ -31,10 +31,11 @@ inline void fill_fft_twiddles(float2* tw) {
     const bool inv = d == 1;
     for (int p = 1; p < PL::NPASS; ++p) {
       const int r = PL::radix(p, inv), Ns = PL::ns(p, inv), off = PL::tw_off(p, inv);
-      for (int k = 0; k < Ns; ++k)
-        for (int i = 1; i < r; ++i) {
+      // [input i-1][k]: the lanes of one load read consecutive k
+      for (int i = 1; i < r; ++i)
+        for (int k = 0; k < Ns; ++k) {
           const HostC w = w_pow((long long)i * k, (long long)Ns * r);
-          tw[off + k * (r - 1) + (i - 1)] = make_float2(float(w.re), float(w.im));
+          tw[off + (i - 1) * Ns + k] = make_float2(float(w.re), float(w.im));
         }
     }
   }

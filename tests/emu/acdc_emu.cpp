@@ -39,13 +39,17 @@ template <class PL>
 void real_fwd(const float* x, float* y, const float* A, const float* D, const int* perm, long long batch,
               int K, unsigned flags, float* saved, const std::vector<unsigned char>& tab) {
   using L = Launch<PL>;
-  std::vector<float4> dq((size_t)K * PL::NSL * PL::T);
+  constexpr int E = PL::NSL * PL::T;
+  std::vector<float4> mq((size_t)K * E * 2);
   for (int k = 0; k < K; ++k)
-    for (int e = 0; e < PL::NSL * PL::T; ++e)
-      dq[(size_t)k * PL::NSL * PL::T + e] =
-          real_dq_entry<PL>(D + (size_t)k * PL::N, (const char*)tab.data(), e);
-  RealArgs a{x, y, A, dq.data(), perm, saved, nullptr, nullptr, nullptr, (const char*)tab.data(), batch, K,
-             flags};
+    for (int e = 0; e < E; ++e) {
+      float4 row[2];
+      real_mq_entry<PL>(D + (size_t)k * PL::N, (const char*)tab.data(), e, row);
+      const int slot = e / PL::T, t = e % PL::T;
+      for (int r = 0; r < 2; ++r) mq[(size_t)k * E * 2 + (size_t)(slot * 2 + r) * PL::T + t] = row[r];
+    }
+  RealArgs a{x, y, A, nullptr, mq.data(), perm, saved, nullptr, nullptr, nullptr, (const char*)tab.data(), batch,
+             K, flags};
   const long long nwg = (batch + L::FWD_ROWS - 1) / L::FWD_ROWS;
   std::vector<float> lds((size_t)L::FWD_ROWS * L::FWD_SLAB);
   for (long long wg = 0; wg < nwg; ++wg)
@@ -75,7 +79,7 @@ void real_bwd(const float* x, const float* gy, const float* A, const float* D, c
   const long long ntiles = (batch + L::BWD_ROWS - 1) / L::BWD_ROWS;
   const long long PS = PL::N + PL::QF;
   std::vector<float> partial((size_t)ntiles * K * PS);
-  RealArgs a{x, nullptr, A, dq.data(), perm, const_cast<float*>(saved), gy, gx, partial.data(),
+  RealArgs a{x, nullptr, A, dq.data(), nullptr, perm, const_cast<float*>(saved), gy, gx, partial.data(),
              (const char*)tab.data(), batch, K, flags};
   std::vector<float> lds((size_t)L::BWD_ROWS * L::BWD_SLAB);
   for (long long wg = 0; wg < ntiles; ++wg)
