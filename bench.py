@@ -39,6 +39,23 @@ def flops_row_layer(N: int, complex_: bool) -> float:
     return (10 * N * lg + 12 * N) if complex_ else (4 * N + 5 * N * lg)
 
 
+def recorded_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the rocprofv3 FETCH_SIZE /
+    WRITE_SIZE record in profiles/, scaled by the copy calibration stored with
+    it; None when there is no record or the kernel sources changed since the
+    counters were taken."""
+    from paper_1511_05946_amd.build import source_digest
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_digest") != source_digest() or kernel not in rec.get("kernels", {}):
+        return None
+    k = rec["kernels"][kernel]
+    return (k["fetch_kib"] * rec["fetch_scale"] + k["write_kib"] * rec["write_scale"]) * 1024.0
+
+
 def cpu_baseline(w, seed: int, budget_s: float = 12.0, max_rows: int = 512):
     """Time the oracle (forward + analytic backward, fp64) on growing row
     chunks of the workload until the budget is used."""
@@ -155,7 +172,8 @@ def main():
     fwd_ms = kern["forward"]["avg_ms"]
     fwd_achieved = w.batch * w.K * f_rl / (fwd_ms * 1e-3) / 1e12
     roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": None,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4),
+            "traffic": recorded_traffic(w.name, "k_real_bwd" if not w.complex else "k_cplx_bwd"),
             "kernel": "k_real_bwd" if not w.complex else "k_cplx_bwd",
             "kernel_avg_ms": round(bwd_ms, 4),
             "algorithmic_flops_per_launch": bwd_flops}

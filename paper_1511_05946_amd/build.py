@@ -24,6 +24,21 @@ HIP_FLAGS = [
 ]
 
 
+def source_digest() -> str:
+    """sha256 over the kernel sources (csrc/*, include/*), in name order: the
+    version tag that recorded profiler counters are tied to."""
+    import hashlib
+    h = hashlib.sha256()
+    for d in (CSRC, INCLUDE):
+        for name in sorted(os.listdir(d)):
+            path = os.path.join(d, name)
+            if os.path.isfile(path):
+                h.update(name.encode())
+                with open(path, "rb") as f:
+                    h.update(f.read())
+    return h.hexdigest()
+
+
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
         if cand and os.path.exists(cand):

@@ -1,8 +1,7 @@
 // HIP kernels for gfx950 and the C ABI declared in include/acdc.h.
 //
 // Kernels (one instantiation per supported width):
-//   k_real_dq      D re-laid out into the per-thread quartet order (tiny)
-//   k_real_mq      per-layer quartet coefficients of the forward middle (tiny)
+//   k_real_mq      per-layer quartet coefficients of the layer middle (tiny)
 //   k_real_fwd     forward cascade, ROWS rows per workgroup, all K layers
 //                  fused, rows kept in registers + one LDS slab per row
 //   k_real_bwd     backward cascade with the reduction of dL/da, dL/dd over
@@ -48,29 +47,19 @@ struct DevCtx {
 };
 
 template <class PL>
-__global__ __launch_bounds__(256) void k_real_dq(const float* __restrict__ D, float4* __restrict__ Dq, int K,
-                                                 const char* __restrict__ tab) {
-  constexpr int E = PL::NSL * PL::T;
-  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (long long)K * E) return;
-  const int k = int(i / E), e = int(i % E);
-  Dq[i] = real_dq_entry<PL>(D + (long long)k * PL::N, tab, e);
-}
-
-template <class PL>
 __global__ __launch_bounds__(256) void k_real_mq(const float* __restrict__ D, float4* __restrict__ Mq, int K,
                                                  const char* __restrict__ tab) {
   constexpr int E = PL::NSL * PL::T;
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i >= (long long)K * E) return;
   const int k = int(i / E), e = int(i % E);
-  float4 row[2];
+  float4 row[3];
   real_mq_entry<PL>(D + (long long)k * PL::N, tab, e, row);
   // layout [k][slot][r][t]
   const int slot = e / PL::T, t = e % PL::T;
-  float4* out = Mq + (long long)k * E * 2 + (long long)slot * 2 * PL::T + t;
-  out[0] = row[0];
-  out[PL::T] = row[1];
+  float4* out = Mq + (long long)k * E * 3 + (long long)slot * 3 * PL::T + t;
+#pragma unroll
+  for (int r = 0; r < 3; ++r) out[r * PL::T] = row[r];
 }
 
 template <class PL>
@@ -100,14 +89,31 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealAr
                                      (long long)blockIdx.x, lds, lds + r * L::BWD_SLAB);
 }
 
+// Batch reduction: a block owns kRedEntries float4 entries of the reduced
+// gradient (over all layers, entry index k * PS4 + e4) and sums them over the
+// tiles with one thread per (entry, phase); phase sums meet in LDS and are
+// added in phase order (tile_phase_sum4 / phases_total4).
+constexpr int kRedEntries = 64;
+static_assert(kRedEntries * kRedPhases == 256, "one thread per (entry, phase)");
+
 template <class PL>
 __global__ __launch_bounds__(256) void k_real_reduce(const float* __restrict__ partial, long long ntiles, int K,
                                                      float* __restrict__ gA, float* __restrict__ gD,
                                                      const char* __restrict__ tab) {
-  constexpr long long PS4 = (PL::N + PL::QF) / 4;
-  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (long long)K * PS4) return;
-  real_reduce_entry4<PL>(partial, ntiles, K, int(i / PS4), int(i % PS4), gA, gD, tab);
+  constexpr long long PS4 = partial_entries4<PL>();
+  __shared__ float4 ph[kRedPhases][kRedEntries];
+  const int lane = threadIdx.x % kRedEntries, g = threadIdx.x / kRedEntries;
+  const long long i = (long long)blockIdx.x * kRedEntries + lane;
+  const long long n = (long long)K * PS4;
+  ph[g][lane] = i < n ? tile_phase_sum4(reinterpret_cast<const float4*>(partial), ntiles, n, i, g)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+  __syncthreads();
+  if (g == 0 && i < n) {
+    float4 all[kRedPhases];
+#pragma unroll
+    for (int q = 0; q < kRedPhases; ++q) all[q] = ph[q][lane];
+    real_reduce_store4<PL>(phases_total4(all), int(i / PS4), int(i % PS4), gA, gD, tab);
+  }
 }
 
 template <class PL>
@@ -140,9 +146,20 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_cplx_bwd(CplxAr
 template <class PL>
 __global__ __launch_bounds__(256) void k_cplx_reduce(const float* __restrict__ partial, long long ntiles, int K,
                                                      float* __restrict__ gA, float* __restrict__ gD) {
-  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (long long)K * PL::N) return;
-  cplx_reduce_entry4<PL>(partial, ntiles, K, int(i / PL::N), int(i % PL::N), gA, gD);
+  constexpr long long PS4 = partial_entries4<PL>();
+  __shared__ float4 ph[kRedPhases][kRedEntries];
+  const int lane = threadIdx.x % kRedEntries, g = threadIdx.x / kRedEntries;
+  const long long i = (long long)blockIdx.x * kRedEntries + lane;
+  const long long n = (long long)K * PS4;
+  ph[g][lane] = i < n ? tile_phase_sum4(reinterpret_cast<const float4*>(partial), ntiles, n, i, g)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+  __syncthreads();
+  if (g == 0 && i < n) {
+    float4 all[kRedPhases];
+#pragma unroll
+    for (int q = 0; q < kRedPhases; ++q) all[q] = ph[q][lane];
+    cplx_reduce_store4<PL>(phases_total4(all), int(i / PS4), int(i % PS4), gA, gD);
+  }
 }
 
 // ------------------------------------------------------------------ host side
@@ -289,13 +306,13 @@ long long bwd_tiles(int64_t batch) {
 size_t elem_floats(uint32_t flags) { return (flags & kFlagComplex) ? 2 : 1; }
 
 struct WsLayout {
-  size_t dq = 0, mq = 0, partial = 0, stash = 0, total = 0;
-  size_t off_dq = 0, off_mq = 0, off_partial = 0, off_stash = 0;
+  size_t mq = 0, partial = 0, stash = 0, total = 0;
+  size_t off_mq = 0, off_partial = 0, off_stash = 0;
 };
 
 template <class PL>
 size_t mq_bytes(int32_t K) {
-  return align256(size_t(K) * PL::NSL * 2 * PL::T * sizeof(float4));
+  return align256(size_t(K) * PL::NSL * 3 * PL::T * sizeof(float4));
 }
 
 WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved) {
@@ -305,16 +322,14 @@ WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool ha
     if constexpr (PL::kComplex) {
       w.partial = align256(size_t(tiles) * K * 4 * PL::N * sizeof(float));
     } else {
-      w.dq = align256(size_t(K) * PL::NSL * PL::T * sizeof(float4));
       w.partial = align256(size_t(tiles) * K * (PL::N + PL::QF) * sizeof(float));
-      if (!have_saved && K > 1 && batch > 0) w.mq = mq_bytes<PL>(K);  // the recomputing forward
+      if (batch > 0) w.mq = mq_bytes<PL>(K);
     }
   };
   if (flags & kFlagComplex) dispatch_complex(N, f);
   else dispatch_real(N, f);
   if (!have_saved && K > 1) w.stash = align256(size_t(K - 1) * size_t(batch) * N * elem_floats(flags) * 4);
-  w.off_dq = 0;
-  w.off_mq = w.dq;
+  w.off_mq = 0;
   w.off_partial = w.off_mq + w.mq;
   w.off_stash = w.off_partial + w.partial;
   w.total = w.off_stash + w.stash;
@@ -326,14 +341,6 @@ size_t fwd_ws(int32_t N, int32_t K, uint32_t flags) {
   if (!(flags & kFlagComplex))
     dispatch_real(N, [&]<class PL>() { b = mq_bytes<PL>(K); });
   return b;
-}
-
-template <class PL>
-int launch_real_dq(const float* D, float4* Dq, int K, const char* tab, hipStream_t s) {
-  const long long n = (long long)K * PL::NSL * PL::T;
-  hipLaunchKernelGGL(k_real_dq<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, D, Dq, K, tab);
-  const hipError_t e = hipGetLastError();
-  return e == hipSuccess ? ACDC_OK : hip_fail(e);
 }
 
 template <class PL>
@@ -423,7 +430,7 @@ extern "C" int acdc_forward(const float* x, float* y, const float* A, const floa
       float4* Mq = static_cast<float4*>(workspace);
       rc = launch_real_mq<PL>(D, Mq, K, tab, s);
       if (rc != ACDC_OK) return;
-      RealArgs a{x, y, A, nullptr, Mq, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
+      RealArgs a{x, y, A, Mq, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
       rc = launch_real_fwd<PL>(a, s);
     });
   }
@@ -479,11 +486,12 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
           return;
         }
       }
-      const long long n = (long long)K * PL::N;
+      const long long n = (long long)K * partial_entries4<PL>();
       hipError_t e;
       {
         ProfScope prof(2, s);
-        hipLaunchKernelGGL(k_cplx_reduce<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, partial, tiles, K,
+        hipLaunchKernelGGL(k_cplx_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(256), 0, s,
+                           partial, tiles, K,
                          grad_A, grad_D);
         e = hipGetLastError();
       }
@@ -494,18 +502,15 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
       using L = Launch<PL>;
       const long long tiles = bwd_tiles<PL>(batch);
       if (batch > 0) {
-        float4* Dq = reinterpret_cast<float4*>(ws + w.off_dq);
-        rc = launch_real_dq<PL>(D, Dq, K, tab, s);
+        float4* Mq = reinterpret_cast<float4*>(ws + w.off_mq);
+        rc = launch_real_mq<PL>(D, Mq, K, tab, s);
         if (rc != ACDC_OK) return;
         if (!have_saved) {
-          float4* Mq = reinterpret_cast<float4*>(ws + w.off_mq);
-          rc = launch_real_mq<PL>(D, Mq, K, tab, s);
-          if (rc != ACDC_OK) return;
-          RealArgs f{x, nullptr, A, nullptr, Mq, perm, stash, nullptr, nullptr, nullptr, tab, batch, K, flags};
+          RealArgs f{x, nullptr, A, Mq, perm, stash, nullptr, nullptr, nullptr, tab, batch, K, flags};
           rc = launch_real_fwd<PL>(f, s);
           if (rc != ACDC_OK) return;
         }
-        RealArgs a{x, nullptr, A, Dq, nullptr, perm, stash, grad_y, grad_x, partial, tab, batch, K, flags};
+        RealArgs a{x, nullptr, A, Mq, perm, stash, grad_y, grad_x, partial, tab, batch, K, flags};
         hipError_t e;
         {
           ProfScope prof(1, s);
@@ -517,11 +522,12 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
           return;
         }
       }
-      const long long n = (long long)K * (PL::N + PL::QF) / 4;
+      const long long n = (long long)K * partial_entries4<PL>();
       hipError_t e;
       {
         ProfScope prof(2, s);
-        hipLaunchKernelGGL(k_real_reduce<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, partial, tiles, K,
+        hipLaunchKernelGGL(k_real_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(256), 0, s,
+                           partial, tiles, K,
                          grad_A, grad_D, tab);
         e = hipGetLastError();
       }

@@ -191,40 +191,23 @@ struct RealOps {
   }
 
   // ------------------------------------------------------ Makhoul quartets
-  // One quartet: from Z[k], Z[M-k] produce the DCT-II outputs
-  // X[k], X[N-k], X[M-k], X[M+k] (orthonormal scaling folded into qa, qb).
-  __host__ __device__ __forceinline__ static void post_one(float2 zk, float2 zm, float4 m0, float4 m1,
-                                                           float (&X)[4]) {
-    const float2 w = make_float2(m0.x, m0.y), qa = make_float2(m0.z, m0.w);
-    const float2 qb = make_float2(m1.x, m1.y);
-    const float2 E = make_float2(zk.x + zm.x, zk.y - zm.y);  // Z[k] + conj Z[M-k]
-    const float2 Od = make_float2(zk.y + zm.y, zm.x - zk.x); // (Z[k] - conj Z[M-k]) / i
-    const float2 wO = cmul(Od, w);
-    const float2 u1 = cmul(cadd(E, wO), qa);
-    const float2 u2 = cmul(csub(E, wO), qb);
-    X[0] = u1.x;
-    X[1] = -u1.y;
-    X[2] = u2.x - u2.y;
-    X[3] = u2.x + u2.y;
-  }
-  // Inverse of post_one for the DCT-III (with the 1/M of the inverse FFT
-  // folded into qap and conj(qb)).
-  __host__ __device__ __forceinline__ static void pre_one(const float (&Y)[4], float2 w, float2 qb, float2 qap,
-                                                          float2& zk, float2& zm) {
-    const float2 Ap = cmul(make_float2(Y[0], -Y[1]), qap);
-    const float2 Bp = cmulc(make_float2(Y[2] + Y[3], Y[3] - Y[2]), qb);
-    const float2 S = cadd(Ap, Bp), Dd = csub(Ap, Bp);
-    const float2 cw = cmulc(Dd, w);                 // conj(w) * Dd
-    const float2 tt = make_float2(-cw.y, cw.x);     // i * conj(w) * Dd
-    zk = cadd(S, tt);
-    zm = make_float2(S.x - tt.x, tt.y - S.y);       // conj(S - tt)
-  }
+  // A quartet slot holds a spectrum pair Z[k], Z[M-k] of the packed row.
+  // The DCT-II outputs of the quartet are (Makhoul's quarter-wave
+  // post-twiddle, with the real-FFT split s1, s2 of `split` below)
+  //   u1 = qa s1:  X[k] = Re u1,  X[N-k] = -Im u1
+  //   u2 = qb s2:  X[M-k] = Re u2 - Im u2,  X[M+k] = Re u2 + Im u2
+  // with qa, qb = W_4N^k times the orthonormal scales.  The DCT-III
+  // pre-twiddle is the inverse map, with the 1/M of the inverse FFT folded
+  // into its twiddles: Ap = (Y0 - i Y1) qap, Bp = (Y2 + Y3 + i (Y3 - Y2))
+  // conj(qb'), S = Ap + Bp, Dd = Ap - Bp, Z'[k] = S + i conj(w) Dd,
+  // Z'[M-k] = conj(S - i conj(w) Dd).  real_mq_entry folds post-twiddle, D
+  // and pre-twiddle into the two symmetric 2x2 maps that sym_back applies.
 
   // Thread 0's first butterfly pair is (0, NB/2): both are self-negating,
   // so its partners are not at the generic register positions.  Permuting
   // those 2*RL registers by pi (new[rho] = old[pi(rho)]) puts every Makhoul
   // pair at (i, 2*RL-1-i); slot 0 then holds the two self-paired values
-  // (Z[0], Z[M/2]), handled by special twiddles.
+  // (Z[0], Z[M/2]), handled by its own table entries.
   __host__ __device__ static constexpr int perm_pi(int rho) {
     return rho < RL / 2       ? rho
            : rho < RL         ? RL + rho - RL / 2
@@ -252,93 +235,73 @@ struct RealOps {
 #pragma unroll
     for (int o = 0; o < 2 * RL; ++o) v[o] = nv[o];
   }
-  // The DCT-III pre-twiddle of thread 0's slot 0 needs its own qb:
+  // The DCT-III pre-twiddle of thread 0's slot 0 needs its own qb':
   // exp(i pi/8) / (2 sqrt(N)).
   static constexpr float kQbRe = float(0.9238795325112867561 / (2.0 * csqrt(double(N))));
   static constexpr float kQbIm = float(0.3826834323650897717 / (2.0 * csqrt(double(N))));
-  __host__ __device__ __forceinline__ static float2 pre_qb(float4 m1, int q, int i, bool sp) {
-    const float2 qb = make_float2(m1.x, m1.y);
-    if (q == 0 && i == 0) return sel2(sp, make_float2(kQbRe, kQbIm), qb);
-    return qb;
-  }
 
-  // Makhoul twiddles (m0, m1) and the quartet-layout diagonal d of every
-  // slot.  Loops over the slots load slot s + PF while slot s computes; the
-  // first PF slots are loaded ahead, in the tail of the preceding FFT.
-  static constexpr int PF = NSL < ACDC_TAB_PF ? NSL : ACDC_TAB_PF;
-  struct SlotTabs {
-    float4 m0[NSL], m1[NSL], d[NSL];
-  };
-  __host__ __device__ __forceinline__ static void load_slot(SlotTabs& tb, int slot, unsigned t, GView tab,
-                                                            GView dq) {
-    const unsigned t16 = t * 16u;
-    tb.m0[slot] = tab.ld4(t16, unsigned(PL::OFF_MK0 + slot * T * 16));
-    tb.m1[slot] = tab.ld4(t16, unsigned(PL::OFF_MK1 + slot * T * 16));
-    tb.d[slot] = dq.ld4(t16, unsigned(slot * T * 16));
-  }
-  __host__ __device__ __forceinline__ static void load_head(SlotTabs& tb, unsigned t, GView tab, GView dq) {
-#pragma unroll
-    for (int s = 0; s < PF; ++s) load_slot(tb, s, t, tab, dq);
-  }
-
-  // Forward middle of a layer, in place per quartet slot: Z (frequency
-  // layout) -> DCT-II quartet -> * d -> DCT-III pre-twiddle -> Z'.
-  __host__ __device__ __forceinline__ static void mid(float2 (&v)[P], unsigned t, GView tab, GView dq,
-                                                      SlotTabs& tb) {
-    const bool sp = (t == 0);
-    permute0(v, sp);
-#pragma unroll
-    for (int q = 0; q < BL / 2; ++q)
-#pragma unroll
-      for (int i = 0; i < RL; ++i) {
-        const int slot = q * RL + i;
-        if (slot + PF < NSL) load_slot(tb, slot + PF, t, tab, dq);
-        ACDC_SCHED_FENCE();
-        const float4 m0 = tb.m0[slot], m1 = tb.m1[slot], d = tb.d[slot];
-        float2& zk = v[2 * q * RL + i];
-        float2& zm = v[2 * q * RL + 2 * RL - 1 - i];
-        float X[4];
-        post_one(zk, zm, m0, m1, X);
-        X[0] *= d.x;
-        X[1] *= d.y;
-        X[2] *= d.z;
-        X[3] *= d.w;
-        pre_one(X, make_float2(m0.x, m0.y), pre_qb(m1, q, i, sp), make_float2(m1.z, m1.w), zk, zm);
-      }
-    unpermute0(v, sp);
-  }
-
-  // Forward middle with the per-layer quartet coefficients of
-  // real_mq_entry (32 operations per slot instead of post_one, * d,
-  // pre_one).  Layout of one layer: [slot][2][T] float4, lane-contiguous;
-  // slot s + PFM loads while slot s computes.
+  // Per-layer quartet coefficients (real_mq_entry), layout of one layer
+  // [slot][3][T] float4, lane-contiguous:
+  //   c0 = (L1_00, L1_01, L1_11, L2_00), c1 = (L2_01, L2_11, w.x, w.y),
+  //   c2 = (qa.x, qa.y, qb.x, qb.y)   (backward only)
+  // Loops over the slots load slot s + PFM while slot s computes; the first
+  // PFM slots are loaded ahead, in the tail of the preceding FFT.
   static constexpr int PFM = NSL < ACDC_MQ_PF ? NSL : ACDC_MQ_PF;
+  template <int NR>
   struct MqTabs {
-    float4 m[NSL][2];
+    float4 m[NSL][NR];
   };
-  __host__ __device__ __forceinline__ static void load_mslot(MqTabs& tb, int slot, unsigned t, GView mq) {
+  template <int NR>
+  __host__ __device__ __forceinline__ static void load_mslot(MqTabs<NR>& tb, int slot, unsigned t, GView mq) {
 #pragma unroll
-    for (int r = 0; r < 2; ++r) tb.m[slot][r] = mq.ld4(t * 16u, unsigned((slot * 2 + r) * T * 16));
+    for (int r = 0; r < NR; ++r) tb.m[slot][r] = mq.ld4(t * 16u, unsigned((slot * 3 + r) * T * 16));
   }
-  __host__ __device__ __forceinline__ static void load_mhead(MqTabs& tb, unsigned t, GView mq) {
+  template <int NR>
+  __host__ __device__ __forceinline__ static void load_mhead(MqTabs<NR>& tb, unsigned t, GView mq) {
 #pragma unroll
     for (int s = 0; s < PFM; ++s) load_mslot(tb, s, t, mq);
   }
-  __host__ __device__ __forceinline__ static void mid_one(float2& zk, float2& zm, float4 c0, float4 c1) {
-    const float2 w = make_float2(c1.z, c1.w);
-    const float2 E = make_float2(zk.x + zm.x, zk.y - zm.y);   // Z[k] + conj Z[M-k]
-    const float2 Od = make_float2(zk.y + zm.y, zm.x - zk.x);  // (Z[k] - conj Z[M-k]) / i
+
+  // Real-FFT split of a Makhoul pair: E = Z[k] + conj Z[M-k],
+  // O = (Z[k] - conj Z[M-k]) / i, s1 = E + w O, s2 = E - w O.
+  struct Split {
+    float2 s1, s2;
+  };
+  __host__ __device__ __forceinline__ static Split split(float2 zk, float2 zm, float2 w) {
+    const float2 E = make_float2(zk.x + zm.x, zk.y - zm.y);
+    const float2 Od = make_float2(zk.y + zm.y, zm.x - zk.x);
     const float2 wO = cmul(Od, w);
-    const float2 s1 = cadd(E, wO), s2 = csub(E, wO);
-    // symmetric 2x2 maps: L1 = [[c0.x, c0.y], [c0.y, c0.z]], L2 = [[c0.w, c1.x], [c1.x, c1.y]]
+    return Split{cadd(E, wO), csub(E, wO)};
+  }
+  // DCT-II outputs X[k], X[N-k], X[M-k], X[M+k] of a split (the
+  // orthonormal scaling is folded into qa, qb).
+  __host__ __device__ __forceinline__ static void post_x(const Split& sp, float2 qa, float2 qb, float (&X)[4]) {
+    const float2 u1 = cmul(sp.s1, qa), u2 = cmul(sp.s2, qb);
+    X[0] = u1.x;
+    X[1] = -u1.y;
+    X[2] = u2.x - u2.y;
+    X[3] = u2.x + u2.y;
+  }
+  // From a split, the D diagonal and the DCT-III pre-twiddle as the two
+  // symmetric 2x2 maps L1 (on s1) and L2 (on s2), then the inverse split:
+  // S = L1 s1 + L2 s2, Dd = L1 s1 - L2 s2, zk = S + i conj(w) Dd,
+  // zm = conj(S - i conj(w) Dd).
+  __host__ __device__ __forceinline__ static void sym_back(const Split& sp, float4 c0, float4 c1, float2& zk,
+                                                           float2& zm) {
+    const float2 w = make_float2(c1.z, c1.w);
+    const float2 s1 = sp.s1, s2 = sp.s2;
     const float2 p1 = make_float2(__builtin_fmaf(c0.y, s1.y, c0.x * s1.x), __builtin_fmaf(c0.z, s1.y, c0.y * s1.x));
     const float2 p2 = make_float2(__builtin_fmaf(c1.x, s2.y, c0.w * s2.x), __builtin_fmaf(c1.y, s2.y, c1.x * s2.x));
     const float2 S = cadd(p1, p2), Dd = csub(p1, p2);
-    const float2 cw = cmulc(Dd, w);  // conj(w) * Dd; tt = i * cw
+    const float2 cw = cmulc(Dd, w);
     zk = make_float2(S.x - cw.y, S.y + cw.x);
     zm = make_float2(S.x + cw.y, cw.x - S.y);
   }
-  __host__ __device__ __forceinline__ static void mid_mq(float2 (&v)[P], unsigned t, GView mq, MqTabs& tb) {
+
+  // Forward middle of a layer, in place per quartet slot: Z (frequency
+  // layout) -> DCT-II quartet -> * d -> DCT-III pre-twiddle -> Z', as
+  // split + sym_back (32 operations per slot).
+  __host__ __device__ __forceinline__ static void mid(float2 (&v)[P], unsigned t, GView mq, MqTabs<2>& tb) {
     const bool sp = (t == 0);
     permute0(v, sp);
 #pragma unroll
@@ -348,7 +311,10 @@ struct RealOps {
         const int slot = q * RL + i;
         if (slot + PFM < NSL) load_mslot(tb, slot + PFM, t, mq);
         ACDC_SCHED_FENCE();
-        mid_one(v[2 * q * RL + i], v[2 * q * RL + 2 * RL - 1 - i], tb.m[slot][0], tb.m[slot][1]);
+        float2& zk = v[2 * q * RL + i];
+        float2& zm = v[2 * q * RL + 2 * RL - 1 - i];
+        const float4 c0 = tb.m[slot][0], c1 = tb.m[slot][1];
+        sym_back(split(zk, zm, make_float2(c1.z, c1.w)), c0, c1, zk, zm);
       }
     unpermute0(v, sp);
   }
@@ -356,9 +322,10 @@ struct RealOps {
   // Backward middle of a layer.  From H-side spectrum v (of u*a) and the
   // upstream spectrum g, per slot: H = DCT-II(v), G = DCT-II(g); the image
   // H*G (the dL/dd term of this row, quartet layout) goes to the slab; then
-  // g <- DCT-III pre-twiddle of G*d.  v is consumed.
-  __host__ __device__ __forceinline__ static void mid_bwd(float2 (&v)[P], float2 (&g)[P], unsigned t, GView tab,
-                                                          GView dq, SlotTabs& tb, float* slab) {
+  // g <- DCT-III pre-twiddle of G*d, from g's split (sym_back).  v is
+  // consumed.
+  __host__ __device__ __forceinline__ static void mid_bwd(float2 (&v)[P], float2 (&g)[P], unsigned t, GView mq,
+                                                          MqTabs<3>& tb, float* slab) {
     const bool sp = (t == 0);
     permute0(v, sp);
     permute0(g, sp);
@@ -367,21 +334,19 @@ struct RealOps {
 #pragma unroll
       for (int i = 0; i < RL; ++i) {
         const int slot = q * RL + i;
-        if (slot + PF < NSL) load_slot(tb, slot + PF, t, tab, dq);
+        if (slot + PFM < NSL) load_mslot(tb, slot + PFM, t, mq);
         ACDC_SCHED_FENCE();
-        const float4 m0 = tb.m0[slot], m1 = tb.m1[slot], d = tb.d[slot];
+        const float4 c0 = tb.m[slot][0], c1 = tb.m[slot][1], c2 = tb.m[slot][2];
+        const float2 w = make_float2(c1.z, c1.w), qa = make_float2(c2.x, c2.y), qb = make_float2(c2.z, c2.w);
         float2& gk = g[2 * q * RL + i];
         float2& gm = g[2 * q * RL + 2 * RL - 1 - i];
         float H[4], G[4];
-        post_one(v[2 * q * RL + i], v[2 * q * RL + 2 * RL - 1 - i], m0, m1, H);
-        post_one(gk, gm, m0, m1, G);
+        post_x(split(v[2 * q * RL + i], v[2 * q * RL + 2 * RL - 1 - i], w), qa, qb, H);
+        const Split sg = split(gk, gm, w);
+        post_x(sg, qa, qb, G);
         reinterpret_cast<float4*>(slab)[slot * T + t] =
             make_float4(H[0] * G[0], H[1] * G[1], H[2] * G[2], H[3] * G[3]);
-        G[0] *= d.x;
-        G[1] *= d.y;
-        G[2] *= d.z;
-        G[3] *= d.w;
-        pre_one(G, make_float2(m0.x, m0.y), pre_qb(m1, q, i, sp), make_float2(m1.z, m1.w), gk, gm);
+        sym_back(sg, c0, c1, gk, gm);
       }
     unpermute0(g, sp);
   }
@@ -394,8 +359,7 @@ struct RealArgs {
   const float* x;
   float* y;            // forward output (may be null: stash-only forward)
   const float* A;
-  const float4* Dq;    // [K][NSL*T] d in quartet layout (backward)
-  const float4* Mq;    // [K][NSL][2][T] forward quartet coefficients
+  const float4* Mq;    // [K][NSL][3][T] quartet coefficients (real_mq_entry)
   const int* perm;     // [K][N] (PERM only)
   float* saved;        // [K-1][batch][N] layer inputs u_1..u_{K-1} (may be null)
   const float* gy;     // backward: upstream gradient
@@ -425,7 +389,7 @@ __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned 
   O::load(GView::of(a.x + row0 * N), roff, v, L, valid);
   for (int k = 0; k < a.K; ++k) {
     const GView ak = GView::of(a.A + (long long)k * N);
-    const GView mq = GView::of(a.Mq + (long long)k * NSL * 2 * T);
+    const GView mq = GView::of(a.Mq + (long long)k * NSL * 3 * T);
     if (permute) {
       O::load_idx(idx, GView::of(a.perm + (long long)k * N), L);
       O::gather(ctx, v, L, slab, idx, [&] { O::load_vec(av, ak, L); });
@@ -435,9 +399,9 @@ __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned 
     if (a.saved != nullptr && k > 0 && valid)
       O::store(GView::of(a.saved + ((long long)(k - 1) * a.batch + row0) * N), roff, v, L);
     O::scale(v, av);
-    typename O::MqTabs tb;
+    typename O::template MqTabs<2> tb;
     O::template fft<false>(ctx, v, t, slab2, tab, [&] { O::load_mhead(tb, t, mq); });
-    O::mid_mq(v, t, mq, tb);
+    O::mid(v, t, mq, tb);
     O::template fft<true>(ctx, v, t, slab2, tab, [] {});
     if ((a.flags & kFlagRelu) && k < a.K - 1) O::relu(v);
   }
@@ -469,7 +433,7 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
   O::load_raw(uv, u_view(a.K - 1), roff, L, valid);
   for (int k = a.K - 1; k >= 0; --k) {
     const GView ak = GView::of(a.A + (long long)k * N);
-    const GView dq = GView::of(a.Dq + (long long)k * NSL * T);
+    const GView mq = GView::of(a.Mq + (long long)k * NSL * 3 * T);
     float* part = a.partial + (tile * a.K + k) * PS;
     // h2 = DCT(u * a), gh3 = DCT(g); dL/dd image h2 * gh3; g <- pre(gh3 * d)
     {
@@ -477,11 +441,11 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
       O::load_vec(av, ak, L);
       O::unpack(uv, v, valid);
       O::scale(v, av);
-      typename O::SlotTabs tb;
+      typename O::template MqTabs<3> tb;
       O::template fft<false>(ctx, v, t, slab2, tab, [] {});
-      O::template fft<false>(ctx, g, t, slab2, tab, [&] { O::load_head(tb, t, tab, dq); });
+      O::template fft<false>(ctx, g, t, slab2, tab, [&] { O::load_mhead(tb, t, mq); });
       ctx.sync_row();
-      O::mid_bwd(v, g, t, tab, dq, tb, slab);
+      O::mid_bwd(v, g, t, mq, tb, slab);
     }
     ctx.sync_all();
     sum_rows<ROWS, PL::SLAB, THREADS, QF>(lds, GView::of(part + N), tid);

@@ -126,21 +126,24 @@ __host__ __device__ __forceinline__ float4 real_dq_entry(const float* Dk, const 
                      (m & 8) ? Dk[idx.w] : 0.f);
 }
 
-// Forward quartet operator of layer k at slot entry e = slot*T + t.
+// Quartet coefficients of layer k at slot entry e = slot*T + t.
 //
-// The middle of a forward layer takes one quartet's spectrum pair
-// (Z[k], Z[M-k]) through the DCT-II post-twiddle, the D diagonal and the
-// DCT-III pre-twiddle (RealOps::post_one / pre_one).  Writing
+// The middle of a layer takes one quartet's spectrum pair (Z[k], Z[M-k])
+// through the DCT-II post-twiddle, the D diagonal and the DCT-III
+// pre-twiddle (the steps listed in RealOps' Makhoul-quartet comment).  With
+// the real-FFT split
 //   E = Z[k] + conj Z[M-k],  O = (Z[k] - conj Z[M-k]) / i,
-//   s1 = E + w O,  s2 = E - w O          (w = W_N^k, the real-FFT split)
+//   s1 = E + w O,  s2 = E - w O          (w = W_N^k)
 // the post-twiddle, the four d values and the pre-twiddle act on s1 and s2
 // separately, each as a 2x2 real matrix:
-//   s1 -> qap * diag(d0, d1) * (qa s1)          (X[k], X[N-k] pair)
-//   s2 -> conj(qb') * H^T diag(d2, d3) H * (qb s2)   (X[M-k], X[M+k] pair)
-// with H = [[1,-1],[1,1]].  Both matrices are symmetric because qap and
-// qb' point along conj(qa) and qb (also for thread 0's self-paired slot),
-// so a slot needs w and 3 + 3 coefficients:
-//   out[0] = (L1_00, L1_01, L1_11, L2_00),  out[1] = (L2_01, L2_11, w.x, w.y).
+//   s1 -> qap * diag(d0, d1) * (qa s1)                (X[k], X[N-k] pair)
+//   s2 -> conj(qb') * H^T diag(d2, d3) H * (qb s2)    (X[M-k], X[M+k] pair)
+// with H = [[1,-1],[1,1]].  Both matrices are symmetric because qap and qb'
+// point along conj(qa) and qb (also for thread 0's self-paired slot), so a
+// slot needs w and 3 + 3 coefficients.  Output rows:
+//   out[0] = (L1_00, L1_01, L1_11, L2_00)
+//   out[1] = (L2_01, L2_11, w.x, w.y)
+//   out[2] = (qa.x, qa.y, qb.x, qb.y)   (the DCT-II outputs the backward needs)
 // Coefficients are formed in double from the fp32 twiddle tables and
 // rounded once.
 struct QuartetD {
@@ -153,13 +156,13 @@ __host__ __device__ inline QuartetD qd_mulc(QuartetD a, QuartetD w) {  // a * co
   return QuartetD{a.x * w.x + a.y * w.y, a.y * w.x - a.x * w.y};
 }
 template <class PL>
-__host__ __device__ inline void real_mq_entry(const float* Dk, const char* tab, int e, float4 (&out)[2]) {
+__host__ __device__ inline void real_mq_entry(const float* Dk, const char* tab, int e, float4 (&out)[3]) {
   const float4 m0 = reinterpret_cast<const float4*>(tab + PL::OFF_MK0)[e];
   const float4 m1 = reinterpret_cast<const float4*>(tab + PL::OFF_MK1)[e];
   const float4 d = real_dq_entry<PL>(Dk, tab, e);
   const QuartetD qa{m0.z, m0.w}, qb{m1.x, m1.y}, qap{m1.z, m1.w};
   // thread 0's slot 0 carries the self-paired values; its pre-twiddle uses
-  // exp(i pi/8) / (2 sqrt(N)) (RealOps::pre_qb)
+  // exp(i pi/8) / (2 sqrt(N))
   const QuartetD qbp = e == 0 ? QuartetD{RealOps<PL>::kQbRe, RealOps<PL>::kQbIm} : qb;
   double L1[2][2], L2[2][2];
   for (int j = 0; j < 2; ++j) {
@@ -179,41 +182,50 @@ __host__ __device__ inline void real_mq_entry(const float* Dk, const char* tab, 
   }
   out[0] = make_float4(float(L1[0][0]), float(0.5 * (L1[0][1] + L1[1][0])), float(L1[1][1]), float(L2[0][0]));
   out[1] = make_float4(float(0.5 * (L2[0][1] + L2[1][0])), float(L2[1][1]), m0.x, m0.y);
+  out[2] = make_float4(m0.z, m0.w, m1.x, m1.y);
 }
 
-// Fixed-order sum over tiles of partial float4 e4 (stride in float4s):
-// blocks of 32 tiles are summed in tile order, then the block sums in order.
-__host__ __device__ __forceinline__ float4 tile_sum4(const float4* partial, long long ntiles, long long stride,
-                                                     long long off) {
-  float4 total = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (long long t0 = 0; t0 < ntiles; t0 += 32) {
-    const long long t1 = (t0 + 32 < ntiles) ? t0 + 32 : ntiles;
-    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 8
-    for (long long t = t0; t < t1; ++t) {
-      const float4 u = partial[t * stride + off];
-      s.x += u.x;
-      s.y += u.y;
-      s.z += u.z;
-      s.w += u.w;
-    }
-    total.x += s.x;
-    total.y += s.y;
-    total.z += s.z;
-    total.w += s.w;
+// Fixed-order batch reduction of the per-tile partials.  Entry e (a float4)
+// of the reduced gradient is the sum over tiles t of partial[t][e]; tiles
+// are split into kRedPhases phases (t mod kRedPhases), each phase is summed
+// in increasing t, and the phase sums are added in phase order.  The GPU
+// kernel runs the phases on separate threads and combines them in LDS; the
+// CPU emulation calls the same functions in the same order.
+constexpr int kRedPhases = 4;
+
+__host__ __device__ __forceinline__ float4 add4(float4 a, float4 b) {
+  return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+
+__host__ __device__ __forceinline__ float4 tile_phase_sum4(const float4* partial, long long ntiles,
+                                                           long long stride, long long e, int phase) {
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  long long t = phase;
+  // loads in groups of 8 ahead of their (in-order) adds
+  for (; t + 7 * kRedPhases < ntiles; t += 8 * kRedPhases) {
+    float4 u[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) u[j] = partial[(t + j * kRedPhases) * stride + e];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s = add4(s, u[j]);
   }
-  return total;
+  for (; t < ntiles; t += kRedPhases) s = add4(s, partial[t * stride + e]);
+  return s;
+}
+
+__host__ __device__ __forceinline__ float4 phases_total4(const float4 (&ph)[kRedPhases]) {
+  float4 s = ph[0];
+#pragma unroll
+  for (int g = 1; g < kRedPhases; ++g) s = add4(s, ph[g]);
+  return s;
 }
 
 // Real path: float4 e4 in [0, (N + QF)/4) of layer k of the reduced
 // gradient.  The first N/4 are dL/da in natural order; the rest are the
 // dL/dd quartets of slot entries e = e4 - N/4, scattered to their indices.
 template <class PL>
-__host__ __device__ __forceinline__ void real_reduce_entry4(const float* partial, long long ntiles, int K, int k,
-                                                            int e4, float* gA, float* gD, const char* tab) {
-  constexpr long long PS4 = (PL::N + PL::QF) / 4;
-  const float4 s = tile_sum4(reinterpret_cast<const float4*>(partial), ntiles, (long long)K * PS4,
-                             (long long)k * PS4 + e4);
+__host__ __device__ __forceinline__ void real_reduce_store4(float4 s, int k, int e4, float* gA, float* gD,
+                                                            const char* tab) {
   if (e4 < PL::N / 4) {
     reinterpret_cast<float4*>(gA + (long long)k * PL::N)[e4] = s;
   } else {
@@ -230,13 +242,16 @@ __host__ __device__ __forceinline__ void real_reduce_entry4(const float* partial
 
 // Complex path: float4 e4 in [0, N) of layer k (dL/da then dL/dd, natural).
 template <class PL>
-__host__ __device__ __forceinline__ void cplx_reduce_entry4(const float* partial, long long ntiles, int K, int k,
-                                                            int e4, float* gA, float* gD) {
-  constexpr long long PS4 = PL::N;  // 4N floats per layer
-  const float4 s = tile_sum4(reinterpret_cast<const float4*>(partial), ntiles, (long long)K * PS4,
-                             (long long)k * PS4 + e4);
+__host__ __device__ __forceinline__ void cplx_reduce_store4(float4 s, int k, int e4, float* gA, float* gD) {
   if (e4 < PL::N / 2) reinterpret_cast<float4*>(gA + (long long)k * 2 * PL::N)[e4] = s;
   else reinterpret_cast<float4*>(gD + (long long)k * 2 * PL::N)[e4 - PL::N / 2] = s;
+}
+
+// Float4 entries per layer of one tile's partial.
+template <class PL>
+constexpr long long partial_entries4() {
+  if constexpr (PL::kComplex) return (long long)PL::N;
+  else return (long long)(PL::N + PL::QF) / 4;
 }
 
 }  // namespace acdc

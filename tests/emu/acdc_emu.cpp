@@ -35,21 +35,42 @@ void run_wg(int threads, F&& body) {
   for (auto& x : th) x.join();
 }
 
+// The batch reduction in the GPU kernel's order: per entry, the phase sums
+// in phase order.
+template <class PL, class Store>
+void reduce_all(const float* partial, long long ntiles, int K, Store&& store) {
+  constexpr long long PS4 = partial_entries4<PL>();
+  const long long n = (long long)K * PS4;
+  for (long long i = 0; i < n; ++i) {
+    float4 ph[kRedPhases];
+    for (int g = 0; g < kRedPhases; ++g)
+      ph[g] = tile_phase_sum4(reinterpret_cast<const float4*>(partial), ntiles, n, i, g);
+    store(phases_total4(ph), int(i / PS4), int(i % PS4));
+  }
+}
+
+// Per-layer quartet coefficients in the kernel's [k][slot][3][T] layout.
+template <class PL>
+std::vector<float4> quartet_coefficients(const float* D, int K, const std::vector<unsigned char>& tab) {
+  constexpr int E = PL::NSL * PL::T;
+  std::vector<float4> mq((size_t)K * E * 3);
+  for (int k = 0; k < K; ++k)
+    for (int e = 0; e < E; ++e) {
+      float4 row[3];
+      real_mq_entry<PL>(D + (size_t)k * PL::N, (const char*)tab.data(), e, row);
+      const int slot = e / PL::T, t = e % PL::T;
+      for (int r = 0; r < 3; ++r) mq[(size_t)k * E * 3 + (size_t)(slot * 3 + r) * PL::T + t] = row[r];
+    }
+  return mq;
+}
+
 template <class PL>
 void real_fwd(const float* x, float* y, const float* A, const float* D, const int* perm, long long batch,
               int K, unsigned flags, float* saved, const std::vector<unsigned char>& tab) {
   using L = Launch<PL>;
   constexpr int E = PL::NSL * PL::T;
-  std::vector<float4> mq((size_t)K * E * 2);
-  for (int k = 0; k < K; ++k)
-    for (int e = 0; e < E; ++e) {
-      float4 row[2];
-      real_mq_entry<PL>(D + (size_t)k * PL::N, (const char*)tab.data(), e, row);
-      const int slot = e / PL::T, t = e % PL::T;
-      for (int r = 0; r < 2; ++r) mq[(size_t)k * E * 2 + (size_t)(slot * 2 + r) * PL::T + t] = row[r];
-    }
-  RealArgs a{x, y, A, nullptr, mq.data(), perm, saved, nullptr, nullptr, nullptr, (const char*)tab.data(), batch,
-             K, flags};
+  const std::vector<float4> mq = quartet_coefficients<PL>(D, K, tab);
+  RealArgs a{x, y, A, mq.data(), perm, saved, nullptr, nullptr, nullptr, (const char*)tab.data(), batch, K, flags};
   const long long nwg = (batch + L::FWD_ROWS - 1) / L::FWD_ROWS;
   std::vector<float> lds((size_t)L::FWD_ROWS * L::FWD_SLAB);
   for (long long wg = 0; wg < nwg; ++wg)
@@ -71,15 +92,11 @@ void real_bwd(const float* x, const float* gy, const float* A, const float* D, c
     real_fwd<PL>(x, nullptr, A, D, perm, batch, K, flags, saved_buf.data(), tab);
     saved = saved_buf.data();
   }
-  std::vector<float4> dq((size_t)K * PL::NSL * PL::T);
-  for (int k = 0; k < K; ++k)
-    for (int e = 0; e < PL::NSL * PL::T; ++e)
-      dq[(size_t)k * PL::NSL * PL::T + e] =
-          real_dq_entry<PL>(D + (size_t)k * PL::N, (const char*)tab.data(), e);
+  const std::vector<float4> mq = quartet_coefficients<PL>(D, K, tab);
   const long long ntiles = (batch + L::BWD_ROWS - 1) / L::BWD_ROWS;
   const long long PS = PL::N + PL::QF;
   std::vector<float> partial((size_t)ntiles * K * PS);
-  RealArgs a{x, nullptr, A, dq.data(), nullptr, perm, const_cast<float*>(saved), gy, gx, partial.data(),
+  RealArgs a{x, nullptr, A, mq.data(), perm, const_cast<float*>(saved), gy, gx, partial.data(),
              (const char*)tab.data(), batch, K, flags};
   std::vector<float> lds((size_t)L::BWD_ROWS * L::BWD_SLAB);
   for (long long wg = 0; wg < ntiles; ++wg)
@@ -88,9 +105,9 @@ void real_bwd(const float* x, const float* gy, const float* A, const float* D, c
       real_backward_row<PL, L::BWD_ROWS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, lds.data(),
                                          lds.data() + (size_t)r * L::BWD_SLAB);
     });
-  for (int k = 0; k < K; ++k)
-    for (int e4 = 0; e4 < PS / 4; ++e4)
-      real_reduce_entry4<PL>(partial.data(), ntiles, K, k, e4, gA, gD, (const char*)tab.data());
+  reduce_all<PL>(partial.data(), ntiles, K, [&](float4 s, int k, int e4) {
+    real_reduce_store4<PL>(s, k, e4, gA, gD, (const char*)tab.data());
+  });
 }
 
 template <class PL>
@@ -131,8 +148,7 @@ void cplx_bwd(const float* x, const float* gy, const float* A, const float* D, c
       cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, lds.data(),
                                          lds.data() + (size_t)r * L::BWD_SLAB);
     });
-  for (int k = 0; k < K; ++k)
-    for (int e4 = 0; e4 < PL::N; ++e4) cplx_reduce_entry4<PL>(partial.data(), ntiles, K, k, e4, gA, gD);
+  reduce_all<PL>(partial.data(), ntiles, K, [&](float4 s, int k, int e4) { cplx_reduce_store4<PL>(s, k, e4, gA, gD); });
 }
 
 }  // namespace
