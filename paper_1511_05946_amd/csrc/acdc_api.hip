@@ -62,31 +62,73 @@ __global__ __launch_bounds__(256) void k_real_mq(const float* __restrict__ D, fl
   for (int r = 0; r < 3; ++r) out[r * PL::T] = row[r];
 }
 
+// Copy of the FFT twiddle table (the first TW_FLOAT2 float2 of the plan's
+// constant table) into LDS; the caller synchronises.
+template <class PL>
+__device__ __forceinline__ void copy_twiddles(float* dst, const char* tab, int tid, int nthreads) {
+  const float2* src = reinterpret_cast<const float2*>(tab);
+  float2* d2 = reinterpret_cast<float2*>(dst);
+  for (int i = tid; i < PL::TW_FLOAT2; i += nthreads) d2[i] = src[i];
+}
+
+// The forward kernel is persistent: workgroup b handles row groups (tiles)
+// b, b + gridDim.x, ...  Rows are independent, so results do not depend on
+// the grid size.
 template <class PL>
 __global__ __launch_bounds__(Launch<PL>::FWD_THREADS)
-__attribute__((amdgpu_waves_per_eu(Launch<PL>::FWD_WPE))) void k_real_fwd(RealArgs a) {
+__attribute__((amdgpu_waves_per_eu(Launch<PL>::FWD_WPE))) void k_real_fwd(RealArgs a, long long ntiles) {
   using L = Launch<PL>;
-  __shared__ float lds[L::FWD_ROWS * L::FWD_SLAB];
+  __shared__ float lds[L::FWD_LDS_FLOATS];
   DevCtx<PL::T> ctx;
   const int tid = threadIdx.x;
   const unsigned t = unsigned(tid) % PL::T;
   int r = tid / PL::T;
   if constexpr (PL::T >= 64) r = __builtin_amdgcn_readfirstlane(r);  // one row per whole wave
-  real_forward_row<PL>(ctx, a, t, (long long)blockIdx.x * L::FWD_ROWS, unsigned(r), lds + r * L::FWD_SLAB);
+  // LDS: [twiddle copy (TW_FLOATS)][row slabs]; the table sits at offset 0
+  // so that its loads address it through the instruction's immediate offset
+  float* const rows = lds + L::TW_FLOATS;
+  float* slab = rows + r * L::FWD_SLAB;
+  if constexpr (L::TW_LDS) {
+    float* twl = lds;
+    copy_twiddles<PL>(twl, a.tab, tid, L::FWD_THREADS);
+    ctx.sync_all();
+    const LdsView tw = LdsView::of(twl);
+    for (long long tile = blockIdx.x; tile < ntiles; tile += gridDim.x)
+      real_forward_row<PL>(ctx, a, t, tile * L::FWD_ROWS, unsigned(r), slab, tw);
+  } else {
+    const GView tw = GView::of(a.tab);
+    for (long long tile = blockIdx.x; tile < ntiles; tile += gridDim.x)
+      real_forward_row<PL>(ctx, a, t, tile * L::FWD_ROWS, unsigned(r), slab, tw);
+  }
 }
 
 template <class PL>
 __global__ __launch_bounds__(Launch<PL>::BWD_THREADS)
 __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealArgs a) {
   using L = Launch<PL>;
-  __shared__ float lds[L::BWD_ROWS * L::BWD_SLAB];
+  __shared__ float lds[L::BWD_LDS_FLOATS];
   DevCtx<PL::T> ctx;
   const int tid = threadIdx.x;
   const unsigned t = unsigned(tid) % PL::T;
   int r = tid / PL::T;
   if constexpr (PL::T >= 64) r = __builtin_amdgcn_readfirstlane(r);  // one row per whole wave
-  real_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS, unsigned(r), tid,
-                                     (long long)blockIdx.x, lds, lds + r * L::BWD_SLAB);
+  // LDS: [twiddle copy (TW_FLOATS)][row slabs]; the table sits at offset 0
+  // so that its loads address it through the instruction's immediate offset
+  float* const rows = lds + L::BWD_TW_FLOATS;
+  float* slab = rows + r * L::BWD_SLAB;
+  // one tile per workgroup (a loop over tiles here would keep its
+  // invariants live across the whole layer loop)
+  const long long tile = blockIdx.x;
+  if constexpr (L::BWD_TW_LDS) {
+    float* twl = lds;
+    copy_twiddles<PL>(twl, a.tab, tid, L::BWD_THREADS);
+    ctx.sync_all();
+    real_backward_row<PL, L::BWD_ROWS>(ctx, a, t, tile * L::BWD_ROWS, unsigned(r), tid, tile, rows, slab,
+                                       LdsView::of(twl));
+  } else {
+    real_backward_row<PL, L::BWD_ROWS>(ctx, a, t, tile * L::BWD_ROWS, unsigned(r), tid, tile, rows, slab,
+                                       GView::of(a.tab));
+  }
 }
 
 // Batch reduction: a block owns kRedEntries float4 entries of the reduced
@@ -266,6 +308,30 @@ int get_table(int N, bool cplx, const char** out) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Workgroups of `kernel` (with `threads` threads) that fit on the current
+// device at once; the persistent kernels launch min(tiles, this).
+std::map<std::pair<const void*, int>, long long> g_resident;
+long long resident_workgroups(const void* kernel, int threads) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::lock_guard<std::mutex> lock(g_mu);
+  auto key = std::make_pair(kernel, dev);
+  auto it = g_resident.find(key);
+  if (it != g_resident.end()) return it->second;
+  int per_cu = 0, cus = 0;
+  long long n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) == hipSuccess &&
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+    n = (long long)per_cu * cus;
+  g_resident[key] = n;
+  return n;
+}
+
+long long persistent_grid(const void* kernel, int threads, long long tiles) {
+  const long long n = resident_workgroups(kernel, threads);
+  return (n > 0 && n < tiles) ? n : tiles;
+}
+
 int check_common(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
   if (flags & ~7u) return ACDC_ERR_INVALID_ARG;
   if ((flags & kFlagComplex) && (flags & kFlagRelu)) return ACDC_ERR_UNSUPPORTED;
@@ -353,9 +419,11 @@ int launch_real_mq(const float* D, float4* Mq, int K, const char* tab, hipStream
 
 template <class PL>
 int launch_real_fwd(const RealArgs& a, hipStream_t s) {
+  const long long tiles = fwd_blocks<PL>(a.batch);
+  const long long grid = persistent_grid(reinterpret_cast<const void*>(&k_real_fwd<PL>), Launch<PL>::FWD_THREADS,
+                                         tiles);
   ProfScope prof(0, s);
-  hipLaunchKernelGGL(k_real_fwd<PL>, dim3(unsigned(fwd_blocks<PL>(a.batch))), dim3(Launch<PL>::FWD_THREADS), 0,
-                     s, a);
+  hipLaunchKernelGGL(k_real_fwd<PL>, dim3(unsigned(grid)), dim3(Launch<PL>::FWD_THREADS), 0, s, a, tiles);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? ACDC_OK : hip_fail(e);
 }

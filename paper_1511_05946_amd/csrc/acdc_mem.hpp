@@ -23,6 +23,8 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 
 struct GView {
+  // tables read through a GView are loaded one FFT pass ahead (cache latency)
+  static constexpr bool kPrefetch = true;
 #if defined(__HIP_DEVICE_COMPILE__)
   __amdgpu_buffer_rsrc_t r;
 #endif
@@ -89,6 +91,19 @@ struct GView {
   }
   __host__ __device__ __forceinline__ void st2(float2 v, unsigned voff, unsigned soff) const {
     *reinterpret_cast<float2*>(p + (voff + soff)) = v;
+  }
+};
+
+// A read-only table copied into LDS, with the same (voffset, soffset)
+// interface as GView's loads.
+struct LdsView {
+  static constexpr bool kPrefetch = false;  // LDS latency: load right before use
+  const char* p;
+  __host__ __device__ __forceinline__ static LdsView of(const void* base) {
+    return LdsView{static_cast<const char*>(base)};
+  }
+  __host__ __device__ __forceinline__ float2 ld2(unsigned voff, unsigned soff) const {
+    return *reinterpret_cast<const float2*>(p + voff + soff);
   }
 };
 

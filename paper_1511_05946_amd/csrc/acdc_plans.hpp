@@ -19,7 +19,10 @@
 #define ACDC_TAB_PF 3  // quartet slots whose tables are loaded ahead
 #endif
 #ifndef ACDC_MQ_PF
-#define ACDC_MQ_PF 3  // quartet-coefficient slots loaded ahead in the forward middle
+#define ACDC_MQ_PF 3  // quartet-coefficient slots loaded ahead in the layer middles
+#endif
+#ifndef ACDC_MQ_PF_BWD
+#define ACDC_MQ_PF_BWD 2  // the same in the backward middle (three float4 per slot)
 #endif
 #ifndef ACDC_LDS_PAD
 #define ACDC_LDS_PAD 1
@@ -74,20 +77,36 @@ struct RealPlan {
       !ACDC_LDS_PAD ? 30 : (ilog2(R0_) >= 2 && (1 << ilog2(R0_)) == R0_ ? ilog2(R0_) : 4);
   static constexpr int FFT_FLOATS = 2 * (M + (M >> PADSH));
   static constexpr int SLAB = cmax(cmax(N, QF), FFT_FLOATS);  // LDS floats per row
-  // twiddle table (float2) offsets: forward passes 1.., then inverse passes 1..
+  // twiddle table (float2) offsets: forward passes 1.., then inverse passes
+  // 1.. -- unless the radix sequence is a palindrome, in which case the
+  // inverse passes have the forward passes' radices and strides and share
+  // their table.
   __host__ __device__ static constexpr int tw_count(int p, bool inv) {
     return p == 0 ? 0 : ns(p, inv) * (radix(p, inv) - 1);
   }
+  __host__ __device__ static constexpr bool palindrome() {
+    for (int p = 0; p < NPASS; ++p)
+      if (rad(p) != rad(NPASS - 1 - p)) return false;
+    return true;
+  }
+  static constexpr int TW_DIRS = palindrome() ? 1 : 2;  // table blocks stored
   __host__ __device__ static constexpr int tw_off(int p, bool inv) {
+    const int dsel = (inv && TW_DIRS == 2) ? 1 : 0;
     int o = 0;
-    for (int d = 0; d < 2; ++d)
+    for (int d = 0; d < TW_DIRS; ++d)
       for (int q = 0; q < NPASS; ++q) {
-        if (d == (inv ? 1 : 0) && q == p) return o;
+        if (d == dsel && q == p) return o;
         o += tw_count(q, d == 1);
       }
     return o;
   }
-  static constexpr int TW_FLOAT2 = tw_off(NPASS, true);
+  __host__ __device__ static constexpr int tw_total() {
+    int o = 0;
+    for (int d = 0; d < TW_DIRS; ++d)
+      for (int q = 0; q < NPASS; ++q) o += tw_count(q, d == 1);
+    return o;
+  }
+  static constexpr int TW_FLOAT2 = tw_total();
   // table block layout in bytes: [fft twiddles][mk0 float4 NSL*T][mk1 float4 NSL*T]
   //                             [qidx int4 NSL*T][qmask int NSL*T]
   static constexpr int OFF_MK0 = ((TW_FLOAT2 * 8 + 255) / 256) * 256;
@@ -133,16 +152,29 @@ struct ComplexPlan {
   __host__ __device__ static constexpr int tw_count(int p, bool inv) {
     return p == 0 ? 0 : ns(p, inv) * (radix(p, inv) - 1);
   }
+  __host__ __device__ static constexpr bool palindrome() {
+    for (int p = 0; p < NPASS; ++p)
+      if (rad(p) != rad(NPASS - 1 - p)) return false;
+    return true;
+  }
+  static constexpr int TW_DIRS = palindrome() ? 1 : 2;
   __host__ __device__ static constexpr int tw_off(int p, bool inv) {
+    const int dsel = (inv && TW_DIRS == 2) ? 1 : 0;
     int o = 0;
-    for (int d = 0; d < 2; ++d)
+    for (int d = 0; d < TW_DIRS; ++d)
       for (int q = 0; q < NPASS; ++q) {
-        if (d == (inv ? 1 : 0) && q == p) return o;
+        if (d == dsel && q == p) return o;
         o += tw_count(q, d == 1);
       }
     return o;
   }
-  static constexpr int TW_FLOAT2 = tw_off(NPASS, true);
+  __host__ __device__ static constexpr int tw_total() {
+    int o = 0;
+    for (int d = 0; d < TW_DIRS; ++d)
+      for (int q = 0; q < NPASS; ++q) o += tw_count(q, d == 1);
+    return o;
+  }
+  static constexpr int TW_FLOAT2 = tw_total();
   static constexpr int TABLE_BYTES = ((TW_FLOAT2 * 8 + 255) / 256) * 256 + 256;
 
   static_assert(N_ % T_ == 0, "threads must divide the row");

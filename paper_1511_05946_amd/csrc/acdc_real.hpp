@@ -183,9 +183,9 @@ struct RealOps {
   // ------------------------------------------------------------ FFT passes
   // Forward: mirrored first pass (chunk-local input), negated last pass
   // (Makhoul partners together); the inverse runs the mirror image.
-  template <bool INV, class Ctx, class Tail>
+  template <bool INV, class Ctx, class TW, class Tail>
   __host__ __device__ __forceinline__ static void fft(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
-                                                      GView tw, Tail&& tail) {
+                                                      TW tw, Tail&& tail) {
     if constexpr (INV) stockham_fft<PL, true, 2, 1>(ctx, v, t, slab, tw, tail);
     else stockham_fft<PL, false, 1, 2>(ctx, v, t, slab, tw, tail);
   }
@@ -244,11 +244,13 @@ struct RealOps {
   // [slot][3][T] float4, lane-contiguous:
   //   c0 = (L1_00, L1_01, L1_11, L2_00), c1 = (L2_01, L2_11, w.x, w.y),
   //   c2 = (qa.x, qa.y, qb.x, qb.y)   (backward only)
-  // Loops over the slots load slot s + PFM while slot s computes; the first
-  // PFM slots are loaded ahead, in the tail of the preceding FFT.
-  static constexpr int PFM = NSL < ACDC_MQ_PF ? NSL : ACDC_MQ_PF;
+  // Loops over the slots load slot s + PF while slot s computes; the first
+  // PF slots are loaded ahead, in the tail of the preceding FFT.
   template <int NR>
   struct MqTabs {
+    // slots loaded ahead: fewer for the backward's three rows per slot
+    static constexpr int PF = NSL < (NR == 2 ? ACDC_MQ_PF : ACDC_MQ_PF_BWD) ? NSL
+                              : (NR == 2 ? ACDC_MQ_PF : ACDC_MQ_PF_BWD);
     float4 m[NSL][NR];
   };
   template <int NR>
@@ -259,7 +261,7 @@ struct RealOps {
   template <int NR>
   __host__ __device__ __forceinline__ static void load_mhead(MqTabs<NR>& tb, unsigned t, GView mq) {
 #pragma unroll
-    for (int s = 0; s < PFM; ++s) load_mslot(tb, s, t, mq);
+    for (int s = 0; s < MqTabs<NR>::PF; ++s) load_mslot(tb, s, t, mq);
   }
 
   // Real-FFT split of a Makhoul pair: E = Z[k] + conj Z[M-k],
@@ -302,6 +304,7 @@ struct RealOps {
   // layout) -> DCT-II quartet -> * d -> DCT-III pre-twiddle -> Z', as
   // split + sym_back (32 operations per slot).
   __host__ __device__ __forceinline__ static void mid(float2 (&v)[P], unsigned t, GView mq, MqTabs<2>& tb) {
+    constexpr int PFM = MqTabs<2>::PF;
     const bool sp = (t == 0);
     permute0(v, sp);
 #pragma unroll
@@ -326,6 +329,7 @@ struct RealOps {
   // consumed.
   __host__ __device__ __forceinline__ static void mid_bwd(float2 (&v)[P], float2 (&g)[P], unsigned t, GView mq,
                                                           MqTabs<3>& tb, float* slab) {
+    constexpr int PFM = MqTabs<3>::PF;
     const bool sp = (t == 0);
     permute0(v, sp);
     permute0(g, sp);
@@ -371,16 +375,15 @@ struct RealArgs {
   unsigned flags;
 };
 
-template <class PL, class Ctx>
+template <class PL, class Ctx, class TW>
 __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned t, long long row0, unsigned rr,
-                                          float* slab) {
+                                          float* slab, TW tab) {
   using O = RealOps<PL>;
   constexpr int N = PL::N, P = PL::P, NSL = PL::NSL, T = PL::T, NCH = O::NCH;
   const long long row = row0 + rr;
   const bool valid = row < a.batch;
   const bool permute = (a.flags & kFlagPerm) != 0;
   const unsigned roff = rr * unsigned(N / 4);
-  const GView tab = GView::of(a.tab);
   const typename O::Lane L = O::lane(t);
   float2* slab2 = reinterpret_cast<float2*>(slab);
   float2 v[P];
@@ -408,9 +411,9 @@ __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned 
   if (a.y != nullptr && valid) O::store(GView::of(a.y + row0 * N), roff, v, L);
 }
 
-template <class PL, int ROWS, class Ctx>
+template <class PL, int ROWS, class Ctx, class TW>
 __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned t, long long row0, unsigned rr,
-                                           int tid, long long tile, float* lds, float* slab) {
+                                           int tid, long long tile, float* lds, float* slab, TW tab) {
   using O = RealOps<PL>;
   constexpr int N = PL::N, P = PL::P, NSL = PL::NSL, T = PL::T, QF = PL::QF, NCH = O::NCH;
   constexpr int THREADS = ROWS * T;
@@ -419,7 +422,6 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
   const bool valid = row < a.batch;
   const bool permute = (a.flags & kFlagPerm) != 0;
   const unsigned roff = rr * unsigned(N / 4);
-  const GView tab = GView::of(a.tab);
   const typename O::Lane L = O::lane(t);
   float2* slab2 = reinterpret_cast<float2*>(slab);
   // layer input u_k: the block input for k = 0, else the stored layer input

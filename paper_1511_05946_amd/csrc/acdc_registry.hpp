@@ -39,27 +39,50 @@ using CP8192 = ComplexPlan<8192, 256, 32, 8, 32>;
 
 // Rows per workgroup.  Forward rows are independent; backward rows of one
 // workgroup are reduced together into one partial of dL/da, dL/dd.
+//
+// Real plans whose rows fit a wave (T <= 64) run 512-thread workgroups
+// (8 waves) that also hold a copy of the FFT twiddle table in LDS when it
+// fits next to the row slabs: every row of the workgroup then reads its
+// twiddles from LDS instead of streaming them from the cache hierarchy.
+// Such workgroups are persistent (each loops over row groups), so the
+// table is copied once per workgroup.
 #ifndef ACDC_FWD_THREADS
 #define ACDC_FWD_THREADS 64
 #endif
 #ifndef ACDC_BWD_THREADS
 #define ACDC_BWD_THREADS 512
 #endif
+#ifndef ACDC_TW_LDS
+#define ACDC_TW_LDS 1
+#endif
+#ifndef ACDC_TW_LDS_BWD
+#define ACDC_TW_LDS_BWD 0
+#endif
+constexpr int kLdsBytes = 160 * 1024;
 template <class PL>
 struct Launch {
-  static constexpr int FWD_ROWS = PL::T >= ACDC_FWD_THREADS ? 1 : ACDC_FWD_THREADS / PL::T;
-  static constexpr int BWD_ROWS =
-      PL::T == 192 ? 2 : (PL::T >= ACDC_BWD_THREADS ? 1 : ACDC_BWD_THREADS / PL::T);
-  static constexpr int FWD_THREADS = FWD_ROWS * PL::T;
-  static constexpr int BWD_THREADS = BWD_ROWS * PL::T;
   static constexpr int FWD_SLAB = PL::kComplex ? PL::SLAB : cmax(PL::N, PL::FFT_FLOATS);  // floats per row
   static constexpr int BWD_SLAB = PL::SLAB;
-  static constexpr int FWD_LDS_BYTES = FWD_ROWS * FWD_SLAB * 4;
-  static constexpr int BWD_LDS_BYTES = BWD_ROWS * BWD_SLAB * 4;
+  static constexpr int WIDE_ROWS = PL::T <= 64 ? 512 / PL::T : 1;
+  static constexpr bool TW_LDS = ACDC_TW_LDS && !PL::kComplex && PL::T <= 64 &&
+                                 WIDE_ROWS * PL::SLAB * 4 + PL::TW_FLOAT2 * 8 <= kLdsBytes;
+  static constexpr int FWD_ROWS =
+      TW_LDS ? WIDE_ROWS : (PL::T >= ACDC_FWD_THREADS ? 1 : ACDC_FWD_THREADS / PL::T);
+  static constexpr int BWD_ROWS =
+      TW_LDS ? WIDE_ROWS : (PL::T == 192 ? 2 : (PL::T >= ACDC_BWD_THREADS ? 1 : ACDC_BWD_THREADS / PL::T));
+  static constexpr bool BWD_TW_LDS = TW_LDS && ACDC_TW_LDS_BWD;
+  static constexpr int FWD_THREADS = FWD_ROWS * PL::T;
+  static constexpr int BWD_THREADS = BWD_ROWS * PL::T;
+  static constexpr int TW_FLOATS = TW_LDS ? PL::TW_FLOAT2 * 2 : 0;  // LDS copy of the twiddles
+  static constexpr int BWD_TW_FLOATS = BWD_TW_LDS ? PL::TW_FLOAT2 * 2 : 0;
+  static constexpr int FWD_LDS_FLOATS = FWD_ROWS * FWD_SLAB + TW_FLOATS;
+  static constexpr int BWD_LDS_FLOATS = BWD_ROWS * BWD_SLAB + BWD_TW_FLOATS;
+  static constexpr int FWD_LDS_BYTES = FWD_LDS_FLOATS * 4;
+  static constexpr int BWD_LDS_BYTES = BWD_LDS_FLOATS * 4;
   // Occupancy the register allocator must reach (512 / WPE registers per lane).
   static constexpr int FWD_WPE = 2;
   static constexpr int BWD_WPE = 2;
-  static_assert(FWD_LDS_BYTES <= 160 * 1024 && BWD_LDS_BYTES <= 160 * 1024, "LDS budget");
+  static_assert(FWD_LDS_BYTES <= kLdsBytes && BWD_LDS_BYTES <= kLdsBytes, "LDS budget");
   static_assert(BWD_THREADS <= 1024 && FWD_THREADS <= 1024, "workgroup size");
 };
 

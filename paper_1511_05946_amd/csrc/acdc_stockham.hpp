@@ -44,7 +44,8 @@ struct PassTw {
   static constexpr int b = PL::P / r;
   static constexpr int NW = kLive ? b * (r - 1) : 1;
   float2 w[NW];
-  __host__ __device__ __forceinline__ void load(unsigned t, GView tw) {
+  template <class TW>
+  __host__ __device__ __forceinline__ void load(unsigned t, TW tw) {
     if constexpr (kLive) {
       constexpr int Ns = PL::ns(PASS, INV);
       constexpr int KIND = (PASS == PL::NPASS - 1) ? KL : 0;
@@ -137,13 +138,33 @@ __host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL:
 
 // Whole transform.  `tail` runs in the last pass right after its twiddle
 // multiply: callers use it to issue the loads of what follows the FFT.
-template <class PL, bool INV, int KF, int KL, class Ctx, class Tail>
+// `tab` is the twiddle table: the global constant table (GView) or its copy
+// in LDS (LdsView).
+template <class PL, bool INV, int KF, int KL, class Ctx, class TW, class Tail>
 __host__ __device__ __forceinline__ void stockham_fft(Ctx& ctx, float2 (&v)[PL::P], unsigned t, float2* slab,
-                                                     GView tab, Tail&& tail) {
+                                                     TW tab, Tail&& tail) {
   constexpr int NP = PL::NPASS;
   PassTw<PL, INV, 0, KF, KL> w0;
   PassTw<PL, INV, 1, KF, KL> w1;
-  if constexpr (NP == 1) {
+  if constexpr (!TW::kPrefetch) {
+    // each pass reads its own twiddles as it starts
+    static_assert(NP <= 4, "up to four passes");
+    PassTw<PL, INV, 2, KF, KL> w2;
+    PassTw<PL, INV, 3, KF, KL> w3;
+    stockham_pass<PL, INV, 0, KF, KL>(ctx, v, t, slab, w0, [&] { if constexpr (NP == 1) tail(); });
+    if constexpr (NP > 1) {
+      w1.load(t, tab);
+      stockham_pass<PL, INV, 1, KF, KL>(ctx, v, t, slab, w1, [&] { if constexpr (NP == 2) tail(); });
+    }
+    if constexpr (NP > 2) {
+      w2.load(t, tab);
+      stockham_pass<PL, INV, 2, KF, KL>(ctx, v, t, slab, w2, [&] { if constexpr (NP == 3) tail(); });
+    }
+    if constexpr (NP > 3) {
+      w3.load(t, tab);
+      stockham_pass<PL, INV, 3, KF, KL>(ctx, v, t, slab, w3, tail);
+    }
+  } else if constexpr (NP == 1) {
     stockham_pass<PL, INV, 0, KF, KL>(ctx, v, t, slab, w0, tail);
   } else {
     stockham_pass<PL, INV, 0, KF, KL>(ctx, v, t, slab, w0, [&] { w1.load(t, tab); });
@@ -163,9 +184,9 @@ __host__ __device__ __forceinline__ void stockham_fft(Ctx& ctx, float2 (&v)[PL::
   }
 }
 
-template <class PL, bool INV, int KF, int KL, class Ctx>
+template <class PL, bool INV, int KF, int KL, class Ctx, class TW>
 __host__ __device__ __forceinline__ void stockham_fft(Ctx& ctx, float2 (&v)[PL::P], unsigned t, float2* slab,
-                                                     GView tab) {
+                                                     TW tab) {
   stockham_fft<PL, INV, KF, KL>(ctx, v, t, slab, tab, [] {});
 }
 

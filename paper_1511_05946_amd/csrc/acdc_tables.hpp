@@ -27,7 +27,7 @@ inline HostC w_pow(long long e, long long L) {
 
 template <class PL>
 inline void fill_fft_twiddles(float2* tw) {
-  for (int d = 0; d < 2; ++d) {
+  for (int d = 0; d < PL::TW_DIRS; ++d) {
     const bool inv = d == 1;
     for (int p = 1; p < PL::NPASS; ++p) {
       const int r = PL::radix(p, inv), Ns = PL::ns(p, inv), off = PL::tw_off(p, inv);

@@ -6,6 +6,7 @@
 // algebra, the plan tables and the reduction order on the CPU; the GPU tests
 // then check the real kernels.  Built by tests/emu/build_emu.py.
 #include <barrier>
+#include <cstring>
 #include <cstdio>
 #include <thread>
 #include <vector>
@@ -72,11 +73,18 @@ void real_fwd(const float* x, float* y, const float* A, const float* D, const in
   const std::vector<float4> mq = quartet_coefficients<PL>(D, K, tab);
   RealArgs a{x, y, A, mq.data(), perm, saved, nullptr, nullptr, nullptr, (const char*)tab.data(), batch, K, flags};
   const long long nwg = (batch + L::FWD_ROWS - 1) / L::FWD_ROWS;
-  std::vector<float> lds((size_t)L::FWD_ROWS * L::FWD_SLAB);
+  std::vector<float> lds((size_t)L::FWD_LDS_FLOATS);
+  float* twl = lds.data();
+  float* rows = lds.data() + L::TW_FLOATS;
+  if (L::TW_LDS) std::memcpy(twl, tab.data(), (size_t)PL::TW_FLOAT2 * 8);
   for (long long wg = 0; wg < nwg; ++wg)
     run_wg(L::FWD_THREADS, [&](HostCtx& ctx, int tid) {
       const int r = tid / PL::T, t = tid % PL::T;
-      real_forward_row<PL>(ctx, a, unsigned(t), wg * L::FWD_ROWS, unsigned(r), lds.data() + (size_t)r * L::FWD_SLAB);
+      float* slab = rows + (size_t)r * L::FWD_SLAB;
+      if constexpr (L::TW_LDS)
+        real_forward_row<PL>(ctx, a, unsigned(t), wg * L::FWD_ROWS, unsigned(r), slab, LdsView::of(twl));
+      else
+        real_forward_row<PL>(ctx, a, unsigned(t), wg * L::FWD_ROWS, unsigned(r), slab, GView::of(tab.data()));
     });
 }
 
@@ -98,12 +106,20 @@ void real_bwd(const float* x, const float* gy, const float* A, const float* D, c
   std::vector<float> partial((size_t)ntiles * K * PS);
   RealArgs a{x, nullptr, A, mq.data(), perm, const_cast<float*>(saved), gy, gx, partial.data(),
              (const char*)tab.data(), batch, K, flags};
-  std::vector<float> lds((size_t)L::BWD_ROWS * L::BWD_SLAB);
+  std::vector<float> lds((size_t)L::BWD_LDS_FLOATS);
+  float* twl = lds.data();
+  float* rows = lds.data() + L::BWD_TW_FLOATS;
+  if (L::BWD_TW_LDS) std::memcpy(twl, tab.data(), (size_t)PL::TW_FLOAT2 * 8);
   for (long long wg = 0; wg < ntiles; ++wg)
     run_wg(L::BWD_THREADS, [&](HostCtx& ctx, int tid) {
       const int r = tid / PL::T, t = tid % PL::T;
-      real_backward_row<PL, L::BWD_ROWS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, lds.data(),
-                                         lds.data() + (size_t)r * L::BWD_SLAB);
+      float* slab = rows + (size_t)r * L::BWD_SLAB;
+      if constexpr (L::BWD_TW_LDS)
+        real_backward_row<PL, L::BWD_ROWS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, rows,
+                                           slab, LdsView::of(twl));
+      else
+        real_backward_row<PL, L::BWD_ROWS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, rows,
+                                           slab, GView::of(tab.data()));
     });
   reduce_all<PL>(partial.data(), ntiles, K, [&](float4 s, int k, int e4) {
     real_reduce_store4<PL>(s, k, e4, gA, gD, (const char*)tab.data());
