@@ -105,6 +105,9 @@ struct LdsView {
   __host__ __device__ __forceinline__ float2 ld2(unsigned voff, unsigned soff) const {
     return *reinterpret_cast<const float2*>(p + voff + soff);
   }
+  __host__ __device__ __forceinline__ float4 ld4(unsigned voff, unsigned soff) const {
+    return *reinterpret_cast<const float4*>(p + voff + soff);
+  }
 };
 
 }  // namespace acdc

@@ -81,8 +81,10 @@ struct RealPlan {
   // 1.. -- unless the radix sequence is a palindrome, in which case the
   // inverse passes have the forward passes' radices and strides and share
   // their table.
+  // Twiddles of a pass are stored in pairs (inputs i, i+1) so one 16-byte
+  // load fetches two; an odd count is padded by one entry per k.
   __host__ __device__ static constexpr int tw_count(int p, bool inv) {
-    return p == 0 ? 0 : ns(p, inv) * (radix(p, inv) - 1);
+    return p == 0 ? 0 : ns(p, inv) * (radix(p, inv) - 1 + ((radix(p, inv) - 1) & 1));
   }
   __host__ __device__ static constexpr bool palindrome() {
     for (int p = 0; p < NPASS; ++p)
@@ -149,8 +151,10 @@ struct ComplexPlan {
       !ACDC_LDS_PAD ? 30 : (ilog2(R0_) >= 2 && (1 << ilog2(R0_)) == R0_ ? ilog2(R0_) : 4);
   static constexpr int FFT_FLOATS = 2 * (N_ + (N_ >> PADSH));
   static constexpr int SLAB = FFT_FLOATS;  // LDS floats per row
+  // Twiddles of a pass are stored in pairs (inputs i, i+1) so one 16-byte
+  // load fetches two; an odd count is padded by one entry per k.
   __host__ __device__ static constexpr int tw_count(int p, bool inv) {
-    return p == 0 ? 0 : ns(p, inv) * (radix(p, inv) - 1);
+    return p == 0 ? 0 : ns(p, inv) * (radix(p, inv) - 1 + ((radix(p, inv) - 1) & 1));
   }
   __host__ __device__ static constexpr bool palindrome() {
     for (int p = 0; p < NPASS; ++p)

@@ -34,7 +34,8 @@ __host__ __device__ __forceinline__ unsigned bfly(unsigned t, int beta) {
 
 // Twiddles of one pass for the butterflies of thread t, held in registers.
 // Input i of butterfly j takes W_{Ns r}^{i k}, k = j mod Ns, stored at
-// [i-1][k] of the pass's table block.
+// [(i-1)/2][k][(i-1)%2] of the pass's table block (pairs of inputs share a
+// 16-byte load; lanes with consecutive k read consecutive pairs).
 // A pass's twiddles are loaded while the previous pass still computes, so
 // the table latency hides behind its DFTs, LDS exchange and barrier.
 template <class PL, bool INV, int PASS, int KF, int KL>
@@ -52,11 +53,18 @@ struct PassTw {
       constexpr unsigned off = unsigned(PL::tw_off(PASS, INV)) * 8u;
 #pragma unroll
       for (int beta = 0; beta < b; ++beta) {
-        // table layout [i-1][k], k = j mod Ns: lanes with consecutive j
-        // read consecutive float2, so one load touches few cache lines
-        const unsigned vo = (bfly<PL, KIND, b>(t, beta) % Ns) * 8u;
+        const unsigned vo = (bfly<PL, KIND, b>(t, beta) % Ns) * 16u;
 #pragma unroll
-        for (int i = 1; i < r; ++i) w[beta * (r - 1) + i - 1] = tw.ld2(vo, off + unsigned((i - 1) * Ns) * 8u);
+        for (int i = 1; i < r; i += 2) {
+          const unsigned so = off + unsigned((i - 1) * Ns) * 8u;  // pair (i-1)/2 starts at (i-1)*Ns float2
+          if (i + 1 < r) {
+            const float4 q = tw.ld4(vo, so);
+            w[beta * (r - 1) + i - 1] = make_float2(q.x, q.y);
+            w[beta * (r - 1) + i] = make_float2(q.z, q.w);
+          } else {
+            w[beta * (r - 1) + i - 1] = tw.ld2(vo, so);
+          }
+        }
       }
     }
   }

@@ -31,11 +31,12 @@ inline void fill_fft_twiddles(float2* tw) {
     const bool inv = d == 1;
     for (int p = 1; p < PL::NPASS; ++p) {
       const int r = PL::radix(p, inv), Ns = PL::ns(p, inv), off = PL::tw_off(p, inv);
-      // [input i-1][k]: the lanes of one load read consecutive k
+      // [pair (i-1)/2][k][(i-1)%2]: one 16-byte load per lane reads the
+      // twiddles of inputs i, i+1, and the lanes of a load read consecutive k
       for (int i = 1; i < r; ++i)
         for (int k = 0; k < Ns; ++k) {
           const HostC w = w_pow((long long)i * k, (long long)Ns * r);
-          tw[off + (i - 1) * Ns + k] = make_float2(float(w.re), float(w.im));
+          tw[off + ((i - 1) / 2) * 2 * Ns + 2 * k + (i - 1) % 2] = make_float2(float(w.re), float(w.im));
         }
     }
   }
