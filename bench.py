@@ -1,7 +1,7 @@
 """Benchmark: ACDC cascade forward + backward on one MI355X.
 
 A step is one training pass of the whole cascade over one batch: the forward
-kernel (which also stores the layer inputs) followed by the backward kernel and
+kernel (which also stores what the backward needs) followed by the backward kernel and
 the fixed-order reduction of dL/da, dL/dd.  Inputs are synthetic and seeded
 (paper_1511_05946_amd.workloads) and already resident in HBM when timing
 starts.
@@ -129,7 +129,7 @@ def main():
     fl = w.flags & ~acdc.FLAG_COMPLEX
     acdc.prepare(w.N, w.flags)
     y = torch.empty_like(xt)
-    saved = torch.empty(acdc.saved_shape(xt, w.K), dtype=xt.dtype, device=dev)
+    saved = acdc.alloc_saved(xt, w.K, w.flags)
 
     def step():
         if args.recompute:

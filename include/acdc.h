@@ -86,31 +86,36 @@ int acdc_supported(int32_t N, uint32_t flags);
  * so that later calls enqueue without host synchronisation.  Optional. */
 int acdc_prepare(int32_t N, uint32_t flags);
 
-/* Bytes of the optional activation buffer `saved` ([K-1][batch][N] elements). */
+/* Bytes of the optional buffer `saved` that acdc_forward fills for
+ * acdc_backward: the layer inputs u_1..u_{K-1}, [K-1][batch][N] elements. */
 size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
 
-/* Bytes of workspace acdc_forward needs (a re-layout of D).  Host only. */
+/* Bytes of workspace acdc_forward needs (the per-layer quartet coefficients
+ * built from D).  Host only. */
 size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
 
 /* Bytes of workspace acdc_backward needs: per-workgroup partial sums of the
- * parameter gradients, the re-layout of D, and -- when have_saved is 0 -- room
- * to recompute the layer inputs (the paper's recompute policy, Sec. 5). */
+ * parameter gradients, the per-layer quartet coefficients, and -- when
+ * have_saved is 0 -- room to recompute the layer inputs (the paper's
+ * recompute policy, Sec. 5.3). */
 size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags, int have_saved);
 
 /* Forward cascade: y = cascade(x).  If `saved` is non-null it also stores the
- * layer inputs u_1..u_{K-1} there (acdc_saved_bytes), for acdc_backward. */
+ * layer inputs u_1..u_{K-1} there, for acdc_backward; saved_bytes must be at
+ * least acdc_saved_bytes(...) (else ACDC_ERR_WORKSPACE, nothing launched). */
 int acdc_forward(const float* x, float* y, const float* A, const float* D, const int32_t* perm,
-                 int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, void* workspace,
-                 size_t workspace_bytes, acdc_stream_t stream);
+                 int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, size_t saved_bytes,
+                 void* workspace, size_t workspace_bytes, acdc_stream_t stream);
 
 /* Backward cascade.  Given x and grad_y = dL/dy, writes grad_x = dL/dx and
  * grad_A, grad_D = dL/da_k, dL/dd_k summed over the batch (overwritten, not
  * accumulated).  `saved` is the buffer filled by acdc_forward for the same x,
- * A, D, perm, or null, in which case the layer inputs are recomputed into the
- * workspace first.  batch == 0 writes zero parameter gradients. */
+ * A, D, perm (saved_bytes as there), or null, in which case the layer inputs
+ * are recomputed into the workspace first.  batch == 0 writes zero parameter
+ * gradients. */
 int acdc_backward(const float* x, const float* grad_y, const float* A, const float* D,
-                  const int32_t* perm, const float* saved, float* grad_x, float* grad_A, float* grad_D,
-                  int64_t batch, int32_t N, int32_t K, uint32_t flags, void* workspace,
+                  const int32_t* perm, const float* saved, size_t saved_bytes, float* grad_x, float* grad_A,
+                  float* grad_D, int64_t batch, int32_t N, int32_t K, uint32_t flags, void* workspace,
                   size_t workspace_bytes, acdc_stream_t stream);
 
 /* Kernel timing for benchmarks (not for the callers' hot path).  While

@@ -44,6 +44,10 @@ def _ptr(t):
     return t.data_ptr()
 
 
+def _nbytes(t) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
 def _dims(x: torch.Tensor, A: torch.Tensor):
     if x.dim() != 2 or A.dim() != 2:
         raise ValueError("x must be [batch, N] and A, D [K, N]")
@@ -80,20 +84,35 @@ def prepare(N: int, flags: int = 0, device=None):
         _check(lib().acdc_prepare(int(N), int(flags)), "acdc_prepare")
 
 
-def saved_shape(x: torch.Tensor, K: int):
-    return (max(K - 1, 0), x.shape[0], x.shape[1])
+def saved_numel(x: torch.Tensor, K: int, flags: int = 0) -> int:
+    """Elements (of x's dtype) of the buffer acdc_forward fills for
+    acdc_backward: the layer inputs u_1..u_{K-1}."""
+    flags = _flags(flags, x)
+    nbytes = lib().acdc_saved_bytes(x.shape[0], x.shape[1], K, flags)
+    return nbytes // x.element_size()
+
+
+def alloc_saved(x: torch.Tensor, K: int, flags: int = 0) -> torch.Tensor:
+    return torch.empty(saved_numel(x, K, flags), dtype=x.dtype, device=x.device)
+
+
+def saved_layer_inputs(saved: torch.Tensor, x: torch.Tensor, K: int) -> torch.Tensor:
+    """View of the layer inputs u_1..u_{K-1} inside a saved buffer, [K-1, batch, N]."""
+    B, N = x.shape
+    return saved[: max(K - 1, 0) * B * N].view(max(K - 1, 0), B, N)
 
 
 def forward(x, A, D, perm=None, flags: int = 0, save: bool = False, out=None, saved=None):
     """y = cascade(x).  Returns (y, saved) where saved holds the layer inputs
-    u_1..u_{K-1} when ``save`` (or a preallocated ``saved``) is given."""
+    u_1..u_{K-1} for acdc_backward when ``save`` (or a preallocated
+    ``saved``) is given."""
     flags = _flags(flags, x)
     cplx = bool(flags & FLAG_COMPLEX)
     B, N, K = _dims(x, A)
     if out is None:
         out = torch.empty_like(x)
     if save and saved is None:
-        saved = torch.empty(saved_shape(x, K), dtype=x.dtype, device=x.device)
+        saved = alloc_saved(x, K, flags)
     _validate({"x": x, "A": A, "D": D, "y": out, "saved": saved,
                "perm": perm if flags & FLAG_PERM else None}, cplx, x.device)
     L = lib()
@@ -102,15 +121,16 @@ def forward(x, A, D, perm=None, flags: int = 0, save: bool = False, out=None, sa
     with torch.cuda.device(x.device):
         rc = L.acdc_forward(_ptr(x), _ptr(out), _ptr(A), _ptr(D),
                             _ptr(perm) if flags & FLAG_PERM else None, B, N, K, flags,
-                            _ptr(saved) if (saved is not None and K > 1) else None,
-                            _ptr(ws), ws_bytes, _stream(x.device))
+                            _ptr(saved) if (saved is not None and saved.numel() > 0) else None,
+                            _nbytes(saved), _ptr(ws), ws_bytes, _stream(x.device))
     _check(rc, "acdc_forward")
     return out, saved
 
 
 def backward(x, grad_y, A, D, perm=None, flags: int = 0, saved=None):
     """(grad_x, grad_A, grad_D); parameter gradients are summed over the batch.
-    Without ``saved`` the layer inputs are recomputed inside the call."""
+    Without ``saved`` (from ``forward(..., save=True)`` on the same inputs)
+    the forward is recomputed inside the call."""
     flags = _flags(flags, x)
     cplx = bool(flags & FLAG_COMPLEX)
     B, N, K = _dims(x, A)
@@ -120,13 +140,14 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0, saved=None):
     _validate({"x": x, "grad_y": grad_y, "A": A, "D": D, "saved": saved,
                "perm": perm if flags & FLAG_PERM else None}, cplx, x.device)
     L = lib()
-    have_saved = 1 if (saved is not None or K == 1) else 0
+    use_saved = saved is not None and saved.numel() > 0
+    have_saved = 1 if (use_saved or K == 1) else 0
     ws_bytes = L.acdc_backward_workspace_bytes(B, N, K, flags, have_saved)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=x.device)
     with torch.cuda.device(x.device):
         rc = L.acdc_backward(_ptr(x), _ptr(grad_y), _ptr(A), _ptr(D),
                              _ptr(perm) if flags & FLAG_PERM else None,
-                             _ptr(saved) if (saved is not None and K > 1) else None,
+                             _ptr(saved) if use_saved else None, _nbytes(saved),
                              _ptr(gx), _ptr(gA), _ptr(gD), B, N, K, flags, _ptr(ws), ws_bytes,
                              _stream(x.device))
     _check(rc, "acdc_backward")

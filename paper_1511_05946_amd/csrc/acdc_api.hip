@@ -371,6 +371,11 @@ long long bwd_tiles(int64_t batch) {
 
 size_t elem_floats(uint32_t flags) { return (flags & kFlagComplex) ? 2 : 1; }
 
+// Floats of the `saved` buffer: the layer inputs u_1..u_{K-1}.
+size_t saved_floats(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
+  return size_t(K - 1) * size_t(batch) * size_t(N) * elem_floats(flags);
+}
+
 struct WsLayout {
   size_t mq = 0, partial = 0, stash = 0, total = 0;
   size_t off_mq = 0, off_partial = 0, off_stash = 0;
@@ -394,7 +399,7 @@ WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool ha
   };
   if (flags & kFlagComplex) dispatch_complex(N, f);
   else dispatch_real(N, f);
-  if (!have_saved && K > 1) w.stash = align256(size_t(K - 1) * size_t(batch) * N * elem_floats(flags) * 4);
+  if (!have_saved && K > 1) w.stash = align256(saved_floats(batch, N, K, flags) * 4);
   w.off_mq = 0;
   w.off_partial = w.off_mq + w.mq;
   w.off_stash = w.off_partial + w.partial;
@@ -456,7 +461,7 @@ extern "C" int acdc_prepare(int32_t N, uint32_t flags) {
 
 extern "C" size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
   if (check_common(batch, N, K, flags) != ACDC_OK) return 0;
-  return size_t(K - 1) * size_t(batch) * size_t(N) * elem_floats(flags) * sizeof(float);
+  return saved_floats(batch, N, K, flags) * sizeof(float);
 }
 
 extern "C" size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
@@ -471,10 +476,11 @@ extern "C" size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_
 }
 
 extern "C" int acdc_forward(const float* x, float* y, const float* A, const float* D, const int32_t* perm,
-                            int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, void* workspace,
-                            size_t workspace_bytes, acdc_stream_t stream) {
+                            int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, size_t saved_bytes,
+                            void* workspace, size_t workspace_bytes, acdc_stream_t stream) {
   int rc = check_common(batch, N, K, flags);
   if (rc != ACDC_OK) return rc;
+  if (saved != nullptr && saved_bytes < saved_floats(batch, N, K, flags) * sizeof(float)) return ACDC_ERR_WORKSPACE;
   const bool perm_on = (flags & kFlagPerm) != 0;
   if (batch == 0) return ACDC_OK;
   rc = check_ptrs({x, y, A, D}, {perm_on ? (const void*)perm : nullptr, saved, workspace});
@@ -506,11 +512,12 @@ extern "C" int acdc_forward(const float* x, float* y, const float* A, const floa
 }
 
 extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A, const float* D,
-                             const int32_t* perm, const float* saved, float* grad_x, float* grad_A,
-                             float* grad_D, int64_t batch, int32_t N, int32_t K, uint32_t flags,
+                             const int32_t* perm, const float* saved, size_t saved_bytes, float* grad_x,
+                             float* grad_A, float* grad_D, int64_t batch, int32_t N, int32_t K, uint32_t flags,
                              void* workspace, size_t workspace_bytes, acdc_stream_t stream) {
   int rc = check_common(batch, N, K, flags);
   if (rc != ACDC_OK) return rc;
+  if (saved != nullptr && saved_bytes < saved_floats(batch, N, K, flags) * sizeof(float)) return ACDC_ERR_WORKSPACE;
   const bool perm_on = (flags & kFlagPerm) != 0;
   rc = check_ptrs({A, D, grad_A, grad_D}, {perm_on ? (const void*)perm : nullptr, saved, workspace});
   if (rc != ACDC_OK) return rc;

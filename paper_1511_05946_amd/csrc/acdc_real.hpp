@@ -190,6 +190,14 @@ struct RealOps {
     else stockham_fft<PL, false, 1, 2>(ctx, v, t, slab, tw, tail);
   }
 
+  // Forward FFTs of two rows' arrays sharing twiddle loads (backward h- and
+  // g-paths).
+  template <class Ctx, class Tail>
+  __host__ __device__ __forceinline__ static void fft2(Ctx& ctx, float2 (&v)[P], float2 (&w)[P], unsigned t,
+                                                       float2* slab, GView tw, Tail&& tail) {
+    stockham_fft2<PL, false, 1, 2>(ctx, v, w, t, slab, tw, tail);
+  }
+
   // ------------------------------------------------------ Makhoul quartets
   // A quartet slot holds a spectrum pair Z[k], Z[M-k] of the packed row.
   // The DCT-II outputs of the quartet are (Makhoul's quarter-wave
@@ -444,8 +452,12 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
       O::unpack(uv, v, valid);
       O::scale(v, av);
       typename O::template MqTabs<3> tb;
+#if ACDC_FFT2
+      O::fft2(ctx, v, g, t, slab2, tab, [&] { O::load_mhead(tb, t, mq); });
+#else
       O::template fft<false>(ctx, v, t, slab2, tab, [] {});
       O::template fft<false>(ctx, g, t, slab2, tab, [&] { O::load_mhead(tb, t, mq); });
+#endif
       ctx.sync_row();
       O::mid_bwd(v, g, t, mq, tb, slab);
     }

@@ -70,28 +70,30 @@ struct PassTw {
   }
 };
 
-// One pass.  `next` is called once this pass no longer needs its own
-// twiddles (it issues the next pass's loads); a scheduling fence keeps those
-// loads ahead of this pass's arithmetic.
-template <class PL, bool INV, int PASS, int KF, int KL, class Ctx, class Next>
-__host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL::P], unsigned t, float2* slab,
-                                                      const PassTw<PL, INV, PASS, KF, KL>& tw, Next&& next) {
-  constexpr int P = PL::P;
-  constexpr int r = PL::radix(PASS, INV);
-  constexpr int Ns = PL::ns(PASS, INV);
-  constexpr int b = P / r;
-  constexpr int stride = PL::M / r;
-  constexpr bool first = (PASS == 0);
-  constexpr bool last = (PASS == PL::NPASS - 1);
-  constexpr int KIND = first ? KF : (last ? KL : 0);
+// The steps of one pass.  Pass p (radix r, stride Ns) owns butterflies j
+// chosen by the KIND policy; it reads inputs j + i*(M/r) from the slab
+// (except the first pass, which starts from registers), multiplies input i
+// by W_{Ns r}^{i (j mod Ns)}, runs the r-point DFT and writes output m to
+// (j - j mod Ns) r + (j mod Ns) + m Ns (except the last pass, whose outputs
+// stay in registers).  Slab indices are padded: a -> a + (a >> PADSH).
+template <class PL, bool INV, int PASS, int KF, int KL>
+struct PassGeo {
+  static constexpr int r = PL::radix(PASS, INV);
+  static constexpr int Ns = PL::ns(PASS, INV);
+  static constexpr int b = PL::P / r;
+  static constexpr int stride = PL::M / r;
+  static constexpr bool first = (PASS == 0);
+  static constexpr bool last = (PASS == PL::NPASS - 1);
+  static constexpr int KIND = first ? KF : (last ? KL : 0);
+  static constexpr unsigned S = PL::PADSH;
   unsigned j[b];
+  __host__ __device__ __forceinline__ explicit PassGeo(unsigned t) {
 #pragma unroll
-  for (int beta = 0; beta < b; ++beta) j[beta] = bfly<PL, KIND, b>(t, beta);
-  constexpr unsigned S = PL::PADSH;
-  if constexpr (!first) {
-    // inputs j + i*stride; stride is a multiple of 2^S, so the padded index
-    // is pad(j) + i*(stride + stride/2^S)
+    for (int beta = 0; beta < b; ++beta) j[beta] = bfly<PL, KIND, b>(t, beta);
+  }
+  __host__ __device__ __forceinline__ void read(float2 (&v)[PL::P], const float2* slab) const {
     if constexpr (stride % (1 << S) == 0) {
+      // stride is a multiple of 2^S: pad(j + i stride) = pad(j) + i (stride + stride/2^S)
       constexpr unsigned sp = stride + (stride >> S);
 #pragma unroll
       for (int beta = 0; beta < b; ++beta) {
@@ -109,19 +111,20 @@ __host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL:
         }
     }
   }
-  if constexpr (PassTw<PL, INV, PASS, KF, KL>::kLive) {
-    // input i of butterfly j times W_{Ns r}^{i (j mod Ns)}
+  __host__ __device__ __forceinline__ void twiddle(float2 (&v)[PL::P],
+                                                   const PassTw<PL, INV, PASS, KF, KL>& tw) const {
+    if constexpr (PassTw<PL, INV, PASS, KF, KL>::kLive) {
 #pragma unroll
-    for (int beta = 0; beta < b; ++beta)
+      for (int beta = 0; beta < b; ++beta)
 #pragma unroll
-      for (int i = 1; i < r; ++i) v[beta * r + i] = ctw<INV>(v[beta * r + i], tw.w[beta * (r - 1) + i - 1]);
+        for (int i = 1; i < r; ++i) v[beta * r + i] = ctw<INV>(v[beta * r + i], tw.w[beta * (r - 1) + i - 1]);
+    }
   }
-  next();
-  ACDC_SCHED_FENCE();
+  __host__ __device__ __forceinline__ static void dft(float2 (&v)[PL::P]) {
 #pragma unroll
-  for (int beta = 0; beta < b; ++beta) Dft<r, INV>::run(&v[beta * r]);
-  if constexpr (!last) {
-    ctx.sync_row();
+    for (int beta = 0; beta < b; ++beta) Dft<r, INV>::run(&v[beta * r]);
+  }
+  __host__ __device__ __forceinline__ void write(const float2 (&v)[PL::P], float2* slab) const {
 #pragma unroll
     for (int beta = 0; beta < b; ++beta) {
       const unsigned k = j[beta] % Ns;
@@ -140,7 +143,58 @@ __host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL:
         }
       }
     }
+  }
+};
+
+// One pass.  `next` is called once this pass no longer needs its own
+// twiddles (it issues the next pass's loads); a scheduling fence keeps those
+// loads ahead of this pass's arithmetic.
+template <class PL, bool INV, int PASS, int KF, int KL, class Ctx, class Next>
+__host__ __device__ __forceinline__ void stockham_pass(Ctx& ctx, float2 (&v)[PL::P], unsigned t, float2* slab,
+                                                      const PassTw<PL, INV, PASS, KF, KL>& tw, Next&& next) {
+  using G = PassGeo<PL, INV, PASS, KF, KL>;
+  const G geo(t);
+  if constexpr (!G::first) geo.read(v, slab);
+  geo.twiddle(v, tw);
+  next();
+  ACDC_SCHED_FENCE();
+  G::dft(v);
+  if constexpr (!G::last) {
     ctx.sync_row();
+    geo.write(v, slab);
+    ctx.sync_row();
+  }
+}
+
+// Two transforms of the same direction on arrays v and w that share the
+// slab: pass by pass, both arrays use one set of twiddle registers, and
+// the exchanges between passes run one array after the other through the
+// slab (write v, read v, write w, read w).
+template <class PL, bool INV, int PASS, int KF, int KL, class Ctx, class Next>
+__host__ __device__ __forceinline__ void stockham_pass2(Ctx& ctx, float2 (&v)[PL::P], float2 (&w)[PL::P],
+                                                       unsigned t, float2* slab,
+                                                       const PassTw<PL, INV, PASS, KF, KL>& tw, Next&& next) {
+  using G = PassGeo<PL, INV, PASS, KF, KL>;
+  const G geo(t);
+  geo.twiddle(v, tw);
+  geo.twiddle(w, tw);
+  ACDC_SCHED_FENCE();
+  G::dft(v);
+  next();  // the next pass's twiddles load while w's butterflies run
+  ACDC_SCHED_FENCE();
+  G::dft(w);
+  if constexpr (!G::last) {
+    // this pass's outputs go through the slab into the next pass's inputs
+    using G1 = PassGeo<PL, INV, PASS + 1, KF, KL>;
+    const G1 geo1(t);
+    ctx.sync_row();
+    geo.write(v, slab);
+    ctx.sync_row();
+    geo1.read(v, slab);
+    ctx.sync_row();
+    geo.write(w, slab);
+    ctx.sync_row();
+    geo1.read(w, slab);
   }
 }
 
@@ -196,6 +250,32 @@ template <class PL, bool INV, int KF, int KL, class Ctx, class TW>
 __host__ __device__ __forceinline__ void stockham_fft(Ctx& ctx, float2 (&v)[PL::P], unsigned t, float2* slab,
                                                      TW tab) {
   stockham_fft<PL, INV, KF, KL>(ctx, v, t, slab, tab, [] {});
+}
+
+// Forward transforms of two arrays sharing each pass's twiddles (global
+// table, loaded one pass ahead).  `tail` runs in the last pass right after
+// its twiddle multiplies.
+template <class PL, bool INV, int KF, int KL, class Ctx, class Tail>
+__host__ __device__ __forceinline__ void stockham_fft2(Ctx& ctx, float2 (&v)[PL::P], float2 (&w)[PL::P],
+                                                      unsigned t, float2* slab, GView tab, Tail&& tail) {
+  constexpr int NP = PL::NPASS;
+  static_assert(NP >= 2 && NP <= 4, "two to four passes");
+  PassTw<PL, INV, 0, KF, KL> w0;
+  PassTw<PL, INV, 1, KF, KL> w1;
+  PassTw<PL, INV, 2, KF, KL> w2;
+  PassTw<PL, INV, 3, KF, KL> w3;
+  stockham_pass2<PL, INV, 0, KF, KL>(ctx, v, w, t, slab, w0, [&] { w1.load(t, tab); });
+  if constexpr (NP == 2) {
+    stockham_pass2<PL, INV, 1, KF, KL>(ctx, v, w, t, slab, w1, tail);
+  } else {
+    stockham_pass2<PL, INV, 1, KF, KL>(ctx, v, w, t, slab, w1, [&] { w2.load(t, tab); });
+    if constexpr (NP == 3) {
+      stockham_pass2<PL, INV, 2, KF, KL>(ctx, v, w, t, slab, w2, tail);
+    } else {
+      stockham_pass2<PL, INV, 2, KF, KL>(ctx, v, w, t, slab, w2, [&] { w3.load(t, tab); });
+      stockham_pass2<PL, INV, 3, KF, KL>(ctx, v, w, t, slab, w3, tail);
+    }
+  }
 }
 
 // Sum the per-row images [rows][SLAB] of a workgroup in fixed row order and

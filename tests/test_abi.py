@@ -94,8 +94,8 @@ def test_forward_rejects_bad_arguments(L):
     p = FakePtr()
     x, y, A, D, perm, ws = (p(i) for i in range(6))
 
-    def fwd(x=x, y=y, A=A, D=D, perm=perm, B=4, N=64, K=2, flags=0, saved=None, ws=ws, wsb=1 << 20):
-        return L.acdc_forward(x, y, A, D, perm, B, N, K, flags, saved, ws, wsb, None)
+    def fwd(x=x, y=y, A=A, D=D, perm=perm, B=4, N=64, K=2, flags=0, saved=None, sb=0, ws=ws, wsb=1 << 20):
+        return L.acdc_forward(x, y, A, D, perm, B, N, K, flags, saved, sb, ws, wsb, None)
 
     assert fwd(N=100) == EUNSUP
     assert fwd(flags=CX | RELU) == EUNSUP
@@ -109,6 +109,8 @@ def test_forward_rejects_bad_arguments(L):
     assert fwd(flags=PERM, perm=None) == EINVAL
     assert fwd(ws=None) == EWS
     assert fwd(wsb=16) == EWS
+    need = L.acdc_saved_bytes(4, 64, 2, 0)
+    assert fwd(saved=p(6), sb=need - 4) == EWS   # saved buffer smaller than its layout
     assert fwd(B=0) == OK                   # empty batch: nothing to do, no HIP call
 
 
@@ -116,9 +118,9 @@ def test_backward_rejects_bad_arguments(L):
     p = FakePtr()
     x, gy, A, D, perm, gx, gA, gD, ws = (p(i) for i in range(9))
 
-    def bwd(x=x, gy=gy, A=A, D=D, perm=perm, saved=None, gx=gx, gA=gA, gD=gD, B=4, N=64, K=2,
+    def bwd(x=x, gy=gy, A=A, D=D, perm=perm, saved=None, sb=0, gx=gx, gA=gA, gD=gD, B=4, N=64, K=2,
             flags=0, ws=ws, wsb=1 << 30):
-        return L.acdc_backward(x, gy, A, D, perm, saved, gx, gA, gD, B, N, K, flags, ws, wsb, None)
+        return L.acdc_backward(x, gy, A, D, perm, saved, sb, gx, gA, gD, B, N, K, flags, ws, wsb, None)
 
     assert bwd(N=48) == EUNSUP
     assert bwd(flags=CX | RELU) == EUNSUP
@@ -131,6 +133,8 @@ def test_backward_rejects_bad_arguments(L):
     assert bwd(flags=PERM, perm=None) == EINVAL
     assert bwd(ws=None) == EWS
     assert bwd(wsb=64) == EWS
+    need = L.acdc_saved_bytes(4, 64, 2, 0)
+    assert bwd(saved=p(9), sb=need - 4) == EWS   # saved buffer smaller than its layout
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

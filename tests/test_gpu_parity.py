@@ -76,7 +76,7 @@ def run_case(acdc, N, K, B, flags, seed=0, save=True, check_bwd=True, rows=None)
     e = rel_err(yg[sel], yr)
     assert e < tol, f"forward rel err {e:.3e}"
     if save and K > 1:
-        sg = host(saved)
+        sg = host(acdc.saved_layer_inputs(saved, xt, K))
         for k in range(1, K):
             assert rel_err(sg[k - 1][sel], cache["u"][k]) < tol
     if not check_bwd:
@@ -89,7 +89,7 @@ def run_case(acdc, N, K, B, flags, seed=0, save=True, check_bwd=True, rows=None)
     print(f"[case]   backward on {len(idx)}/{len(sel)} rows + {len(xs) - len(idx)} refill rows", flush=True)
     xst = dev(xs)
     sv = None
-    if save and K > 1:
+    if save:
         _, sv = acdc.forward(xst, At, Dt, pt, flags & ~CX, save=True)
     gx, gA, gD = acdc.backward(xst, dev(gys), At, Dt, pt, flags & ~CX, saved=sv)
     rx, rA, rD = O.backward(xs, gys, A, D, perm, flags)
@@ -227,7 +227,7 @@ def test_outputs_fully_written(acdc):
     x, A, D, perm, gy = make_inputs(N, K, B, flags, 7)
     xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
     y = torch.full_like(xt, float("nan"))
-    saved = torch.full((K - 1, B, N), float("nan"), device="cuda")
+    saved = torch.full((acdc.saved_numel(xt, K, flags),), float("nan"), device="cuda")
     acdc.forward(xt, At, Dt, pt, flags, out=y, saved=saved)
     assert np.isfinite(host(y)).all() and np.isfinite(host(saved)).all()
     gx, gA, gD = acdc.backward(xt, gyt, At, Dt, pt, flags, saved=saved)
