@@ -94,12 +94,11 @@ struct RealOps {
 #pragma unroll
     for (int n = 0; n < NCH; ++n) h[n] = g.ld4((ch_lc(L, n) + ro) * 16u, ch_cc(n) * 16u);
   }
-  __host__ __device__ __forceinline__ static void unpack(const float4 (&h)[NCH], float2 (&v)[P], bool valid) {
-    const float z = valid ? 1.0f : 0.0f;
+  __host__ __device__ __forceinline__ static void unpack(const float4 (&h)[NCH], float2 (&v)[P]) {
     int n = 0;
     for_chunks(v, Lane{0, 0}, [&](unsigned, unsigned, float2& lo, float2& hi) {
-      lo = make_float2(h[n].x * z, h[n].z * z);
-      hi = make_float2(h[n].w * z, h[n].y * z);
+      lo = make_float2(h[n].x, h[n].z);
+      hi = make_float2(h[n].w, h[n].y);
       ++n;
     });
   }
@@ -107,7 +106,10 @@ struct RealOps {
                                                        bool valid) {
     float4 h[NCH];
     load_raw(h, g, roff, L, valid);
-    unpack(h, v, valid);
+    const float z = valid ? 1.0f : 0.0f;
+#pragma unroll
+    for (int n = 0; n < NCH; ++n) h[n] = make_float4(h[n].x * z, h[n].y * z, h[n].z * z, h[n].w * z);
+    unpack(h, v);
   }
   __host__ __device__ __forceinline__ static void store(GView g, unsigned roff, float2 (&v)[P], Lane L) {
     for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
@@ -212,14 +214,17 @@ struct RealOps {
   // and pre-twiddle into the two symmetric 2x2 maps that sym_back applies.
 
   // Thread 0's first butterfly pair is (0, NB/2): both are self-negating,
-  // so its partners are not at the generic register positions.  Permuting
-  // those 2*RL registers by pi (new[rho] = old[pi(rho)]) puts every Makhoul
-  // pair at (i, 2*RL-1-i); slot 0 then holds the two self-paired values
-  // (Z[0], Z[M/2]), handled by its own table entries.
+  // so their Makhoul partners are not at the generic register positions.
+  // With A = v[0..RL) the outputs of butterfly 0 (Z[j NB]) and B = v[RL..2RL)
+  // those of butterfly NB/2 (Z[NB/2 + j NB]), partners are A_j, A_RL-j and
+  // B_j, B_RL-1-j.  The permutation new[rho] = old[pi(rho)] below moves only
+  // the blocks v[RL/2..RL) and v[3RL/2..2RL): slot i < RL/2 then pairs A_i
+  // with A_RL-i (slot 0: the self-paired Z[0], Z[M/2], with their own table
+  // entries) and slot i >= RL/2 pairs B_i with B_RL-1-i.
   __host__ __device__ static constexpr int perm_pi(int rho) {
     return rho < RL / 2       ? rho
-           : rho < RL         ? RL + rho - RL / 2
-           : rho < 3 * RL / 2 ? rho + RL / 2
+           : rho < RL         ? RL + rho
+           : rho < 3 * RL / 2 ? rho
            : rho < 2 * RL - 1 ? rho - RL + 1
                               : RL / 2;
   }
@@ -229,20 +234,29 @@ struct RealOps {
       if (perm_pi(rho) == o) r = rho;
     return r;
   }
-  __host__ __device__ __forceinline__ static void permute0(float2 (&v)[P], bool sp) {
+  // Every lane selects per moved register (thread 0 takes the permuted
+  // value): one select per moved float.
+  __host__ __device__ static constexpr bool moved(int rho) { return (rho % RL) >= RL / 2; }
+  template <bool INV>
+  __host__ __device__ __forceinline__ static void perm0(float2 (&v)[P], bool sp) {
     float2 nv[2 * RL];
 #pragma unroll
-    for (int rho = 0; rho < 2 * RL; ++rho) nv[rho] = perm_pi(rho) == rho ? v[rho] : sel2(sp, v[perm_pi(rho)], v[rho]);
+    for (int rho = 0; rho < 2 * RL; ++rho) {
+      const int src = INV ? perm_pi_inv(rho) : perm_pi(rho);
+      nv[rho] = moved(rho) ? sel2(sp, v[src], v[rho]) : v[rho];
+    }
 #pragma unroll
     for (int rho = 0; rho < 2 * RL; ++rho) v[rho] = nv[rho];
   }
-  __host__ __device__ __forceinline__ static void unpermute0(float2 (&v)[P], bool sp) {
-    float2 nv[2 * RL];
-#pragma unroll
-    for (int o = 0; o < 2 * RL; ++o) nv[o] = perm_pi_inv(o) == o ? v[o] : sel2(sp, v[perm_pi_inv(o)], v[o]);
-#pragma unroll
-    for (int o = 0; o < 2 * RL; ++o) v[o] = nv[o];
-  }
+  __host__ __device__ __forceinline__ static void permute0(float2 (&v)[P], bool sp) { perm0<false>(v, sp); }
+  __host__ __device__ __forceinline__ static void unpermute0(float2 (&v)[P], bool sp) { perm0<true>(v, sp); }
+  static_assert([] {
+    for (int rho = 0; rho < 2 * RL; ++rho)
+      if (moved(rho) != (perm_pi(rho) != rho) || moved(perm_pi(rho)) != moved(rho) ||
+          perm_pi(perm_pi_inv(rho)) != rho)
+        return false;
+    return true;
+  }(), "thread 0's permutation moves exactly the blocks v[RL/2..RL), v[3RL/2..2RL)");
   // The DCT-III pre-twiddle of thread 0's slot 0 needs its own qb':
   // exp(i pi/8) / (2 sqrt(N)).
   static constexpr float kQbRe = float(0.9238795325112867561 / (2.0 * csqrt(double(N))));
@@ -251,7 +265,7 @@ struct RealOps {
   // Per-layer quartet coefficients (real_mq_entry), layout of one layer
   // [slot][3][T] float4, lane-contiguous:
   //   c0 = (L1_00, L1_01, L1_11, L2_00), c1 = (L2_01, L2_11, w.x, w.y),
-  //   c2 = (qa.x, qa.y, qb.x, qb.y)   (backward only)
+  //   c2 = (qa.x, qa.y, qbr.x, qbr.y), qbr = (1 + i) qb   (backward only)
   // Loops over the slots load slot s + PF while slot s computes; the first
   // PF slots are loaded ahead, in the tail of the preceding FFT.
   template <int NR>
@@ -283,14 +297,17 @@ struct RealOps {
     const float2 wO = cmul(Od, w);
     return Split{cadd(E, wO), csub(E, wO)};
   }
-  // DCT-II outputs X[k], X[N-k], X[M-k], X[M+k] of a split (the
-  // orthonormal scaling is folded into qa, qb).
-  __host__ __device__ __forceinline__ static void post_x(const Split& sp, float2 qa, float2 qb, float (&X)[4]) {
-    const float2 u1 = cmul(sp.s1, qa), u2 = cmul(sp.s2, qb);
+  // DCT-II outputs of a split, up to the sign of X[N-k]: returns
+  // (X[k], -X[N-k], X[M-k], X[M+k]), with the orthonormal scaling folded
+  // into qa and qbr = (1 + i) qb, so u1 = qa s1 = X[k] - i X[N-k] and
+  // u2 = qbr s2 = X[M-k] + i X[M+k].  The backward only forms products of
+  // two such images, where the sign cancels.
+  __host__ __device__ __forceinline__ static void post_x(const Split& sp, float2 qa, float2 qbr, float (&X)[4]) {
+    const float2 u1 = cmul(sp.s1, qa), u2 = cmul(sp.s2, qbr);
     X[0] = u1.x;
-    X[1] = -u1.y;
-    X[2] = u2.x - u2.y;
-    X[3] = u2.x + u2.y;
+    X[1] = u1.y;
+    X[2] = u2.x;
+    X[3] = u2.y;
   }
   // From a split, the D diagonal and the DCT-III pre-twiddle as the two
   // symmetric 2x2 maps L1 (on s1) and L2 (on s2), then the inverse split:
@@ -349,13 +366,13 @@ struct RealOps {
         if (slot + PFM < NSL) load_mslot(tb, slot + PFM, t, mq);
         ACDC_SCHED_FENCE();
         const float4 c0 = tb.m[slot][0], c1 = tb.m[slot][1], c2 = tb.m[slot][2];
-        const float2 w = make_float2(c1.z, c1.w), qa = make_float2(c2.x, c2.y), qb = make_float2(c2.z, c2.w);
+        const float2 w = make_float2(c1.z, c1.w), qa = make_float2(c2.x, c2.y), qbr = make_float2(c2.z, c2.w);
         float2& gk = g[2 * q * RL + i];
         float2& gm = g[2 * q * RL + 2 * RL - 1 - i];
         float H[4], G[4];
-        post_x(split(v[2 * q * RL + i], v[2 * q * RL + 2 * RL - 1 - i], w), qa, qb, H);
+        post_x(split(v[2 * q * RL + i], v[2 * q * RL + 2 * RL - 1 - i], w), qa, qbr, H);
         const Split sg = split(gk, gm, w);
-        post_x(sg, qa, qb, G);
+        post_x(sg, qa, qbr, G);
         reinterpret_cast<float4*>(slab)[slot * T + t] =
             make_float4(H[0] * G[0], H[1] * G[1], H[2] * G[2], H[3] * G[3]);
         sym_back(sg, c0, c1, gk, gm);
@@ -432,6 +449,10 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
   const unsigned roff = rr * unsigned(N / 4);
   const typename O::Lane L = O::lane(t);
   float2* slab2 = reinterpret_cast<float2*>(slab);
+  // A row past the batch end reads the block's first row for u_k but starts
+  // from g = 0, which every step keeps exactly zero (linear transforms,
+  // diagonal scalings, masks); its images H * G and u * g therefore vanish
+  // without masking u, as long as that first row is finite.
   // layer input u_k: the block input for k = 0, else the stored layer input
   const float* const x0 = a.x + row0 * N;
   const float* const s0 = a.saved + (row0 - a.batch) * N;
@@ -449,7 +470,7 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
     {
       float2 v[P];
       O::load_vec(av, ak, L);
-      O::unpack(uv, v, valid);
+      O::unpack(uv, v);
       O::scale(v, av);
       typename O::template MqTabs<3> tb;
 #if ACDC_FFT2
@@ -471,11 +492,10 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
       // mask is off, so masking gh1 first leaves u * gh1 unchanged.  Then
       // the dL/da image u * gh1 (spatial, natural order) goes to the slab.
       const bool mask = (a.flags & kFlagRelu) && k > 0;
-      const float z = valid ? 1.0f : 0.0f;
       ctx.sync_row();
       int n = 0;
       O::for_chunks(g, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
-        const float4 u = make_float4(uv[n].x * z, uv[n].y * z, uv[n].z * z, uv[n].w * z);
+        const float4 u = uv[n];
         ++n;
         if (mask) {
           lo = make_float2(u.x > 0.f ? lo.x : 0.f, u.z > 0.f ? lo.y : 0.f);

@@ -55,6 +55,15 @@ using CP8192 = ComplexPlan<8192, 256, 32, 8, 32>;
 #ifndef ACDC_TW_LDS
 #define ACDC_TW_LDS 1
 #endif
+// Workgroup size for rows of at most 16 threads (small N): fewer rows per
+// workgroup give more workgroups at a given batch.
+#ifndef ACDC_NARROW_THREADS
+#define ACDC_NARROW_THREADS 256
+#endif
+// Rows per backward workgroup for the three-wave rows of N = 9216.
+#ifndef ACDC_BWD_ROWS_T192
+#define ACDC_BWD_ROWS_T192 2
+#endif
 #ifndef ACDC_TW_LDS_BWD
 #define ACDC_TW_LDS_BWD 0
 #endif
@@ -63,13 +72,13 @@ template <class PL>
 struct Launch {
   static constexpr int FWD_SLAB = PL::kComplex ? PL::SLAB : cmax(PL::N, PL::FFT_FLOATS);  // floats per row
   static constexpr int BWD_SLAB = PL::SLAB;
-  static constexpr int WIDE_ROWS = PL::T <= 64 ? 512 / PL::T : 1;
+  static constexpr int WIDE_ROWS = PL::T <= 16 ? ACDC_NARROW_THREADS / PL::T : PL::T <= 64 ? 512 / PL::T : 1;
   static constexpr bool TW_LDS = ACDC_TW_LDS && !PL::kComplex && PL::T <= 64 &&
                                  WIDE_ROWS * PL::SLAB * 4 + PL::TW_FLOAT2 * 8 <= kLdsBytes;
   static constexpr int FWD_ROWS =
       TW_LDS ? WIDE_ROWS : (PL::T >= ACDC_FWD_THREADS ? 1 : ACDC_FWD_THREADS / PL::T);
   static constexpr int BWD_ROWS =
-      TW_LDS ? WIDE_ROWS : (PL::T == 192 ? 2 : (PL::T >= ACDC_BWD_THREADS ? 1 : ACDC_BWD_THREADS / PL::T));
+      TW_LDS ? WIDE_ROWS : (PL::T == 192 ? ACDC_BWD_ROWS_T192 : (PL::T >= ACDC_BWD_THREADS ? 1 : ACDC_BWD_THREADS / PL::T));
   static constexpr bool BWD_TW_LDS = TW_LDS && ACDC_TW_LDS_BWD;
   static constexpr int FWD_THREADS = FWD_ROWS * PL::T;
   static constexpr int BWD_THREADS = BWD_ROWS * PL::T;
@@ -205,7 +214,9 @@ __host__ __device__ inline void real_mq_entry(const float* Dk, const char* tab, 
   }
   out[0] = make_float4(float(L1[0][0]), float(0.5 * (L1[0][1] + L1[1][0])), float(L1[1][1]), float(L2[0][0]));
   out[1] = make_float4(float(0.5 * (L2[0][1] + L2[1][0])), float(L2[1][1]), m0.x, m0.y);
-  out[2] = make_float4(m0.z, m0.w, m1.x, m1.y);
+  // qb rotated by (1 + i): the backward image then reads X[M-k], X[M+k] off
+  // one complex product
+  out[2] = make_float4(m0.z, m0.w, float(double(m1.x) - double(m1.y)), float(double(m1.x) + double(m1.y)));
 }
 
 // Fixed-order batch reduction of the per-tile partials.  Entry e (a float4)

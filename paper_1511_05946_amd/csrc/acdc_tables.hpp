@@ -52,7 +52,7 @@ inline int real_slot_k(int t, int slot) {
   const int p = t + T * q;
   if (p != 0) return p + i * NB;
   if (i == 0) return -2;
-  return i < RL / 2 ? i * NB : NB / 2 + (i - RL / 2) * NB;
+  return i < RL / 2 ? i * NB : NB / 2 + i * NB;
 }
 
 // Returns false if the quartet slots do not cover every DCT index exactly once.
