@@ -19,6 +19,9 @@ Conventions (row vectors throughout, as in the paper's Sec. 1 eq. (1) y = xW):
 * ``A``, ``D``     [K, N] diagonals a_k, d_k of layer k (A_k = diag(a_k))
 * ``perm``         [K, N] int; ``perm[k]`` *gathers* the input of layer k:
                    u_k[n] = z_{k-1}[perm[k][n]]
+* ``B``            [K, N] optional additive bias of each layer's D-domain
+                   term, h3 = h2 * d_k + b_k (Sec. 6.2: biases added to the
+                   D matrices, none on A)
 * ``flags``        bit 0 PERM, bit 1 RELU (after layers 0..K-2), bit 2 COMPLEX
 
 Readings of the paper used here (each listed in the design doc):
@@ -88,12 +91,14 @@ def _transforms(N: int, complex_: bool):
     return C, C.T.copy()
 
 
-def _check(x, A, D, perm, flags):
+def _check(x, A, D, perm, flags, B=None):
     x = np.asarray(x)
     A = np.asarray(A)
     D = np.asarray(D)
     if x.ndim != 2 or A.ndim != 2 or D.shape != A.shape or A.shape[1] != x.shape[1]:
         raise ValueError("shapes: x [B,N], A and D [K,N]")
+    if B is not None and np.shape(B) != A.shape:
+        raise ValueError("B must be [K,N]")
     if (flags & FLAG_COMPLEX) and (flags & FLAG_RELU):
         raise ValueError("ReLU is not defined for the complex variant")
     if flags & FLAG_PERM:
@@ -104,26 +109,27 @@ def _check(x, A, D, perm, flags):
             if not np.array_equal(np.sort(perm[k]), np.arange(A.shape[1])):
                 raise ValueError(f"perm[{k}] is not a permutation")
     dt = np.complex128 if flags & FLAG_COMPLEX else np.float64
-    return x.astype(dt), A.astype(dt), D.astype(dt), perm
+    Bd = np.zeros(A.shape, dt) if B is None else np.asarray(B).astype(dt)
+    return x.astype(dt), A.astype(dt), D.astype(dt), perm, Bd
 
 
-def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False):
+def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False, B=None):
     """Cascade forward y = x prod_k [P_k] A_k T D_k T^{-1}  (eq. for AFDF_K in
-    Sec. 3, made real in Sec. 4 as ACDC_K; permutations and ReLU interleaved as
-    in Sec. 6.2).
+    Sec. 3, made real in Sec. 4 as ACDC_K; permutations, ReLU and the D-domain
+    biases as in Sec. 6.2).
 
     Per layer k (row vectors, Sec. 4 notation):
         u_k = z[:, perm[k]]          (if PERM)
         h1  = u_k * a_k              (x A)
         h2  = h1 @ T                 (x A C)
-        h3  = h2 * d_k               (x A C D)
+        h3  = h2 * d_k + b_k         (x A C D, plus the bias if B is given)
         v_k = h3 @ Tinv              (x A C D C^{-1})
         z   = max(v_k, 0)            (if RELU and k < K-1) else v_k
 
     Returns y, or (y, cache) with cache = dict(u=[...], h2=[...], v=[...]) of
     per-layer float64 arrays when ``keep`` is true.
     """
-    x, A, D, perm = _check(x, A, D, perm, flags)
+    x, A, D, perm, Bd = _check(x, A, D, perm, flags, B)
     K, N = A.shape
     T, Tinv = _transforms(N, bool(flags & FLAG_COMPLEX))
     relu = bool(flags & FLAG_RELU)
@@ -137,7 +143,7 @@ def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False):
             u = z[:, perm[k]] if flags & FLAG_PERM else z
             h1 = u * A[k]
             h2 = h1 @ T
-            h3 = h2 * D[k]
+            h3 = h2 * D[k] + Bd[k]
             v = h3 @ Tinv
             z = np.maximum(v, 0.0) if (relu and k < K - 1) else v
             if keep:
@@ -148,7 +154,7 @@ def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False):
     return (y, cache) if keep else y
 
 
-def backward(x, grad_y, A, D, perm=None, flags: int = 0):
+def backward(x, grad_y, A, D, perm=None, flags: int = 0, B=None):
     """Analytic backward of the cascade (Sec. 4 derivative block, applied
     layer by layer in reverse; ReLU and permutation steps of Sec. 6.2).
 
@@ -156,6 +162,7 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0):
         g    = g * (v_k > 0)                  (if RELU and k < K-1)
         gh3  = g @ C                          (dL/dh3 = C dL/dy in the paper's
                                                column form; row form g C)
+        db_k = sum_rows gh3                   (the bias enters h3 additively)
         dd_k = sum_rows h2_k * gh3            (dL/dd = h2 . C dL/dy)
         gh1  = (gh3 * d_k) @ C^T              (C^{-1} d . C dL/dy)
         da_k = sum_rows u_k * gh1             (dL/da = x . C^{-1} d . C dL/dy)
@@ -166,10 +173,12 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0):
         gh3 = g @ F / N, dd_k = sum conj(h2_k) gh3, gh1 = (gh3 conj(d_k)) @ conj(F),
         da_k = sum conj(u_k) gh1, gu = gh1 conj(a_k).
 
-    Returns (grad_x [B,N], grad_A [K,N], grad_D [K,N]); the parameter
-    gradients are sums over the batch.
+    Returns (grad_x [B,N], grad_A [K,N], grad_D [K,N]), and grad_B [K,N] as a
+    fourth element when B is given; the parameter gradients are sums over the
+    batch.  (B changes the stored h2 only through the forward values the
+    backward recomputes: the ReLU masks of a biased cascade.)
     """
-    x, A, D, perm = _check(x, A, D, perm, flags)
+    x, A, D, perm, Bd = _check(x, A, D, perm, flags, B)
     cplx = bool(flags & FLAG_COMPLEX)
     gy = np.asarray(grad_y).astype(np.complex128 if cplx else np.float64)
     if gy.shape != x.shape:
@@ -184,14 +193,16 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0):
     grad_x = np.empty_like(x)
     grad_A = np.zeros_like(A)
     grad_D = np.zeros_like(D)
+    grad_B = np.zeros_like(D)
     for r0 in range(0, x.shape[0], _CHUNK):
         xs = x[r0:r0 + _CHUNK]
-        _, cache = forward(xs, A, D, perm, flags, keep=True)
+        _, cache = forward(xs, A, D, perm, flags, keep=True, B=Bd)
         g = gy[r0:r0 + _CHUNK]
         for k in range(K - 1, -1, -1):
             if relu and k < K - 1:
                 g = g * (cache["v"][k] > 0.0)
             gh3 = g @ Tinv_H
+            grad_B[k] += np.sum(gh3, axis=0)
             h2 = cache["h2"][k]
             grad_D[k] += np.sum((np.conj(h2) if cplx else h2) * gh3, axis=0)
             gh1 = (gh3 * (np.conj(D[k]) if cplx else D[k])) @ T_H
@@ -204,6 +215,8 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0):
             else:
                 g = gu
         grad_x[r0:r0 + _CHUNK] = g
+    if B is not None:
+        return grad_x, grad_A, grad_D, grad_B
     return grad_x, grad_A, grad_D
 
 

@@ -38,17 +38,18 @@ def rand_case(rng, B, N, K, flags, relu_input=False):
     return x, A, D, perm, gy
 
 
-def lib_forward(x, A, D, perm, flags):
+def lib_forward(x, A, D, perm, flags, B=None):
     """The cascade written with library transforms only (scipy DCT-II/III
     'ortho', numpy FFT): the special case the oracle must reduce to."""
     z = np.asarray(x)
     K = A.shape[0]
+    Bz = np.zeros(A.shape) if B is None else B
     for k in range(K):
         u = z[:, perm[k]] if flags & P else z
         if flags & CX:
-            v = np.fft.ifft(np.fft.fft(u * A[k], axis=1) * D[k], axis=1)
+            v = np.fft.ifft(np.fft.fft(u * A[k], axis=1) * D[k] + Bz[k], axis=1)
         else:
-            v = scipy.fft.idct(scipy.fft.dct(u * A[k], type=2, norm="ortho", axis=1) * D[k],
+            v = scipy.fft.idct(scipy.fft.dct(u * A[k], type=2, norm="ortho", axis=1) * D[k] + Bz[k],
                                type=2, norm="ortho", axis=1)
         z = np.maximum(v, 0) if (flags & R and k < K - 1) else v
     return z
@@ -311,6 +312,126 @@ def test_backward_batch_split_additivity():
     np.testing.assert_allclose(gx, np.concatenate([gx1, gx2]), atol=1e-13)
     np.testing.assert_allclose(gA, gA1 + gA2, atol=1e-12)
     np.testing.assert_allclose(gD, gD1 + gD2, atol=1e-12)
+
+
+# ------------------------------------------- D-domain bias (Sec. 6.2)
+
+def rand_bias(rng, K, N, cplx):
+    b = rng.normal(0, .3, (K, N))
+    return b + 1j * rng.normal(0, .3, (K, N)) if cplx else b
+
+
+@pytest.mark.parametrize("cplx", [False, True])
+def test_bias_with_zero_D_is_inverse_transform_of_bias(cplx):
+    # D = 0 removes the input: every output row is b C^{-1} (scipy's
+    # orthonormal DCT-III) or b F^{-1} (numpy's inverse FFT).
+    rng = np.random.default_rng(500 + cplx)
+    flags = CX if cplx else 0
+    x, A, D, perm, _ = rand_case(rng, 5, 16, 1, flags)
+    b = rand_bias(rng, 1, 16, cplx)
+    y = O.forward(x, A, np.zeros_like(D), perm, flags, B=b)
+    ref = np.fft.ifft(b[0]) if cplx else scipy.fft.idct(b[0], type=2, norm="ortho")
+    np.testing.assert_allclose(y, np.broadcast_to(ref, y.shape), atol=1e-14)
+
+
+@pytest.mark.parametrize("flags", [0, P | R, CX | P])
+def test_bias_forward_equals_library_transforms(flags):
+    rng = np.random.default_rng(510 + flags)
+    x, A, D, perm, _ = rand_case(rng, 7, 32, 3, flags, relu_input=True)
+    b = rand_bias(rng, 3, 32, bool(flags & CX))
+    np.testing.assert_allclose(O.forward(x, A, D, perm, flags, B=b), lib_forward(x, A, D, perm, flags, b),
+                               atol=1e-12)
+
+
+@pytest.mark.parametrize("cplx", [False, True])
+def test_bias_gradient_single_layer_closed_form(cplx):
+    # One layer: dL/db = sum_rows g C (scipy's orthonormal DCT-II of each
+    # gradient row) or sum_rows g F / N (numpy FFT / N); the other gradients
+    # do not depend on b.
+    rng = np.random.default_rng(520 + cplx)
+    flags = CX if cplx else 0
+    x, A, D, perm, gy = rand_case(rng, 6, 16, 1, flags)
+    b = rand_bias(rng, 1, 16, cplx)
+    gx, gA, gD, gB = O.backward(x, gy, A, D, perm, flags, B=b)
+    ref = (np.fft.fft(gy, axis=1) / 16 if cplx else scipy.fft.dct(gy, type=2, norm="ortho", axis=1)).sum(0)
+    np.testing.assert_allclose(gB[0], ref, atol=1e-12)
+    gx0, gA0, gD0 = O.backward(x, gy, A, D, perm, flags)
+    for a, c in ((gx, gx0), (gA, gA0), (gD, gD0)):
+        np.testing.assert_allclose(a, c, atol=1e-13)
+
+
+def test_bias_gradient_finite_differences():
+    rng = np.random.default_rng(530)
+    flags = P | R
+    x, A, D, perm, gy = rand_case(rng, 3, 8, 3, flags)
+    b = rand_bias(rng, 3, 8, False)
+    _, cache = O.forward(x, A, D, perm, flags, keep=True, B=b)
+    assert min(np.abs(cache["v"][k]).min() for k in range(2)) > 1e-4, "re-seed: ReLU kink too close"
+    gB = O.backward(x, gy, A, D, perm, flags, B=b)[3]
+    eps = 1e-6
+    fd = np.zeros_like(b)
+    for idx in np.ndindex(*b.shape):
+        bp, bm = b.copy(), b.copy()
+        bp[idx] += eps
+        bm[idx] -= eps
+        fd[idx] = (np.sum(gy * lib_forward(x, A, D, perm, flags, bp)) -
+                   np.sum(gy * lib_forward(x, A, D, perm, flags, bm))) / (2 * eps)
+    np.testing.assert_allclose(gB, fd, atol=1e-7, rtol=1e-6)
+
+
+@pytest.mark.parametrize("flags", [P | R, CX | P])
+def test_bias_backward_matches_torch_autograd(flags):
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(540 + flags)
+    N, K, B = 32, 3, 5
+    cplx = bool(flags & CX)
+    x, A, D, perm, gy = rand_case(rng, B, N, K, flags)
+    b = rand_bias(rng, K, N, cplx)
+    dt = torch.complex128 if cplx else torch.float64
+    Ct = torch.tensor(scipy.fft.dct(np.eye(N), type=2, norm="ortho", axis=1), dtype=torch.float64)
+    xt, At, Dt, Bt = (torch.tensor(v, dtype=dt, requires_grad=True) for v in (x, A, D, b))
+    z = xt
+    for k in range(K):
+        u = z[:, torch.as_tensor(perm[k])] if flags & P else z
+        if cplx:
+            v = torch.fft.ifft(torch.fft.fft(u * At[k], dim=1) * Dt[k] + Bt[k], dim=1)
+        else:
+            v = (((u * At[k]) @ Ct) * Dt[k] + Bt[k]) @ Ct.T
+        z = torch.relu(v) if (flags & R and k < K - 1) else v
+    z.backward(torch.tensor(gy, dtype=dt))
+    gx, gA, gD, gB = O.backward(x, gy, A, D, perm, flags, B=b)
+    for a, t in ((gx, xt), (gA, At), (gD, Dt), (gB, Bt)):
+        np.testing.assert_allclose(a, t.grad.numpy(), atol=1e-10)
+
+
+def test_bias_planted_mistakes_are_caught(monkeypatch):
+    good = O.forward
+
+    def spatial_bias(x, A, D, perm=None, flags=0, keep=False, B=None):
+        # bias added after the inverse transform instead of in the D domain
+        y = good(x, A, D, perm, flags, keep)
+        if B is None:
+            return y
+        if keep:
+            return y[0] + B[-1], y[1]
+        return y + B[-1]
+    monkeypatch.setattr(O, "forward", spatial_bias)
+    with pytest.raises(AssertionError):
+        test_bias_with_zero_D_is_inverse_transform_of_bias(False)
+    monkeypatch.setattr(O, "forward", good)
+
+    good_bwd = O.backward
+
+    def spatial_grad(x, gy, A, D, perm=None, flags=0, B=None):
+        # dL/db taken as the spatial row sum instead of its transform
+        out = good_bwd(x, gy, A, D, perm, flags, B)
+        if B is None:
+            return out
+        return out[:3] + (np.broadcast_to(np.asarray(gy).sum(0), np.shape(B)).copy(),)
+    monkeypatch.setattr(O, "backward", spatial_grad)
+    with pytest.raises(AssertionError):
+        test_bias_gradient_single_layer_closed_form(False)
+    monkeypatch.setattr(O, "backward", good_bwd)
 
 
 # ------------------------------------------------------ paper's printed numbers
