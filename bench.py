@@ -63,17 +63,18 @@ def cpu_baseline(w, seed: int, budget_s: float = 12.0, max_rows: int = 512):
     from threadpoolctl import threadpool_info
 
     from oracle import acdc_oracle as O
-    from paper_1511_05946_amd.workloads import make_inputs
+    from paper_1511_05946_amd.workloads import FLAG_BIAS, make_bias, make_inputs
 
     x, A, D, perm, gy = make_inputs(w.N, w.K, min(w.batch, max_rows), w.flags, seed)
+    bias = make_bias(w.N, w.K, seed) if w.flags & FLAG_BIAS else None
     rows = 0
     t_total = 0.0
     chunk = 16 if w.N >= 4096 else 64
     while rows < x.shape[0] and t_total < budget_s:
         sl = slice(rows, min(rows + chunk, x.shape[0]))
         t0 = time.perf_counter()
-        O.forward(x[sl], A, D, perm, w.flags)
-        O.backward(x[sl], gy[sl], A, D, perm, w.flags)
+        O.forward(x[sl], A, D, perm, w.flags & 7, B=bias)
+        O.backward(x[sl], gy[sl], A, D, perm, w.flags & 7, B=bias)
         t_total += time.perf_counter() - t0
         rows = sl.stop
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
@@ -109,7 +110,7 @@ def main():
 
     import paper_1511_05946_amd.acdc as acdc
     from paper_1511_05946_amd._lib import lib
-    from paper_1511_05946_amd.workloads import HEADLINE, WORKLOADS, make_inputs
+    from paper_1511_05946_amd.workloads import FLAG_BIAS, HEADLINE, WORKLOADS, make_bias, make_inputs
 
     w = WORKLOADS[args.workload or HEADLINE]
     dev = torch.device("cuda:0")
@@ -126,6 +127,7 @@ def main():
     x, A, D, perm, gy = make_inputs(w.N, w.K, w.batch, w.flags, args.seed)
     t = lambda a: torch.from_numpy(a).to(dev)
     xt, At, Dt, pt, gyt = t(x), t(A), t(D), t(perm), t(gy)
+    bt = t(make_bias(w.N, w.K, args.seed)) if w.flags & FLAG_BIAS else None
     fl = w.flags & ~acdc.FLAG_COMPLEX
     acdc.prepare(w.N, w.flags)
     y = torch.empty_like(xt)
@@ -133,10 +135,10 @@ def main():
 
     def step():
         if args.recompute:
-            acdc.forward(xt, At, Dt, pt, fl, out=y)
-            return acdc.backward(xt, gyt, At, Dt, pt, fl, saved=None)
-        acdc.forward(xt, At, Dt, pt, fl, out=y, saved=saved)
-        return acdc.backward(xt, gyt, At, Dt, pt, fl, saved=saved)
+            acdc.forward(xt, At, Dt, pt, fl, out=y, bias=bt)
+            return acdc.backward(xt, gyt, At, Dt, pt, fl, saved=None, bias=bt)
+        acdc.forward(xt, At, Dt, pt, fl, out=y, saved=saved, bias=bt)
+        return acdc.backward(xt, gyt, At, Dt, pt, fl, saved=saved, bias=bt)
 
     for _ in range(args.warmup):
         step()
@@ -183,7 +185,8 @@ def main():
         "metric": METRIC, "value": round(value, 1), "unit": UNIT, "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "c64" if w.complex else "f32",
-        "data": "synthetic (seeded; x ~ relu(N(0,1)), A,D ~ N(1,0.1^2), random permutations)",
+        "data": "synthetic (seeded; x ~ relu(N(0,1)), A,D ~ N(1,0.1^2), random permutations"
+                + (", D-domain biases ~ N(0,0.1^2))" if bt is not None else ")"),
         "config": {"workload": w.name, "N": w.N, "K": w.K, "batch": w.batch,
                    "flags": w.flags, "parallelism": "single GPU",
                    "backward": "recompute" if args.recompute else "saved layer inputs"},

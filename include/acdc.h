@@ -18,19 +18,25 @@
  * through a fixed permutation and applying ReLU between layers (Sec. 6.2):
  *
  *     u_k = z_{k-1}[perm[k]]      (if ACDC_FLAG_PERM; z_{-1} = x)
- *     v_k = u_k A_k C D_k C^{-1}
+ *     v_k = (u_k A_k C D_k + b_k) C^{-1}   (b_k only with ACDC_FLAG_BIAS)
  *     z_k = max(v_k, 0)           (if ACDC_FLAG_RELU and k < K-1), else v_k
  *     y   = z_{K-1}
  *
+ * The bias b_k is added to the D-domain term of each layer, where Sec. 6.2
+ * puts the additive biases of its cascade (on D, none on A), so that it
+ * lands just before the ReLU.
+ *
  * The backward pass gives dL/dx, dL/da_k, dL/dd_k (Sec. 4 derivative block)
- * with the parameter gradients summed over the batch.  Complex gradients use
- * the convention grad = dL/dRe + i dL/dIm (so dL/dx = dL/dy W^H).
+ * and, with a bias, dL/db_k = sum over rows of the DCT-II of dL/dv_k, with
+ * the parameter gradients summed over the batch.  Complex gradients use the
+ * convention grad = dL/dRe + i dL/dIm (so dL/dx = dL/dy W^H).
  *
  * Memory.  Every pointer is a device pointer on the current HIP device unless
  * stated otherwise.  Arrays are contiguous, row-major, 16-byte aligned:
  *   x, y, grad_y, grad_x   [batch][N]   float (ACDC) or interleaved complex64
  *                                       (AFDF: 2N floats per row)
  *   A, D, grad_A, grad_D   [K][N]       same element type as x
+ *   bias, grad_bias        [K][N]       float (ACDC_FLAG_BIAS, real layers only)
  *   perm                   [K][N]       int32, each row a permutation of 0..N-1
  *   saved                  [K-1][batch][N] layer inputs u_1..u_{K-1}
  * The caller owns every buffer, including the workspaces; the library only
@@ -66,15 +72,17 @@ extern "C" {
 typedef struct ihipStream_t* acdc_stream_t;
 
 enum acdc_flags {
-  ACDC_FLAG_PERM = 1u,    /* gather each layer's input through perm[k] */
-  ACDC_FLAG_RELU = 2u,    /* ReLU after layers 0..K-2 (not with COMPLEX) */
-  ACDC_FLAG_COMPLEX = 4u  /* complex AFDF layers on interleaved complex64 */
+  ACDC_FLAG_PERM = 1u,       /* gather each layer's input through perm[k] */
+  ACDC_FLAG_RELU = 2u,       /* ReLU after layers 0..K-2 (not with COMPLEX) */
+  ACDC_FLAG_COMPLEX = 4u,    /* complex AFDF layers on interleaved complex64 */
+  ACDC_FLAG_BIAS = 8u,       /* add b_k to each layer's D-domain term (not with COMPLEX) */
+  ACDC_FLAG_ACCUMULATE = 16u /* backward adds into grad_A, grad_D, grad_bias instead of overwriting */
 };
 
 enum acdc_status {
   ACDC_OK = 0,
   ACDC_ERR_INVALID_ARG = -1, /* null/misaligned/aliased pointer, bad size or flag */
-  ACDC_ERR_UNSUPPORTED = -2, /* width N not built, or COMPLEX|RELU */
+  ACDC_ERR_UNSUPPORTED = -2, /* width N not built, or COMPLEX with RELU or BIAS */
   ACDC_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required */
   ACDC_ERR_HIP = -4          /* a HIP runtime call failed */
 };
@@ -95,28 +103,33 @@ size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
 size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
 
 /* Bytes of workspace acdc_backward needs: per-workgroup partial sums of the
- * parameter gradients, the per-layer quartet coefficients, and -- when
- * have_saved is 0 -- room to recompute the layer inputs (the paper's
- * recompute policy, Sec. 5.3). */
+ * parameter gradients, the per-layer quartet coefficients, the batch sums
+ * behind the bias gradient (ACDC_FLAG_BIAS), and -- when have_saved is 0 --
+ * room to recompute the layer inputs (the paper's recompute policy,
+ * Sec. 5.3). */
 size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags, int have_saved);
 
-/* Forward cascade: y = cascade(x).  If `saved` is non-null it also stores the
- * layer inputs u_1..u_{K-1} there, for acdc_backward; saved_bytes must be at
- * least acdc_saved_bytes(...) (else ACDC_ERR_WORKSPACE, nothing launched). */
-int acdc_forward(const float* x, float* y, const float* A, const float* D, const int32_t* perm,
-                 int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, size_t saved_bytes,
-                 void* workspace, size_t workspace_bytes, acdc_stream_t stream);
+/* Forward cascade: y = cascade(x).  `bias` is read with ACDC_FLAG_BIAS and
+ * ignored (may be null) otherwise; `perm` likewise with ACDC_FLAG_PERM.  If
+ * `saved` is non-null it also stores the layer inputs u_1..u_{K-1} there, for
+ * acdc_backward; saved_bytes must be at least acdc_saved_bytes(...) (else
+ * ACDC_ERR_WORKSPACE, nothing launched). */
+int acdc_forward(const float* x, float* y, const float* A, const float* D, const float* bias,
+                 const int32_t* perm, int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved,
+                 size_t saved_bytes, void* workspace, size_t workspace_bytes, acdc_stream_t stream);
 
 /* Backward cascade.  Given x and grad_y = dL/dy, writes grad_x = dL/dx and
- * grad_A, grad_D = dL/da_k, dL/dd_k summed over the batch (overwritten, not
- * accumulated).  `saved` is the buffer filled by acdc_forward for the same x,
- * A, D, perm (saved_bytes as there), or null, in which case the layer inputs
- * are recomputed into the workspace first.  batch == 0 writes zero parameter
- * gradients. */
-int acdc_backward(const float* x, const float* grad_y, const float* A, const float* D,
+ * grad_A, grad_D = dL/da_k, dL/dd_k summed over the batch, and with
+ * ACDC_FLAG_BIAS grad_bias = dL/db_k (bias and grad_bias are then required,
+ * and ignored otherwise).  The parameter gradients are overwritten, or with
+ * ACDC_FLAG_ACCUMULATE added to what the arrays hold.  `saved` is the buffer
+ * filled by acdc_forward for the same x, A, D, bias, perm (saved_bytes as
+ * there), or null, in which case the layer inputs are recomputed into the
+ * workspace first.  batch == 0 gives zero parameter gradients. */
+int acdc_backward(const float* x, const float* grad_y, const float* A, const float* D, const float* bias,
                   const int32_t* perm, const float* saved, size_t saved_bytes, float* grad_x, float* grad_A,
-                  float* grad_D, int64_t batch, int32_t N, int32_t K, uint32_t flags, void* workspace,
-                  size_t workspace_bytes, acdc_stream_t stream);
+                  float* grad_D, float* grad_bias, int64_t batch, int32_t N, int32_t K, uint32_t flags,
+                  void* workspace, size_t workspace_bytes, acdc_stream_t stream);
 
 /* Kernel timing for benchmarks (not for the callers' hot path).  While
  * enabled, each launch of the forward-cascade kernel (kind 0), the

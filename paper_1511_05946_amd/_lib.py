@@ -24,9 +24,9 @@ SIGNATURES = {
     "acdc_saved_bytes": (_SZ, [_I64, _I32, _I32, _U32]),
     "acdc_forward_workspace_bytes": (_SZ, [_I64, _I32, _I32, _U32]),
     "acdc_backward_workspace_bytes": (_SZ, [_I64, _I32, _I32, _U32, ctypes.c_int]),
-    "acdc_forward": (ctypes.c_int, [_P, _P, _P, _P, _P, _I64, _I32, _I32, _U32, _P, _SZ, _P, _SZ, _P]),
+    "acdc_forward": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _I64, _I32, _I32, _U32, _P, _SZ, _P, _SZ, _P]),
     "acdc_backward": (ctypes.c_int,
-                      [_P, _P, _P, _P, _P, _P, _SZ, _P, _P, _P, _I64, _I32, _I32, _U32, _P, _SZ, _P]),
+                      [_P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P, _P, _P, _I64, _I32, _I32, _U32, _P, _SZ, _P]),
     "acdc_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "acdc_profile_read": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     "acdc_status_string": (ctypes.c_char_p, [ctypes.c_int]),

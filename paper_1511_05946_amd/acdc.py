@@ -6,7 +6,9 @@ is enqueued on the current torch stream of that device.
 
 Layer (Sec. 4 of arXiv:1511.05946): y = x A C D C^{-1} on row vectors, C the
 orthonormal DCT-II; the complex AFDF layer of Sec. 3 uses the DFT.  A cascade
-chains K layers with optional fixed permutations and ReLU between them.
+chains K layers with optional fixed permutations and ReLU between them, and
+optionally a bias b_k added to each layer's D-domain term (Sec. 6.2):
+y = (x A C D + b) C^{-1}.
 """
 
 from __future__ import annotations
@@ -18,6 +20,8 @@ from ._lib import lib, status_string
 FLAG_PERM = 1
 FLAG_RELU = 2
 FLAG_COMPLEX = 4
+FLAG_BIAS = 8
+FLAG_ACCUMULATE = 16
 
 
 class ACDCError(RuntimeError):
@@ -32,9 +36,11 @@ def _check(rc: int, what: str):
         raise ACDCError(f"{what}: {status_string(rc)}{extra}")
 
 
-def _flags(flags: int, x: torch.Tensor) -> int:
+def _flags(flags: int, x: torch.Tensor, bias=None) -> int:
     if x.is_complex():
         flags |= FLAG_COMPLEX
+    if bias is not None:
+        flags |= FLAG_BIAS
     return flags
 
 
@@ -102,24 +108,24 @@ def saved_layer_inputs(saved: torch.Tensor, x: torch.Tensor, K: int) -> torch.Te
     return saved[: max(K - 1, 0) * B * N].view(max(K - 1, 0), B, N)
 
 
-def forward(x, A, D, perm=None, flags: int = 0, save: bool = False, out=None, saved=None):
-    """y = cascade(x).  Returns (y, saved) where saved holds the layer inputs
-    u_1..u_{K-1} for acdc_backward when ``save`` (or a preallocated
-    ``saved``) is given."""
-    flags = _flags(flags, x)
+def forward(x, A, D, perm=None, flags: int = 0, save: bool = False, out=None, saved=None, bias=None):
+    """y = cascade(x), with the D-domain biases ``bias`` [K, N] if given.
+    Returns (y, saved) where saved holds the layer inputs u_1..u_{K-1} for
+    acdc_backward when ``save`` (or a preallocated ``saved``) is given."""
+    flags = _flags(flags, x, bias)
     cplx = bool(flags & FLAG_COMPLEX)
     B, N, K = _dims(x, A)
     if out is None:
         out = torch.empty_like(x)
     if save and saved is None:
         saved = alloc_saved(x, K, flags)
-    _validate({"x": x, "A": A, "D": D, "y": out, "saved": saved,
+    _validate({"x": x, "A": A, "D": D, "bias": bias, "y": out, "saved": saved,
                "perm": perm if flags & FLAG_PERM else None}, cplx, x.device)
     L = lib()
     ws_bytes = L.acdc_forward_workspace_bytes(B, N, K, flags)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=x.device)
     with torch.cuda.device(x.device):
-        rc = L.acdc_forward(_ptr(x), _ptr(out), _ptr(A), _ptr(D),
+        rc = L.acdc_forward(_ptr(x), _ptr(out), _ptr(A), _ptr(D), _ptr(bias),
                             _ptr(perm) if flags & FLAG_PERM else None, B, N, K, flags,
                             _ptr(saved) if (saved is not None and saved.numel() > 0) else None,
                             _nbytes(saved), _ptr(ws), ws_bytes, _stream(x.device))
@@ -127,50 +133,61 @@ def forward(x, A, D, perm=None, flags: int = 0, save: bool = False, out=None, sa
     return out, saved
 
 
-def backward(x, grad_y, A, D, perm=None, flags: int = 0, saved=None):
-    """(grad_x, grad_A, grad_D); parameter gradients are summed over the batch.
-    Without ``saved`` (from ``forward(..., save=True)`` on the same inputs)
-    the forward is recomputed inside the call."""
-    flags = _flags(flags, x)
+def backward(x, grad_y, A, D, perm=None, flags: int = 0, saved=None, bias=None, grads=None):
+    """(grad_x, grad_A, grad_D), plus grad_bias when ``bias`` is given; the
+    parameter gradients are summed over the batch.  Without ``saved`` (from
+    ``forward(..., save=True)`` on the same inputs) the forward is recomputed
+    inside the call.  ``grads`` = (grad_A, grad_D[, grad_bias]) tensors to
+    write into; with FLAG_ACCUMULATE in ``flags`` the sums are added to them."""
+    flags = _flags(flags, x, bias)
     cplx = bool(flags & FLAG_COMPLEX)
     B, N, K = _dims(x, A)
     gx = torch.empty_like(x)
-    gA = torch.empty_like(A)
-    gD = torch.empty_like(D)
-    _validate({"x": x, "grad_y": grad_y, "A": A, "D": D, "saved": saved,
-               "perm": perm if flags & FLAG_PERM else None}, cplx, x.device)
+    if grads is None:
+        if flags & FLAG_ACCUMULATE:
+            raise ValueError("FLAG_ACCUMULATE needs the gradient tensors to add into (grads=...)")
+        grads = (torch.empty_like(A), torch.empty_like(D)) + ((torch.empty_like(bias),) if bias is not None else ())
+    gA, gD = grads[0], grads[1]
+    gB = grads[2] if bias is not None else None
+    _validate({"x": x, "grad_y": grad_y, "A": A, "D": D, "bias": bias, "saved": saved, "grad_A": gA,
+               "grad_D": gD, "grad_bias": gB, "perm": perm if flags & FLAG_PERM else None}, cplx, x.device)
     L = lib()
     use_saved = saved is not None and saved.numel() > 0
     have_saved = 1 if (use_saved or K == 1) else 0
     ws_bytes = L.acdc_backward_workspace_bytes(B, N, K, flags, have_saved)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=x.device)
     with torch.cuda.device(x.device):
-        rc = L.acdc_backward(_ptr(x), _ptr(grad_y), _ptr(A), _ptr(D),
+        rc = L.acdc_backward(_ptr(x), _ptr(grad_y), _ptr(A), _ptr(D), _ptr(bias),
                              _ptr(perm) if flags & FLAG_PERM else None,
                              _ptr(saved) if use_saved else None, _nbytes(saved),
-                             _ptr(gx), _ptr(gA), _ptr(gD), B, N, K, flags, _ptr(ws), ws_bytes,
+                             _ptr(gx), _ptr(gA), _ptr(gD), _ptr(gB), B, N, K, flags, _ptr(ws), ws_bytes,
                              _stream(x.device))
     _check(rc, "acdc_backward")
-    return gx, gA, gD
+    return (gx, gA, gD, gB) if bias is not None else (gx, gA, gD)
 
 
 class ACDCCascade(torch.autograd.Function):
     """autograd wrapper: stores the layer inputs in the forward pass."""
 
     @staticmethod
-    def forward(ctx, x, A, D, perm, flags):
-        y, saved = forward(x.contiguous(), A.contiguous(), D.contiguous(), perm, flags, save=True)
-        ctx.save_for_backward(x, A, D, perm if perm is not None else torch.empty(0), saved)
+    def forward(ctx, x, A, D, perm, flags, bias=None):
+        y, saved = forward(x.contiguous(), A.contiguous(), D.contiguous(), perm, flags, save=True,
+                           bias=bias.contiguous() if bias is not None else None)
+        ctx.save_for_backward(x, A, D, perm if perm is not None else torch.empty(0),
+                              bias if bias is not None else torch.empty(0), saved)
         ctx.flags = flags
         ctx.has_perm = perm is not None
+        ctx.has_bias = bias is not None
         return y
 
     @staticmethod
     def backward(ctx, gy):
-        x, A, D, perm, saved = ctx.saved_tensors
-        gx, gA, gD = backward(x, gy.contiguous(), A, D, perm if ctx.has_perm else None, ctx.flags, saved)
-        return gx, gA, gD, None, None
+        x, A, D, perm, bias, saved = ctx.saved_tensors
+        out = backward(x, gy.contiguous(), A, D, perm if ctx.has_perm else None, ctx.flags, saved,
+                       bias=bias if ctx.has_bias else None)
+        gB = out[3] if ctx.has_bias else None
+        return out[0], out[1], out[2], None, None, gB
 
 
-def acdc_cascade(x, A, D, perm=None, flags: int = 0):
-    return ACDCCascade.apply(x, A, D, perm, flags)
+def acdc_cascade(x, A, D, perm=None, flags: int = 0, bias=None):
+    return ACDCCascade.apply(x, A, D, perm, flags, bias)

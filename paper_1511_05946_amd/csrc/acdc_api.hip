@@ -7,6 +7,7 @@
 //   k_real_bwd     backward cascade with the reduction of dL/da, dL/dd over
 //                  the workgroup's rows into one partial per workgroup
 //   k_real_reduce  fixed-order sum of the partials over workgroups
+//   k_real_dct     DCT-II of the batch sums of g (bias gradient, tiny)
 //   k_cplx_*       the same for the complex AFDF layers
 #include <hip/hip_runtime.h>
 
@@ -47,19 +48,19 @@ struct DevCtx {
 };
 
 template <class PL>
-__global__ __launch_bounds__(256) void k_real_mq(const float* __restrict__ D, float4* __restrict__ Mq, int K,
-                                                 const char* __restrict__ tab) {
+__global__ __launch_bounds__(256) void k_real_mq(const float* __restrict__ D, const float* __restrict__ Bias,
+                                                 float4* __restrict__ Mq, int K, const char* __restrict__ tab) {
   constexpr int E = PL::NSL * PL::T;
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i >= (long long)K * E) return;
   const int k = int(i / E), e = int(i % E);
-  float4 row[3];
-  real_mq_entry<PL>(D + (long long)k * PL::N, tab, e, row);
+  float4 row[kMqRows];
+  real_mq_entry<PL>(D + (long long)k * PL::N, Bias != nullptr ? Bias + (long long)k * PL::N : nullptr, tab, e, row);
   // layout [k][slot][r][t]
   const int slot = e / PL::T, t = e % PL::T;
-  float4* out = Mq + (long long)k * E * 3 + (long long)slot * 3 * PL::T + t;
+  float4* out = Mq + (long long)k * E * kMqRows + (long long)slot * kMqRows * PL::T + t;
 #pragma unroll
-  for (int r = 0; r < 3; ++r) out[r * PL::T] = row[r];
+  for (int r = 0; r < kMqRows; ++r) out[r * PL::T] = row[r];
 }
 
 // Copy of the FFT twiddle table (the first TW_FLOAT2 float2 of the plan's
@@ -74,7 +75,7 @@ __device__ __forceinline__ void copy_twiddles(float* dst, const char* tab, int t
 // The forward kernel is persistent: workgroup b handles row groups (tiles)
 // b, b + gridDim.x, ...  Rows are independent, so results do not depend on
 // the grid size.
-template <class PL>
+template <class PL, bool BIAS>
 __global__ __launch_bounds__(Launch<PL>::FWD_THREADS)
 __attribute__((amdgpu_waves_per_eu(Launch<PL>::FWD_WPE))) void k_real_fwd(RealArgs a, long long ntiles) {
   using L = Launch<PL>;
@@ -94,15 +95,15 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::FWD_WPE))) void k_real_fwd(RealAr
     ctx.sync_all();
     const LdsView tw = LdsView::of(twl);
     for (long long tile = blockIdx.x; tile < ntiles; tile += gridDim.x)
-      real_forward_row<PL>(ctx, a, t, tile * L::FWD_ROWS, unsigned(r), slab, tw);
+      real_forward_row<PL, BIAS>(ctx, a, t, tile * L::FWD_ROWS, unsigned(r), slab, tw);
   } else {
     const GView tw = GView::of(a.tab);
     for (long long tile = blockIdx.x; tile < ntiles; tile += gridDim.x)
-      real_forward_row<PL>(ctx, a, t, tile * L::FWD_ROWS, unsigned(r), slab, tw);
+      real_forward_row<PL, BIAS>(ctx, a, t, tile * L::FWD_ROWS, unsigned(r), slab, tw);
   }
 }
 
-template <class PL>
+template <class PL, bool BIAS>
 __global__ __launch_bounds__(Launch<PL>::BWD_THREADS)
 __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealArgs a) {
   using L = Launch<PL>;
@@ -123,10 +124,10 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealAr
     float* twl = lds;
     copy_twiddles<PL>(twl, a.tab, tid, L::BWD_THREADS);
     ctx.sync_all();
-    real_backward_row<PL, L::BWD_ROWS>(ctx, a, t, tile * L::BWD_ROWS, unsigned(r), tid, tile, rows, slab,
+    real_backward_row<PL, L::BWD_ROWS, BIAS>(ctx, a, t, tile * L::BWD_ROWS, unsigned(r), tid, tile, rows, slab,
                                        LdsView::of(twl));
   } else {
-    real_backward_row<PL, L::BWD_ROWS>(ctx, a, t, tile * L::BWD_ROWS, unsigned(r), tid, tile, rows, slab,
+    real_backward_row<PL, L::BWD_ROWS, BIAS>(ctx, a, t, tile * L::BWD_ROWS, unsigned(r), tid, tile, rows, slab,
                                        GView::of(a.tab));
   }
 }
@@ -141,8 +142,9 @@ static_assert(kRedEntries * kRedPhases == 256, "one thread per (entry, phase)");
 template <class PL>
 __global__ __launch_bounds__(256) void k_real_reduce(const float* __restrict__ partial, long long ntiles, int K,
                                                      float* __restrict__ gA, float* __restrict__ gD,
-                                                     const char* __restrict__ tab) {
-  constexpr long long PS4 = partial_entries4<PL>();
+                                                     float* __restrict__ gS, const char* __restrict__ tab,
+                                                     int bias, int accumulate) {
+  const long long PS4 = partial_entries4<PL>(bias != 0);
   __shared__ float4 ph[kRedPhases][kRedEntries];
   const int lane = threadIdx.x % kRedEntries, g = threadIdx.x / kRedEntries;
   const long long i = (long long)blockIdx.x * kRedEntries + lane;
@@ -154,8 +156,20 @@ __global__ __launch_bounds__(256) void k_real_reduce(const float* __restrict__ p
     float4 all[kRedPhases];
 #pragma unroll
     for (int q = 0; q < kRedPhases; ++q) all[q] = ph[q][lane];
-    real_reduce_store4<PL>(phases_total4(all), int(i / PS4), int(i % PS4), gA, gD, tab);
+    real_reduce_store4<PL>(phases_total4(all), int(i / PS4), int(i % PS4), gA, gD, gS, tab, accumulate != 0);
   }
+}
+
+// Bias gradient: grad_b[k] (+)= DCT-II of the batch sum of g at layer k.
+// One workgroup of T threads per layer.
+template <class PL>
+__global__ __launch_bounds__(PL::T) void k_real_dct(const float* __restrict__ S, float* __restrict__ gB,
+                                                    const float4* __restrict__ Mq, const char* __restrict__ tab,
+                                                    int accumulate) {
+  __shared__ float lds[Launch<PL>::FWD_SLAB];
+  DevCtx<PL::T> ctx;
+  const long long k = blockIdx.x;
+  real_dct_row<PL>(ctx, S + k * PL::N, gB + k * PL::N, Mq, accumulate != 0, threadIdx.x, lds, GView::of(tab), tab);
 }
 
 template <class PL>
@@ -187,7 +201,8 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_cplx_bwd(CplxAr
 
 template <class PL>
 __global__ __launch_bounds__(256) void k_cplx_reduce(const float* __restrict__ partial, long long ntiles, int K,
-                                                     float* __restrict__ gA, float* __restrict__ gD) {
+                                                     float* __restrict__ gA, float* __restrict__ gD,
+                                                     int accumulate) {
   constexpr long long PS4 = partial_entries4<PL>();
   __shared__ float4 ph[kRedPhases][kRedEntries];
   const int lane = threadIdx.x % kRedEntries, g = threadIdx.x / kRedEntries;
@@ -200,7 +215,7 @@ __global__ __launch_bounds__(256) void k_cplx_reduce(const float* __restrict__ p
     float4 all[kRedPhases];
 #pragma unroll
     for (int q = 0; q < kRedPhases; ++q) all[q] = ph[q][lane];
-    cplx_reduce_store4<PL>(phases_total4(all), int(i / PS4), int(i % PS4), gA, gD);
+    cplx_reduce_store4<PL>(phases_total4(all), int(i / PS4), int(i % PS4), gA, gD, accumulate != 0);
   }
 }
 
@@ -332,9 +347,15 @@ long long persistent_grid(const void* kernel, int threads, long long tiles) {
   return (n > 0 && n < tiles) ? n : tiles;
 }
 
+constexpr uint32_t kAllFlags = kFlagPerm | kFlagRelu | kFlagComplex | kFlagBias | kFlagAccumulate;
+
+bool flags_supported(uint32_t flags) {
+  return !((flags & kFlagComplex) && (flags & (kFlagRelu | kFlagBias)));
+}
+
 int check_common(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
-  if (flags & ~7u) return ACDC_ERR_INVALID_ARG;
-  if ((flags & kFlagComplex) && (flags & kFlagRelu)) return ACDC_ERR_UNSUPPORTED;
+  if (flags & ~kAllFlags) return ACDC_ERR_INVALID_ARG;
+  if (!flags_supported(flags)) return ACDC_ERR_UNSUPPORTED;
   if (batch < 0 || K < 1 || K > 65535 || N < 1) return ACDC_ERR_INVALID_ARG;
   if (!supported(N, flags)) return ACDC_ERR_UNSUPPORTED;
   if (batch > (int64_t(1) << 40) / N) return ACDC_ERR_INVALID_ARG;
@@ -377,24 +398,25 @@ size_t saved_floats(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
 }
 
 struct WsLayout {
-  size_t mq = 0, partial = 0, stash = 0, total = 0;
-  size_t off_mq = 0, off_partial = 0, off_stash = 0;
+  size_t mq = 0, partial = 0, gs = 0, stash = 0, total = 0;
+  size_t off_mq = 0, off_partial = 0, off_gs = 0, off_stash = 0;
 };
 
 template <class PL>
 size_t mq_bytes(int32_t K) {
-  return align256(size_t(K) * PL::NSL * 3 * PL::T * sizeof(float4));
+  return align256(size_t(K) * PL::NSL * kMqRows * PL::T * sizeof(float4));
 }
 
 WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved) {
   WsLayout w;
+  const bool bias = (flags & kFlagBias) != 0;
   auto f = [&]<class PL>() {
     const long long tiles = bwd_tiles<PL>(batch);
-    if constexpr (PL::kComplex) {
-      w.partial = align256(size_t(tiles) * K * 4 * PL::N * sizeof(float));
-    } else {
-      w.partial = align256(size_t(tiles) * K * (PL::N + PL::QF) * sizeof(float));
-      if (batch > 0) w.mq = mq_bytes<PL>(K);
+    w.partial = align256(size_t(tiles) * K * partial_entries4<PL>(bias) * sizeof(float4));
+    if constexpr (!PL::kComplex) {
+      // the bias gradient's DCT reads w, qa, qb' from the quartet table
+      if (batch > 0 || bias) w.mq = mq_bytes<PL>(K);
+      if (bias) w.gs = align256(size_t(K) * PL::N * sizeof(float));
     }
   };
   if (flags & kFlagComplex) dispatch_complex(N, f);
@@ -402,7 +424,8 @@ WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool ha
   if (!have_saved && K > 1) w.stash = align256(saved_floats(batch, N, K, flags) * 4);
   w.off_mq = 0;
   w.off_partial = w.off_mq + w.mq;
-  w.off_stash = w.off_partial + w.partial;
+  w.off_gs = w.off_partial + w.partial;
+  w.off_stash = w.off_gs + w.gs;
   w.total = w.off_stash + w.stash;
   return w;
 }
@@ -415,20 +438,26 @@ size_t fwd_ws(int32_t N, int32_t K, uint32_t flags) {
 }
 
 template <class PL>
-int launch_real_mq(const float* D, float4* Mq, int K, const char* tab, hipStream_t s) {
+int launch_real_mq(const float* D, const float* Bias, float4* Mq, int K, const char* tab, hipStream_t s) {
   const long long n = (long long)K * PL::NSL * PL::T;
-  hipLaunchKernelGGL(k_real_mq<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, D, Mq, K, tab);
+  hipLaunchKernelGGL(k_real_mq<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, D, Bias, Mq, K, tab);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? ACDC_OK : hip_fail(e);
 }
 
+template <class PL, bool BIAS>
+void launch_real_fwd_k(const RealArgs& a, hipStream_t s) {
+  const long long tiles = fwd_blocks<PL>(a.batch);
+  const long long grid = persistent_grid(reinterpret_cast<const void*>(&k_real_fwd<PL, BIAS>),
+                                         Launch<PL>::FWD_THREADS, tiles);
+  hipLaunchKernelGGL((k_real_fwd<PL, BIAS>), dim3(unsigned(grid)), dim3(Launch<PL>::FWD_THREADS), 0, s, a, tiles);
+}
+
 template <class PL>
 int launch_real_fwd(const RealArgs& a, hipStream_t s) {
-  const long long tiles = fwd_blocks<PL>(a.batch);
-  const long long grid = persistent_grid(reinterpret_cast<const void*>(&k_real_fwd<PL>), Launch<PL>::FWD_THREADS,
-                                         tiles);
   ProfScope prof(0, s);
-  hipLaunchKernelGGL(k_real_fwd<PL>, dim3(unsigned(grid)), dim3(Launch<PL>::FWD_THREADS), 0, s, a, tiles);
+  if (a.flags & kFlagBias) launch_real_fwd_k<PL, true>(a, s);
+  else launch_real_fwd_k<PL, false>(a, s);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? ACDC_OK : hip_fail(e);
 }
@@ -448,8 +477,8 @@ int launch_cplx_fwd(const CplxArgs& a, hipStream_t s) {
 using namespace acdc;
 
 extern "C" int acdc_supported(int32_t N, uint32_t flags) {
-  if (flags & ~7u) return 0;
-  if ((flags & kFlagComplex) && (flags & kFlagRelu)) return 0;
+  if (flags & ~kAllFlags) return 0;
+  if (!flags_supported(flags)) return 0;
   return supported(N, flags) ? 1 : 0;
 }
 
@@ -475,18 +504,21 @@ extern "C" size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_
   return bwd_layout(batch, N, K, flags, have_saved != 0).total;
 }
 
-extern "C" int acdc_forward(const float* x, float* y, const float* A, const float* D, const int32_t* perm,
-                            int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, size_t saved_bytes,
-                            void* workspace, size_t workspace_bytes, acdc_stream_t stream) {
+extern "C" int acdc_forward(const float* x, float* y, const float* A, const float* D, const float* bias,
+                            const int32_t* perm, int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved,
+                            size_t saved_bytes, void* workspace, size_t workspace_bytes, acdc_stream_t stream) {
   int rc = check_common(batch, N, K, flags);
   if (rc != ACDC_OK) return rc;
   if (saved != nullptr && saved_bytes < saved_floats(batch, N, K, flags) * sizeof(float)) return ACDC_ERR_WORKSPACE;
   const bool perm_on = (flags & kFlagPerm) != 0;
+  const bool bias_on = (flags & kFlagBias) != 0;
   if (batch == 0) return ACDC_OK;
-  rc = check_ptrs({x, y, A, D}, {perm_on ? (const void*)perm : nullptr, saved, workspace});
+  rc = check_ptrs({x, y, A, D}, {perm_on ? (const void*)perm : nullptr, bias_on ? (const void*)bias : nullptr,
+                                 saved, workspace});
   if (rc != ACDC_OK) return rc;
-  if (perm_on && perm == nullptr) return ACDC_ERR_INVALID_ARG;
-  if (!distinct({y, saved}, {x, y, A, D, perm, saved, workspace})) return ACDC_ERR_INVALID_ARG;
+  if ((perm_on && perm == nullptr) || (bias_on && bias == nullptr)) return ACDC_ERR_INVALID_ARG;
+  if (!bias_on) bias = nullptr;
+  if (!distinct({y, saved}, {x, y, A, D, bias, perm, saved, workspace})) return ACDC_ERR_INVALID_ARG;
   const size_t need = fwd_ws(N, K, flags);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return ACDC_ERR_WORKSPACE;
   const bool cplx = (flags & kFlagComplex) != 0;
@@ -502,7 +534,7 @@ extern "C" int acdc_forward(const float* x, float* y, const float* A, const floa
   } else {
     dispatch_real(N, [&]<class PL>() {
       float4* Mq = static_cast<float4*>(workspace);
-      rc = launch_real_mq<PL>(D, Mq, K, tab, s);
+      rc = launch_real_mq<PL>(D, bias, Mq, K, tab, s);
       if (rc != ACDC_OK) return;
       RealArgs a{x, y, A, Mq, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
       rc = launch_real_fwd<PL>(a, s);
@@ -512,21 +544,30 @@ extern "C" int acdc_forward(const float* x, float* y, const float* A, const floa
 }
 
 extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A, const float* D,
-                             const int32_t* perm, const float* saved, size_t saved_bytes, float* grad_x,
-                             float* grad_A, float* grad_D, int64_t batch, int32_t N, int32_t K, uint32_t flags,
-                             void* workspace, size_t workspace_bytes, acdc_stream_t stream) {
+                             const float* bias, const int32_t* perm, const float* saved, size_t saved_bytes,
+                             float* grad_x, float* grad_A, float* grad_D, float* grad_bias, int64_t batch,
+                             int32_t N, int32_t K, uint32_t flags, void* workspace, size_t workspace_bytes,
+                             acdc_stream_t stream) {
   int rc = check_common(batch, N, K, flags);
   if (rc != ACDC_OK) return rc;
   if (saved != nullptr && saved_bytes < saved_floats(batch, N, K, flags) * sizeof(float)) return ACDC_ERR_WORKSPACE;
   const bool perm_on = (flags & kFlagPerm) != 0;
-  rc = check_ptrs({A, D, grad_A, grad_D}, {perm_on ? (const void*)perm : nullptr, saved, workspace});
+  const bool bias_on = (flags & kFlagBias) != 0;
+  const int accumulate = (flags & kFlagAccumulate) != 0 ? 1 : 0;
+  if (!bias_on) {
+    bias = nullptr;
+    grad_bias = nullptr;
+  }
+  rc = check_ptrs({A, D, grad_A, grad_D}, {perm_on ? (const void*)perm : nullptr, bias, grad_bias, saved, workspace});
   if (rc != ACDC_OK) return rc;
+  if (bias_on && (bias == nullptr || grad_bias == nullptr)) return ACDC_ERR_INVALID_ARG;
   if (batch > 0) {
     rc = check_ptrs({x, grad_y, grad_x}, {});
     if (rc != ACDC_OK) return rc;
     if (perm_on && perm == nullptr) return ACDC_ERR_INVALID_ARG;
   }
-  if (!distinct({grad_x, grad_A, grad_D}, {x, grad_y, A, D, perm, saved, grad_x, grad_A, grad_D, workspace}))
+  if (!distinct({grad_x, grad_A, grad_D, grad_bias},
+                {x, grad_y, A, D, bias, perm, saved, grad_x, grad_A, grad_D, grad_bias, workspace}))
     return ACDC_ERR_INVALID_ARG;
   const bool have_saved = saved != nullptr || K == 1;
   const WsLayout w = bwd_layout(batch, N, K, flags, have_saved);
@@ -566,8 +607,7 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
       {
         ProfScope prof(2, s);
         hipLaunchKernelGGL(k_cplx_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(256), 0, s,
-                           partial, tiles, K,
-                         grad_A, grad_D);
+                           partial, tiles, K, grad_A, grad_D, accumulate);
         e = hipGetLastError();
       }
       rc = e == hipSuccess ? ACDC_OK : hip_fail(e);
@@ -576,10 +616,13 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
     dispatch_real(N, [&]<class PL>() {
       using L = Launch<PL>;
       const long long tiles = bwd_tiles<PL>(batch);
-      if (batch > 0) {
-        float4* Mq = reinterpret_cast<float4*>(ws + w.off_mq);
-        rc = launch_real_mq<PL>(D, Mq, K, tab, s);
+      float4* Mq = reinterpret_cast<float4*>(ws + w.off_mq);
+      float* gS = bias_on ? reinterpret_cast<float*>(ws + w.off_gs) : nullptr;
+      if (batch > 0 || bias_on) {
+        rc = launch_real_mq<PL>(D, bias, Mq, K, tab, s);
         if (rc != ACDC_OK) return;
+      }
+      if (batch > 0) {
         if (!have_saved) {
           RealArgs f{x, nullptr, A, Mq, perm, stash, nullptr, nullptr, nullptr, tab, batch, K, flags};
           rc = launch_real_fwd<PL>(f, s);
@@ -589,7 +632,8 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
         hipError_t e;
         {
           ProfScope prof(1, s);
-          hipLaunchKernelGGL(k_real_bwd<PL>, dim3(unsigned(tiles)), dim3(L::BWD_THREADS), 0, s, a);
+          if (bias_on) hipLaunchKernelGGL((k_real_bwd<PL, true>), dim3(unsigned(tiles)), dim3(L::BWD_THREADS), 0, s, a);
+          else hipLaunchKernelGGL((k_real_bwd<PL, false>), dim3(unsigned(tiles)), dim3(L::BWD_THREADS), 0, s, a);
           e = hipGetLastError();
         }
         if (e != hipSuccess) {
@@ -597,14 +641,18 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
           return;
         }
       }
-      const long long n = (long long)K * partial_entries4<PL>();
+      const long long n = (long long)K * partial_entries4<PL>(bias_on);
       hipError_t e;
       {
         ProfScope prof(2, s);
         hipLaunchKernelGGL(k_real_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(256), 0, s,
-                           partial, tiles, K,
-                         grad_A, grad_D, tab);
+                           partial, tiles, K, grad_A, grad_D, gS, tab, bias_on ? 1 : 0, accumulate);
         e = hipGetLastError();
+        if (e == hipSuccess && bias_on) {
+          hipLaunchKernelGGL(k_real_dct<PL>, dim3(unsigned(K)), dim3(PL::T), 0, s, gS, grad_bias, Mq, tab,
+                             accumulate);
+          e = hipGetLastError();
+        }
       }
       rc = e == hipSuccess ? ACDC_OK : hip_fail(e);
     });

@@ -32,7 +32,10 @@
 
 namespace acdc {
 
-enum : unsigned { kFlagPerm = 1u, kFlagRelu = 2u, kFlagComplex = 4u };
+enum : unsigned { kFlagPerm = 1u, kFlagRelu = 2u, kFlagComplex = 4u, kFlagBias = 8u, kFlagAccumulate = 16u };
+
+// Rows of the per-layer quartet-coefficient table (real_mq_entry).
+constexpr int kMqRows = 4;
 
 __host__ __device__ __forceinline__ float2 sel2(bool c, float2 a, float2 b) {
   return make_float2(c ? a.x : b.x, c ? a.y : b.y);
@@ -263,28 +266,36 @@ struct RealOps {
   static constexpr float kQbIm = float(0.3826834323650897717 / (2.0 * csqrt(double(N))));
 
   // Per-layer quartet coefficients (real_mq_entry), layout of one layer
-  // [slot][3][T] float4, lane-contiguous:
+  // [slot][kMqRows][T] float4, lane-contiguous:
   //   c0 = (L1_00, L1_01, L1_11, L2_00), c1 = (L2_01, L2_11, w.x, w.y),
   //   c2 = (qa.x, qa.y, qbr.x, qbr.y), qbr = (1 + i) qb   (backward only)
-  // Loops over the slots load slot s + PF while slot s computes; the first
-  // PF slots are loaded ahead, in the tail of the preceding FFT.
-  template <int NR>
+  //   c3 = (dzk.x, dzk.y, dzm.x, dzm.y)  D-domain bias through the
+  //        pre-twiddle (forward with a bias only)
+  // A loop over the slots loads NR of those rows (c0, c1 and, for NR = 3,
+  // row R2) of slot s + PF while slot s computes; the first PF slots are
+  // loaded ahead, in the tail of the preceding FFT.
+  template <int NR, int R2 = 2>
   struct MqTabs {
-    // slots loaded ahead: fewer for the backward's three rows per slot
+    // slots loaded ahead: fewer when three rows are loaded per slot
     static constexpr int PF = NSL < (NR == 2 ? ACDC_MQ_PF : ACDC_MQ_PF_BWD) ? NSL
                               : (NR == 2 ? ACDC_MQ_PF : ACDC_MQ_PF_BWD);
+    static constexpr int row(int r) { return r < 2 ? r : R2; }
     float4 m[NSL][NR];
   };
-  template <int NR>
-  __host__ __device__ __forceinline__ static void load_mslot(MqTabs<NR>& tb, int slot, unsigned t, GView mq) {
+  template <int NR, int R2>
+  __host__ __device__ __forceinline__ static void load_mslot(MqTabs<NR, R2>& tb, int slot, unsigned t, GView mq) {
 #pragma unroll
-    for (int r = 0; r < NR; ++r) tb.m[slot][r] = mq.ld4(t * 16u, unsigned((slot * 3 + r) * T * 16));
+    for (int r = 0; r < NR; ++r)
+      tb.m[slot][r] = mq.ld4(t * 16u, unsigned((slot * kMqRows + MqTabs<NR, R2>::row(r)) * T * 16));
   }
-  template <int NR>
-  __host__ __device__ __forceinline__ static void load_mhead(MqTabs<NR>& tb, unsigned t, GView mq) {
+  template <int NR, int R2>
+  __host__ __device__ __forceinline__ static void load_mhead(MqTabs<NR, R2>& tb, unsigned t, GView mq) {
 #pragma unroll
-    for (int s = 0; s < MqTabs<NR>::PF; ++s) load_mslot(tb, s, t, mq);
+    for (int s = 0; s < MqTabs<NR, R2>::PF; ++s) load_mslot(tb, s, t, mq);
   }
+  // Forward middle's table: c0, c1, plus c3 with a bias.
+  template <bool BIAS>
+  using FwdTabs = MqTabs<BIAS ? 3 : 2, 3>;
 
   // Real-FFT split of a Makhoul pair: E = Z[k] + conj Z[M-k],
   // O = (Z[k] - conj Z[M-k]) / i, s1 = E + w O, s2 = E - w O.
@@ -326,10 +337,11 @@ struct RealOps {
   }
 
   // Forward middle of a layer, in place per quartet slot: Z (frequency
-  // layout) -> DCT-II quartet -> * d -> DCT-III pre-twiddle -> Z', as
-  // split + sym_back (32 operations per slot).
-  __host__ __device__ __forceinline__ static void mid(float2 (&v)[P], unsigned t, GView mq, MqTabs<2>& tb) {
-    constexpr int PFM = MqTabs<2>::PF;
+  // layout) -> DCT-II quartet -> * d (+ b) -> DCT-III pre-twiddle -> Z', as
+  // split + sym_back (32 operations per slot; 4 more add the bias term).
+  template <bool BIAS>
+  __host__ __device__ __forceinline__ static void mid(float2 (&v)[P], unsigned t, GView mq, FwdTabs<BIAS>& tb) {
+    constexpr int PFM = FwdTabs<BIAS>::PF;
     const bool sp = (t == 0);
     permute0(v, sp);
 #pragma unroll
@@ -343,6 +355,11 @@ struct RealOps {
         float2& zm = v[2 * q * RL + 2 * RL - 1 - i];
         const float4 c0 = tb.m[slot][0], c1 = tb.m[slot][1];
         sym_back(split(zk, zm, make_float2(c1.z, c1.w)), c0, c1, zk, zm);
+        if constexpr (BIAS) {
+          const float4 c3 = tb.m[slot][2];
+          zk = make_float2(zk.x + c3.x, zk.y + c3.y);
+          zm = make_float2(zm.x + c3.z, zm.y + c3.w);
+        }
       }
     unpermute0(v, sp);
   }
@@ -400,7 +417,9 @@ struct RealArgs {
   unsigned flags;
 };
 
-template <class PL, class Ctx, class TW>
+// BIAS: the layers add the D-domain bias (Sec. 6.2), carried by row c3 of
+// the quartet table.
+template <class PL, bool BIAS, class Ctx, class TW>
 __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned t, long long row0, unsigned rr,
                                           float* slab, TW tab) {
   using O = RealOps<PL>;
@@ -417,7 +436,7 @@ __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned 
   O::load(GView::of(a.x + row0 * N), roff, v, L, valid);
   for (int k = 0; k < a.K; ++k) {
     const GView ak = GView::of(a.A + (long long)k * N);
-    const GView mq = GView::of(a.Mq + (long long)k * NSL * 3 * T);
+    const GView mq = GView::of(a.Mq + (long long)k * NSL * kMqRows * T);
     if (permute) {
       O::load_idx(idx, GView::of(a.perm + (long long)k * N), L);
       O::gather(ctx, v, L, slab, idx, [&] { O::load_vec(av, ak, L); });
@@ -427,22 +446,23 @@ __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned 
     if (a.saved != nullptr && k > 0 && valid)
       O::store(GView::of(a.saved + ((long long)(k - 1) * a.batch + row0) * N), roff, v, L);
     O::scale(v, av);
-    typename O::template MqTabs<2> tb;
+    typename O::template FwdTabs<BIAS> tb;
     O::template fft<false>(ctx, v, t, slab2, tab, [&] { O::load_mhead(tb, t, mq); });
-    O::mid(v, t, mq, tb);
+    O::template mid<BIAS>(v, t, mq, tb);
     O::template fft<true>(ctx, v, t, slab2, tab, [] {});
     if ((a.flags & kFlagRelu) && k < a.K - 1) O::relu(v);
   }
   if (a.y != nullptr && valid) O::store(GView::of(a.y + row0 * N), roff, v, L);
 }
 
-template <class PL, int ROWS, class Ctx, class TW>
+template <class PL, int ROWS, bool BIAS, class Ctx, class TW>
 __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned t, long long row0, unsigned rr,
                                            int tid, long long tile, float* lds, float* slab, TW tab) {
   using O = RealOps<PL>;
   constexpr int N = PL::N, P = PL::P, NSL = PL::NSL, T = PL::T, QF = PL::QF, NCH = O::NCH;
   constexpr int THREADS = ROWS * T;
-  constexpr long long PS = N + QF;
+  // tile partial per layer: [dL/da image N | dL/dd quartet image QF | row sum of g N (bias only)]
+  constexpr long long PS = N + QF + (BIAS ? N : 0);
   const long long row = row0 + rr;
   const bool valid = row < a.batch;
   const bool permute = (a.flags & kFlagPerm) != 0;
@@ -464,8 +484,20 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
   O::load_raw(uv, u_view(a.K - 1), roff, L, valid);
   for (int k = a.K - 1; k >= 0; --k) {
     const GView ak = GView::of(a.A + (long long)k * N);
-    const GView mq = GView::of(a.Mq + (long long)k * NSL * 3 * T);
+    const GView mq = GView::of(a.Mq + (long long)k * NSL * kMqRows * T);
     float* part = a.partial + (tile * a.K + k) * PS;
+    if constexpr (BIAS) {
+      // dL/db_k = sum over rows of DCT(g) = DCT(sum over rows of g): the
+      // tile sums g here (spatial, natural order); one DCT per layer of the
+      // batch sum follows the reduction.
+      ctx.sync_row();
+      O::for_chunks(g, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
+        reinterpret_cast<float4*>(slab)[lc + cc] = make_float4(lo.x, hi.y, lo.y, hi.x);
+      });
+      ctx.sync_all();
+      sum_rows<ROWS, PL::SLAB, THREADS, N>(lds, GView::of(part + N + QF), tid);
+      ctx.sync_all();
+    }
     // h2 = DCT(u * a), gh3 = DCT(g); dL/dd image h2 * gh3; g <- pre(gh3 * d)
     {
       float2 v[P];
@@ -521,6 +553,41 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
     }
   }
   if (valid) O::store(GView::of(a.gx + row0 * N), roff, g, L);
+}
+
+// DCT-II of one row (the bias gradient): out (+)= S C.  Forward FFT, then
+// per quartet slot the real-FFT split and the post-twiddle of the backward's
+// image (post_x), with w, qa, qbr from rows c1, c2 of a quartet table (they
+// do not depend on d).  One row per T threads.
+template <class PL, class Ctx, class TW>
+__host__ __device__ void real_dct_row(Ctx& ctx, const float* S, float* out, const float4* Mq, bool accumulate,
+                                      unsigned t, float* slab, TW tab, const char* tabc) {
+  using O = RealOps<PL>;
+  constexpr int P = PL::P, T = PL::T, RL = PL::RL, BL = PL::BL;
+  const typename O::Lane L = O::lane(t);
+  float2 v[P];
+  O::load(GView::of(S), 0u, v, L, true);
+  O::template fft<false>(ctx, v, t, reinterpret_cast<float2*>(slab), tab, [] {});
+  O::permute0(v, t == 0);
+  const GView mq = GView::of(Mq);
+#pragma unroll
+  for (int q = 0; q < BL / 2; ++q)
+#pragma unroll
+    for (int i = 0; i < RL; ++i) {
+      const int slot = q * RL + i, e = slot * T + int(t);
+      const float4 c1 = mq.ld4(t * 16u, unsigned((slot * kMqRows + 1) * T * 16));
+      const float4 c2 = mq.ld4(t * 16u, unsigned((slot * kMqRows + 2) * T * 16));
+      float X[4];
+      O::post_x(O::split(v[2 * q * RL + i], v[2 * q * RL + 2 * RL - 1 - i], make_float2(c1.z, c1.w)),
+                make_float2(c2.x, c2.y), make_float2(c2.z, c2.w), X);
+      X[1] = -X[1];
+      const int4 idx = reinterpret_cast<const int4*>(tabc + PL::OFF_QIDX)[e];
+      const int sm = (reinterpret_cast<const int*>(tabc + PL::OFF_QMASK)[e] >> 4) & 0xF;
+      const int id[4] = {idx.x, idx.y, idx.z, idx.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (sm & (1 << j)) out[id[j]] = accumulate ? out[id[j]] + X[j] : X[j];
+    }
 }
 
 }  // namespace acdc

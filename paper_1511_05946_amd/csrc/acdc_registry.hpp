@@ -175,7 +175,8 @@ __host__ __device__ __forceinline__ float4 real_dq_entry(const float* Dk, const 
 // slot needs w and 3 + 3 coefficients.  Output rows:
 //   out[0] = (L1_00, L1_01, L1_11, L2_00)
 //   out[1] = (L2_01, L2_11, w.x, w.y)
-//   out[2] = (qa.x, qa.y, qb.x, qb.y)   (the DCT-II outputs the backward needs)
+//   out[2] = (qa.x, qa.y, qbr.x, qbr.y) (the DCT-II outputs the backward needs)
+//   out[3] = the D-domain bias through the pre-twiddle (zero without bias)
 // Coefficients are formed in double from the fp32 twiddle tables and
 // rounded once.
 struct QuartetD {
@@ -188,7 +189,8 @@ __host__ __device__ inline QuartetD qd_mulc(QuartetD a, QuartetD w) {  // a * co
   return QuartetD{a.x * w.x + a.y * w.y, a.y * w.x - a.x * w.y};
 }
 template <class PL>
-__host__ __device__ inline void real_mq_entry(const float* Dk, const char* tab, int e, float4 (&out)[3]) {
+__host__ __device__ inline void real_mq_entry(const float* Dk, const float* Bk, const char* tab, int e,
+                                              float4 (&out)[kMqRows]) {
   const float4 m0 = reinterpret_cast<const float4*>(tab + PL::OFF_MK0)[e];
   const float4 m1 = reinterpret_cast<const float4*>(tab + PL::OFF_MK1)[e];
   const float4 d = real_dq_entry<PL>(Dk, tab, e);
@@ -217,6 +219,19 @@ __host__ __device__ inline void real_mq_entry(const float* Dk, const char* tab, 
   // qb rotated by (1 + i): the backward image then reads X[M-k], X[M+k] off
   // one complex product
   out[2] = make_float4(m0.z, m0.w, float(double(m1.x) - double(m1.y)), float(double(m1.x) + double(m1.y)));
+  // D-domain bias: Y gains b, so Ap gains (b0 - i b1) qap and Bp gains
+  // (b2 + b3 + i (b3 - b2)) conj(qb'); S = Ap + Bp, Dd = Ap - Bp give the
+  // constant (zk, zm) = (S + i conj(w) Dd, conj(S - i conj(w) Dd)) added
+  // after the 2x2 maps.
+  out[3] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (Bk != nullptr) {
+    const float4 b = real_dq_entry<PL>(Bk, tab, e);
+    const QuartetD ap = qd_mul(QuartetD{b.x, -double(b.y)}, qap);
+    const QuartetD bp = qd_mulc(QuartetD{double(b.z) + b.w, double(b.w) - b.z}, qbp);
+    const QuartetD S{ap.x + bp.x, ap.y + bp.y}, Dd{ap.x - bp.x, ap.y - bp.y};
+    const QuartetD cw = qd_mulc(Dd, QuartetD{m0.x, m0.y});  // Dd conj(w)
+    out[3] = make_float4(float(S.x - cw.y), float(S.y + cw.x), float(S.x + cw.y), float(cw.x - S.y));
+  }
 }
 
 // Fixed-order batch reduction of the per-tile partials.  Entry e (a float4)
@@ -254,38 +269,49 @@ __host__ __device__ __forceinline__ float4 phases_total4(const float4 (&ph)[kRed
   return s;
 }
 
-// Real path: float4 e4 in [0, (N + QF)/4) of layer k of the reduced
-// gradient.  The first N/4 are dL/da in natural order; the rest are the
-// dL/dd quartets of slot entries e = e4 - N/4, scattered to their indices.
+__host__ __device__ __forceinline__ void put4(float4* p, float4 s, bool accumulate) {
+  *p = accumulate ? add4(*p, s) : s;
+}
+__host__ __device__ __forceinline__ void put1(float* p, float s, bool accumulate) {
+  *p = accumulate ? *p + s : s;
+}
+
+// Real path: float4 e4 of layer k of the reduced gradient.  The first N/4
+// are dL/da in natural order; the next QF/4 are the dL/dd quartets of slot
+// entries e = e4 - N/4, scattered to their indices; with a bias the last N/4
+// are the batch sum of g (spatial), stored to gS for its DCT.
 template <class PL>
 __host__ __device__ __forceinline__ void real_reduce_store4(float4 s, int k, int e4, float* gA, float* gD,
-                                                            const char* tab) {
+                                                            float* gS, const char* tab, bool accumulate) {
   if (e4 < PL::N / 4) {
-    reinterpret_cast<float4*>(gA + (long long)k * PL::N)[e4] = s;
-  } else {
+    put4(reinterpret_cast<float4*>(gA + (long long)k * PL::N) + e4, s, accumulate);
+  } else if (e4 < (PL::N + PL::QF) / 4) {
     const int st = e4 - PL::N / 4;
     const int sm = (reinterpret_cast<const int*>(tab + PL::OFF_QMASK)[st] >> 4) & 0xF;
     const int4 idx = reinterpret_cast<const int4*>(tab + PL::OFF_QIDX)[st];
     float* gd = gD + (long long)k * PL::N;
-    if (sm & 1) gd[idx.x] = s.x;
-    if (sm & 2) gd[idx.y] = s.y;
-    if (sm & 4) gd[idx.z] = s.z;
-    if (sm & 8) gd[idx.w] = s.w;
+    if (sm & 1) put1(gd + idx.x, s.x, accumulate);
+    if (sm & 2) put1(gd + idx.y, s.y, accumulate);
+    if (sm & 4) put1(gd + idx.z, s.z, accumulate);
+    if (sm & 8) put1(gd + idx.w, s.w, accumulate);
+  } else {
+    reinterpret_cast<float4*>(gS + (long long)k * PL::N)[e4 - (PL::N + PL::QF) / 4] = s;
   }
 }
 
 // Complex path: float4 e4 in [0, N) of layer k (dL/da then dL/dd, natural).
 template <class PL>
-__host__ __device__ __forceinline__ void cplx_reduce_store4(float4 s, int k, int e4, float* gA, float* gD) {
-  if (e4 < PL::N / 2) reinterpret_cast<float4*>(gA + (long long)k * 2 * PL::N)[e4] = s;
-  else reinterpret_cast<float4*>(gD + (long long)k * 2 * PL::N)[e4 - PL::N / 2] = s;
+__host__ __device__ __forceinline__ void cplx_reduce_store4(float4 s, int k, int e4, float* gA, float* gD,
+                                                            bool accumulate) {
+  if (e4 < PL::N / 2) put4(reinterpret_cast<float4*>(gA + (long long)k * 2 * PL::N) + e4, s, accumulate);
+  else put4(reinterpret_cast<float4*>(gD + (long long)k * 2 * PL::N) + (e4 - PL::N / 2), s, accumulate);
 }
 
 // Float4 entries per layer of one tile's partial.
 template <class PL>
-constexpr long long partial_entries4() {
+constexpr long long partial_entries4(bool bias = false) {
   if constexpr (PL::kComplex) return (long long)PL::N;
-  else return (long long)(PL::N + PL::QF) / 4;
+  else return (long long)(PL::N + PL::QF + (bias ? PL::N : 0)) / 4;
 }
 
 }  // namespace acdc

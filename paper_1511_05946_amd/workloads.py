@@ -17,6 +17,11 @@ consecutive layers, Sec. 6.2), then the upstream gradient g_y.
   and the imaginary parts N(0, 0.1^2).
 * g_y ~ N(0, 1) (real and imaginary parts independently for the complex
   variant).
+
+The D-domain biases of the BIAS workloads (Sec. 6.2 adds them to the D
+matrices and starts them at 0; a trained cascade holds small nonzero values)
+come from a stream of their own, ``default_rng((seed, 8))``, so that the
+draws above do not change: b ~ N(0, 0.1^2), float32, [K, N].
 """
 
 from __future__ import annotations
@@ -28,6 +33,8 @@ import numpy as np
 FLAG_PERM = 1
 FLAG_RELU = 2
 FLAG_COMPLEX = 4
+FLAG_BIAS = 8
+FLAG_ACCUMULATE = 16
 
 
 @dataclass(frozen=True)
@@ -44,9 +51,10 @@ class Workload:
         return bool(self.flags & FLAG_COMPLEX)
 
 
-# The five workloads: one single layer, a permuted cascade, the headline
-# permuted ReLU cascade at N=4096, a non-power-of-two ReLU cascade at the
-# width of a flattened 6x6x256 conv map, and the complex AFDF cascade.
+# The workloads: one single layer, a permuted cascade, the headline permuted
+# ReLU cascade at N=4096, a non-power-of-two ReLU cascade at the width of a
+# flattened 6x6x256 conv map, the complex AFDF cascade, and the headline
+# cascade with D-domain biases.
 WORKLOADS = {
     "acdc_n256_k1": Workload("acdc_n256_k1", 256, 1, 64, 0,
                              "single ACDC layer N=256, batch 64, fp32"),
@@ -64,6 +72,11 @@ WORKLOADS = {
                                    FLAG_PERM | FLAG_COMPLEX,
                                    "complex AFDF cascade N=4096 K=8 batch 2048, complex64, "
                                    "permutations"),
+    # the headline cascade with the D-domain biases of Sec. 6.2
+    "acdc_n4096_k12_perm_relu_bias": Workload("acdc_n4096_k12_perm_relu_bias", 4096, 12, 8192,
+                                              FLAG_PERM | FLAG_RELU | FLAG_BIAS,
+                                              "ACDC cascade N=4096 K=12 batch 8192, fp32, "
+                                              "permutations + ReLU + D-domain biases"),
 }
 
 HEADLINE = "acdc_n4096_k12_perm_relu"
@@ -101,6 +114,12 @@ def make_inputs(N: int, K: int, batch: int, flags: int, seed: int = 0,
         gy = rng.standard_normal((batch, N))
     dt = np.complex64 if cplx else np.float32
     return (x.astype(dt), A.astype(dt), D.astype(dt), perm, gy.astype(dt))
+
+
+def make_bias(N: int, K: int, seed: int = 0) -> np.ndarray:
+    """D-domain biases b ~ N(0, 0.1^2), float32 [K, N], from their own stream."""
+    rng = np.random.default_rng((seed, 8))
+    return rng.normal(0.0, 0.1, (K, N)).astype(np.float32)
 
 
 def make_workload(name: str, seed: int = 0, batch: int | None = None):

@@ -39,8 +39,7 @@ void run_wg(int threads, F&& body) {
 // The batch reduction in the GPU kernel's order: per entry, the phase sums
 // in phase order.
 template <class PL, class Store>
-void reduce_all(const float* partial, long long ntiles, int K, Store&& store) {
-  constexpr long long PS4 = partial_entries4<PL>();
+void reduce_all(const float* partial, long long ntiles, int K, long long PS4, Store&& store) {
   const long long n = (long long)K * PS4;
   for (long long i = 0; i < n; ++i) {
     float4 ph[kRedPhases];
@@ -50,29 +49,26 @@ void reduce_all(const float* partial, long long ntiles, int K, Store&& store) {
   }
 }
 
-// Per-layer quartet coefficients in the kernel's [k][slot][3][T] layout.
+// Per-layer quartet coefficients in the kernel's [k][slot][kMqRows][T] layout.
 template <class PL>
-std::vector<float4> quartet_coefficients(const float* D, int K, const std::vector<unsigned char>& tab) {
+std::vector<float4> quartet_coefficients(const float* D, const float* B, int K, const std::vector<unsigned char>& tab) {
   constexpr int E = PL::NSL * PL::T;
-  std::vector<float4> mq((size_t)K * E * 3);
+  std::vector<float4> mq((size_t)K * E * kMqRows);
   for (int k = 0; k < K; ++k)
     for (int e = 0; e < E; ++e) {
-      float4 row[3];
-      real_mq_entry<PL>(D + (size_t)k * PL::N, (const char*)tab.data(), e, row);
+      float4 row[kMqRows];
+      real_mq_entry<PL>(D + (size_t)k * PL::N, B ? B + (size_t)k * PL::N : nullptr, (const char*)tab.data(), e, row);
       const int slot = e / PL::T, t = e % PL::T;
-      for (int r = 0; r < 3; ++r) mq[(size_t)k * E * 3 + (size_t)(slot * 3 + r) * PL::T + t] = row[r];
+      for (int r = 0; r < kMqRows; ++r)
+        mq[(size_t)k * E * kMqRows + (size_t)(slot * kMqRows + r) * PL::T + t] = row[r];
     }
   return mq;
 }
 
-template <class PL>
-void real_fwd(const float* x, float* y, const float* A, const float* D, const int* perm, long long batch,
-              int K, unsigned flags, float* saved, const std::vector<unsigned char>& tab) {
+template <class PL, bool BIAS>
+void real_fwd_k(const RealArgs& a, const std::vector<unsigned char>& tab) {
   using L = Launch<PL>;
-  constexpr int E = PL::NSL * PL::T;
-  const std::vector<float4> mq = quartet_coefficients<PL>(D, K, tab);
-  RealArgs a{x, y, A, mq.data(), perm, saved, nullptr, nullptr, nullptr, (const char*)tab.data(), batch, K, flags};
-  const long long nwg = (batch + L::FWD_ROWS - 1) / L::FWD_ROWS;
+  const long long nwg = (a.batch + L::FWD_ROWS - 1) / L::FWD_ROWS;
   std::vector<float> lds((size_t)L::FWD_LDS_FLOATS);
   float* twl = lds.data();
   float* rows = lds.data() + L::TW_FLOATS;
@@ -82,48 +78,69 @@ void real_fwd(const float* x, float* y, const float* A, const float* D, const in
       const int r = tid / PL::T, t = tid % PL::T;
       float* slab = rows + (size_t)r * L::FWD_SLAB;
       if constexpr (L::TW_LDS)
-        real_forward_row<PL>(ctx, a, unsigned(t), wg * L::FWD_ROWS, unsigned(r), slab, LdsView::of(twl));
+        real_forward_row<PL, BIAS>(ctx, a, unsigned(t), wg * L::FWD_ROWS, unsigned(r), slab, LdsView::of(twl));
       else
-        real_forward_row<PL>(ctx, a, unsigned(t), wg * L::FWD_ROWS, unsigned(r), slab, GView::of(tab.data()));
+        real_forward_row<PL, BIAS>(ctx, a, unsigned(t), wg * L::FWD_ROWS, unsigned(r), slab, GView::of(tab.data()));
     });
 }
 
 template <class PL>
-void real_bwd(const float* x, const float* gy, const float* A, const float* D, const int* perm,
-              const float* saved_in, float* gx, float* gA, float* gD, long long batch, int K, unsigned flags,
-              const std::vector<unsigned char>& tab) {
+void real_fwd(const float* x, float* y, const float* A, const float* D, const float* B, const int* perm,
+              long long batch, int K, unsigned flags, float* saved, const std::vector<unsigned char>& tab) {
+  const std::vector<float4> mq = quartet_coefficients<PL>(D, (flags & kFlagBias) ? B : nullptr, K, tab);
+  RealArgs a{x, y, A, mq.data(), perm, saved, nullptr, nullptr, nullptr, (const char*)tab.data(), batch, K, flags};
+  if (flags & kFlagBias) real_fwd_k<PL, true>(a, tab);
+  else real_fwd_k<PL, false>(a, tab);
+}
+
+template <class PL, bool BIAS>
+void real_bwd_k(const RealArgs& a, long long ntiles, float* lds_rows, const std::vector<unsigned char>& tab) {
   using L = Launch<PL>;
+  for (long long wg = 0; wg < ntiles; ++wg)
+    run_wg(L::BWD_THREADS, [&](HostCtx& ctx, int tid) {
+      const int r = tid / PL::T, t = tid % PL::T;
+      float* slab = lds_rows + (size_t)r * L::BWD_SLAB;
+      real_backward_row<PL, L::BWD_ROWS, BIAS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, lds_rows,
+                                               slab, GView::of(tab.data()));
+    });
+}
+
+template <class PL>
+void real_bwd(const float* x, const float* gy, const float* A, const float* D, const float* B, const int* perm,
+              const float* saved_in, float* gx, float* gA, float* gD, float* gB, long long batch, int K,
+              unsigned flags, const std::vector<unsigned char>& tab) {
+  using L = Launch<PL>;
+  static_assert(!L::BWD_TW_LDS, "the emulation follows the global-twiddle backward");
+  const bool bias = (flags & kFlagBias) != 0;
+  const bool acc = (flags & kFlagAccumulate) != 0;
   std::vector<float> saved_buf;
   const float* saved = saved_in;
   if (saved == nullptr && K > 1) {
     saved_buf.resize((size_t)(K - 1) * batch * PL::N);
-    real_fwd<PL>(x, nullptr, A, D, perm, batch, K, flags, saved_buf.data(), tab);
+    real_fwd<PL>(x, nullptr, A, D, B, perm, batch, K, flags, saved_buf.data(), tab);
     saved = saved_buf.data();
   }
-  const std::vector<float4> mq = quartet_coefficients<PL>(D, K, tab);
+  const std::vector<float4> mq = quartet_coefficients<PL>(D, bias ? B : nullptr, K, tab);
   const long long ntiles = (batch + L::BWD_ROWS - 1) / L::BWD_ROWS;
-  const long long PS = PL::N + PL::QF;
-  std::vector<float> partial((size_t)ntiles * K * PS);
+  const long long PS4 = partial_entries4<PL>(bias);
+  std::vector<float> partial((size_t)ntiles * K * PS4 * 4);
   RealArgs a{x, nullptr, A, mq.data(), perm, const_cast<float*>(saved), gy, gx, partial.data(),
              (const char*)tab.data(), batch, K, flags};
   std::vector<float> lds((size_t)L::BWD_LDS_FLOATS);
-  float* twl = lds.data();
-  float* rows = lds.data() + L::BWD_TW_FLOATS;
-  if (L::BWD_TW_LDS) std::memcpy(twl, tab.data(), (size_t)PL::TW_FLOAT2 * 8);
-  for (long long wg = 0; wg < ntiles; ++wg)
-    run_wg(L::BWD_THREADS, [&](HostCtx& ctx, int tid) {
-      const int r = tid / PL::T, t = tid % PL::T;
-      float* slab = rows + (size_t)r * L::BWD_SLAB;
-      if constexpr (L::BWD_TW_LDS)
-        real_backward_row<PL, L::BWD_ROWS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, rows,
-                                           slab, LdsView::of(twl));
-      else
-        real_backward_row<PL, L::BWD_ROWS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, rows,
-                                           slab, GView::of(tab.data()));
-    });
-  reduce_all<PL>(partial.data(), ntiles, K, [&](float4 s, int k, int e4) {
-    real_reduce_store4<PL>(s, k, e4, gA, gD, (const char*)tab.data());
+  if (bias) real_bwd_k<PL, true>(a, ntiles, lds.data(), tab);
+  else real_bwd_k<PL, false>(a, ntiles, lds.data(), tab);
+  std::vector<float> gS(bias ? (size_t)K * PL::N : 0);
+  reduce_all<PL>(partial.data(), ntiles, K, PS4, [&](float4 s, int k, int e4) {
+    real_reduce_store4<PL>(s, k, e4, gA, gD, gS.data(), (const char*)tab.data(), acc);
   });
+  if (bias) {
+    std::vector<float> lds1((size_t)L::FWD_SLAB);
+    for (int k = 0; k < K; ++k)
+      run_wg(PL::T, [&](HostCtx& ctx, int t) {
+        real_dct_row<PL>(ctx, gS.data() + (size_t)k * PL::N, gB + (size_t)k * PL::N, mq.data(), acc, unsigned(t),
+                         lds1.data(), GView::of(tab.data()), (const char*)tab.data());
+      });
+  }
 }
 
 template <class PL>
@@ -164,13 +181,15 @@ void cplx_bwd(const float* x, const float* gy, const float* A, const float* D, c
       cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, lds.data(),
                                          lds.data() + (size_t)r * L::BWD_SLAB);
     });
-  reduce_all<PL>(partial.data(), ntiles, K, [&](float4 s, int k, int e4) { cplx_reduce_store4<PL>(s, k, e4, gA, gD); });
+  reduce_all<PL>(partial.data(), ntiles, K, partial_entries4<PL>(), [&](float4 s, int k, int e4) {
+    cplx_reduce_store4<PL>(s, k, e4, gA, gD, (flags & kFlagAccumulate) != 0);
+  });
 }
 
 }  // namespace
 
-extern "C" int acdc_emu_forward(const float* x, float* y, const float* A, const float* D, const int* perm,
-                                long long batch, int N, int K, unsigned flags, float* saved) {
+extern "C" int acdc_emu_forward(const float* x, float* y, const float* A, const float* D, const float* B,
+                                const int* perm, long long batch, int N, int K, unsigned flags, float* saved) {
   int rc = -2;
   if (flags & kFlagComplex) {
     dispatch_complex(N, [&]<class PL>() {
@@ -186,7 +205,7 @@ extern "C" int acdc_emu_forward(const float* x, float* y, const float* A, const 
         rc = -5;
         return;
       }
-      real_fwd<PL>(x, y, A, D, perm, batch, K, flags, saved, tab);
+      real_fwd<PL>(x, y, A, D, B, perm, batch, K, flags, saved, tab);
       rc = 0;
     });
   }
@@ -194,8 +213,8 @@ extern "C" int acdc_emu_forward(const float* x, float* y, const float* A, const 
 }
 
 extern "C" int acdc_emu_backward(const float* x, const float* gy, const float* A, const float* D,
-                                 const int* perm, const float* saved, float* gx, float* gA, float* gD,
-                                 long long batch, int N, int K, unsigned flags) {
+                                 const float* B, const int* perm, const float* saved, float* gx, float* gA,
+                                 float* gD, float* gB, long long batch, int N, int K, unsigned flags) {
   int rc = -2;
   if (flags & kFlagComplex) {
     dispatch_complex(N, [&]<class PL>() {
@@ -211,7 +230,7 @@ extern "C" int acdc_emu_backward(const float* x, const float* gy, const float* A
         rc = -5;
         return;
       }
-      real_bwd<PL>(x, gy, A, D, perm, saved, gx, gA, gD, batch, K, flags, tab);
+      real_bwd<PL>(x, gy, A, D, B, perm, saved, gx, gA, gD, gB, batch, K, flags, tab);
       rc = 0;
     });
   }

@@ -53,7 +53,8 @@ def test_supported_widths(L):
         assert L.acdc_supported(N, 0) == 0
     assert L.acdc_supported(9216, CX) == 0
     assert L.acdc_supported(4096, CX | RELU) == 0
-    assert L.acdc_supported(4096, 8) == 0
+    assert L.acdc_supported(4096, 8) == 1          # BIAS
+    assert L.acdc_supported(4096, 32) == 0         # unknown flag bit
 
 
 def test_status_strings(L):
@@ -90,40 +91,49 @@ class FakePtr:
         return self.base + 64 * i
 
 
+BIAS, ACC = 8, 16
+
+
 def test_forward_rejects_bad_arguments(L):
     p = FakePtr()
-    x, y, A, D, perm, ws = (p(i) for i in range(6))
+    x, y, A, D, perm, ws, b = (p(i) for i in range(7))
 
-    def fwd(x=x, y=y, A=A, D=D, perm=perm, B=4, N=64, K=2, flags=0, saved=None, sb=0, ws=ws, wsb=1 << 20):
-        return L.acdc_forward(x, y, A, D, perm, B, N, K, flags, saved, sb, ws, wsb, None)
+    def fwd(x=x, y=y, A=A, D=D, b=None, perm=perm, B=4, N=64, K=2, flags=0, saved=None, sb=0, ws=ws,
+            wsb=1 << 20):
+        return L.acdc_forward(x, y, A, D, b, perm, B, N, K, flags, saved, sb, ws, wsb, None)
 
     assert fwd(N=100) == EUNSUP
     assert fwd(flags=CX | RELU) == EUNSUP
-    assert fwd(flags=16) == EINVAL
+    assert fwd(flags=CX | BIAS, b=b) == EUNSUP
+    assert fwd(flags=32) == EINVAL
     assert fwd(K=0) == EINVAL
     assert fwd(B=-1) == EINVAL
     assert fwd(x=None) == EINVAL
     assert fwd(y=None) == EINVAL
     assert fwd(A=x + 4) == EINVAL           # misaligned
     assert fwd(y=x) == EINVAL               # aliasing
+    assert fwd(y=b, b=b, flags=BIAS) == EINVAL
     assert fwd(flags=PERM, perm=None) == EINVAL
+    assert fwd(flags=BIAS) == EINVAL        # bias required with BIAS
+    assert fwd(flags=BIAS, b=b + 4) == EINVAL
     assert fwd(ws=None) == EWS
     assert fwd(wsb=16) == EWS
     need = L.acdc_saved_bytes(4, 64, 2, 0)
-    assert fwd(saved=p(6), sb=need - 4) == EWS   # saved buffer smaller than its layout
+    assert fwd(saved=p(7), sb=need - 4) == EWS   # saved buffer smaller than its layout
     assert fwd(B=0) == OK                   # empty batch: nothing to do, no HIP call
 
 
 def test_backward_rejects_bad_arguments(L):
     p = FakePtr()
-    x, gy, A, D, perm, gx, gA, gD, ws = (p(i) for i in range(9))
+    x, gy, A, D, perm, gx, gA, gD, ws, b, gb = (p(i) for i in range(11))
 
-    def bwd(x=x, gy=gy, A=A, D=D, perm=perm, saved=None, sb=0, gx=gx, gA=gA, gD=gD, B=4, N=64, K=2,
-            flags=0, ws=ws, wsb=1 << 30):
-        return L.acdc_backward(x, gy, A, D, perm, saved, sb, gx, gA, gD, B, N, K, flags, ws, wsb, None)
+    def bwd(x=x, gy=gy, A=A, D=D, b=None, perm=perm, saved=None, sb=0, gx=gx, gA=gA, gD=gD, gb=None, B=4,
+            N=64, K=2, flags=0, ws=ws, wsb=1 << 30):
+        return L.acdc_backward(x, gy, A, D, b, perm, saved, sb, gx, gA, gD, gb, B, N, K, flags, ws, wsb, None)
 
     assert bwd(N=48) == EUNSUP
     assert bwd(flags=CX | RELU) == EUNSUP
+    assert bwd(flags=CX | BIAS, b=b, gb=gb) == EUNSUP
     assert bwd(K=-3) == EINVAL
     assert bwd(gy=None) == EINVAL
     assert bwd(gA=None) == EINVAL
@@ -131,10 +141,27 @@ def test_backward_rejects_bad_arguments(L):
     assert bwd(gA=gD) == EINVAL
     assert bwd(gD=A + 8) == EINVAL
     assert bwd(flags=PERM, perm=None) == EINVAL
+    assert bwd(flags=BIAS, b=b) == EINVAL        # grad_bias required with BIAS
+    assert bwd(flags=BIAS, gb=gb) == EINVAL      # bias required with BIAS
+    assert bwd(flags=BIAS, b=b, gb=gA) == EINVAL  # aliased gradients
+    assert bwd(flags=BIAS | ACC, b=b, gb=gb + 4) == EINVAL
     assert bwd(ws=None) == EWS
     assert bwd(wsb=64) == EWS
     need = L.acdc_saved_bytes(4, 64, 2, 0)
-    assert bwd(saved=p(9), sb=need - 4) == EWS   # saved buffer smaller than its layout
+    assert bwd(saved=p(11), sb=need - 4) == EWS   # saved buffer smaller than its layout
+    # the bias gradient needs workspace even for an empty batch
+    assert L.acdc_backward_workspace_bytes(0, 64, 2, BIAS, 1) > 0
+    assert bwd(B=0, flags=BIAS, b=b, gb=gb, ws=None) == EWS
+
+
+def test_bias_workspace_sizes(L):
+    plain = L.acdc_backward_workspace_bytes(8192, 4096, 12, PERM | RELU, 1)
+    biased = L.acdc_backward_workspace_bytes(8192, 4096, 12, PERM | RELU | BIAS, 1)
+    # one more N-float partial per tile and layer, plus the [K, N] batch sums
+    assert biased >= plain + 12 * 4096 * 4
+    assert L.acdc_supported(4096, PERM | RELU | BIAS | ACC) == 1
+    assert L.acdc_supported(4096, CX | BIAS) == 0
+    assert L.acdc_supported(4096, CX | ACC) == 1
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

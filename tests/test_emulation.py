@@ -15,7 +15,7 @@ import numpy as np
 import pytest
 
 from oracle import acdc_oracle as O
-from paper_1511_05946_amd.workloads import make_inputs
+from paper_1511_05946_amd.workloads import FLAG_ACCUMULATE, FLAG_BIAS, make_bias, make_inputs
 from tests.helpers import TOL_COMPLEX, TOL_REAL, rel_err, relu_safe_rows
 
 sys.path.insert(0, os.path.join(os.path.dirname(__file__), "emu"))
@@ -28,9 +28,9 @@ def emu():
     import build_emu
     L = ctypes.CDLL(build_emu.build())
     P = ctypes.c_void_p
-    L.acdc_emu_forward.argtypes = [P, P, P, P, P, ctypes.c_longlong, ctypes.c_int, ctypes.c_int,
+    L.acdc_emu_forward.argtypes = [P, P, P, P, P, P, ctypes.c_longlong, ctypes.c_int, ctypes.c_int,
                                    ctypes.c_uint, P]
-    L.acdc_emu_backward.argtypes = [P, P, P, P, P, P, P, P, P, ctypes.c_longlong, ctypes.c_int,
+    L.acdc_emu_backward.argtypes = [P, P, P, P, P, P, P, P, P, P, P, ctypes.c_longlong, ctypes.c_int,
                                     ctypes.c_int, ctypes.c_uint]
     return L
 
@@ -41,11 +41,12 @@ def _p(a):
 
 def check(L, N, K, B, flags, seed=0, with_saved=False):
     x, A, D, perm, gy = make_inputs(N, K, B, flags, seed)
+    bias = make_bias(N, K, seed) if flags & FLAG_BIAS else None
     tol = TOL_COMPLEX if flags & O.FLAG_COMPLEX else TOL_REAL
     y = np.zeros_like(x)
     saved = np.zeros((max(K - 1, 0), B, N), x.dtype) if with_saved else None
-    assert L.acdc_emu_forward(_p(x), _p(y), _p(A), _p(D), _p(perm), B, N, K, flags, _p(saved)) == 0
-    yr, cache = O.forward(x, A, D, perm, flags, keep=True)
+    assert L.acdc_emu_forward(_p(x), _p(y), _p(A), _p(D), _p(bias), _p(perm), B, N, K, flags, _p(saved)) == 0
+    yr, cache = O.forward(x, A, D, perm, flags & 7, keep=True, B=bias)
     assert rel_err(y, yr) < tol
     if with_saved and K > 1:
         for k in range(1, K):
@@ -54,13 +55,16 @@ def check(L, N, K, B, flags, seed=0, with_saved=False):
     x, gy = np.ascontiguousarray(x[keep]), np.ascontiguousarray(gy[keep])
     Bk = x.shape[0]
     gx, gA, gD = np.zeros_like(x), np.zeros_like(A), np.zeros_like(D)
+    gB = np.zeros_like(A) if bias is not None else None
     sv = np.ascontiguousarray(saved[:, keep]) if (with_saved and K > 1) else None
-    assert L.acdc_emu_backward(_p(x), _p(gy), _p(A), _p(D), _p(perm), _p(sv), _p(gx), _p(gA), _p(gD),
-                               Bk, N, K, flags) == 0
-    rx, rA, rD = O.backward(x, gy, A, D, perm, flags)
-    assert rel_err(gx, rx) < tol
-    assert rel_err(gA, rA) < tol
-    assert rel_err(gD, rD) < tol
+    assert L.acdc_emu_backward(_p(x), _p(gy), _p(A), _p(D), _p(bias), _p(perm), _p(sv), _p(gx), _p(gA), _p(gD),
+                               _p(gB), Bk, N, K, flags) == 0
+    ref = O.backward(x, gy, A, D, perm, flags & 7, B=bias)
+    assert rel_err(gx, ref[0]) < tol
+    assert rel_err(gA, ref[1]) < tol
+    assert rel_err(gD, ref[2]) < tol
+    if bias is not None:
+        assert rel_err(gB, ref[3]) < tol
 
 
 @pytest.mark.parametrize("N", [8, 16, 32, 64, 128, 256, 512, 1024])
@@ -80,3 +84,29 @@ def test_real_4096_with_saved(emu):
 
 def test_real_9216_three_waves_per_row(emu):
     check(emu, 9216, 2, 2, O.FLAG_PERM | O.FLAG_RELU, seed=2)
+
+
+@pytest.mark.parametrize("N", [8, 16, 64, 256, 1024])
+def test_real_bias(emu, N):
+    check(emu, N, 3, 9, O.FLAG_PERM | O.FLAG_RELU | FLAG_BIAS, seed=N + 1)
+
+
+def test_real_bias_4096_with_saved(emu):
+    check(emu, 4096, 2, 3, O.FLAG_PERM | O.FLAG_RELU | FLAG_BIAS, seed=3, with_saved=True)
+
+
+def test_accumulate_adds_to_gradients(emu):
+    # ACCUMULATE adds the batch sums to what grad_A, grad_D, grad_bias hold.
+    N, K, B = 64, 2, 5
+    flags = O.FLAG_PERM | FLAG_BIAS
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, 7)
+    bias = make_bias(N, K, 7)
+    outs = []
+    for acc in (0, FLAG_ACCUMULATE):
+        gx = np.zeros_like(x)
+        g = [np.full_like(A, 0.5) for _ in range(3)]
+        assert emu.acdc_emu_backward(_p(x), _p(gy), _p(A), _p(D), _p(bias), _p(perm), None, _p(gx), _p(g[0]),
+                                     _p(g[1]), _p(g[2]), B, N, K, flags | acc) == 0
+        outs.append(g)
+    for plain, added in zip(*outs):
+        np.testing.assert_allclose(added, plain + 0.5, rtol=1e-6, atol=1e-6)

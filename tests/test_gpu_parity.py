@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 from oracle import acdc_oracle as O
-from paper_1511_05946_amd.workloads import WORKLOADS, make_inputs
+from paper_1511_05946_amd.workloads import FLAG_ACCUMULATE, FLAG_BIAS, WORKLOADS, make_bias, make_inputs
 from tests.helpers import TOL_COMPLEX, TOL_REAL, rel_err, relu_safe_rows
 
 pytestmark = pytest.mark.gpu
@@ -44,7 +44,7 @@ def host(t):
 MIN_BWD_ROWS = 4
 
 
-def refill_safe_rows(xs, gys, A, D, perm, flags, need, seed, chunk=8, max_draws=96):
+def refill_safe_rows(xs, gys, A, D, perm, flags, need, seed, chunk=8, max_draws=96, bias=None):
     """Append seeded extra rows (same distribution as the workload: x =
     max(N(0,1), 0), g_y ~ N(0,1)) whose oracle forward keeps every ReLU
     decision clear of zero, until `need` rows are available."""
@@ -56,7 +56,7 @@ def refill_safe_rows(xs, gys, A, D, perm, flags, need, seed, chunk=8, max_draws=
         xe = np.maximum(rng.standard_normal((chunk, N)), 0.0).astype(np.float32)
         ge = rng.standard_normal((chunk, N)).astype(np.float32)
         drawn += chunk
-        _, c = O.forward(xe, A, D, perm, flags, keep=True)
+        _, c = O.forward(xe, A, D, perm, flags & 7, keep=True, B=bias)
         ok = relu_safe_rows(c["v"], K)
         xs = np.concatenate([xs, xe[ok]])[:need] if len(xs) < need else xs
         gys = np.concatenate([gys, ge[ok]])[:len(xs)]
@@ -67,12 +67,14 @@ def refill_safe_rows(xs, gys, A, D, perm, flags, need, seed, chunk=8, max_draws=
 def run_case(acdc, N, K, B, flags, seed=0, save=True, check_bwd=True, rows=None):
     print(f"[case] N={N} K={K} B={B} flags={flags} seed={seed} save={save}", flush=True)
     x, A, D, perm, gy = make_inputs(N, K, B, flags, seed)
+    bias = make_bias(N, K, seed) if flags & FLAG_BIAS else None
+    bt = dev(bias) if bias is not None else None
     tol = TOL_COMPLEX if flags & CX else TOL_REAL
     xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
-    y, saved = acdc.forward(xt, At, Dt, pt, flags & ~CX, save=save)
+    y, saved = acdc.forward(xt, At, Dt, pt, flags & ~CX, save=save, bias=bt)
     yg = host(y)
     sel = np.arange(B) if rows is None else rows
-    yr, cache = O.forward(x[sel], A, D, perm, flags, keep=True)
+    yr, cache = O.forward(x[sel], A, D, perm, flags & 7, keep=True, B=bias)
     e = rel_err(yg[sel], yr)
     assert e < tol, f"forward rel err {e:.3e}"
     if save and K > 1:
@@ -85,15 +87,15 @@ def run_case(acdc, N, K, B, flags, seed=0, save=True, check_bwd=True, rows=None)
     idx = sel[keep]
     xs, gys = x[idx], gy[idx]
     if flags & R and K > 1:
-        xs, gys = refill_safe_rows(xs, gys, A, D, perm, flags, min(len(sel), MIN_BWD_ROWS), seed)
+        xs, gys = refill_safe_rows(xs, gys, A, D, perm, flags, min(len(sel), MIN_BWD_ROWS), seed, bias=bias)
     print(f"[case]   backward on {len(idx)}/{len(sel)} rows + {len(xs) - len(idx)} refill rows", flush=True)
     xst = dev(xs)
     sv = None
     if save:
-        _, sv = acdc.forward(xst, At, Dt, pt, flags & ~CX, save=True)
-    gx, gA, gD = acdc.backward(xst, dev(gys), At, Dt, pt, flags & ~CX, saved=sv)
-    rx, rA, rD = O.backward(xs, gys, A, D, perm, flags)
-    for name, g, r in (("grad_x", gx, rx), ("grad_A", gA, rA), ("grad_D", gD, rD)):
+        _, sv = acdc.forward(xst, At, Dt, pt, flags & ~CX, save=True, bias=bt)
+    got = acdc.backward(xst, dev(gys), At, Dt, pt, flags & ~CX, saved=sv, bias=bt)
+    ref = O.backward(xs, gys, A, D, perm, flags & 7, B=bias)
+    for name, g, r in zip(("grad_x", "grad_A", "grad_D", "grad_bias"), got, ref):
         e = rel_err(host(g), r)
         assert e < tol, f"{name} rel err {e:.3e}"
 
@@ -125,7 +127,7 @@ def test_single_layer_and_single_row(acdc, save):
 def test_workloads_small_batch(acdc, name):
     w = WORKLOADS[name]
     B = {"acdc_n256_k1": 64, "acdc_n1024_k12_perm": 96, "acdc_n4096_k12_perm_relu": 48,
-         "acdc_n9216_k16_perm_relu": 12, "afdf_n4096_k8_perm": 24}[name]
+         "acdc_n9216_k16_perm_relu": 12, "afdf_n4096_k8_perm": 24, "acdc_n4096_k12_perm_relu_bias": 48}[name]
     if name == "acdc_n9216_k16_perm_relu":
         # At N=9216, K=16 nearly every row has some ReLU decision within
         # 1e-5 * rms of zero (the near-identity layers keep the input's zeros
@@ -149,24 +151,26 @@ def test_workloads_full_size_sampled(acdc, name):
     nsamp = 12 if w.N >= 9216 else 16
     rows = np.sort(rng.choice(w.batch, nsamp, replace=False))
     run_case(acdc, w.N, w.K, w.batch, w.flags, seed=0, rows=rows, check_bwd=False)
-    # grad_x rows and additivity of grad_A/grad_D on the full batch
+    # grad_x rows and additivity of the parameter gradients on the full batch
     x, A, D, perm, gy = make_inputs(w.N, w.K, w.batch, w.flags, 0)
+    bias = make_bias(w.N, w.K, 0) if w.flags & FLAG_BIAS else None
+    bt = dev(bias) if bias is not None else None
     fl = w.flags & ~CX
     xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
-    _, sv = acdc.forward(xt, At, Dt, pt, fl, save=True)
-    gx, gA, gD = acdc.backward(xt, gyt, At, Dt, pt, fl, saved=sv)
+    _, sv = acdc.forward(xt, At, Dt, pt, fl, save=True, bias=bt)
+    full = acdc.backward(xt, gyt, At, Dt, pt, fl, saved=sv, bias=bt)
     h = w.batch // 2
-    gA1 = acdc.backward(xt[:h].contiguous(), gyt[:h].contiguous(), At, Dt, pt, fl)[1]
-    gD1 = acdc.backward(xt[:h].contiguous(), gyt[:h].contiguous(), At, Dt, pt, fl)[2]
-    _, gA2, gD2 = acdc.backward(xt[h:].contiguous(), gyt[h:].contiguous(), At, Dt, pt, fl)
+    part1 = acdc.backward(xt[:h].contiguous(), gyt[:h].contiguous(), At, Dt, pt, fl, bias=bt)
+    part2 = acdc.backward(xt[h:].contiguous(), gyt[h:].contiguous(), At, Dt, pt, fl, bias=bt)
     tol = TOL_COMPLEX if w.complex else TOL_REAL
-    assert rel_err(host(gA), host(gA1 + gA2)) < tol
-    assert rel_err(host(gD), host(gD1 + gD2)) < tol
-    _, cache = O.forward(x[rows], A, D, perm, w.flags, keep=True)
+    for g, g1, g2 in list(zip(full, part1, part2))[1:]:
+        assert rel_err(host(g), host(g1 + g2)) < tol
+    gx = full[0]
+    _, cache = O.forward(x[rows], A, D, perm, w.flags & 7, keep=True, B=bias)
     keep = relu_safe_rows(cache["v"], w.K) if w.flags & R else np.ones(len(rows), bool)
     print(f"[case]   grad_x checked on {int(keep.sum())}/{len(rows)} sampled rows", flush=True)
     if keep.any():
-        rx, _, _ = O.backward(x[rows][keep], gy[rows][keep], A, D, perm, w.flags)
+        rx = O.backward(x[rows][keep], gy[rows][keep], A, D, perm, w.flags & 7, B=bias)[0]
         assert rel_err(host(gx)[rows][keep], rx) < tol
     else:
         # only at N=9216, K=16 (see test_workloads_small_batch)
@@ -261,3 +265,74 @@ def test_autograd_wrapper(acdc):
     assert rel_err(host(xt.grad), rx) < TOL_REAL
     assert rel_err(host(At.grad), rA) < TOL_REAL
     assert rel_err(host(Dt.grad), rD) < TOL_REAL
+
+
+# ----------------------------------------------- D-domain bias, accumulation
+
+@pytest.mark.parametrize("N", [8, 64, 256, 1024, 2048, 4096, 9216, 16384])
+def test_bias_widths(acdc, N):
+    B = 67 if N <= 4096 else 5                           # a ragged last workgroup
+    run_case(acdc, N, 3, B, P | R | FLAG_BIAS, seed=N + 3)
+
+
+@pytest.mark.parametrize("save", [True, False])
+def test_bias_single_layer_and_recompute(acdc, save):
+    run_case(acdc, 4096, 1, 3, FLAG_BIAS, save=save, seed=11)
+    run_case(acdc, 1024, 4, 9, P | R | FLAG_BIAS, save=save, seed=12)
+
+
+def test_bias_zero_D_closed_form(acdc):
+    # D = 0: every output row is the inverse DCT of b (oracle at fp64)
+    N, K, B = 4096, 1, 4
+    x, A, D, _, _ = make_inputs(N, K, B, 0, 13)
+    b = make_bias(N, K, 13)
+    y, _ = acdc.forward(dev(x), dev(A), dev(np.zeros_like(D)), None, 0, bias=dev(b))
+    ref = O.forward(x, A, np.zeros_like(D), None, 0, B=b)
+    assert rel_err(host(y), ref) < TOL_REAL
+
+
+@pytest.mark.parametrize("flags", [P | R | FLAG_BIAS, P | R, CX | P])
+def test_accumulate_adds_bitwise(acdc, flags):
+    import torch
+    N, K, B = 2048, 3, 37
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, 14)
+    bias = make_bias(N, K, 14) if flags & FLAG_BIAS else None
+    bt = dev(bias) if bias is not None else None
+    fl = flags & ~CX
+    xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
+    _, sv = acdc.forward(xt, At, Dt, pt, fl, save=True, bias=bt)
+    plain = acdc.backward(xt, gyt, At, Dt, pt, fl, saved=sv, bias=bt)
+    pre = [torch.randn(A.shape, dtype=At.dtype, device="cuda", generator=torch.Generator("cuda").manual_seed(i))
+           for i in range(len(plain) - 1)]
+    grads = tuple(p.clone() for p in pre)
+    acc = acdc.backward(xt, gyt, At, Dt, pt, fl | FLAG_ACCUMULATE, saved=sv, bias=bt, grads=grads)
+    assert np.array_equal(host(acc[0]), host(plain[0]))
+    for g, p0, g0 in zip(acc[1:], pre, plain[1:]):
+        assert g.data_ptr() in [t.data_ptr() for t in grads]
+        assert np.array_equal(host(g), host(p0 + g0))
+
+
+def test_bias_empty_batch(acdc):
+    import torch
+    N, K = 256, 2
+    A = torch.ones((K, N), device="cuda")
+    b = torch.ones((K, N), device="cuda")
+    x = torch.empty((0, N), device="cuda")
+    gx, gA, gD, gB = acdc.backward(x, x.clone(), A, A.clone(), None, 0, bias=b)
+    assert not host(gA).any() and not host(gD).any() and not host(gB).any()
+
+
+def test_bias_autograd_wrapper(acdc):
+    N, K, B, flags = 256, 4, 16, P | R
+    # seed 16: no ReLU decision of this batch within 1e-5 * rms of zero
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, 16)
+    b = make_bias(N, K, 16)
+    xt = dev(x).requires_grad_(True)
+    bt = dev(b).requires_grad_(True)
+    y = acdc.acdc_cascade(xt, dev(A), dev(D), dev(perm), flags, bt)
+    y.backward(dev(gy))
+    _, cache = O.forward(x, A, D, perm, flags, keep=True, B=b)
+    assert relu_safe_rows(cache["v"], K).all()
+    rx, _, _, rB = O.backward(x, gy, A, D, perm, flags, B=b)
+    assert rel_err(host(xt.grad), rx) < TOL_REAL
+    assert rel_err(host(bt.grad), rB) < TOL_REAL
