@@ -133,23 +133,24 @@ def forward(x, A, D, perm=None, flags: int = 0, save: bool = False, out=None, sa
     return out, saved
 
 
-def backward(x, grad_y, A, D, perm=None, flags: int = 0, saved=None, bias=None, grads=None):
+def backward(x, grad_y, A, D, perm=None, flags: int = 0, saved=None, bias=None, grads=None, out=None):
     """(grad_x, grad_A, grad_D), plus grad_bias when ``bias`` is given; the
     parameter gradients are summed over the batch.  Without ``saved`` (from
     ``forward(..., save=True)`` on the same inputs) the forward is recomputed
     inside the call.  ``grads`` = (grad_A, grad_D[, grad_bias]) tensors to
-    write into; with FLAG_ACCUMULATE in ``flags`` the sums are added to them."""
+    write into; with FLAG_ACCUMULATE in ``flags`` the sums are added to them.
+    ``out``: a tensor to write grad_x into."""
     flags = _flags(flags, x, bias)
     cplx = bool(flags & FLAG_COMPLEX)
     B, N, K = _dims(x, A)
-    gx = torch.empty_like(x)
+    gx = torch.empty_like(x) if out is None else out
     if grads is None:
         if flags & FLAG_ACCUMULATE:
             raise ValueError("FLAG_ACCUMULATE needs the gradient tensors to add into (grads=...)")
         grads = (torch.empty_like(A), torch.empty_like(D)) + ((torch.empty_like(bias),) if bias is not None else ())
     gA, gD = grads[0], grads[1]
     gB = grads[2] if bias is not None else None
-    _validate({"x": x, "grad_y": grad_y, "A": A, "D": D, "bias": bias, "saved": saved, "grad_A": gA,
+    _validate({"x": x, "grad_y": grad_y, "grad_x": gx, "A": A, "D": D, "bias": bias, "saved": saved, "grad_A": gA,
                "grad_D": gD, "grad_bias": gB, "perm": perm if flags & FLAG_PERM else None}, cplx, x.device)
     L = lib()
     use_saved = saved is not None and saved.numel() > 0
