@@ -122,6 +122,18 @@ def make_bias(N: int, K: int, seed: int = 0) -> np.ndarray:
     return rng.normal(0.0, 0.1, (K, N)).astype(np.float32)
 
 
+def make_linreg(seed: int = 0, rows: int = 10000, N: int = 32):
+    """Synthetic linear-regression data of Sec. 6.1: X [rows, N] and
+    W_true [N, N] uniform on [0, 1), and the noise eps ~ N(0, 1e-4) (variance)
+    of the targets Y = X W_true + eps, all float32.  Returns (X, W_true, eps);
+    the caller forms Y."""
+    rng = np.random.default_rng((seed, 61))
+    X = rng.uniform(0.0, 1.0, (rows, N))
+    W = rng.uniform(0.0, 1.0, (N, N))
+    eps = rng.normal(0.0, 1e-2, (rows, N))
+    return X.astype(np.float32), W.astype(np.float32), eps.astype(np.float32)
+
+
 def make_workload(name: str, seed: int = 0, batch: int | None = None):
     """Inputs for one of the named workloads (optionally with another batch)."""
     w = WORKLOADS[name]
