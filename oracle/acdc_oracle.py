@@ -6,9 +6,11 @@ TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 tables or constants with that path.
 
 Everything is computed in float64 (complex128 for the AFDF variant) with dense
-O(N^2) matrices built directly from their definitions.  There is no fast
-transform, no blocking and no fusion: each function follows the paper's
-statement of the layer in the order the paper gives it.
+O(N^2) matrices built directly from their definitions (up to N = DENSE_MAX;
+wider rows apply the same matrices through scipy's / numpy's transforms,
+which the pins equate with the dense matrices).  There is no blocking and no
+fusion: each function follows the paper's statement of the layer in the
+order the paper gives it.
 
 Paper: Moczulski, Denil, Appleyard, de Freitas, "ACDC: A Structured Efficient
 Linear Layer", ICLR 2016 (arXiv:1511.05946).
@@ -78,17 +80,51 @@ def dft_matrix(N: int) -> np.ndarray:
     return np.exp(-2j * np.pi * ((n * k) % N).astype(np.float64) / N)
 
 
-def _transforms(N: int, complex_: bool):
-    """Return (T, Tinv) with Tinv the exact inverse of T.
+# Widths up to this use the dense matrices above; wider rows apply the same
+# matrices through the library routines that tests/test_oracle.py equates
+# with them (scipy's orthonormal DCT-II / DCT-III, numpy's FFT), since an
+# N x N matrix no longer fits comfortably in memory (32768^2 doubles = 8.6 GB).
+DENSE_MAX = 16384
 
-    ACDC (Sec. 4): T = C, Tinv = C^T (C orthogonal).
-    AFDF (Sec. 3): T = F, Tinv = conj(F) / N.
+
+class _LibraryTransform:
+    """The row-vector product h @ M for a DCT or DFT matrix M, evaluated by a
+    library transform along the last axis.  Only __rmatmul__ is defined, so
+    `h @ op` reads like the dense code it replaces."""
+
+    __array_ufunc__ = None  # make numpy defer `ndarray @ op` to __rmatmul__
+
+    def __init__(self, fn):
+        self.fn = fn
+
+    def __rmatmul__(self, h):
+        return self.fn(np.asarray(h))
+
+
+def _transforms(N: int, complex_: bool):
+    """Return (T, Tinv, Tinv_H, T_H): the forward transform, its exact
+    inverse, and the conjugate transposes the backward applies (row form).
+
+    ACDC (Sec. 4): T = C, Tinv = C^T (C orthogonal), so Tinv_H = C, T_H = C^T.
+    AFDF (Sec. 3): T = F, Tinv = conj(F) / N, so Tinv_H = F / N, T_H = conj(F).
     """
+    if N <= DENSE_MAX:
+        if complex_:
+            F = dft_matrix(N)
+            T, Tinv = F, np.conj(F) / N
+        else:
+            C = dct_matrix(N)
+            T, Tinv = C, C.T.copy()
+        return T, Tinv, np.conj(Tinv).T, np.conj(T).T
+    import scipy.fft
     if complex_:
-        F = dft_matrix(N)
-        return F, np.conj(F) / N
-    C = dct_matrix(N)
-    return C, C.T.copy()
+        return (_LibraryTransform(lambda h: np.fft.fft(h, axis=-1)),
+                _LibraryTransform(lambda h: np.fft.ifft(h, axis=-1)),
+                _LibraryTransform(lambda h: np.fft.fft(h, axis=-1) / N),
+                _LibraryTransform(lambda h: np.fft.ifft(h, axis=-1) * N))
+    dct = _LibraryTransform(lambda h: scipy.fft.dct(h, type=2, norm="ortho", axis=-1))
+    idct = _LibraryTransform(lambda h: scipy.fft.idct(h, type=2, norm="ortho", axis=-1))
+    return dct, idct, dct, idct
 
 
 def _check(x, A, D, perm, flags, B=None):
@@ -131,7 +167,7 @@ def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False, B=None):
     """
     x, A, D, perm, Bd = _check(x, A, D, perm, flags, B)
     K, N = A.shape
-    T, Tinv = _transforms(N, bool(flags & FLAG_COMPLEX))
+    T, Tinv, _, _ = _transforms(N, bool(flags & FLAG_COMPLEX))
     relu = bool(flags & FLAG_RELU)
     y = np.empty_like(x)
     cache = {"u": [np.empty_like(x) for _ in range(K)],
@@ -184,11 +220,10 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0, B=None):
     if gy.shape != x.shape:
         raise ValueError("grad_y must match x")
     K, N = A.shape
-    T, Tinv = _transforms(N, cplx)
     # Backward transforms: row form of the transposed (conjugate-transposed
-    # for AFDF) forward matrices.
-    Tinv_H = np.conj(Tinv).T  # C for ACDC, F / N for AFDF
-    T_H = np.conj(T).T        # C^T for ACDC, conj(F) for AFDF
+    # for AFDF) forward matrices: Tinv_H = C for ACDC, F / N for AFDF;
+    # T_H = C^T for ACDC, conj(F) for AFDF.
+    _, _, Tinv_H, T_H = _transforms(N, cplx)
     relu = bool(flags & FLAG_RELU)
     grad_x = np.empty_like(x)
     grad_A = np.zeros_like(A)
@@ -223,7 +258,7 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0, B=None):
 def layer_matrix(a, d, complex_: bool = False) -> np.ndarray:
     """Dense matrix of one layer, A T D T^{-1} (Sec. 4 / Sec. 3); N small."""
     N = len(a)
-    T, Tinv = _transforms(N, complex_)
+    T, Tinv, _, _ = _transforms(N, complex_)
     dt = np.complex128 if complex_ else np.float64
     return np.diag(np.asarray(a, dt)) @ T @ np.diag(np.asarray(d, dt)) @ Tinv
 

@@ -314,6 +314,24 @@ def test_backward_batch_split_additivity():
     np.testing.assert_allclose(gD, gD1 + gD2, atol=1e-12)
 
 
+# --------------------------------- wide rows: library transforms for dense ones
+
+@pytest.mark.parametrize("flags", [P | R, CX | P])
+@pytest.mark.parametrize("N", [64, 1024])
+def test_library_transform_path_equals_dense(monkeypatch, flags, N):
+    # Rows wider than DENSE_MAX apply C, C^T (F, F^{-1}) through scipy/numpy
+    # transforms; on widths where both exist the two paths agree.
+    rng = np.random.default_rng(600 + N + flags)
+    x, A, D, perm, gy = rand_case(rng, 5, N, 3, flags, relu_input=True)
+    b = rand_bias(rng, 3, N, bool(flags & CX))
+    dense = O.forward(x, A, D, perm, flags, B=b), O.backward(x, gy, A, D, perm, flags, B=b)
+    monkeypatch.setattr(O, "DENSE_MAX", 4)
+    lib = O.forward(x, A, D, perm, flags, B=b), O.backward(x, gy, A, D, perm, flags, B=b)
+    np.testing.assert_allclose(lib[0], dense[0], atol=1e-11)
+    for a, c in zip(lib[1], dense[1]):
+        np.testing.assert_allclose(a, c, atol=1e-10)
+
+
 # ------------------------------------------- D-domain bias (Sec. 6.2)
 
 def rand_bias(rng, K, N, cplx):
