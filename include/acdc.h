@@ -55,8 +55,8 @@
  * device uploads its constant table synchronously.  Results are bitwise
  * reproducible for identical inputs on the same device.
  *
- * Supported widths (acdc_supported): ACDC N in {8, 16, ..., 16384} and 9216;
- * AFDF N in {8, 16, ..., 8192}.  Batch sizes from 0 upward; K >= 1.
+ * Supported widths (acdc_supported): ACDC N in {8, 16, ..., 32768} and 9216;
+ * AFDF N in {8, 16, ..., 16384}.  Batch sizes from 0 upward; K >= 1.
  */
 #ifndef ACDC_H_
 #define ACDC_H_

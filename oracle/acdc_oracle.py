@@ -83,8 +83,9 @@ def dft_matrix(N: int) -> np.ndarray:
 # Widths up to this use the dense matrices above; wider rows apply the same
 # matrices through the library routines that tests/test_oracle.py equates
 # with them (scipy's orthonormal DCT-II / DCT-III, numpy's FFT), since an
-# N x N matrix no longer fits comfortably in memory (32768^2 doubles = 8.6 GB).
-DENSE_MAX = 16384
+# N x N matrix no longer fits comfortably in memory (16384^2 complex doubles
+# take 4.3 GB).
+DENSE_MAX = 8192
 
 
 class _LibraryTransform:

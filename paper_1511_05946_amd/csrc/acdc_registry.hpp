@@ -23,6 +23,7 @@ using RP4096 = RealPlan<4096, 64, 16, 8, 16>;
 using RP8192 = RealPlan<8192, 128, 16, 16, 16>;
 using RP9216 = RealPlan<9216, 192, 12, 8, 4, 12>;
 using RP16384 = RealPlan<16384, 256, 16, 32, 16>;
+using RP32768 = RealPlan<32768, 512, 16, 8, 8, 16>;
 
 // Complex AFDF plans: N -> (threads per row, radices of the N-point FFT).
 using CP8 = ComplexPlan<8, 1, 2, 4>;
@@ -36,6 +37,7 @@ using CP1024 = ComplexPlan<1024, 32, 32, 32>;
 using CP2048 = ComplexPlan<2048, 64, 32, 2, 32>;
 using CP4096 = ComplexPlan<4096, 128, 32, 4, 32>;
 using CP8192 = ComplexPlan<8192, 256, 32, 8, 32>;
+using CP16384 = ComplexPlan<16384, 512, 32, 16, 32>;
 
 // Rows per workgroup.  Forward rows are independent; backward rows of one
 // workgroup are reduced together into one partial of dL/da, dL/dd.
@@ -127,6 +129,7 @@ inline bool dispatch_real(int N, F&& f) {
     case 8192: return run_plan<RP8192>(f);
     case 9216: return run_plan<RP9216>(f);
     case 16384: return run_plan<RP16384>(f);
+    case 32768: return run_plan<RP32768>(f);
     default: return false;
   }
 }
@@ -145,6 +148,7 @@ inline bool dispatch_complex(int N, F&& f) {
     case 2048: return run_plan<CP2048>(f);
     case 4096: return run_plan<CP4096>(f);
     case 8192: return run_plan<CP8192>(f);
+    case 16384: return run_plan<CP16384>(f);
     default: return false;
   }
 }

@@ -44,13 +44,14 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_supported_widths(L):
-    for N in (8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096, 8192, 9216, 16384):
+    for N in (8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096, 8192, 9216, 16384, 32768):
         assert L.acdc_supported(N, 0) == 1
         assert L.acdc_supported(N, PERM | RELU) == 1
-    for N in (8, 64, 1024, 4096, 8192):
+    for N in (8, 64, 1024, 4096, 8192, 16384):
         assert L.acdc_supported(N, CX | PERM) == 1
-    for N in (0, 2, 4, 6, 12, 100, 1000, 3072, 32768):
+    for N in (0, 2, 4, 6, 12, 100, 1000, 3072, 65536):
         assert L.acdc_supported(N, 0) == 0
+    assert L.acdc_supported(32768, CX) == 0
     assert L.acdc_supported(9216, CX) == 0
     assert L.acdc_supported(4096, CX | RELU) == 0
     assert L.acdc_supported(4096, 8) == 1          # BIAS

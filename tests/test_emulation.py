@@ -86,6 +86,22 @@ def test_real_9216_three_waves_per_row(emu):
     check(emu, 9216, 2, 2, O.FLAG_PERM | O.FLAG_RELU, seed=2)
 
 
+# Rows of 512 threads take minutes in the emulation (one OS thread per GPU
+# thread, 512-way barriers); run with ACDC_EMU_WIDE=1.  The GPU parity tests
+# cover these widths on every run.
+wide = pytest.mark.skipif(os.environ.get("ACDC_EMU_WIDE") != "1", reason="set ACDC_EMU_WIDE=1 (slow)")
+
+
+@wide
+def test_real_32768_eight_waves_per_row(emu):
+    check(emu, 32768, 2, 1, O.FLAG_PERM | O.FLAG_RELU | FLAG_BIAS, seed=4)
+
+
+@wide
+def test_complex_16384_eight_waves_per_row(emu):
+    check(emu, 16384, 2, 1, O.FLAG_COMPLEX | O.FLAG_PERM, seed=5)
+
+
 @pytest.mark.parametrize("N", [8, 16, 64, 256, 1024])
 def test_real_bias(emu, N):
     check(emu, N, 3, 9, O.FLAG_PERM | O.FLAG_RELU | FLAG_BIAS, seed=N + 1)

@@ -106,12 +106,12 @@ def test_real_widths(acdc, N, flags):
     run_case(acdc, N, 3, 67, flags, seed=N + flags)          # 67: a ragged last workgroup
 
 
-@pytest.mark.parametrize("N", [8192, 9216, 16384])
+@pytest.mark.parametrize("N", [8192, 9216, 16384, 32768])
 def test_real_wide_rows(acdc, N):
     run_case(acdc, N, 2, 5, P | R, seed=N)
 
 
-@pytest.mark.parametrize("N", [8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096, 8192])
+@pytest.mark.parametrize("N", [8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096, 8192, 16384])
 def test_complex_widths(acdc, N):
     run_case(acdc, N, 3, 11, CX | P, seed=N)
 
@@ -269,7 +269,7 @@ def test_autograd_wrapper(acdc):
 
 # ----------------------------------------------- D-domain bias, accumulation
 
-@pytest.mark.parametrize("N", [8, 64, 256, 1024, 2048, 4096, 9216, 16384])
+@pytest.mark.parametrize("N", [8, 64, 256, 1024, 2048, 4096, 9216, 16384, 32768])
 def test_bias_widths(acdc, N):
     B = 67 if N <= 4096 else 5                           # a ragged last workgroup
     run_case(acdc, N, 3, B, P | R | FLAG_BIAS, seed=N + 3)
