@@ -38,7 +38,9 @@
  *   A, D, grad_A, grad_D   [K][N]       same element type as x
  *   bias, grad_bias        [K][N]       float (ACDC_FLAG_BIAS, real layers only)
  *   perm                   [K][N]       int32, each row a permutation of 0..N-1
- *   saved                  [K-1][batch][N] layer inputs u_1..u_{K-1}
+ *   saved                  [L][batch][N] layer inputs: u_1..u_{K-1} in slots 0..K-2, and with
+ *                          ACDC_FLAG_PERM u_0 = x gathered through perm[0] in slot K-1
+ *                          (L = K-1, or K with ACDC_FLAG_PERM)
  * The caller owns every buffer, including the workspaces; the library only
  * owns a small per-(device, N) table of constants built on first use (or by
  * acdc_prepare) and kept until the process ends.
@@ -95,7 +97,8 @@ int acdc_supported(int32_t N, uint32_t flags);
 int acdc_prepare(int32_t N, uint32_t flags);
 
 /* Bytes of the optional buffer `saved` that acdc_forward fills for
- * acdc_backward: the layer inputs u_1..u_{K-1}, [K-1][batch][N] elements. */
+ * acdc_backward: the layer inputs u_1..u_{K-1}, [K-1][batch][N] elements,
+ * plus u_0 (x gathered through perm[0]) in a last slot with ACDC_FLAG_PERM. */
 size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
 
 /* Bytes of workspace acdc_forward needs (the per-layer quartet coefficients
@@ -104,14 +107,14 @@ size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_
 
 /* Bytes of workspace acdc_backward needs: per-workgroup partial sums of the
  * parameter gradients, the per-layer quartet coefficients, the batch sums
- * behind the bias gradient (ACDC_FLAG_BIAS), and -- when have_saved is 0 --
- * room to recompute the layer inputs (the paper's recompute policy,
- * Sec. 5.3). */
+ * behind the bias gradient (ACDC_FLAG_BIAS), and -- when have_saved is 0 and
+ * acdc_saved_bytes(...) is not 0 -- room to recompute the layer inputs (the
+ * paper's recompute policy, Sec. 5.3). */
 size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags, int have_saved);
 
 /* Forward cascade: y = cascade(x).  `bias` is read with ACDC_FLAG_BIAS and
  * ignored (may be null) otherwise; `perm` likewise with ACDC_FLAG_PERM.  If
- * `saved` is non-null it also stores the layer inputs u_1..u_{K-1} there, for
+ * `saved` is non-null it also stores the layer inputs (see acdc_saved_bytes) there, for
  * acdc_backward; saved_bytes must be at least acdc_saved_bytes(...) (else
  * ACDC_ERR_WORKSPACE, nothing launched). */
 int acdc_forward(const float* x, float* y, const float* A, const float* D, const float* bias,

@@ -92,7 +92,8 @@ def prepare(N: int, flags: int = 0, device=None):
 
 def saved_numel(x: torch.Tensor, K: int, flags: int = 0) -> int:
     """Elements (of x's dtype) of the buffer acdc_forward fills for
-    acdc_backward: the layer inputs u_1..u_{K-1}."""
+    acdc_backward: the layer inputs u_1..u_{K-1}, preceded by u_0 (x gathered
+    through perm[0]) with FLAG_PERM."""
     flags = _flags(flags, x)
     nbytes = lib().acdc_saved_bytes(x.shape[0], x.shape[1], K, flags)
     return nbytes // x.element_size()
@@ -102,10 +103,13 @@ def alloc_saved(x: torch.Tensor, K: int, flags: int = 0) -> torch.Tensor:
     return torch.empty(saved_numel(x, K, flags), dtype=x.dtype, device=x.device)
 
 
-def saved_layer_inputs(saved: torch.Tensor, x: torch.Tensor, K: int) -> torch.Tensor:
-    """View of the layer inputs u_1..u_{K-1} inside a saved buffer, [K-1, batch, N]."""
+def saved_layer_inputs(saved: torch.Tensor, x: torch.Tensor, K: int, flags: int = 0) -> torch.Tensor:
+    """View of the layer inputs inside a saved buffer, [slots, batch, N]:
+    u_1..u_{K-1} in slots 0..K-2, and with FLAG_PERM u_0 (x gathered through
+    perm[0]) in slot K-1."""
     B, N = x.shape
-    return saved[: max(K - 1, 0) * B * N].view(max(K - 1, 0), B, N)
+    L = K - 1 + (1 if flags & FLAG_PERM else 0)
+    return saved[: L * B * N].view(L, B, N)
 
 
 def forward(x, A, D, perm=None, flags: int = 0, save: bool = False, out=None, saved=None, bias=None):
@@ -154,7 +158,7 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0, saved=None, bias=None, 
                "grad_D": gD, "grad_bias": gB, "perm": perm if flags & FLAG_PERM else None}, cplx, x.device)
     L = lib()
     use_saved = saved is not None and saved.numel() > 0
-    have_saved = 1 if (use_saved or K == 1) else 0
+    have_saved = 1 if (use_saved or saved_numel(x, K, flags) == 0) else 0
     ws_bytes = L.acdc_backward_workspace_bytes(B, N, K, flags, have_saved)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=x.device)
     with torch.cuda.device(x.device):

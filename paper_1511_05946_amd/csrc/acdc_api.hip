@@ -392,9 +392,11 @@ long long bwd_tiles(int64_t batch) {
 
 size_t elem_floats(uint32_t flags) { return (flags & kFlagComplex) ? 2 : 1; }
 
-// Floats of the `saved` buffer: the layer inputs u_1..u_{K-1}.
+// Floats of the `saved` buffer: the layer inputs u_1..u_{K-1}, preceded by
+// u_0 (x gathered through perm[0]) with PERM.
+size_t saved_layers(int32_t K, uint32_t flags) { return size_t(K - 1) + ((flags & kFlagPerm) ? 1 : 0); }
 size_t saved_floats(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
-  return size_t(K - 1) * size_t(batch) * size_t(N) * elem_floats(flags);
+  return saved_layers(K, flags) * size_t(batch) * size_t(N) * elem_floats(flags);
 }
 
 struct WsLayout {
@@ -421,7 +423,7 @@ WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool ha
   };
   if (flags & kFlagComplex) dispatch_complex(N, f);
   else dispatch_real(N, f);
-  if (!have_saved && K > 1) w.stash = align256(saved_floats(batch, N, K, flags) * 4);
+  if (!have_saved) w.stash = align256(saved_floats(batch, N, K, flags) * 4);
   w.off_mq = 0;
   w.off_partial = w.off_mq + w.mq;
   w.off_gs = w.off_partial + w.partial;
@@ -569,7 +571,8 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
   if (!distinct({grad_x, grad_A, grad_D, grad_bias},
                 {x, grad_y, A, D, bias, perm, saved, grad_x, grad_A, grad_D, grad_bias, workspace}))
     return ACDC_ERR_INVALID_ARG;
-  const bool have_saved = saved != nullptr || K == 1;
+  // nothing to recompute when no layer input needs storing (K == 1 without PERM)
+  const bool have_saved = saved != nullptr || saved_layers(K, flags) == 0;
   const WsLayout w = bwd_layout(batch, N, K, flags, have_saved);
   if (w.total > 0 && (workspace == nullptr || workspace_bytes < w.total)) return ACDC_ERR_WORKSPACE;
   const bool cplx = (flags & kFlagComplex) != 0;

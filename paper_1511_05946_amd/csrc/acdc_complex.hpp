@@ -135,8 +135,9 @@ __host__ __device__ void cplx_forward_row(Ctx& ctx, const CplxArgs& a, unsigned 
   O::load(GView::of(a.x + row0 * RS), roff, v, t, valid);
   for (int k = 0; k < a.K; ++k) {
     if (a.flags & 1u) O::gather(ctx, v, t, slab2, GView::of(a.perm + (long long)k * N));
-    if (a.saved != nullptr && k > 0 && valid)
-      O::store(GView::of(a.saved + ((long long)(k - 1) * a.batch + row0) * RS), roff, v, t);
+    // stash u_k: u_1..u_{K-1} in slots 0..K-2, and with PERM u_0 in slot K-1
+    if (a.saved != nullptr && (k > 0 || (a.flags & 1u)) && valid)
+      O::store(GView::of(a.saved + ((long long)(k > 0 ? k - 1 : a.K - 1) * a.batch + row0) * RS), roff, v, t);
     O::template scale<false>(v, GView::of(a.A + k * RS), t);
     O::template fft<false>(ctx, v, t, slab2, tab);
     O::template scale_freq<false>(v, GView::of(a.D + k * RS), invN, t);
@@ -162,7 +163,10 @@ __host__ __device__ void cplx_backward_row(Ctx& ctx, const CplxArgs& a, unsigned
   float2 g[P];
   O::load(GView::of(a.gy + row0 * RS), roff, g, t, valid);
   for (int k = a.K - 1; k >= 0; --k) {
-    const GView ug = GView::of(k == 0 ? a.x + row0 * RS : a.saved + ((long long)(k - 1) * a.batch + row0) * RS);
+    // u_k: stash slot k - 1; u_0 = x, or with PERM stash slot K - 1
+    const long long slot = k > 0 ? k - 1 : a.K - 1;
+    const GView ug = GView::of(k == 0 && !(a.flags & 1u) ? a.x + row0 * RS
+                                                         : a.saved + (slot * a.batch + row0) * RS);
     const GView ak = GView::of(a.A + k * RS);
     float* part = a.partial + (tile * a.K + k) * PS;
     float2 h[P];

@@ -407,7 +407,8 @@ struct RealArgs {
   const float* A;
   const float4* Mq;    // [K][NSL][3][T] quartet coefficients (real_mq_entry)
   const int* perm;     // [K][N] (PERM only)
-  float* saved;        // [K-1][batch][N] layer inputs u_1..u_{K-1} (may be null)
+  float* saved;        // layer inputs [slots][batch][N]: u_1..u_{K-1} in slots 0..K-2, and with
+                       // PERM u_0 in slot K-1 (may be null)
   const float* gy;     // backward: upstream gradient
   float* gx;           // backward: input gradient
   float* partial;      // backward: [tiles][K][N + QF] per-tile sums
@@ -443,8 +444,11 @@ __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned 
     } else {
       O::load_vec(av, ak, L);
     }
-    if (a.saved != nullptr && k > 0 && valid)
-      O::store(GView::of(a.saved + ((long long)(k - 1) * a.batch + row0) * N), roff, v, L);
+    // stash u_k for the backward: u_1..u_{K-1} in slots 0..K-2, and with
+    // PERM u_0 = x gathered through perm[0] in slot K-1 (so the backward
+    // needs no gather of x)
+    if (a.saved != nullptr && valid && (k > 0 || permute))
+      O::store(GView::of(a.saved + ((long long)(k > 0 ? k - 1 : a.K - 1) * a.batch + row0) * N), roff, v, L);
     O::scale(v, av);
     typename O::template FwdTabs<BIAS> tb;
     O::template fft<false>(ctx, v, t, slab2, tab, [&] { O::load_mhead(tb, t, mq); });
@@ -473,10 +477,12 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
   // from g = 0, which every step keeps exactly zero (linear transforms,
   // diagonal scalings, masks); its images H * G and u * g therefore vanish
   // without masking u, as long as that first row is finite.
-  // layer input u_k: the block input for k = 0, else the stored layer input
+  // layer input u_k: stash slot k - 1 for k > 0; for k = 0 the block input
+  // itself, or with PERM stash slot K - 1 (x gathered through perm[0])
   const float* const x0 = a.x + row0 * N;
   const float* const s0 = a.saved + (row0 - a.batch) * N;
-  auto u_view = [&](int k) { return GView::of(k == 0 ? x0 : s0 + (long long)k * a.batch * N); };
+  const float* const u0 = permute ? s0 + (long long)a.K * a.batch * N : x0;  // slot K-1 with PERM
+  auto u_view = [&](int k) { return GView::of(k == 0 ? u0 : s0 + (long long)k * a.batch * N); };
   float2 g[P];
   float4 uv[NCH], av[NCH];
   int4 idx[NCH];

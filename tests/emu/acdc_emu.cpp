@@ -115,8 +115,9 @@ void real_bwd(const float* x, const float* gy, const float* A, const float* D, c
   const bool acc = (flags & kFlagAccumulate) != 0;
   std::vector<float> saved_buf;
   const float* saved = saved_in;
-  if (saved == nullptr && K > 1) {
-    saved_buf.resize((size_t)(K - 1) * batch * PL::N);
+  const size_t layers = size_t(K - 1) + ((flags & kFlagPerm) ? 1 : 0);  // u_0 too with PERM
+  if (saved == nullptr && layers > 0) {
+    saved_buf.resize(layers * batch * PL::N);
     real_fwd<PL>(x, nullptr, A, D, B, perm, batch, K, flags, saved_buf.data(), tab);
     saved = saved_buf.data();
   }
@@ -164,8 +165,9 @@ void cplx_bwd(const float* x, const float* gy, const float* A, const float* D, c
   using L = Launch<PL>;
   std::vector<float> saved_buf;
   const float* saved = saved_in;
-  if (saved == nullptr && K > 1) {
-    saved_buf.resize((size_t)(K - 1) * batch * 2 * PL::N);
+  const size_t layers = size_t(K - 1) + ((flags & kFlagPerm) ? 1 : 0);  // u_0 too with PERM
+  if (saved == nullptr && layers > 0) {
+    saved_buf.resize(layers * batch * 2 * PL::N);
     cplx_fwd<PL>(x, nullptr, A, D, perm, batch, K, flags, saved_buf.data(), tab);
     saved = saved_buf.data();
   }

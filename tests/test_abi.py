@@ -65,12 +65,14 @@ def test_status_strings(L):
 
 
 def test_sizes(L):
-    assert L.acdc_saved_bytes(8192, 4096, 12, PERM | RELU) == 11 * 8192 * 4096 * 4
+    assert L.acdc_saved_bytes(8192, 4096, 12, PERM | RELU) == 12 * 8192 * 4096 * 4   # u_0 .. u_11
+    assert L.acdc_saved_bytes(8192, 4096, 12, RELU) == 11 * 8192 * 4096 * 4          # u_1 .. u_11
     assert L.acdc_saved_bytes(10, 64, 1, 0) == 0
+    assert L.acdc_saved_bytes(10, 64, 1, PERM) == 10 * 64 * 4
     assert L.acdc_saved_bytes(10, 64, 3, CX) == 2 * 10 * 64 * 8
     ws_saved = L.acdc_backward_workspace_bytes(8192, 4096, 12, PERM | RELU, 1)
     ws_recompute = L.acdc_backward_workspace_bytes(8192, 4096, 12, PERM | RELU, 0)
-    assert ws_saved > 0 and ws_recompute >= ws_saved + 11 * 8192 * 4096 * 4
+    assert ws_saved > 0 and ws_recompute >= ws_saved + 12 * 8192 * 4096 * 4
     assert L.acdc_forward_workspace_bytes(8192, 4096, 12, 0) > 0
     assert L.acdc_forward_workspace_bytes(10, 4096, 12, CX) == 0
     # invalid combinations report 0

@@ -39,24 +39,29 @@ def _p(a):
     return None if a is None else a.ctypes.data
 
 
-def check(L, N, K, B, flags, seed=0, with_saved=False):
+def check(L, N, K, B, flags, seed=0, with_saved=False, perm0=False):
     x, A, D, perm, gy = make_inputs(N, K, B, flags, seed)
+    if perm0:
+        # the workloads keep perm[0] the identity; any permutation is valid
+        perm[0] = np.random.default_rng(seed + 99).permutation(N).astype(np.int32)
     bias = make_bias(N, K, seed) if flags & FLAG_BIAS else None
     tol = TOL_COMPLEX if flags & O.FLAG_COMPLEX else TOL_REAL
     y = np.zeros_like(x)
-    saved = np.zeros((max(K - 1, 0), B, N), x.dtype) if with_saved else None
+    first = 0 if flags & O.FLAG_PERM else 1             # u_0 is stashed too with PERM
+    saved = np.zeros((K - first, B, N), x.dtype) if with_saved else None
     assert L.acdc_emu_forward(_p(x), _p(y), _p(A), _p(D), _p(bias), _p(perm), B, N, K, flags, _p(saved)) == 0
     yr, cache = O.forward(x, A, D, perm, flags & 7, keep=True, B=bias)
     assert rel_err(y, yr) < tol
-    if with_saved and K > 1:
-        for k in range(1, K):
-            assert rel_err(saved[k - 1], cache["u"][k]) < tol
+    if with_saved:
+        # u_k in slot k - 1; with PERM u_0 (x gathered through perm[0]) in slot K - 1
+        for k in range(first, K):
+            assert rel_err(saved[k - 1 if k > 0 else K - 1], cache["u"][k]) < tol
     keep = relu_safe_rows(cache["v"], K) if flags & O.FLAG_RELU else np.ones(B, bool)
     x, gy = np.ascontiguousarray(x[keep]), np.ascontiguousarray(gy[keep])
     Bk = x.shape[0]
     gx, gA, gD = np.zeros_like(x), np.zeros_like(A), np.zeros_like(D)
     gB = np.zeros_like(A) if bias is not None else None
-    sv = np.ascontiguousarray(saved[:, keep]) if (with_saved and K > 1) else None
+    sv = np.ascontiguousarray(saved[:, keep]) if (with_saved and K - first > 0) else None
     assert L.acdc_emu_backward(_p(x), _p(gy), _p(A), _p(D), _p(bias), _p(perm), _p(sv), _p(gx), _p(gA), _p(gD),
                                _p(gB), Bk, N, K, flags) == 0
     ref = O.backward(x, gy, A, D, perm, flags & 7, B=bias)
@@ -76,6 +81,13 @@ def test_real_small(emu, N, flags):
 @pytest.mark.parametrize("N", [8, 16, 64, 256, 1024])
 def test_complex_small(emu, N):
     check(emu, N, 2, 5, O.FLAG_COMPLEX | O.FLAG_PERM, seed=N)
+
+
+@pytest.mark.parametrize("flags", [O.FLAG_PERM | O.FLAG_RELU, O.FLAG_COMPLEX | O.FLAG_PERM])
+@pytest.mark.parametrize("K", [1, 3])
+def test_first_layer_permutation(emu, flags, K):
+    check(emu, 256, K, 5, flags, seed=21 + K, perm0=True)
+    check(emu, 256, K, 5, flags, seed=31 + K, perm0=True, with_saved=True)
 
 
 def test_real_4096_with_saved(emu):

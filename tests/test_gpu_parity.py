@@ -64,9 +64,12 @@ def refill_safe_rows(xs, gys, A, D, perm, flags, need, seed, chunk=8, max_draws=
     return np.ascontiguousarray(xs), np.ascontiguousarray(gys)
 
 
-def run_case(acdc, N, K, B, flags, seed=0, save=True, check_bwd=True, rows=None):
-    print(f"[case] N={N} K={K} B={B} flags={flags} seed={seed} save={save}", flush=True)
+def run_case(acdc, N, K, B, flags, seed=0, save=True, check_bwd=True, rows=None, perm0=False):
+    print(f"[case] N={N} K={K} B={B} flags={flags} seed={seed} save={save} perm0={perm0}", flush=True)
     x, A, D, perm, gy = make_inputs(N, K, B, flags, seed)
+    if perm0:
+        # the workloads keep perm[0] the identity; any permutation is valid
+        perm[0] = np.random.default_rng(seed + 99).permutation(N).astype(np.int32)
     bias = make_bias(N, K, seed) if flags & FLAG_BIAS else None
     bt = dev(bias) if bias is not None else None
     tol = TOL_COMPLEX if flags & CX else TOL_REAL
@@ -77,10 +80,11 @@ def run_case(acdc, N, K, B, flags, seed=0, save=True, check_bwd=True, rows=None)
     yr, cache = O.forward(x[sel], A, D, perm, flags & 7, keep=True, B=bias)
     e = rel_err(yg[sel], yr)
     assert e < tol, f"forward rel err {e:.3e}"
-    if save and K > 1:
-        sg = host(acdc.saved_layer_inputs(saved, xt, K))
-        for k in range(1, K):
-            assert rel_err(sg[k - 1][sel], cache["u"][k]) < tol
+    if save:
+        # u_k in slot k - 1; with PERM u_0 (x gathered through perm[0]) in slot K - 1
+        sg = host(acdc.saved_layer_inputs(saved, xt, K, flags))
+        for k in range(0 if flags & P else 1, K):
+            assert rel_err(sg[k - 1 if k > 0 else K - 1][sel], cache["u"][k]) < tol
     if not check_bwd:
         return
     keep = relu_safe_rows(cache["v"], K) if flags & R else np.ones(len(sel), bool)
@@ -114,6 +118,13 @@ def test_real_wide_rows(acdc, N):
 @pytest.mark.parametrize("N", [8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096, 8192, 16384])
 def test_complex_widths(acdc, N):
     run_case(acdc, N, 3, 11, CX | P, seed=N)
+
+
+@pytest.mark.parametrize("save", [True, False])
+@pytest.mark.parametrize("N,flags", [(1024, P | R), (4096, P | R | FLAG_BIAS), (9216, P | R), (2048, CX | P)])
+def test_first_layer_permutation(acdc, N, flags, save):
+    run_case(acdc, N, 1, 7, flags, seed=40 + N, save=save, perm0=True)
+    run_case(acdc, N, 3, 7, flags, seed=41 + N, save=save, perm0=True)
 
 
 @pytest.mark.parametrize("save", [True, False])
