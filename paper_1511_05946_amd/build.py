@@ -18,7 +18,7 @@ LIB = os.path.join(PKG, "libacdc.so")
 
 # -packed-fp32-ops: keep every fp32 operation a plain VOP (no v_pk_*_f32).
 HIP_FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++20", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++20", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
 ]
@@ -47,16 +47,35 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False, extra_flags: list[str] | None = None) -> str:
-    src = os.path.join(CSRC, "acdc_api.hip")
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIP_FLAGS, *(extra_flags or []), "-I", INCLUDE, "-I", CSRC, src, "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    proc = subprocess.run(cmd, capture_output=True, text=True)
-    if proc.returncode != 0:
-        sys.stderr.write(proc.stdout + proc.stderr)
-        raise RuntimeError(f"hipcc failed ({proc.returncode})")
-    os.replace(tmp, LIB)
+    """Compile every csrc/*.hip to an object (in parallel), then link libacdc.so."""
+    import tempfile
+    srcs = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
+    with tempfile.TemporaryDirectory(prefix="acdc_build_") as tmpdir:
+        objs, procs = [], []
+        for src in srcs:
+            obj = os.path.join(tmpdir, os.path.basename(src) + ".o")
+            cmd = [hipcc(), *HIP_FLAGS, *(extra_flags or []), "-I", INCLUDE, "-I", CSRC, "-c", src, "-o", obj]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)))
+            objs.append(obj)
+        failed = False
+        for src, proc in procs:
+            out, err = proc.communicate()
+            if proc.returncode != 0:
+                sys.stderr.write(out + err)
+                failed = True
+        if failed:
+            raise RuntimeError("hipcc failed")
+        tmp = LIB + ".tmp"
+        cmd = [hipcc(), "--offload-arch=gfx950", "-fPIC", "-shared", *objs, "-o", tmp]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        proc = subprocess.run(cmd, capture_output=True, text=True)
+        if proc.returncode != 0:
+            sys.stderr.write(proc.stdout + proc.stderr)
+            raise RuntimeError(f"hipcc link failed ({proc.returncode})")
+        os.replace(tmp, LIB)
     return LIB
 
 

@@ -8,6 +8,8 @@
 //                  the workgroup's rows into one partial per workgroup
 //   k_real_reduce  fixed-order sum of the partials over workgroups
 //   k_real_dct     DCT-II of the batch sums of g (bias gradient, tiny)
+// The multi-pass path (acdc_multipass.hip) serves widths beyond the fused
+// plans and ACDC_FLAG_MULTIPASS; its host sequence is at the end of this file.
 //   k_cplx_*       the same for the complex AFDF layers
 #include <hip/hip_runtime.h>
 
@@ -18,34 +20,11 @@
 #include <vector>
 
 #include "acdc.h"
+#include "acdc_devctx.hpp"
+#include "acdc_multipass.hpp"
 #include "acdc_registry.hpp"
 
 namespace acdc {
-
-// LDS synchronisation for a row spread over T threads.  A row that fits in
-// one wavefront only needs its LDS accesses kept in program order (LDS
-// operations of a wavefront execute in order); wider rows use the workgroup
-// barrier.
-template <int T>
-struct DevCtx {
-  // Barriers order LDS only ("local" fences): global loads issued ahead of
-  // a barrier stay in flight across it.
-  __device__ __forceinline__ static void lds_barrier() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-  }
-  __device__ __forceinline__ void sync_row() {
-    if constexpr (T > 64) {
-      lds_barrier();
-    } else {
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    }
-  }
-  __device__ __forceinline__ void sync_all() { lds_barrier(); }
-};
 
 template <class PL>
 __global__ __launch_bounds__(256) void k_real_mq(const float* __restrict__ D, const float* __restrict__ Bias,
@@ -276,12 +255,23 @@ struct ProfScope {
   }
 };
 
-bool supported(int N, unsigned flags) {
+bool fused_supported(int N, unsigned flags) {
   bool ok = false;
   auto probe = [&]<class PL>() { ok = true; };
   if (flags & kFlagComplex) dispatch_complex(N, probe);
   else dispatch_real(N, probe);
   return ok;
+}
+
+// Multi-pass path: real layers of power-of-two width 256 ... 2^22.
+bool mp_width(long long N) { return N >= 256 && N <= (1LL << 22) && (N & (N - 1)) == 0; }
+bool use_multipass(int N, unsigned flags) {
+  if (flags & kFlagComplex) return false;
+  return (flags & kFlagMultipass) != 0 || !fused_supported(N, flags);
+}
+bool supported(int N, unsigned flags) {
+  if (flags & kFlagComplex) return !(flags & kFlagMultipass) && fused_supported(N, flags);
+  return use_multipass(N, flags) ? mp_width(N) : true;
 }
 
 // Constant table of (N, complex) on the current device; built and uploaded
@@ -347,7 +337,7 @@ long long persistent_grid(const void* kernel, int threads, long long tiles) {
   return (n > 0 && n < tiles) ? n : tiles;
 }
 
-constexpr uint32_t kAllFlags = kFlagPerm | kFlagRelu | kFlagComplex | kFlagBias | kFlagAccumulate;
+constexpr uint32_t kAllFlags = kFlagPerm | kFlagRelu | kFlagComplex | kFlagBias | kFlagAccumulate | kFlagMultipass;
 
 bool flags_supported(uint32_t flags) {
   return !((flags & kFlagComplex) && (flags & (kFlagRelu | kFlagBias)));
@@ -473,6 +463,223 @@ int launch_cplx_fwd(const CplxArgs& a, hipStream_t s) {
   return e == hipSuccess ? ACDC_OK : hip_fail(e);
 }
 
+// ------------------------------------------------------ multi-pass path
+
+mp::Geo mp_geo(long long N) {
+  mp::Geo g;
+  g.M = N / 2;
+  g.L = int(g.M < 8192 ? g.M : 8192);
+  const long long ratio = g.M / g.L;
+  g.R1 = ratio == 1 ? 1 : int(ratio <= 16 ? ratio : 16);
+  g.R2 = ratio <= 16 ? 1 : int(ratio / 16);
+  return g;
+}
+
+struct MpTabs {
+  const float2* tw = nullptr;
+  QuartetTabs q{};
+  const char* seg = nullptr;  // the complex plan table of the segment length
+};
+std::map<std::pair<int, int>, void*> g_mp_tables;  // (device, N) -> device table
+
+int get_mp_tables(int N, MpTabs* out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e);
+  const mp::Geo g = mp_geo(N);
+  int rc = get_table(g.L, true, &out->seg);
+  if (rc != ACDC_OK) return rc;
+  void* d = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto it = g_mp_tables.find({dev, N});
+    if (it != g_mp_tables.end()) d = it->second;
+  }
+  if (d == nullptr) {
+    std::vector<unsigned char> host;
+    if (!build_mp_tables(N, host)) return ACDC_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto it = g_mp_tables.find({dev, N});
+    if (it != g_mp_tables.end()) {
+      d = it->second;
+    } else {
+      e = hipMalloc(&d, host.size());
+      if (e != hipSuccess) return hip_fail(e);
+      e = hipMemcpy(d, host.data(), host.size(), hipMemcpyHostToDevice);
+      if (e != hipSuccess) {
+        (void)hipFree(d);
+        return hip_fail(e);
+      }
+      g_mp_tables[{dev, N}] = d;
+    }
+  }
+  const char* base = static_cast<const char*>(d);
+  const MpTableLayout l = mp_table_layout(N);
+  out->tw = reinterpret_cast<const float2*>(base + l.tw);
+  const double qb = 1.0 / (2.0 * std::sqrt(double(N)));
+  out->q = QuartetTabs{reinterpret_cast<const float4*>(base + l.mk0), reinterpret_cast<const float4*>(base + l.mk1),
+                       reinterpret_cast<const int4*>(base + l.qidx), reinterpret_cast<const int*>(base + l.qmask),
+                       float(0.9238795325112867561 * qb), float(0.3826834323650897717 * qb)};
+  return ACDC_OK;
+}
+
+size_t mp_mq_bytes(long long N, int K) { return align256(size_t(K) * size_t(N / 4) * kMqRows * sizeof(float4)); }
+size_t mp_rows_bytes(int64_t batch, long long N) { return align256(size_t(batch) * size_t(N) * sizeof(float)); }
+
+// Forward workspace: quartet coefficients, the packed spectrum, the layer output.
+size_t mp_fwd_ws(int64_t batch, int32_t N, int32_t K) {
+  return mp_mq_bytes(N, K) + 2 * mp_rows_bytes(batch, N);
+}
+
+// Backward workspace: quartet coefficients, the h and g spectra (contiguous,
+// transformed together), dL/dv of the current layer, the next layer's g,
+// the three images, the column-sum blocks, and the recompute stash.
+struct MpBwdWs {
+  size_t mq = 0, zhg = 0, gh1 = 0, gbuf = 0, imgD = 0, imgA = 0, imgB = 0, part = 0, stash = 0, total = 0;
+};
+MpBwdWs mp_bwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved) {
+  MpBwdWs w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  const size_t rows = size_t(batch) * size_t(N) * sizeof(float);
+  w.mq = take(mp_mq_bytes(N, K));
+  w.zhg = take(2 * rows);
+  w.gh1 = take(rows);
+  w.gbuf = take(rows);
+  w.imgD = take(rows);
+  w.imgA = take(rows);
+  w.imgB = take((flags & kFlagBias) ? rows : 0);
+  w.part = take(size_t((batch + mp::kColRows - 1) / mp::kColRows) * size_t(N) * sizeof(float));
+  w.stash = take(have_saved ? 0 : saved_floats(batch, N, K, flags) * sizeof(float));
+  w.total = off;
+  return w;
+}
+
+#define MP_TRY(call)                          \
+  do {                                        \
+    const hipError_t e_ = (call);             \
+    if (e_ != hipSuccess) return hip_fail(e_); \
+  } while (0)
+
+int mp_fft(float2* Z, long long rows, const mp::Geo& g, const MpTabs& t, bool inverse, hipStream_t s) {
+  if (!inverse) {
+    if (g.R1 > 1) MP_TRY(mp::dif(Z, rows, g, g.M, g.R1, t.tw, s));
+    if (g.R2 > 1) MP_TRY(mp::dif(Z, rows, g, g.M / g.R1, g.R2, t.tw, s));
+    MP_TRY(mp::segments(Z, rows * (g.M / g.L), g.L, false, t.seg, s));
+  } else {
+    MP_TRY(mp::segments(Z, rows * (g.M / g.L), g.L, true, t.seg, s));
+    if (g.R2 > 1) MP_TRY(mp::dit(Z, rows, g, g.M / g.R1, g.R2, t.tw, s));
+    if (g.R1 > 1) MP_TRY(mp::dit(Z, rows, g, g.M, g.R1, t.tw, s));
+  }
+  return ACDC_OK;
+}
+
+// Stash slot of layer input u_k (the fused path's layout): k - 1, or K - 1
+// for u_0 with PERM.
+float* mp_slot(float* saved, int k, int K, long long batch, long long N, bool perm_on) {
+  if (saved == nullptr) return nullptr;
+  if (k > 0) return saved + (long long)(k - 1) * batch * N;
+  return perm_on ? saved + (long long)(K - 1) * batch * N : nullptr;
+}
+
+int mp_forward_layers(const float* x, float* y, const float* A, const float4* Mq, const int32_t* perm,
+                      int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, float2* Z, float* zbuf,
+                      const MpTabs& t, hipStream_t s) {
+  const mp::Geo g = mp_geo(N);
+  const bool perm_on = (flags & kFlagPerm) != 0, relu = (flags & kFlagRelu) != 0;
+  for (int k = 0; k < K; ++k) {
+    const float* src = k == 0 ? x : zbuf;
+    MP_TRY(mp::pack(src, perm_on ? perm + (long long)k * N : nullptr, A + (long long)k * N,
+                    mp_slot(saved, k, K, batch, N, perm_on), Z, batch, N, s));
+    int rc = mp_fft(Z, batch, g, t, false, s);
+    if (rc != ACDC_OK) return rc;
+    MP_TRY(mp::mid_fwd(Z, Mq + (long long)k * (N / 4) * kMqRows, batch, g, (flags & kFlagBias) != 0, s));
+    rc = mp_fft(Z, batch, g, t, true, s);
+    if (rc != ACDC_OK) return rc;
+    MP_TRY(mp::unpack(Z, (k == K - 1 && y != nullptr) ? y : zbuf, batch, N, relu && k < K - 1, s));
+  }
+  return ACDC_OK;
+}
+
+int mp_forward(const float* x, float* y, const float* A, const float* D, const float* bias, const int32_t* perm,
+               int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, void* workspace, hipStream_t s) {
+  MpTabs t;
+  int rc = get_mp_tables(N, &t);
+  if (rc != ACDC_OK) return rc;
+  char* ws = static_cast<char*>(workspace);
+  float4* Mq = reinterpret_cast<float4*>(ws);
+  float2* Z = reinterpret_cast<float2*>(ws + mp_mq_bytes(N, K));
+  float* zbuf = reinterpret_cast<float*>(ws + mp_mq_bytes(N, K) + mp_rows_bytes(batch, N));
+  ProfScope prof(0, s);
+  MP_TRY(mp::mq(D, bias, Mq, K, N / 4, t.q, s));
+  return mp_forward_layers(x, y, A, Mq, perm, batch, N, K, flags, saved, Z, zbuf, t, s);
+}
+
+int mp_backward(const float* x, const float* grad_y, const float* A, const float* D, const float* bias,
+                const int32_t* perm, const float* saved, float* grad_x, float* grad_A, float* grad_D,
+                float* grad_bias, int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved,
+                void* workspace, hipStream_t s) {
+  MpTabs t;
+  int rc = get_mp_tables(N, &t);
+  if (rc != ACDC_OK) return rc;
+  const MpBwdWs w = mp_bwd_ws(batch, N, K, flags, have_saved);
+  char* ws = static_cast<char*>(workspace);
+  float4* Mq = reinterpret_cast<float4*>(ws + w.mq);
+  float2* Zh = reinterpret_cast<float2*>(ws + w.zhg);
+  float2* Zg = Zh + batch * (N / 2);
+  float* gh1 = reinterpret_cast<float*>(ws + w.gh1);
+  float* gbuf = reinterpret_cast<float*>(ws + w.gbuf);
+  float* imgD = reinterpret_cast<float*>(ws + w.imgD);
+  float* imgA = reinterpret_cast<float*>(ws + w.imgA);
+  float* imgB = (flags & kFlagBias) ? reinterpret_cast<float*>(ws + w.imgB) : nullptr;
+  float* part = reinterpret_cast<float*>(ws + w.part);
+  float* stash = have_saved ? const_cast<float*>(saved) : reinterpret_cast<float*>(ws + w.stash);
+  const mp::Geo g = mp_geo(N);
+  const bool perm_on = (flags & kFlagPerm) != 0, relu = (flags & kFlagRelu) != 0;
+  const bool acc = (flags & kFlagAccumulate) != 0;
+  ProfScope prof(1, s);
+  if (batch > 0) {
+    MP_TRY(mp::mq(D, bias, Mq, K, N / 4, t.q, s));
+    if (!have_saved) {
+      // recompute the layer inputs into the workspace (Zh, gh1 are free until the layer loop)
+      rc = mp_forward_layers(x, nullptr, A, Mq, perm, batch, N, K, flags, stash, Zh, gh1, t, s);
+      if (rc != ACDC_OK) return rc;
+    }
+  }
+  for (int k = K - 1; k >= 0; --k) {
+    float* gA = grad_A + (long long)k * N;
+    float* gD = grad_D + (long long)k * N;
+    float* gB = grad_bias ? grad_bias + (long long)k * N : nullptr;
+    if (batch > 0) {
+      const float* u = k > 0 || perm_on ? mp_slot(stash, k, K, batch, N, perm_on) : x;
+      const float* ak = A + (long long)k * N;
+      MP_TRY(mp::pack(k == K - 1 ? grad_y : gbuf, nullptr, nullptr, nullptr, Zg, batch, N, s));
+      MP_TRY(mp::pack(u, nullptr, ak, nullptr, Zh, batch, N, s));
+      rc = mp_fft(Zh, 2 * batch, g, t, false, s);  // Zh and Zg are contiguous
+      if (rc != ACDC_OK) return rc;
+      MP_TRY(mp::mid_bwd(Zh, Zg, Mq + (long long)k * (N / 4) * kMqRows, batch, g, imgD, imgB, s));
+      MP_TRY(mp::colsum(imgD, batch, N, part, gD, &t.q, acc, s));
+      if (gB) MP_TRY(mp::colsum(imgB, batch, N, part, gB, &t.q, acc, s));
+      rc = mp_fft(Zg, batch, g, t, true, s);
+      if (rc != ACDC_OK) return rc;
+      MP_TRY(mp::unpack(Zg, gh1, batch, N, false, s));
+      MP_TRY(mp::dA(gh1, u, ak, perm_on ? perm + (long long)k * N : nullptr, relu && k > 0, imgA,
+                    k == 0 ? grad_x : gbuf, batch, N, s));
+      MP_TRY(mp::colsum(imgA, batch, N, part, gA, nullptr, acc, s));
+    } else {
+      // no rows: zero (or unchanged, accumulating) parameter gradients
+      MP_TRY(mp::colsum(nullptr, 0, N, part, gD, &t.q, acc, s));
+      if (gB) MP_TRY(mp::colsum(nullptr, 0, N, part, gB, &t.q, acc, s));
+      MP_TRY(mp::colsum(nullptr, 0, N, part, gA, nullptr, acc, s));
+    }
+  }
+  return ACDC_OK;
+}
+
 }  // namespace
 }  // namespace acdc
 
@@ -486,6 +693,10 @@ extern "C" int acdc_supported(int32_t N, uint32_t flags) {
 
 extern "C" int acdc_prepare(int32_t N, uint32_t flags) {
   if (!acdc_supported(N, flags)) return ACDC_ERR_UNSUPPORTED;
+  if (use_multipass(N, flags)) {
+    MpTabs t;
+    return get_mp_tables(N, &t);
+  }
   const char* tab = nullptr;
   return get_table(N, (flags & kFlagComplex) != 0, &tab);
 }
@@ -497,13 +708,16 @@ extern "C" size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t
 
 extern "C" size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
   if (check_common(batch, N, K, flags) != ACDC_OK) return 0;
+  if (use_multipass(N, flags)) return mp_fwd_ws(batch, N, K);
   return fwd_ws(N, K, flags);
 }
 
 extern "C" size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags,
                                                 int have_saved) {
   if (check_common(batch, N, K, flags) != ACDC_OK) return 0;
-  return bwd_layout(batch, N, K, flags, have_saved != 0).total;
+  const bool hs = have_saved != 0 || saved_layers(K, flags) == 0;
+  if (use_multipass(N, flags)) return mp_bwd_ws(batch, N, K, flags, hs).total;
+  return bwd_layout(batch, N, K, flags, hs).total;
 }
 
 extern "C" int acdc_forward(const float* x, float* y, const float* A, const float* D, const float* bias,
@@ -521,8 +735,12 @@ extern "C" int acdc_forward(const float* x, float* y, const float* A, const floa
   if ((perm_on && perm == nullptr) || (bias_on && bias == nullptr)) return ACDC_ERR_INVALID_ARG;
   if (!bias_on) bias = nullptr;
   if (!distinct({y, saved}, {x, y, A, D, bias, perm, saved, workspace})) return ACDC_ERR_INVALID_ARG;
-  const size_t need = fwd_ws(N, K, flags);
+  const bool multipass = use_multipass(N, flags);
+  const size_t need = multipass ? mp_fwd_ws(batch, N, K) : fwd_ws(N, K, flags);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return ACDC_ERR_WORKSPACE;
+  if (multipass)
+    return mp_forward(x, y, A, D, bias, perm, batch, N, K, flags, saved, workspace,
+                      reinterpret_cast<hipStream_t>(stream));
   const bool cplx = (flags & kFlagComplex) != 0;
   const char* tab = nullptr;
   rc = get_table(N, cplx, &tab);
@@ -573,6 +791,12 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
     return ACDC_ERR_INVALID_ARG;
   // nothing to recompute when no layer input needs storing (K == 1 without PERM)
   const bool have_saved = saved != nullptr || saved_layers(K, flags) == 0;
+  if (use_multipass(N, flags)) {
+    const size_t need = mp_bwd_ws(batch, N, K, flags, have_saved).total;
+    if (workspace == nullptr || workspace_bytes < need) return ACDC_ERR_WORKSPACE;
+    return mp_backward(x, grad_y, A, D, bias, perm, saved, grad_x, grad_A, grad_D, grad_bias, batch, N, K, flags,
+                       have_saved, workspace, reinterpret_cast<hipStream_t>(stream));
+  }
   const WsLayout w = bwd_layout(batch, N, K, flags, have_saved);
   if (w.total > 0 && (workspace == nullptr || workspace_bytes < w.total)) return ACDC_ERR_WORKSPACE;
   const bool cplx = (flags & kFlagComplex) != 0;

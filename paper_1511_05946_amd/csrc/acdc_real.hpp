@@ -32,13 +32,63 @@
 
 namespace acdc {
 
-enum : unsigned { kFlagPerm = 1u, kFlagRelu = 2u, kFlagComplex = 4u, kFlagBias = 8u, kFlagAccumulate = 16u };
+enum : unsigned {
+  kFlagPerm = 1u,
+  kFlagRelu = 2u,
+  kFlagComplex = 4u,
+  kFlagBias = 8u,
+  kFlagAccumulate = 16u,
+  kFlagMultipass = 32u
+};
 
 // Rows of the per-layer quartet-coefficient table (real_mq_entry).
 constexpr int kMqRows = 4;
 
 __host__ __device__ __forceinline__ float2 sel2(bool c, float2 a, float2 b) {
   return make_float2(c ? a.x : b.x, c ? a.y : b.y);
+}
+
+// ------------------------------------------------------ Makhoul quartets
+// The per-quartet arithmetic shared by the fused row bodies and the
+// multi-pass path (which holds the spectrum in HBM between passes).
+
+// Real-FFT split of a Makhoul pair: E = Z[k] + conj Z[M-k],
+// O = (Z[k] - conj Z[M-k]) / i, s1 = E + w O, s2 = E - w O.
+struct Split {
+  float2 s1, s2;
+};
+__host__ __device__ __forceinline__ Split quartet_split(float2 zk, float2 zm, float2 w) {
+  const float2 E = make_float2(zk.x + zm.x, zk.y - zm.y);
+  const float2 Od = make_float2(zk.y + zm.y, zm.x - zk.x);
+  const float2 wO = cmul(Od, w);
+  return Split{cadd(E, wO), csub(E, wO)};
+}
+// DCT-II outputs of a split, up to the sign of X[N-k]: returns
+// (X[k], -X[N-k], X[M-k], X[M+k]), with the orthonormal scaling folded
+// into qa and qbr = (1 + i) qb, so u1 = qa s1 = X[k] - i X[N-k] and
+// u2 = qbr s2 = X[M-k] + i X[M+k].  The backward only forms products of
+// two such images, where the sign cancels.
+__host__ __device__ __forceinline__ void quartet_post(const Split& sp, float2 qa, float2 qbr, float (&X)[4]) {
+  const float2 u1 = cmul(sp.s1, qa), u2 = cmul(sp.s2, qbr);
+  X[0] = u1.x;
+  X[1] = u1.y;
+  X[2] = u2.x;
+  X[3] = u2.y;
+}
+// From a split, the D diagonal and the DCT-III pre-twiddle as the two
+// symmetric 2x2 maps L1 (on s1) and L2 (on s2), then the inverse split:
+// S = L1 s1 + L2 s2, Dd = L1 s1 - L2 s2, zk = S + i conj(w) Dd,
+// zm = conj(S - i conj(w) Dd).
+__host__ __device__ __forceinline__ void quartet_back(const Split& sp, float4 c0, float4 c1, float2& zk,
+                                                     float2& zm) {
+  const float2 w = make_float2(c1.z, c1.w);
+  const float2 s1 = sp.s1, s2 = sp.s2;
+  const float2 p1 = make_float2(__builtin_fmaf(c0.y, s1.y, c0.x * s1.x), __builtin_fmaf(c0.z, s1.y, c0.y * s1.x));
+  const float2 p2 = make_float2(__builtin_fmaf(c1.x, s2.y, c0.w * s2.x), __builtin_fmaf(c1.y, s2.y, c1.x * s2.x));
+  const float2 S = cadd(p1, p2), Dd = csub(p1, p2);
+  const float2 cw = cmulc(Dd, w);
+  zk = make_float2(S.x - cw.y, S.y + cw.x);
+  zm = make_float2(S.x + cw.y, cw.x - S.y);
 }
 
 template <class PL>
@@ -297,43 +347,16 @@ struct RealOps {
   template <bool BIAS>
   using FwdTabs = MqTabs<BIAS ? 3 : 2, 3>;
 
-  // Real-FFT split of a Makhoul pair: E = Z[k] + conj Z[M-k],
-  // O = (Z[k] - conj Z[M-k]) / i, s1 = E + w O, s2 = E - w O.
-  struct Split {
-    float2 s1, s2;
-  };
+  using Split = acdc::Split;
   __host__ __device__ __forceinline__ static Split split(float2 zk, float2 zm, float2 w) {
-    const float2 E = make_float2(zk.x + zm.x, zk.y - zm.y);
-    const float2 Od = make_float2(zk.y + zm.y, zm.x - zk.x);
-    const float2 wO = cmul(Od, w);
-    return Split{cadd(E, wO), csub(E, wO)};
+    return quartet_split(zk, zm, w);
   }
-  // DCT-II outputs of a split, up to the sign of X[N-k]: returns
-  // (X[k], -X[N-k], X[M-k], X[M+k]), with the orthonormal scaling folded
-  // into qa and qbr = (1 + i) qb, so u1 = qa s1 = X[k] - i X[N-k] and
-  // u2 = qbr s2 = X[M-k] + i X[M+k].  The backward only forms products of
-  // two such images, where the sign cancels.
   __host__ __device__ __forceinline__ static void post_x(const Split& sp, float2 qa, float2 qbr, float (&X)[4]) {
-    const float2 u1 = cmul(sp.s1, qa), u2 = cmul(sp.s2, qbr);
-    X[0] = u1.x;
-    X[1] = u1.y;
-    X[2] = u2.x;
-    X[3] = u2.y;
+    quartet_post(sp, qa, qbr, X);
   }
-  // From a split, the D diagonal and the DCT-III pre-twiddle as the two
-  // symmetric 2x2 maps L1 (on s1) and L2 (on s2), then the inverse split:
-  // S = L1 s1 + L2 s2, Dd = L1 s1 - L2 s2, zk = S + i conj(w) Dd,
-  // zm = conj(S - i conj(w) Dd).
   __host__ __device__ __forceinline__ static void sym_back(const Split& sp, float4 c0, float4 c1, float2& zk,
                                                            float2& zm) {
-    const float2 w = make_float2(c1.z, c1.w);
-    const float2 s1 = sp.s1, s2 = sp.s2;
-    const float2 p1 = make_float2(__builtin_fmaf(c0.y, s1.y, c0.x * s1.x), __builtin_fmaf(c0.z, s1.y, c0.y * s1.x));
-    const float2 p2 = make_float2(__builtin_fmaf(c1.x, s2.y, c0.w * s2.x), __builtin_fmaf(c1.y, s2.y, c1.x * s2.x));
-    const float2 S = cadd(p1, p2), Dd = csub(p1, p2);
-    const float2 cw = cmulc(Dd, w);
-    zk = make_float2(S.x - cw.y, S.y + cw.x);
-    zm = make_float2(S.x + cw.y, cw.x - S.y);
+    quartet_back(sp, c0, c1, zk, zm);
   }
 
   // Forward middle of a layer, in place per quartet slot: Z (frequency

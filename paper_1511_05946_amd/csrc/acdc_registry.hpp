@@ -153,13 +153,32 @@ inline bool dispatch_complex(int N, F&& f) {
   }
 }
 
-// d of layer k at the four quartet indices of slot entry e = slot*T + t.
+// The per-entry quartet tables of a width N: Makhoul twiddle blocks mk0,
+// mk1, the four DCT indices of each entry and their masks (low nibble: the
+// d values to read; high nibble: the image values to store).  The fused
+// plans index them by slot entry e = slot*T + t, the multi-pass path by the
+// quartet number; entry 0 is the self-paired quartet (Z[0], Z[M/2]) in both.
+struct QuartetTabs {
+  const float4* mk0;
+  const float4* mk1;
+  const int4* qidx;
+  const int* qmask;
+  float qb0_re, qb0_im;  // entry 0's DCT-III pre-twiddle exp(i pi/8) / (2 sqrt(N))
+};
 template <class PL>
-__host__ __device__ __forceinline__ float4 real_dq_entry(const float* Dk, const char* tab, int e) {
-  const int4 idx = reinterpret_cast<const int4*>(tab + PL::OFF_QIDX)[e];
-  const int m = reinterpret_cast<const int*>(tab + PL::OFF_QMASK)[e] & 0xF;
-  return make_float4((m & 1) ? Dk[idx.x] : 0.f, (m & 2) ? Dk[idx.y] : 0.f, (m & 4) ? Dk[idx.z] : 0.f,
-                     (m & 8) ? Dk[idx.w] : 0.f);
+__host__ __device__ __forceinline__ QuartetTabs quartet_tabs(const char* tab) {
+  return QuartetTabs{reinterpret_cast<const float4*>(tab + PL::OFF_MK0),
+                     reinterpret_cast<const float4*>(tab + PL::OFF_MK1),
+                     reinterpret_cast<const int4*>(tab + PL::OFF_QIDX),
+                     reinterpret_cast<const int*>(tab + PL::OFF_QMASK), RealOps<PL>::kQbRe, RealOps<PL>::kQbIm};
+}
+
+// A layer vector (d or b) at the four quartet indices of entry e.
+__host__ __device__ __forceinline__ float4 quartet_gather(const float* Vk, const QuartetTabs& q, int e) {
+  const int4 idx = q.qidx[e];
+  const int m = q.qmask[e] & 0xF;
+  return make_float4((m & 1) ? Vk[idx.x] : 0.f, (m & 2) ? Vk[idx.y] : 0.f, (m & 4) ? Vk[idx.z] : 0.f,
+                     (m & 8) ? Vk[idx.w] : 0.f);
 }
 
 // Quartet coefficients of layer k at slot entry e = slot*T + t.
@@ -192,16 +211,15 @@ __host__ __device__ inline QuartetD qd_mul(QuartetD a, QuartetD w) {
 __host__ __device__ inline QuartetD qd_mulc(QuartetD a, QuartetD w) {  // a * conj(w)
   return QuartetD{a.x * w.x + a.y * w.y, a.y * w.x - a.x * w.y};
 }
-template <class PL>
-__host__ __device__ inline void real_mq_entry(const float* Dk, const float* Bk, const char* tab, int e,
-                                              float4 (&out)[kMqRows]) {
-  const float4 m0 = reinterpret_cast<const float4*>(tab + PL::OFF_MK0)[e];
-  const float4 m1 = reinterpret_cast<const float4*>(tab + PL::OFF_MK1)[e];
-  const float4 d = real_dq_entry<PL>(Dk, tab, e);
+__host__ __device__ inline void quartet_coeffs(const float* Dk, const float* Bk, const QuartetTabs& q, int e,
+                                               float4 (&out)[kMqRows]) {
+  const float4 m0 = q.mk0[e];
+  const float4 m1 = q.mk1[e];
+  const float4 d = quartet_gather(Dk, q, e);
   const QuartetD qa{m0.z, m0.w}, qb{m1.x, m1.y}, qap{m1.z, m1.w};
   // thread 0's slot 0 carries the self-paired values; its pre-twiddle uses
   // exp(i pi/8) / (2 sqrt(N))
-  const QuartetD qbp = e == 0 ? QuartetD{RealOps<PL>::kQbRe, RealOps<PL>::kQbIm} : qb;
+  const QuartetD qbp = e == 0 ? QuartetD{q.qb0_re, q.qb0_im} : qb;
   double L1[2][2], L2[2][2];
   for (int j = 0; j < 2; ++j) {
     const QuartetD s{double(j == 0), double(j == 1)};
@@ -229,13 +247,19 @@ __host__ __device__ inline void real_mq_entry(const float* Dk, const float* Bk, 
   // after the 2x2 maps.
   out[3] = make_float4(0.f, 0.f, 0.f, 0.f);
   if (Bk != nullptr) {
-    const float4 b = real_dq_entry<PL>(Bk, tab, e);
+    const float4 b = quartet_gather(Bk, q, e);
     const QuartetD ap = qd_mul(QuartetD{b.x, -double(b.y)}, qap);
     const QuartetD bp = qd_mulc(QuartetD{double(b.z) + b.w, double(b.w) - b.z}, qbp);
     const QuartetD S{ap.x + bp.x, ap.y + bp.y}, Dd{ap.x - bp.x, ap.y - bp.y};
     const QuartetD cw = qd_mulc(Dd, QuartetD{m0.x, m0.y});  // Dd conj(w)
     out[3] = make_float4(float(S.x - cw.y), float(S.y + cw.x), float(S.x + cw.y), float(cw.x - S.y));
   }
+}
+
+template <class PL>
+__host__ __device__ inline void real_mq_entry(const float* Dk, const float* Bk, const char* tab, int e,
+                                              float4 (&out)[kMqRows]) {
+  quartet_coeffs(Dk, Bk, quartet_tabs<PL>(tab), e, out);
 }
 
 // Fixed-order batch reduction of the per-tile partials.  Entry e (a float4)

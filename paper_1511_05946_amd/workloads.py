@@ -35,6 +35,7 @@ FLAG_RELU = 2
 FLAG_COMPLEX = 4
 FLAG_BIAS = 8
 FLAG_ACCUMULATE = 16
+FLAG_MULTIPASS = 32
 
 
 @dataclass(frozen=True)

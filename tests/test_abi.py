@@ -49,13 +49,23 @@ def test_supported_widths(L):
         assert L.acdc_supported(N, PERM | RELU) == 1
     for N in (8, 64, 1024, 4096, 8192, 16384):
         assert L.acdc_supported(N, CX | PERM) == 1
-    for N in (0, 2, 4, 6, 12, 100, 1000, 3072, 65536):
+    for N in (0, 2, 4, 6, 12, 100, 1000, 3072, 1 << 23):
         assert L.acdc_supported(N, 0) == 0
     assert L.acdc_supported(32768, CX) == 0
+    # multi-pass: any power of two 256 ... 2^22, real layers only
+    MP = 32
+    for N in (65536, 1 << 19, 1 << 22):
+        assert L.acdc_supported(N, PERM | RELU) == 1
+        assert L.acdc_supported(N, CX) == 0
+    for N in (256, 4096, 32768):
+        assert L.acdc_supported(N, MP | PERM) == 1
+    for N in (128, 9216, 3072):
+        assert L.acdc_supported(N, MP) == 0
+    assert L.acdc_supported(1024, MP | CX) == 0
     assert L.acdc_supported(9216, CX) == 0
     assert L.acdc_supported(4096, CX | RELU) == 0
     assert L.acdc_supported(4096, 8) == 1          # BIAS
-    assert L.acdc_supported(4096, 32) == 0         # unknown flag bit
+    assert L.acdc_supported(4096, 64) == 0         # unknown flag bit
 
 
 def test_status_strings(L):
@@ -108,7 +118,7 @@ def test_forward_rejects_bad_arguments(L):
     assert fwd(N=100) == EUNSUP
     assert fwd(flags=CX | RELU) == EUNSUP
     assert fwd(flags=CX | BIAS, b=b) == EUNSUP
-    assert fwd(flags=32) == EINVAL
+    assert fwd(flags=64) == EINVAL
     assert fwd(K=0) == EINVAL
     assert fwd(B=-1) == EINVAL
     assert fwd(x=None) == EINVAL

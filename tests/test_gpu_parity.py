@@ -11,7 +11,8 @@ import numpy as np
 import pytest
 
 from oracle import acdc_oracle as O
-from paper_1511_05946_amd.workloads import FLAG_ACCUMULATE, FLAG_BIAS, WORKLOADS, make_bias, make_inputs
+from paper_1511_05946_amd.workloads import (FLAG_ACCUMULATE, FLAG_BIAS, FLAG_MULTIPASS, WORKLOADS, make_bias,
+                                            make_inputs)
 from tests.helpers import TOL_COMPLEX, TOL_REAL, rel_err, relu_safe_rows
 
 pytestmark = pytest.mark.gpu
@@ -347,3 +348,76 @@ def test_bias_autograd_wrapper(acdc):
     rx, _, _, rB = O.backward(x, gy, A, D, perm, flags, B=b)
     assert rel_err(host(xt.grad), rx) < TOL_REAL
     assert rel_err(host(bt.grad), rB) < TOL_REAL
+
+
+# ------------------------------------------------------------ multi-pass path
+
+MP = FLAG_MULTIPASS
+
+
+@pytest.mark.parametrize("N", [256, 4096, 32768])
+def test_multipass_fused_widths(acdc, N):
+    # the same widths as the fused kernels, forced through the multi-pass path
+    run_case(acdc, N, 3, 9, P | R | FLAG_BIAS | MP, seed=N + 5)
+
+
+@pytest.mark.parametrize("N,K,B,flags", [(65536, 2, 3, P | R | FLAG_BIAS), (1 << 18, 2, 2, P | FLAG_BIAS),
+                                         (1 << 20, 2, 2, P | FLAG_BIAS)])
+def test_multipass_wide_rows(acdc, N, K, B, flags):
+    # 65536: one radix-4 pass; 2^18: one radix-16 pass; 2^20: radix-16 then
+    # radix-4.  Rows of 2^18 and more nearly always hold a ReLU decision
+    # within 1e-5 rms of zero, so those run without ReLU.
+    run_case(acdc, N, K, B, flags, seed=N + 7)
+
+
+@pytest.mark.parametrize("save", [True, False])
+def test_multipass_first_layer_permutation_and_recompute(acdc, save):
+    run_case(acdc, 65536, 2, 3, P | R, seed=71, save=save, perm0=True)
+    run_case(acdc, 65536, 1, 3, P, seed=72, save=save, perm0=True)
+    run_case(acdc, 65536, 1, 2, 0, seed=73, save=save)
+
+
+def test_multipass_matches_fused(acdc):
+    N, K, B, flags = 4096, 4, 24, P | FLAG_BIAS
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, 74)
+    b = make_bias(N, K, 74)
+    xt, At, Dt, pt, gyt, bt = dev(x), dev(A), dev(D), dev(perm), dev(gy), dev(b)
+    yf, sf = acdc.forward(xt, At, Dt, pt, flags, save=True, bias=bt)
+    ym, sm = acdc.forward(xt, At, Dt, pt, flags | MP, save=True, bias=bt)
+    assert rel_err(host(ym), host(yf).astype(np.float64)) < 1e-5
+    gf = acdc.backward(xt, gyt, At, Dt, pt, flags, saved=sf, bias=bt)
+    gm = acdc.backward(xt, gyt, At, Dt, pt, flags | MP, saved=sm, bias=bt)
+    for u, v in zip(gm, gf):
+        assert rel_err(host(u), host(v).astype(np.float64)) < 1e-5
+
+
+def test_multipass_accumulate_and_determinism(acdc):
+    import torch
+    N, K, B, flags = 65536, 2, 3, P | R | FLAG_BIAS
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, 75)
+    b = make_bias(N, K, 75)
+    xt, At, Dt, pt, gyt, bt = dev(x), dev(A), dev(D), dev(perm), dev(gy), dev(b)
+    y1, s1 = acdc.forward(xt, At, Dt, pt, flags, save=True, bias=bt)
+    y2, s2 = acdc.forward(xt, At, Dt, pt, flags, save=True, bias=bt)
+    assert np.array_equal(host(y1), host(y2)) and np.array_equal(host(s1), host(s2))
+    plain = acdc.backward(xt, gyt, At, Dt, pt, flags, saved=s1, bias=bt)
+    again = acdc.backward(xt, gyt, At, Dt, pt, flags, saved=None, bias=bt)
+    for u, v in zip(plain, again):
+        assert np.array_equal(host(u), host(v))
+    pre = [torch.full_like(At, 0.25) for _ in range(3)]
+    grads = tuple(p.clone() for p in pre)
+    acc = acdc.backward(xt, gyt, At, Dt, pt, flags | FLAG_ACCUMULATE, saved=s1, bias=bt, grads=grads)
+    for g, p0, g0 in zip(acc[1:], pre, plain[1:]):
+        assert np.array_equal(host(g), host(p0 + g0))
+
+
+def test_multipass_empty_batch(acdc):
+    import torch
+    N, K = 65536, 2
+    A = torch.ones((K, N), device="cuda")
+    b = torch.ones((K, N), device="cuda")
+    x = torch.empty((0, N), device="cuda")
+    y, _ = acdc.forward(x, A, A.clone(), None, 0, bias=b)
+    assert y.shape == (0, N)
+    gx, gA, gD, gB = acdc.backward(x, x.clone(), A, A.clone(), None, 0, bias=b)
+    assert not host(gA).any() and not host(gD).any() and not host(gB).any()
