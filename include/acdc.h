@@ -57,8 +57,15 @@
  * device uploads its constant table synchronously.  Results are bitwise
  * reproducible for identical inputs on the same device.
  *
- * Supported widths (acdc_supported): ACDC N in {8, 16, ..., 32768} and 9216;
- * AFDF N in {8, 16, ..., 16384}.  Batch sizes from 0 upward; K >= 1.
+ * Supported widths (acdc_supported): ACDC N in {8, 16, ..., 32768} and 9216
+ * with the fused kernels (one row per workgroup or wave, all K layers in one
+ * launch); AFDF N in {8, 16, ..., 16384}.  Real layers of power-of-two width
+ * 256 ... 2^22 also run multi-pass (the multiple-call scheme of Sec. 5.2:
+ * each layer's FFT goes through HBM in several launches, with hand-written
+ * passes).  That path serves the widths past 32768, and any power-of-two
+ * width with ACDC_FLAG_MULTIPASS; it needs more workspace (see the
+ * *_workspace_bytes calls), and its permutation indices are read modulo N.
+ * Batch sizes from 0 upward; K >= 1.
  */
 #ifndef ACDC_H_
 #define ACDC_H_
@@ -78,7 +85,8 @@ enum acdc_flags {
   ACDC_FLAG_RELU = 2u,       /* ReLU after layers 0..K-2 (not with COMPLEX) */
   ACDC_FLAG_COMPLEX = 4u,    /* complex AFDF layers on interleaved complex64 */
   ACDC_FLAG_BIAS = 8u,       /* add b_k to each layer's D-domain term (not with COMPLEX) */
-  ACDC_FLAG_ACCUMULATE = 16u /* backward adds into grad_A, grad_D, grad_bias instead of overwriting */
+  ACDC_FLAG_ACCUMULATE = 16u, /* backward adds into grad_A, grad_D, grad_bias instead of overwriting */
+  ACDC_FLAG_MULTIPASS = 32u   /* run the multi-pass path (below) even where a fused plan exists */
 };
 
 enum acdc_status {
