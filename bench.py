@@ -79,8 +79,9 @@ def cpu_baseline(w, seed: int, budget_s: float = 12.0, max_rows: int = 512):
         rows = sl.stop
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     return {"value": rows * w.K / t_total, "unit": UNIT, "cores": int(threads), "kind": "oracle",
-            "sample": f"{rows} of {w.batch} rows, full N={w.N}, K={w.K}, fwd + bwd, "
-                      f"O(N^2) fp64 dense-matrix oracle, {t_total:.1f} s"}
+            "sample": f"{rows} of {w.batch} rows, full N={w.N}, K={w.K}, fwd + bwd, fp64 oracle "
+                      + ("(O(N^2) dense matrices" if w.N <= O.DENSE_MAX else "(library DCT/FFT above N=8192")
+                      + f"), {t_total:.1f} s"}
 
 
 def main():
@@ -91,6 +92,8 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--recompute", action="store_true",
                     help="backward recomputes the layer inputs instead of using the forward's")
+    ap.add_argument("--multipass", action="store_true",
+                    help="run the layers through the multi-pass (HBM) path instead of the fused kernels")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -129,9 +132,13 @@ def main():
     xt, At, Dt, pt, gyt = t(x), t(A), t(D), t(perm), t(gy)
     bt = t(make_bias(w.N, w.K, args.seed)) if w.flags & FLAG_BIAS else None
     fl = w.flags & ~acdc.FLAG_COMPLEX
-    acdc.prepare(w.N, w.flags)
+    if args.multipass:
+        fl |= acdc.FLAG_MULTIPASS
+    # the fused kernels cover ACDC widths up to 32768; wider rows run multi-pass
+    multipass = not w.complex and (args.multipass or w.N > 32768)
+    acdc.prepare(w.N, fl | (acdc.FLAG_COMPLEX if w.complex else 0))
     y = torch.empty_like(xt)
-    saved = acdc.alloc_saved(xt, w.K, w.flags)
+    saved = acdc.alloc_saved(xt, w.K, fl)
 
     def step():
         if args.recompute:
@@ -175,8 +182,9 @@ def main():
     fwd_achieved = w.batch * w.K * f_rl / (fwd_ms * 1e-3) / 1e12
     roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4),
-            "traffic": recorded_traffic(w.name, "k_real_bwd" if not w.complex else "k_cplx_bwd"),
-            "kernel": "k_real_bwd" if not w.complex else "k_cplx_bwd",
+            "traffic": None if multipass else recorded_traffic(w.name, "k_real_bwd" if not w.complex else "k_cplx_bwd"),
+            "kernel": ("multi-pass backward (whole launch sequence)" if multipass
+                       else "k_real_bwd" if not w.complex else "k_cplx_bwd"),
             "kernel_avg_ms": round(bwd_ms, 4),
             "algorithmic_flops_per_launch": bwd_flops}
     # fraction of the whole-step roofline (fwd+bwd algorithmic flops at peak)
@@ -189,7 +197,8 @@ def main():
                 + (", D-domain biases ~ N(0,0.1^2))" if bt is not None else ")"),
         "config": {"workload": w.name, "N": w.N, "K": w.K, "batch": w.batch,
                    "flags": w.flags, "parallelism": "single GPU",
-                   "backward": "recompute" if args.recompute else "saved layer inputs"},
+                   "backward": "recompute" if args.recompute else "saved layer inputs",
+                   "path": "multi-pass" if multipass else "fused"},
         "roofline": roof,
         "step_roofline_frac": round(step_flops / (ms_step * 1e-3) / 1e12 / PEAK_FP32_TFLOPS, 4),
         "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]} for k, v in kern.items()},

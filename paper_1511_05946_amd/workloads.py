@@ -54,8 +54,8 @@ class Workload:
 
 # The workloads: one single layer, a permuted cascade, the headline permuted
 # ReLU cascade at N=4096, a non-power-of-two ReLU cascade at the width of a
-# flattened 6x6x256 conv map, the complex AFDF cascade, and the headline
-# cascade with D-domain biases.
+# flattened 6x6x256 conv map, the complex AFDF cascade, a cascade wider than
+# the fused kernels, and the headline cascade with D-domain biases.
 WORKLOADS = {
     "acdc_n256_k1": Workload("acdc_n256_k1", 256, 1, 64, 0,
                              "single ACDC layer N=256, batch 64, fp32"),
@@ -73,6 +73,11 @@ WORKLOADS = {
                                    FLAG_PERM | FLAG_COMPLEX,
                                    "complex AFDF cascade N=4096 K=8 batch 2048, complex64, "
                                    "permutations"),
+    # past the fused kernels' width: the multi-pass path
+    "acdc_n65536_k12_perm_relu": Workload("acdc_n65536_k12_perm_relu", 65536, 12, 512,
+                                          FLAG_PERM | FLAG_RELU,
+                                          "ACDC cascade N=65536 K=12 batch 512, fp32, permutations + ReLU "
+                                          "(multi-pass)"),
     # the headline cascade with the D-domain biases of Sec. 6.2
     "acdc_n4096_k12_perm_relu_bias": Workload("acdc_n4096_k12_perm_relu_bias", 4096, 12, 8192,
                                               FLAG_PERM | FLAG_RELU | FLAG_BIAS,

@@ -139,14 +139,16 @@ def test_single_layer_and_single_row(acdc, save):
 def test_workloads_small_batch(acdc, name):
     w = WORKLOADS[name]
     B = {"acdc_n256_k1": 64, "acdc_n1024_k12_perm": 96, "acdc_n4096_k12_perm_relu": 48,
-         "acdc_n9216_k16_perm_relu": 12, "afdf_n4096_k8_perm": 24, "acdc_n4096_k12_perm_relu_bias": 48}[name]
-    if name == "acdc_n9216_k16_perm_relu":
-        # At N=9216, K=16 nearly every row has some ReLU decision within
-        # 1e-5 * rms of zero (the near-identity layers keep the input's zeros
-        # small), so backward parity runs on the same width at K=4, where
-        # margin-safe rows are common; the K=16 forward is checked on all rows.
+         "acdc_n9216_k16_perm_relu": 12, "afdf_n4096_k8_perm": 24, "acdc_n4096_k12_perm_relu_bias": 48,
+         "acdc_n65536_k12_perm_relu": 4}[name]
+    if name in ("acdc_n9216_k16_perm_relu", "acdc_n65536_k12_perm_relu"):
+        # At N=9216, K=16 (and N=65536, K=12) nearly every row has some ReLU
+        # decision within 1e-5 * rms of zero (the near-identity layers keep
+        # the input's zeros small), so backward parity runs on the same width
+        # at K=4 (K=2), where margin-safe rows are common; the deep forward is
+        # checked on all rows.
         run_case(acdc, w.N, w.K, B, w.flags, seed=0, check_bwd=False)
-        run_case(acdc, w.N, 4, B, w.flags, seed=0)
+        run_case(acdc, w.N, 4 if w.N == 9216 else 2, B, w.flags, seed=0)
         return
     run_case(acdc, w.N, w.K, B, w.flags, seed=0)
 
@@ -185,8 +187,8 @@ def test_workloads_full_size_sampled(acdc, name):
         rx = O.backward(x[rows][keep], gy[rows][keep], A, D, perm, w.flags & 7, B=bias)[0]
         assert rel_err(host(gx)[rows][keep], rx) < tol
     else:
-        # only at N=9216, K=16 (see test_workloads_small_batch)
-        assert w.N == 9216
+        # only for the widest ReLU cascades (see test_workloads_small_batch)
+        assert w.N >= 9216
     torch.cuda.synchronize()
 
 
