@@ -565,15 +565,29 @@ MpBwdWs mp_bwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have
     if (e_ != hipSuccess) return hip_fail(e_); \
   } while (0)
 
-int mp_fft(float2* Z, long long rows, const mp::Geo& g, const MpTabs& t, bool inverse, hipStream_t s) {
-  if (!inverse) {
-    if (g.R1 > 1) MP_TRY(mp::dif(Z, rows, g, g.M, g.R1, t.tw, s));
-    if (g.R2 > 1) MP_TRY(mp::dif(Z, rows, g, g.M / g.R1, g.R2, t.tw, s));
-    MP_TRY(mp::segments(Z, rows * (g.M / g.L), g.L, false, t.seg, s));
+// Pack rows of src (gathered through perm, stashed, scaled by a; each may
+// be null) and run the forward FFT: the first DIF pass takes the packing.
+int mp_pack_fft(const float* src, const int32_t* perm, const float* a, float* stash, float2* Z, long long rows,
+                long long N, const mp::Geo& g, const MpTabs& t, hipStream_t s) {
+  if (g.R1 > 1) {
+    MP_TRY(mp::pack_dif(src, perm, a, stash, Z, rows, g.M, g.R1, t.tw, s));
   } else {
-    MP_TRY(mp::segments(Z, rows * (g.M / g.L), g.L, true, t.seg, s));
-    if (g.R2 > 1) MP_TRY(mp::dit(Z, rows, g, g.M / g.R1, g.R2, t.tw, s));
-    if (g.R1 > 1) MP_TRY(mp::dit(Z, rows, g, g.M, g.R1, t.tw, s));
+    MP_TRY(mp::pack(src, perm, a, stash, Z, rows, N, s));
+  }
+  if (g.R2 > 1) MP_TRY(mp::dif(Z, rows, g, g.M / g.R1, g.R2, t.tw, s));
+  MP_TRY(mp::segments(Z, rows * (g.M / g.L), g.L, false, t.seg, s));
+  return ACDC_OK;
+}
+
+// Inverse FFT, then unpack (+ ReLU) into dst: the last DIT pass takes the unpacking.
+int mp_ifft_unpack(float2* Z, float* dst, long long rows, long long N, bool relu, const mp::Geo& g, const MpTabs& t,
+                   hipStream_t s) {
+  MP_TRY(mp::segments(Z, rows * (g.M / g.L), g.L, true, t.seg, s));
+  if (g.R2 > 1) MP_TRY(mp::dit(Z, rows, g, g.M / g.R1, g.R2, t.tw, s));
+  if (g.R1 > 1) {
+    MP_TRY(mp::dit_unpack(Z, dst, rows, g.M, g.R1, t.tw, relu, s));
+  } else {
+    MP_TRY(mp::unpack(Z, dst, rows, N, relu, s));
   }
   return ACDC_OK;
 }
@@ -593,14 +607,12 @@ int mp_forward_layers(const float* x, float* y, const float* A, const float4* Mq
   const bool perm_on = (flags & kFlagPerm) != 0, relu = (flags & kFlagRelu) != 0;
   for (int k = 0; k < K; ++k) {
     const float* src = k == 0 ? x : zbuf;
-    MP_TRY(mp::pack(src, perm_on ? perm + (long long)k * N : nullptr, A + (long long)k * N,
-                    mp_slot(saved, k, K, batch, N, perm_on), Z, batch, N, s));
-    int rc = mp_fft(Z, batch, g, t, false, s);
+    int rc = mp_pack_fft(src, perm_on ? perm + (long long)k * N : nullptr, A + (long long)k * N,
+                         mp_slot(saved, k, K, batch, N, perm_on), Z, batch, N, g, t, s);
     if (rc != ACDC_OK) return rc;
     MP_TRY(mp::mid_fwd(Z, Mq + (long long)k * (N / 4) * kMqRows, batch, g, (flags & kFlagBias) != 0, s));
-    rc = mp_fft(Z, batch, g, t, true, s);
+    rc = mp_ifft_unpack(Z, (k == K - 1 && y != nullptr) ? y : zbuf, batch, N, relu && k < K - 1, g, t, s);
     if (rc != ACDC_OK) return rc;
-    MP_TRY(mp::unpack(Z, (k == K - 1 && y != nullptr) ? y : zbuf, batch, N, relu && k < K - 1, s));
   }
   return ACDC_OK;
 }
@@ -630,7 +642,7 @@ int mp_backward(const float* x, const float* grad_y, const float* A, const float
   char* ws = static_cast<char*>(workspace);
   float4* Mq = reinterpret_cast<float4*>(ws + w.mq);
   float2* Zh = reinterpret_cast<float2*>(ws + w.zhg);
-  float2* Zg = Zh + batch * (N / 2);
+  float2* Zg = Zh + batch * (N / 2);  // the g spectra follow the h spectra
   float* gh1 = reinterpret_cast<float*>(ws + w.gh1);
   float* gbuf = reinterpret_cast<float*>(ws + w.gbuf);
   float* imgD = reinterpret_cast<float*>(ws + w.imgD);
@@ -657,16 +669,15 @@ int mp_backward(const float* x, const float* grad_y, const float* A, const float
     if (batch > 0) {
       const float* u = k > 0 || perm_on ? mp_slot(stash, k, K, batch, N, perm_on) : x;
       const float* ak = A + (long long)k * N;
-      MP_TRY(mp::pack(k == K - 1 ? grad_y : gbuf, nullptr, nullptr, nullptr, Zg, batch, N, s));
-      MP_TRY(mp::pack(u, nullptr, ak, nullptr, Zh, batch, N, s));
-      rc = mp_fft(Zh, 2 * batch, g, t, false, s);  // Zh and Zg are contiguous
+      rc = mp_pack_fft(k == K - 1 ? grad_y : gbuf, nullptr, nullptr, nullptr, Zg, batch, N, g, t, s);
+      if (rc != ACDC_OK) return rc;
+      rc = mp_pack_fft(u, nullptr, ak, nullptr, Zh, batch, N, g, t, s);
       if (rc != ACDC_OK) return rc;
       MP_TRY(mp::mid_bwd(Zh, Zg, Mq + (long long)k * (N / 4) * kMqRows, batch, g, imgD, imgB, s));
       MP_TRY(mp::colsum(imgD, batch, N, part, gD, &t.q, acc, s));
       if (gB) MP_TRY(mp::colsum(imgB, batch, N, part, gB, &t.q, acc, s));
-      rc = mp_fft(Zg, batch, g, t, true, s);
+      rc = mp_ifft_unpack(Zg, gh1, batch, N, false, g, t, s);
       if (rc != ACDC_OK) return rc;
-      MP_TRY(mp::unpack(Zg, gh1, batch, N, false, s));
       MP_TRY(mp::dA(gh1, u, ak, perm_on ? perm + (long long)k * N : nullptr, relu && k > 0, imgA,
                     k == 0 ? grad_x : gbuf, batch, N, s));
       MP_TRY(mp::colsum(imgA, batch, N, part, gA, nullptr, acc, s));

@@ -12,15 +12,26 @@ namespace {
 
 constexpr int kThreads = 256;
 
+// Workgroups go to the 8 XCDs (each with its own L2) in turn: workgroup w
+// runs on XCD w mod 8.  Grids are a multiple of 8 workgroups, and gindex()
+// hands XCD x the x-th contiguous eighth of the grid, so the workgroups
+// that gather from one row share that XCD's L2.
+constexpr int kXcds = 8;
+
 dim3 grid_for(long long n) {
   long long blocks = (n + kThreads - 1) / kThreads;
   if (blocks > 65536) blocks = 65536;
-  if (blocks < 1) blocks = 1;
+  blocks = (blocks + kXcds - 1) / kXcds * kXcds;
+  if (blocks < kXcds) blocks = kXcds;
   return dim3(unsigned(blocks));
 }
 
 __device__ __forceinline__ long long gstride() { return (long long)gridDim.x * blockDim.x; }
-__device__ __forceinline__ long long gindex() { return (long long)blockIdx.x * blockDim.x + threadIdx.x; }
+__device__ __forceinline__ long long gindex() {
+  const unsigned per_xcd = gridDim.x / kXcds;
+  const unsigned blk = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  return (long long)blk * blockDim.x + threadIdx.x;
+}
 
 __global__ __launch_bounds__(kThreads) void k_pack(const float* __restrict__ src, const int* __restrict__ perm,
                                                    const float* __restrict__ a, float* __restrict__ stash,
@@ -82,6 +93,72 @@ __global__ __launch_bounds__(kThreads) void k_dit(float2* __restrict__ Z, long l
     Dft<R, true>::run(y);
 #pragma unroll
     for (int j = 0; j < R; ++j) Z[base + n + j * Q] = y[j];
+  }
+}
+
+// The first DIF pass (on whole rows, S = M) with the packing folded in:
+// butterfly n gathers, scales and packs its R inputs m = n + j M/R straight
+// from the spatial rows (stashing the gathered values), saving one pass.
+__device__ __forceinline__ float2 packed_value(const float* row, const int* perm, const float* a, float* srow,
+                                               long long m, long long M, long long N) {
+  long long i0, i1;
+  pack_idx(m, M, i0, i1);
+  float u0 = row[perm ? (perm[i0] & (N - 1)) : i0];
+  float u1 = row[perm ? (perm[i1] & (N - 1)) : i1];
+  if (srow) {
+    srow[i0] = u0;
+    srow[i1] = u1;
+  }
+  if (a) {
+    u0 *= a[i0];
+    u1 *= a[i1];
+  }
+  return make_float2(u0, u1);
+}
+
+template <int R>
+__global__ __launch_bounds__(kThreads) void k_pack_dif(const float* __restrict__ src, const int* __restrict__ perm,
+                                                       const float* __restrict__ a, float* __restrict__ stash,
+                                                       float2* __restrict__ Z, long long B, long long M,
+                                                       const float2* __restrict__ twM) {
+  const long long N = 2 * M, Q = M / R, total = B * Q;
+  for (long long i = gindex(); i < total; i += gstride()) {
+    const long long b = i / Q, n = i % Q;
+    const float* row = src + b * N;
+    float* srow = stash ? stash + b * N : nullptr;
+    float2 x[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) x[j] = packed_value(row, perm, a, srow, n + j * Q, M, N);
+    Dft<R, false>::run(x);
+#pragma unroll
+    for (int r = 1; r < R; ++r) x[r] = cmul(x[r], twM[n * r]);
+#pragma unroll
+    for (int r = 0; r < R; ++r) Z[b * M + r * Q + n] = x[r];
+  }
+}
+
+// The last DIT pass (S = M) with the unpacking (and ReLU) folded in.
+template <int R>
+__global__ __launch_bounds__(kThreads) void k_dit_unpack(const float2* __restrict__ Z, float* __restrict__ dst,
+                                                         long long B, long long M, const float2* __restrict__ twM,
+                                                         int relu) {
+  const long long N = 2 * M, Q = M / R, total = B * Q;
+  for (long long i = gindex(); i < total; i += gstride()) {
+    const long long b = i / Q, n = i % Q;
+    float2 y[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) y[r] = Z[b * M + r * Q + n];
+#pragma unroll
+    for (int r = 1; r < R; ++r) y[r] = cmulc(y[r], twM[n * r]);
+    Dft<R, true>::run(y);
+    float* row = dst + b * N;
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      long long i0, i1;
+      pack_idx(n + j * Q, M, i0, i1);
+      row[i0] = relu ? (y[j].x > 0.f ? y[j].x : 0.f) : y[j].x;
+      row[i1] = relu ? (y[j].y > 0.f ? y[j].y : 0.f) : y[j].y;
+    }
   }
 }
 
@@ -291,6 +368,33 @@ hipError_t dit(float2* Z, long long B, const Geo& g, long long S, int R, const f
     case 4: hipLaunchKernelGGL(k_dit<4>, grid, block, 0, s, Z, B, g.M, S, twM); break;
     case 8: hipLaunchKernelGGL(k_dit<8>, grid, block, 0, s, Z, B, g.M, S, twM); break;
     case 16: hipLaunchKernelGGL(k_dit<16>, grid, block, 0, s, Z, B, g.M, S, twM); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t pack_dif(const float* src, const int* perm, const float* a, float* stash, float2* Z, long long B,
+                    long long M, int R, const float2* twM, hipStream_t s) {
+  const dim3 grid = grid_for(B * (M / R)), block(kThreads);
+  switch (R) {
+    case 2: hipLaunchKernelGGL(k_pack_dif<2>, grid, block, 0, s, src, perm, a, stash, Z, B, M, twM); break;
+    case 4: hipLaunchKernelGGL(k_pack_dif<4>, grid, block, 0, s, src, perm, a, stash, Z, B, M, twM); break;
+    case 8: hipLaunchKernelGGL(k_pack_dif<8>, grid, block, 0, s, src, perm, a, stash, Z, B, M, twM); break;
+    case 16: hipLaunchKernelGGL(k_pack_dif<16>, grid, block, 0, s, src, perm, a, stash, Z, B, M, twM); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t dit_unpack(const float2* Z, float* dst, long long B, long long M, int R, const float2* twM, bool relu,
+                      hipStream_t s) {
+  const dim3 grid = grid_for(B * (M / R)), block(kThreads);
+  const int rl = relu ? 1 : 0;
+  switch (R) {
+    case 2: hipLaunchKernelGGL(k_dit_unpack<2>, grid, block, 0, s, Z, dst, B, M, twM, rl); break;
+    case 4: hipLaunchKernelGGL(k_dit_unpack<4>, grid, block, 0, s, Z, dst, B, M, twM, rl); break;
+    case 8: hipLaunchKernelGGL(k_dit_unpack<8>, grid, block, 0, s, Z, dst, B, M, twM, rl); break;
+    case 16: hipLaunchKernelGGL(k_dit_unpack<16>, grid, block, 0, s, Z, dst, B, M, twM, rl); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -65,6 +65,13 @@ hipError_t pack(const float* src, const int* perm, const float* a, float* stash,
 hipError_t dif(float2* Z, long long B, const Geo& g, long long S, int R, const float2* twM, hipStream_t s);
 hipError_t dit(float2* Z, long long B, const Geo& g, long long S, int R, const float2* twM, hipStream_t s);
 hipError_t segments(float2* Z, long long nseg, int L, bool inverse, const char* seg_tab, hipStream_t s);
+// pack + the first DIF pass (radix R on whole rows), and the last DIT pass +
+// unpack (+ ReLU): the same results as the separate launches, two passes
+// over the batch fewer.
+hipError_t pack_dif(const float* src, const int* perm, const float* a, float* stash, float2* Z, long long B,
+                    long long M, int R, const float2* twM, hipStream_t s);
+hipError_t dit_unpack(const float2* Z, float* dst, long long B, long long M, int R, const float2* twM, bool relu,
+                      hipStream_t s);
 hipError_t mq(const float* D, const float* Bias, float4* Mq, int K, long long NQ, const QuartetTabs& q,
               hipStream_t s);
 hipError_t mid_fwd(float2* Z, const float4* Mq, long long B, const Geo& g, bool bias, hipStream_t s);

@@ -62,6 +62,11 @@ using CP16384 = ComplexPlan<16384, 512, 32, 16, 32>;
 #ifndef ACDC_NARROW_THREADS
 #define ACDC_NARROW_THREADS 256
 #endif
+// A row width (threads) above one wave whose forward also keeps the twiddles
+// in LDS (0: none).
+#ifndef ACDC_TW_LDS_T
+#define ACDC_TW_LDS_T 0
+#endif
 // Rows per backward workgroup for the three-wave rows of N = 9216.
 #ifndef ACDC_BWD_ROWS_T192
 #define ACDC_BWD_ROWS_T192 2
@@ -75,12 +80,13 @@ struct Launch {
   static constexpr int FWD_SLAB = PL::kComplex ? PL::SLAB : cmax(PL::N, PL::FFT_FLOATS);  // floats per row
   static constexpr int BWD_SLAB = PL::SLAB;
   static constexpr int WIDE_ROWS = PL::T <= 16 ? ACDC_NARROW_THREADS / PL::T : PL::T <= 64 ? 512 / PL::T : 1;
-  static constexpr bool TW_LDS = ACDC_TW_LDS && !PL::kComplex && PL::T <= 64 &&
+  static constexpr bool TW_LDS = ACDC_TW_LDS && !PL::kComplex && (PL::T <= 64 || PL::T == ACDC_TW_LDS_T) &&
                                  WIDE_ROWS * PL::SLAB * 4 + PL::TW_FLOAT2 * 8 <= kLdsBytes;
   static constexpr int FWD_ROWS =
       TW_LDS ? WIDE_ROWS : (PL::T >= ACDC_FWD_THREADS ? 1 : ACDC_FWD_THREADS / PL::T);
   static constexpr int BWD_ROWS =
-      TW_LDS ? WIDE_ROWS : (PL::T == 192 ? ACDC_BWD_ROWS_T192 : (PL::T >= ACDC_BWD_THREADS ? 1 : ACDC_BWD_THREADS / PL::T));
+      PL::T == 192 ? ACDC_BWD_ROWS_T192
+                   : (TW_LDS ? WIDE_ROWS : (PL::T >= ACDC_BWD_THREADS ? 1 : ACDC_BWD_THREADS / PL::T));
   static constexpr bool BWD_TW_LDS = TW_LDS && ACDC_TW_LDS_BWD;
   static constexpr int FWD_THREADS = FWD_ROWS * PL::T;
   static constexpr int BWD_THREADS = BWD_ROWS * PL::T;
