@@ -526,16 +526,38 @@ int get_mp_tables(int N, MpTabs* out) {
 size_t mp_mq_bytes(long long N, int K) { return align256(size_t(K) * size_t(N / 4) * kMqRows * sizeof(float4)); }
 size_t mp_rows_bytes(int64_t batch, long long N) { return align256(size_t(batch) * size_t(N) * sizeof(float)); }
 
-// Forward workspace: quartet coefficients, the packed spectrum, the layer output.
-size_t mp_fwd_ws(int64_t batch, int32_t N, int32_t K) {
-  return mp_mq_bytes(N, K) + 2 * mp_rows_bytes(batch, N);
+size_t mp_perm_bytes(long long N, uint32_t flags) {
+  return (flags & kFlagPerm) ? align256(mp::perm_table_ints(N) * sizeof(int)) : 0;
+}
+
+// Forward workspace: quartet coefficients, the packed spectrum (also the
+// permutation's scratch), the layer output; with PERM the permuted layer
+// input (when no stash takes it) and the permutation tables.
+struct MpFwdWs {
+  size_t mq = 0, z = 0, zbuf = 0, ubuf = 0, ptab = 0, total = 0;
+};
+MpFwdWs mp_fwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
+  MpFwdWs w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  w.mq = take(mp_mq_bytes(N, K));
+  w.z = take(mp_rows_bytes(batch, N));
+  w.zbuf = take(mp_rows_bytes(batch, N));
+  w.ubuf = take((flags & kFlagPerm) ? mp_rows_bytes(batch, N) : 0);
+  w.ptab = take(mp_perm_bytes(N, flags));
+  w.total = off;
+  return w;
 }
 
 // Backward workspace: quartet coefficients, the h and g spectra (contiguous,
 // transformed together), dL/dv of the current layer, the next layer's g,
 // the three images, the column-sum blocks, and the recompute stash.
 struct MpBwdWs {
-  size_t mq = 0, zhg = 0, gh1 = 0, gbuf = 0, imgD = 0, imgA = 0, imgB = 0, part = 0, stash = 0, total = 0;
+  size_t mq = 0, zhg = 0, gh1 = 0, gbuf = 0, imgD = 0, imgA = 0, imgB = 0, part = 0, stash = 0, ptab = 0, total = 0;
 };
 MpBwdWs mp_bwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved) {
   MpBwdWs w;
@@ -555,6 +577,7 @@ MpBwdWs mp_bwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have
   w.imgB = take((flags & kFlagBias) ? rows : 0);
   w.part = take(size_t((batch + mp::kColRows - 1) / mp::kColRows) * size_t(N) * sizeof(float));
   w.stash = take(have_saved ? 0 : saved_floats(batch, N, K, flags) * sizeof(float));
+  w.ptab = take(mp_perm_bytes(N, flags));
   w.total = off;
   return w;
 }
@@ -565,14 +588,14 @@ MpBwdWs mp_bwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have
     if (e_ != hipSuccess) return hip_fail(e_); \
   } while (0)
 
-// Pack rows of src (gathered through perm, stashed, scaled by a; each may
-// be null) and run the forward FFT: the first DIF pass takes the packing.
-int mp_pack_fft(const float* src, const int32_t* perm, const float* a, float* stash, float2* Z, long long rows,
-                long long N, const mp::Geo& g, const MpTabs& t, hipStream_t s) {
+// Pack rows of src (stashed, scaled by a; each may be null) and run the
+// forward FFT: the first DIF pass takes the packing.
+int mp_pack_fft(const float* src, const float* a, float* stash, float2* Z, long long rows, long long N,
+                const mp::Geo& g, const MpTabs& t, hipStream_t s) {
   if (g.R1 > 1) {
-    MP_TRY(mp::pack_dif(src, perm, a, stash, Z, rows, g.M, g.R1, t.tw, s));
+    MP_TRY(mp::pack_dif(src, a, stash, Z, rows, g.M, g.R1, t.tw, s));
   } else {
-    MP_TRY(mp::pack(src, perm, a, stash, Z, rows, N, s));
+    MP_TRY(mp::pack(src, a, stash, Z, rows, N, s));
   }
   if (g.R2 > 1) MP_TRY(mp::dif(Z, rows, g, g.M / g.R1, g.R2, t.tw, s));
   MP_TRY(mp::segments(Z, rows * (g.M / g.L), g.L, false, t.seg, s));
@@ -600,15 +623,27 @@ float* mp_slot(float* saved, int k, int K, long long batch, long long N, bool pe
   return perm_on ? saved + (long long)(K - 1) * batch * N : nullptr;
 }
 
+// The K forward layers.  With PERM, the permuted input u_k goes to its
+// stash slot (or to ubuf without a stash), Z serving as the permutation's
+// scratch; without, the packing stashes z itself.
 int mp_forward_layers(const float* x, float* y, const float* A, const float4* Mq, const int32_t* perm,
                       int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, float2* Z, float* zbuf,
-                      const MpTabs& t, hipStream_t s) {
+                      float* ubuf, const mp::PermTabs& pt, const MpTabs& t, hipStream_t s) {
   const mp::Geo g = mp_geo(N);
   const bool perm_on = (flags & kFlagPerm) != 0, relu = (flags & kFlagRelu) != 0;
   for (int k = 0; k < K; ++k) {
     const float* src = k == 0 ? x : zbuf;
-    int rc = mp_pack_fft(src, perm_on ? perm + (long long)k * N : nullptr, A + (long long)k * N,
-                         mp_slot(saved, k, K, batch, N, perm_on), Z, batch, N, g, t, s);
+    float* slot = mp_slot(saved, k, K, batch, N, perm_on);
+    const float* u = src;
+    if (perm_on) {
+      const int32_t* pk = perm + (long long)k * N;
+      float* udst = slot != nullptr ? slot : ubuf;
+      MP_TRY(mp::perm_build(pk, N, pt, s));
+      MP_TRY(mp::permute(src, udst, reinterpret_cast<float*>(Z), pk, pt, batch, N, s));
+      u = udst;
+      slot = nullptr;  // already stashed
+    }
+    int rc = mp_pack_fft(u, A + (long long)k * N, slot, Z, batch, N, g, t, s);
     if (rc != ACDC_OK) return rc;
     MP_TRY(mp::mid_fwd(Z, Mq + (long long)k * (N / 4) * kMqRows, batch, g, (flags & kFlagBias) != 0, s));
     rc = mp_ifft_unpack(Z, (k == K - 1 && y != nullptr) ? y : zbuf, batch, N, relu && k < K - 1, g, t, s);
@@ -622,13 +657,17 @@ int mp_forward(const float* x, float* y, const float* A, const float* D, const f
   MpTabs t;
   int rc = get_mp_tables(N, &t);
   if (rc != ACDC_OK) return rc;
+  const MpFwdWs w = mp_fwd_ws(batch, N, K, flags);
   char* ws = static_cast<char*>(workspace);
-  float4* Mq = reinterpret_cast<float4*>(ws);
-  float2* Z = reinterpret_cast<float2*>(ws + mp_mq_bytes(N, K));
-  float* zbuf = reinterpret_cast<float*>(ws + mp_mq_bytes(N, K) + mp_rows_bytes(batch, N));
+  float4* Mq = reinterpret_cast<float4*>(ws + w.mq);
+  float2* Z = reinterpret_cast<float2*>(ws + w.z);
+  float* zbuf = reinterpret_cast<float*>(ws + w.zbuf);
+  float* ubuf = reinterpret_cast<float*>(ws + w.ubuf);
+  const mp::PermTabs pt = mp::perm_tables_at(reinterpret_cast<int*>(ws + w.ptab), N);
   ProfScope prof(0, s);
   MP_TRY(mp::mq(D, bias, Mq, K, N / 4, t.q, s));
-  return mp_forward_layers(x, y, A, Mq, perm, batch, N, K, flags, saved, Z, zbuf, t, s);
+  if (batch == 0) return ACDC_OK;
+  return mp_forward_layers(x, y, A, Mq, perm, batch, N, K, flags, saved, Z, zbuf, ubuf, pt, t, s);
 }
 
 int mp_backward(const float* x, const float* grad_y, const float* A, const float* D, const float* bias,
@@ -650,6 +689,7 @@ int mp_backward(const float* x, const float* grad_y, const float* A, const float
   float* imgB = (flags & kFlagBias) ? reinterpret_cast<float*>(ws + w.imgB) : nullptr;
   float* part = reinterpret_cast<float*>(ws + w.part);
   float* stash = have_saved ? const_cast<float*>(saved) : reinterpret_cast<float*>(ws + w.stash);
+  const mp::PermTabs pt = mp::perm_tables_at(reinterpret_cast<int*>(ws + w.ptab), N);
   const mp::Geo g = mp_geo(N);
   const bool perm_on = (flags & kFlagPerm) != 0, relu = (flags & kFlagRelu) != 0;
   const bool acc = (flags & kFlagAccumulate) != 0;
@@ -658,7 +698,7 @@ int mp_backward(const float* x, const float* grad_y, const float* A, const float
     MP_TRY(mp::mq(D, bias, Mq, K, N / 4, t.q, s));
     if (!have_saved) {
       // recompute the layer inputs into the workspace (Zh, gh1 are free until the layer loop)
-      rc = mp_forward_layers(x, nullptr, A, Mq, perm, batch, N, K, flags, stash, Zh, gh1, t, s);
+      rc = mp_forward_layers(x, nullptr, A, Mq, perm, batch, N, K, flags, stash, Zh, gh1, nullptr, pt, t, s);
       if (rc != ACDC_OK) return rc;
     }
   }
@@ -669,17 +709,25 @@ int mp_backward(const float* x, const float* grad_y, const float* A, const float
     if (batch > 0) {
       const float* u = k > 0 || perm_on ? mp_slot(stash, k, K, batch, N, perm_on) : x;
       const float* ak = A + (long long)k * N;
-      rc = mp_pack_fft(k == K - 1 ? grad_y : gbuf, nullptr, nullptr, nullptr, Zg, batch, N, g, t, s);
+      rc = mp_pack_fft(k == K - 1 ? grad_y : gbuf, nullptr, nullptr, Zg, batch, N, g, t, s);
       if (rc != ACDC_OK) return rc;
-      rc = mp_pack_fft(u, nullptr, ak, nullptr, Zh, batch, N, g, t, s);
+      rc = mp_pack_fft(u, ak, nullptr, Zh, batch, N, g, t, s);
       if (rc != ACDC_OK) return rc;
       MP_TRY(mp::mid_bwd(Zh, Zg, Mq + (long long)k * (N / 4) * kMqRows, batch, g, imgD, imgB, s));
       MP_TRY(mp::colsum(imgD, batch, N, part, gD, &t.q, acc, s));
       if (gB) MP_TRY(mp::colsum(imgB, batch, N, part, gB, &t.q, acc, s));
       rc = mp_ifft_unpack(Zg, gh1, batch, N, false, g, t, s);
       if (rc != ACDC_OK) return rc;
-      MP_TRY(mp::dA(gh1, u, ak, perm_on ? perm + (long long)k * N : nullptr, relu && k > 0, imgA,
-                    k == 0 ? grad_x : gbuf, batch, N, s));
+      float* gnext = k == 0 ? grad_x : gbuf;
+      if (perm_on) {
+        // Zh and Zg are free again: the permutation's scratch
+        const int32_t* pk = perm + (long long)k * N;
+        MP_TRY(mp::perm_build(pk, N, pt, s));
+        MP_TRY(mp::dA_permute(gh1, u, ak, relu && k > 0, imgA, gnext, reinterpret_cast<float*>(Zh), pk, pt, batch,
+                              N, s));
+      } else {
+        MP_TRY(mp::dA(gh1, u, ak, relu && k > 0, imgA, gnext, batch, N, s));
+      }
       MP_TRY(mp::colsum(imgA, batch, N, part, gA, nullptr, acc, s));
     } else {
       // no rows: zero (or unchanged, accumulating) parameter gradients
@@ -719,7 +767,7 @@ extern "C" size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t
 
 extern "C" size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
   if (check_common(batch, N, K, flags) != ACDC_OK) return 0;
-  if (use_multipass(N, flags)) return mp_fwd_ws(batch, N, K);
+  if (use_multipass(N, flags)) return mp_fwd_ws(batch, N, K, flags).total;
   return fwd_ws(N, K, flags);
 }
 
@@ -747,7 +795,7 @@ extern "C" int acdc_forward(const float* x, float* y, const float* A, const floa
   if (!bias_on) bias = nullptr;
   if (!distinct({y, saved}, {x, y, A, D, bias, perm, saved, workspace})) return ACDC_ERR_INVALID_ARG;
   const bool multipass = use_multipass(N, flags);
-  const size_t need = multipass ? mp_fwd_ws(batch, N, K) : fwd_ws(N, K, flags);
+  const size_t need = multipass ? mp_fwd_ws(batch, N, K, flags).total : fwd_ws(N, K, flags);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return ACDC_ERR_WORKSPACE;
   if (multipass)
     return mp_forward(x, y, A, D, bias, perm, batch, N, K, flags, saved, workspace,

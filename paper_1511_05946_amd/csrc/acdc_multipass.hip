@@ -17,6 +17,7 @@ constexpr int kThreads = 256;
 // hands XCD x the x-th contiguous eighth of the grid, so the workgroups
 // that gather from one row share that XCD's L2.
 constexpr int kXcds = 8;
+constexpr int kPermThreads = 512;
 
 dim3 grid_for(long long n) {
   long long blocks = (n + kThreads - 1) / kThreads;
@@ -33,26 +34,30 @@ __device__ __forceinline__ long long gindex() {
   return (long long)blk * blockDim.x + threadIdx.x;
 }
 
-__global__ __launch_bounds__(kThreads) void k_pack(const float* __restrict__ src, const int* __restrict__ perm,
-                                                   const float* __restrict__ a, float* __restrict__ stash,
-                                                   float2* __restrict__ Z, long long B, long long N) {
-  const long long M = N / 2, total = B * M;
+// Makhoul packing by float4 chunks: chunk q of a row (floats 4q .. 4q+3)
+// holds complex value m = q as (h.x, h.z) and m = M-1-q as (h.w, h.y).
+__device__ __forceinline__ float2 chunk_even(float4 h) { return make_float2(h.x, h.z); }
+__device__ __forceinline__ float2 chunk_odd(float4 h) { return make_float2(h.w, h.y); }
+__device__ __forceinline__ float4 chunk_of(float2 even, float2 odd) { return make_float4(even.x, odd.y, even.y, odd.x); }
+__device__ __forceinline__ float4 scale4(float4 h, float4 a) {
+  return make_float4(h.x * a.x, h.y * a.y, h.z * a.z, h.w * a.w);
+}
+__device__ __forceinline__ float4 relu4(float4 h) {
+  return make_float4(h.x > 0.f ? h.x : 0.f, h.y > 0.f ? h.y : 0.f, h.z > 0.f ? h.z : 0.f, h.w > 0.f ? h.w : 0.f);
+}
+
+// Chunk q (q < M/2) of row b: Z[q] and Z[M-1-q], scaled by a, stashed.
+__global__ __launch_bounds__(kThreads) void k_pack(const float* __restrict__ src, const float* __restrict__ a,
+                                                   float* __restrict__ stash, float2* __restrict__ Z, long long B,
+                                                   long long N) {
+  const long long M = N / 2, H = M / 2, total = B * H;
   for (long long i = gindex(); i < total; i += gstride()) {
-    const long long b = i / M, m = i % M;
-    long long i0, i1;
-    pack_idx(m, M, i0, i1);
-    const float* row = src + b * N;
-    float u0 = row[perm ? (perm[i0] & (N - 1)) : i0];
-    float u1 = row[perm ? (perm[i1] & (N - 1)) : i1];
-    if (stash) {
-      stash[b * N + i0] = u0;
-      stash[b * N + i1] = u1;
-    }
-    if (a) {
-      u0 *= a[i0];
-      u1 *= a[i1];
-    }
-    Z[i] = make_float2(u0, u1);
+    const long long b = i / H, q = i % H;
+    float4 h = reinterpret_cast<const float4*>(src + b * N)[q];
+    if (stash) reinterpret_cast<float4*>(stash + b * N)[q] = h;
+    if (a) h = scale4(h, reinterpret_cast<const float4*>(a)[q]);
+    Z[b * M + q] = chunk_even(h);
+    Z[b * M + M - 1 - q] = chunk_odd(h);
   }
 }
 
@@ -96,68 +101,88 @@ __global__ __launch_bounds__(kThreads) void k_dit(float2* __restrict__ Z, long l
   }
 }
 
-// The first DIF pass (on whole rows, S = M) with the packing folded in:
-// butterfly n gathers, scales and packs its R inputs m = n + j M/R straight
-// from the spatial rows (stashing the gathered values), saving one pass.
-__device__ __forceinline__ float2 packed_value(const float* row, const int* perm, const float* a, float* srow,
-                                               long long m, long long M, long long N) {
-  long long i0, i1;
-  pack_idx(m, M, i0, i1);
-  float u0 = row[perm ? (perm[i0] & (N - 1)) : i0];
-  float u1 = row[perm ? (perm[i1] & (N - 1)) : i1];
-  if (srow) {
-    srow[i0] = u0;
-    srow[i1] = u1;
-  }
-  if (a) {
-    u0 *= a[i0];
-    u1 *= a[i1];
-  }
-  return make_float2(u0, u1);
-}
-
+// The first DIF pass (on whole rows, S = M) with the packing folded in.
+// Butterfly n takes m = n + j Q (Q = M/R); for j < R/2 that is the even
+// part of chunk n + j Q, for j >= R/2 the odd part of chunk
+// nb + (R-1-j) Q, nb = Q-1-n.  So butterflies n and nb read the same R
+// chunks, and one thread runs both (n < Q/2): every access contiguous.
 template <int R>
-__global__ __launch_bounds__(kThreads) void k_pack_dif(const float* __restrict__ src, const int* __restrict__ perm,
-                                                       const float* __restrict__ a, float* __restrict__ stash,
-                                                       float2* __restrict__ Z, long long B, long long M,
-                                                       const float2* __restrict__ twM) {
-  const long long N = 2 * M, Q = M / R, total = B * Q;
+__global__ __launch_bounds__(kThreads) void k_pack_dif(const float* __restrict__ src, const float* __restrict__ a,
+                                                       float* __restrict__ stash, float2* __restrict__ Z, long long B,
+                                                       long long M, const float2* __restrict__ twM) {
+  const long long N = 2 * M, Q = M / R, H = Q / 2, total = B * H;
   for (long long i = gindex(); i < total; i += gstride()) {
-    const long long b = i / Q, n = i % Q;
-    const float* row = src + b * N;
-    float* srow = stash ? stash + b * N : nullptr;
-    float2 x[R];
+    const long long b = i / H, n = i % H, nb = Q - 1 - n;
+    const float4* row4 = reinterpret_cast<const float4*>(src + b * N);
+    float4* st4 = stash ? reinterpret_cast<float4*>(stash + b * N) : nullptr;
+    const float4* a4 = reinterpret_cast<const float4*>(a);
+    float2 x[R], xb[R];
 #pragma unroll
-    for (int j = 0; j < R; ++j) x[j] = packed_value(row, perm, a, srow, n + j * Q, M, N);
+    for (int j = 0; j < R / 2; ++j) {
+      const long long q = n + j * Q, qb = nb + j * Q;
+      float4 h = row4[q], hb = row4[qb];
+      if (st4) {
+        st4[q] = h;
+        st4[qb] = hb;
+      }
+      if (a4) {
+        h = scale4(h, a4[q]);
+        hb = scale4(hb, a4[qb]);
+      }
+      x[j] = chunk_even(h);
+      xb[R - 1 - j] = chunk_odd(h);
+      xb[j] = chunk_even(hb);
+      x[R - 1 - j] = chunk_odd(hb);
+    }
     Dft<R, false>::run(x);
+    Dft<R, false>::run(xb);
 #pragma unroll
-    for (int r = 1; r < R; ++r) x[r] = cmul(x[r], twM[n * r]);
+    for (int r = 1; r < R; ++r) {
+      x[r] = cmul(x[r], twM[n * r]);
+      xb[r] = cmul(xb[r], twM[nb * r]);
+    }
+    float2* zrow = Z + b * M;
 #pragma unroll
-    for (int r = 0; r < R; ++r) Z[b * M + r * Q + n] = x[r];
+    for (int r = 0; r < R; ++r) {
+      zrow[r * Q + n] = x[r];
+      zrow[r * Q + nb] = xb[r];
+    }
   }
 }
 
-// The last DIT pass (S = M) with the unpacking (and ReLU) folded in.
+// The last DIT pass (S = M) with the unpacking (and ReLU) folded in: the
+// mirror image of k_pack_dif, butterflies n and Q-1-n writing R chunks.
 template <int R>
 __global__ __launch_bounds__(kThreads) void k_dit_unpack(const float2* __restrict__ Z, float* __restrict__ dst,
                                                          long long B, long long M, const float2* __restrict__ twM,
                                                          int relu) {
-  const long long N = 2 * M, Q = M / R, total = B * Q;
+  const long long N = 2 * M, Q = M / R, H = Q / 2, total = B * H;
   for (long long i = gindex(); i < total; i += gstride()) {
-    const long long b = i / Q, n = i % Q;
-    float2 y[R];
+    const long long b = i / H, n = i % H, nb = Q - 1 - n;
+    const float2* zrow = Z + b * M;
+    float2 y[R], yb[R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) y[r] = Z[b * M + r * Q + n];
+    for (int r = 0; r < R; ++r) {
+      y[r] = zrow[r * Q + n];
+      yb[r] = zrow[r * Q + nb];
+    }
 #pragma unroll
-    for (int r = 1; r < R; ++r) y[r] = cmulc(y[r], twM[n * r]);
+    for (int r = 1; r < R; ++r) {
+      y[r] = cmulc(y[r], twM[n * r]);
+      yb[r] = cmulc(yb[r], twM[nb * r]);
+    }
     Dft<R, true>::run(y);
-    float* row = dst + b * N;
+    Dft<R, true>::run(yb);
+    float4* out4 = reinterpret_cast<float4*>(dst + b * N);
 #pragma unroll
-    for (int j = 0; j < R; ++j) {
-      long long i0, i1;
-      pack_idx(n + j * Q, M, i0, i1);
-      row[i0] = relu ? (y[j].x > 0.f ? y[j].x : 0.f) : y[j].x;
-      row[i1] = relu ? (y[j].y > 0.f ? y[j].y : 0.f) : y[j].y;
+    for (int j = 0; j < R / 2; ++j) {
+      float4 h = chunk_of(y[j], yb[R - 1 - j]), hb = chunk_of(yb[j], y[R - 1 - j]);
+      if (relu) {
+        h = relu4(h);
+        hb = relu4(hb);
+      }
+      out4[n + j * Q] = h;
+      out4[nb + j * Q] = hb;
     }
   }
 }
@@ -267,31 +292,283 @@ __global__ __launch_bounds__(kThreads) void k_mid_bwd(const float2* __restrict__
 
 __global__ __launch_bounds__(kThreads) void k_unpack(const float2* __restrict__ Z, float* __restrict__ dst,
                                                      long long B, long long N, int relu) {
-  const long long M = N / 2, total = B * M;
+  const long long M = N / 2, H = M / 2, total = B * H;
   for (long long i = gindex(); i < total; i += gstride()) {
-    const long long b = i / M, m = i % M;
-    long long i0, i1;
-    pack_idx(m, M, i0, i1);
-    const float2 z = Z[i];
-    dst[b * N + i0] = relu ? (z.x > 0.f ? z.x : 0.f) : z.x;
-    dst[b * N + i1] = relu ? (z.y > 0.f ? z.y : 0.f) : z.y;
+    const long long b = i / H, q = i % H;
+    float4 h = chunk_of(Z[b * M + q], Z[b * M + M - 1 - q]);
+    if (relu) h = relu4(h);
+    reinterpret_cast<float4*>(dst + b * N)[q] = h;
   }
 }
 
 // dL/da image u * gh1 (gh1 masked where the previous layer's ReLU was off:
-// u = 0 there), and dL/du = gh1 * a scattered back through the gather.
+// u = 0 there), and dL/du = gh1 * a (no permutation).
 __global__ __launch_bounds__(kThreads) void k_dA(const float* __restrict__ gh1, const float* __restrict__ u,
-                                                 const float* __restrict__ a, const int* __restrict__ perm,
-                                                 int mask, float* __restrict__ imgA, float* __restrict__ gnext,
-                                                 long long B, long long N) {
+                                                 const float* __restrict__ a, int mask, float* __restrict__ imgA,
+                                                 float* __restrict__ gnext, long long B, long long N) {
   const long long total = B * N;
   for (long long i = gindex(); i < total; i += gstride()) {
-    const long long b = i / N, n = i % N;
+    const long long n = i % N;
     const float uu = u[i];
     float gh = gh1[i];
     if (mask && !(uu > 0.f)) gh = 0.f;
     imgA[i] = uu * gh;
-    gnext[b * N + (perm ? (perm[n] & (N - 1)) : n)] = gh * a[n];
+    gnext[i] = gh * a[n];
+  }
+}
+
+// ------------------------------------------------------------ permutations
+// out[b][n] = in[b][src[n]] in chunks of C = min(N, kPermChunk) floats held
+// in LDS (see acdc_multipass.hpp).  Pass A: workgroup (b, c) loads source
+// chunk c and writes the C values it sources to tmp[b][cC + i], ordered by
+// destination chunk, then destination.  Pass B: workgroup (b, d) reads the
+// nC runs of tmp bound for chunk d into LDS (run-contiguous loads), then
+// writes chunk d in order.  The backward runs the adjoint: the same tables
+// with each pass's reads and writes exchanged.  Table entries are masked
+// into range, so a malformed perm yields wrong values, never a stray access.
+
+// Pass A table build, step 1: per block of kThreads destinations (all in
+// one chunk d, as C is a multiple of kThreads), the count of each source
+// chunk: cntS[blk][c].
+__global__ __launch_bounds__(kThreads) void k_pt_count(const int* __restrict__ src, long long N, int C, int nC,
+                                                       int* __restrict__ cntS) {
+  __shared__ int h[kPermMaxChunks];
+  for (int c = threadIdx.x; c < nC; c += kThreads) h[c] = 0;
+  __syncthreads();
+  const long long n = (long long)blockIdx.x * kThreads + threadIdx.x;
+  atomicAdd(&h[int((src[n] & (N - 1)) / C)], 1);
+  __syncthreads();
+  for (int c = threadIdx.x; c < nC; c += kThreads) cntS[(long long)blockIdx.x * nC + c] = h[c];
+}
+
+// Step 2, one thread per (d, c): the running count over chunk d's blocks
+// (bpre[blk][c], exclusive) and the total cnt[d][c].
+__global__ __launch_bounds__(kThreads) void k_pt_blocks(const int* __restrict__ cntS, int C, int nC,
+                                                        int* __restrict__ bpre, int* __restrict__ cnt) {
+  const int i = blockIdx.x * kThreads + threadIdx.x;
+  if (i >= nC * nC) return;
+  const int d = i / nC, c = i % nC, per = C / kThreads;
+  int run = 0;
+  for (int j = 0; j < per; ++j) {
+    const long long blk = (long long)d * per + j;
+    bpre[blk * nC + c] = run;
+    run += cntS[blk * nC + c];
+  }
+  cnt[i] = run;
+}
+
+// Step 3, one workgroup: off[d][c] = c C + sum over d' < d of cnt[d'][c]
+// (the tmp position of run (c, d)) and lst[d][c] = sum over c' < c of
+// cnt[d][c'] (its LDS position in pass B).
+__global__ __launch_bounds__(kThreads) void k_pt_offsets(const int* __restrict__ cnt, int C, int nC,
+                                                         int* __restrict__ off, int* __restrict__ lst) {
+  for (int c = threadIdx.x; c < nC; c += kThreads) {
+    long long run = (long long)c * C;
+    for (int d = 0; d < nC; ++d) {
+      off[d * nC + c] = int(run);
+      run += cnt[d * nC + c];
+    }
+  }
+  for (int d = threadIdx.x; d < nC; d += kThreads) {
+    int run = 0;
+    for (int c = 0; c < nC; ++c) {
+      lst[d * nC + c] = run;
+      run += cnt[d * nC + c];
+    }
+  }
+}
+
+// Step 4: every destination n takes a place in its run (the order inside a
+// block's share of a run is whatever the LDS counter hands out; the tables
+// stay consistent, and the permuted values do not depend on it):
+// srcA[tpos] = src[n] - c C, gposB[d C + slot] = tpos, locB[n] = slot.
+__global__ __launch_bounds__(kThreads) void k_pt_place(const int* __restrict__ src, long long N, int C, int nC,
+                                                       const int* __restrict__ bpre, const int* __restrict__ off,
+                                                       const int* __restrict__ lst, int* __restrict__ srcA,
+                                                       int* __restrict__ gposB, int* __restrict__ locB) {
+  __shared__ int h[kPermMaxChunks];
+  for (int c = threadIdx.x; c < nC; c += kThreads) h[c] = 0;
+  __syncthreads();
+  const long long n = (long long)blockIdx.x * kThreads + threadIdx.x;
+  const int sv = int(src[n] & (N - 1)), c = sv / C, d = int(n / C);
+  const int p = bpre[(long long)blockIdx.x * nC + c] + atomicAdd(&h[c], 1);
+  const long long tpos = ((long long)off[d * nC + c] + p) & (N - 1);
+  const int slot = (lst[d * nC + c] + p) & (C - 1);
+  srcA[tpos] = sv & (C - 1);
+  gposB[(long long)d * C + slot] = int(tpos);
+  locB[n] = slot;
+}
+
+// The pass kernels keep kPermBatch loads in flight per thread: with two
+// 64 KB workgroups per CU, one load at a time would leave them bound by
+// memory latency.  Element i of a chunk goes to thread i mod kPermThreads.
+constexpr int kPermBatch = 8;
+constexpr int kPermStep = kPermBatch * kPermThreads;
+// With more than one chunk, C = kPermChunk and the loops of pass B and of
+// the adjoint passes run whole steps; k_pt_a and k_pt_bt also serve a
+// single chunk (C = N, any power of two from 256) and take plain loops when
+// C is not a whole number of steps.
+static_assert(kPermChunk % kPermStep == 0, "whole steps per chunk");
+
+// Chunk copy HBM -> LDS (float4, contiguous).
+__device__ __forceinline__ void chunk_to_lds(float4* __restrict__ lds4, const float4* __restrict__ g4, int C) {
+  if ((C / 4) % kPermStep == 0) {
+    for (int i0 = threadIdx.x; i0 < C / 4; i0 += kPermStep) {
+      float4 v[kPermBatch];
+#pragma unroll
+      for (int u = 0; u < kPermBatch; ++u) v[u] = g4[i0 + u * kPermThreads];
+#pragma unroll
+      for (int u = 0; u < kPermBatch; ++u) lds4[i0 + u * kPermThreads] = v[u];
+    }
+  } else {
+    for (int i = threadIdx.x; i < C / 4; i += kPermThreads) lds4[i] = g4[i];
+  }
+}
+// Chunk copy LDS -> HBM (float4, contiguous).
+__device__ __forceinline__ void chunk_from_lds(float4* __restrict__ g4, const float4* __restrict__ lds4, int C) {
+  for (int i = threadIdx.x; i < C / 4; i += kPermThreads) g4[i] = lds4[i];
+}
+
+// Forward pass A (or, with one chunk, the whole permutation with tab = perm):
+// out[b][cC + i] = in[b][cC + tab[cC + i]].
+__global__ __launch_bounds__(kPermThreads) void k_pt_a(const float* __restrict__ in, float* __restrict__ out,
+                                                       const int* __restrict__ tab, long long N, int C, int nC,
+                                                       long long work) {
+  __shared__ float4 lds4[kPermChunk / 4];
+  const float* lds = reinterpret_cast<const float*>(lds4);
+  for (long long w = blockIdx.x; w < work; w += gridDim.x) {
+    const long long b = w / nC, c = w % nC, base = b * N + c * C;
+    chunk_to_lds(lds4, reinterpret_cast<const float4*>(in + base), C);
+    __syncthreads();
+    const int* t = tab + c * C;
+    if (C % kPermStep == 0) {
+      for (int i0 = threadIdx.x; i0 < C; i0 += kPermStep) {
+        int id[kPermBatch];
+#pragma unroll
+        for (int u = 0; u < kPermBatch; ++u) id[u] = t[i0 + u * kPermThreads] & (C - 1);
+#pragma unroll
+        for (int u = 0; u < kPermBatch; ++u) out[base + i0 + u * kPermThreads] = lds[id[u]];
+      }
+    } else {
+      for (int i = threadIdx.x; i < C; i += kPermThreads) out[base + i] = lds[t[i] & (C - 1)];
+    }
+    __syncthreads();
+  }
+}
+
+// Forward pass B: out[b][dC + j] = L[locB[dC + j]], L[j] = tmp[b][gposB[dC + j]].
+__global__ __launch_bounds__(kPermThreads) void k_pt_b(const float* __restrict__ tmp, float* __restrict__ out,
+                                                       const int* __restrict__ gposB, const int* __restrict__ locB,
+                                                       long long N, int C, int nC, long long work) {
+  __shared__ float lds[kPermChunk];
+  for (long long w = blockIdx.x; w < work; w += gridDim.x) {
+    const long long b = w / nC, d = w % nC, base = b * N + d * C;
+    const int* gp = gposB + d * C;
+    const int* lc = locB + d * C;
+    const float* trow = tmp + b * N;
+    for (int j0 = threadIdx.x; j0 < C; j0 += kPermStep) {
+      int id[kPermBatch];
+      float v[kPermBatch];
+#pragma unroll
+      for (int u = 0; u < kPermBatch; ++u) id[u] = gp[j0 + u * kPermThreads] & (N - 1);
+#pragma unroll
+      for (int u = 0; u < kPermBatch; ++u) v[u] = trow[id[u]];
+#pragma unroll
+      for (int u = 0; u < kPermBatch; ++u) lds[j0 + u * kPermThreads] = v[u];
+    }
+    __syncthreads();
+    for (int j0 = threadIdx.x; j0 < C; j0 += kPermStep) {
+      int id[kPermBatch];
+#pragma unroll
+      for (int u = 0; u < kPermBatch; ++u) id[u] = lc[j0 + u * kPermThreads] & (C - 1);
+#pragma unroll
+      for (int u = 0; u < kPermBatch; ++u) out[base + j0 + u * kPermThreads] = lds[id[u]];
+    }
+    __syncthreads();
+  }
+}
+
+// Backward, first pass (the adjoint of pass B, or with one chunk of the
+// whole permutation, loc = perm and no gpos), with the dL/da step folded
+// in: for n in chunk d, gm = gh1 (0 where mask and u <= 0), imgA = u gm,
+// L[loc[n]] = gm a[n]; then out[b][gpos[dC + j]] = L[j] (out[b][dC + j]
+// without gpos).
+__global__ __launch_bounds__(kPermThreads) void k_pt_bt(const float* __restrict__ gh1, const float* __restrict__ u,
+                                                        const float* __restrict__ a, int mask,
+                                                        float* __restrict__ imgA, float* __restrict__ out,
+                                                        const int* __restrict__ gpos, const int* __restrict__ loc,
+                                                        long long N, int C, int nC, long long work) {
+  __shared__ float4 lds4[kPermChunk / 4];
+  float* lds = reinterpret_cast<float*>(lds4);
+  for (long long w = blockIdx.x; w < work; w += gridDim.x) {
+    const long long b = w / nC, d = w % nC, base = b * N + d * C;
+    const int* lc = loc + d * C;
+    const float* ad = a + d * C;
+    auto one = [&](int j, float uu, float gh, float av, int id) {
+      const float g = (mask && !(uu > 0.f)) ? 0.f : gh;
+      imgA[base + j] = uu * g;
+      lds[id & (C - 1)] = g * av;
+    };
+    if (C % kPermStep == 0) {
+      for (int j0 = threadIdx.x; j0 < C; j0 += kPermStep) {
+        float uu[kPermBatch], gh[kPermBatch], av[kPermBatch];
+        int id[kPermBatch];
+#pragma unroll
+        for (int q = 0; q < kPermBatch; ++q) {
+          const int j = j0 + q * kPermThreads;
+          uu[q] = u[base + j];
+          gh[q] = gh1[base + j];
+          av[q] = ad[j];
+          id[q] = lc[j];
+        }
+#pragma unroll
+        for (int q = 0; q < kPermBatch; ++q) one(j0 + q * kPermThreads, uu[q], gh[q], av[q], id[q]);
+      }
+    } else {
+      for (int j = threadIdx.x; j < C; j += kPermThreads) one(j, u[base + j], gh1[base + j], ad[j], lc[j]);
+    }
+    __syncthreads();
+    if (gpos) {
+      const int* gp = gpos + d * C;
+      float* orow = out + b * N;
+      for (int j0 = threadIdx.x; j0 < C; j0 += kPermStep) {
+        int id[kPermBatch];
+#pragma unroll
+        for (int q = 0; q < kPermBatch; ++q) id[q] = gp[j0 + q * kPermThreads] & (N - 1);
+#pragma unroll
+        for (int q = 0; q < kPermBatch; ++q) orow[id[q]] = lds[j0 + q * kPermThreads];
+      }
+    } else {
+      chunk_from_lds(reinterpret_cast<float4*>(out + base), lds4, C);
+    }
+    __syncthreads();
+  }
+}
+
+// Backward, second pass (the adjoint of pass A): L[srcA[cC + i]] =
+// tmp[b][cC + i], then out[b][cC + i] = L[i].
+__global__ __launch_bounds__(kPermThreads) void k_pt_at(const float* __restrict__ tmp, float* __restrict__ out,
+                                                        const int* __restrict__ srcA, long long N, int C, int nC,
+                                                        long long work) {
+  __shared__ float4 lds4[kPermChunk / 4];
+  float* lds = reinterpret_cast<float*>(lds4);
+  for (long long w = blockIdx.x; w < work; w += gridDim.x) {
+    const long long b = w / nC, c = w % nC, base = b * N + c * C;
+    const int* t = srcA + c * C;
+    for (int i0 = threadIdx.x; i0 < C; i0 += kPermStep) {
+      int id[kPermBatch];
+      float v[kPermBatch];
+#pragma unroll
+      for (int q = 0; q < kPermBatch; ++q) {
+        id[q] = t[i0 + q * kPermThreads] & (C - 1);
+        v[q] = tmp[base + i0 + q * kPermThreads];
+      }
+#pragma unroll
+      for (int q = 0; q < kPermBatch; ++q) lds[id[q]] = v[q];
+    }
+    __syncthreads();
+    chunk_from_lds(reinterpret_cast<float4*>(out + base), lds4, C);
+    __syncthreads();
   }
 }
 
@@ -343,9 +620,8 @@ bool with_seg_plan(int L, F&& f) {
 
 }  // namespace
 
-hipError_t pack(const float* src, const int* perm, const float* a, float* stash, float2* Z, long long B, long long N,
-                hipStream_t s) {
-  hipLaunchKernelGGL(k_pack, grid_for(B * (N / 2)), dim3(kThreads), 0, s, src, perm, a, stash, Z, B, N);
+hipError_t pack(const float* src, const float* a, float* stash, float2* Z, long long B, long long N, hipStream_t s) {
+  hipLaunchKernelGGL(k_pack, grid_for(B * (N / 4)), dim3(kThreads), 0, s, src, a, stash, Z, B, N);
   return hipGetLastError();
 }
 
@@ -373,14 +649,14 @@ hipError_t dit(float2* Z, long long B, const Geo& g, long long S, int R, const f
   return hipGetLastError();
 }
 
-hipError_t pack_dif(const float* src, const int* perm, const float* a, float* stash, float2* Z, long long B,
-                    long long M, int R, const float2* twM, hipStream_t s) {
-  const dim3 grid = grid_for(B * (M / R)), block(kThreads);
+hipError_t pack_dif(const float* src, const float* a, float* stash, float2* Z, long long B, long long M, int R,
+                    const float2* twM, hipStream_t s) {
+  const dim3 grid = grid_for(B * (M / R / 2)), block(kThreads);
   switch (R) {
-    case 2: hipLaunchKernelGGL(k_pack_dif<2>, grid, block, 0, s, src, perm, a, stash, Z, B, M, twM); break;
-    case 4: hipLaunchKernelGGL(k_pack_dif<4>, grid, block, 0, s, src, perm, a, stash, Z, B, M, twM); break;
-    case 8: hipLaunchKernelGGL(k_pack_dif<8>, grid, block, 0, s, src, perm, a, stash, Z, B, M, twM); break;
-    case 16: hipLaunchKernelGGL(k_pack_dif<16>, grid, block, 0, s, src, perm, a, stash, Z, B, M, twM); break;
+    case 2: hipLaunchKernelGGL(k_pack_dif<2>, grid, block, 0, s, src, a, stash, Z, B, M, twM); break;
+    case 4: hipLaunchKernelGGL(k_pack_dif<4>, grid, block, 0, s, src, a, stash, Z, B, M, twM); break;
+    case 8: hipLaunchKernelGGL(k_pack_dif<8>, grid, block, 0, s, src, a, stash, Z, B, M, twM); break;
+    case 16: hipLaunchKernelGGL(k_pack_dif<16>, grid, block, 0, s, src, a, stash, Z, B, M, twM); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -388,7 +664,7 @@ hipError_t pack_dif(const float* src, const int* perm, const float* a, float* st
 
 hipError_t dit_unpack(const float2* Z, float* dst, long long B, long long M, int R, const float2* twM, bool relu,
                       hipStream_t s) {
-  const dim3 grid = grid_for(B * (M / R)), block(kThreads);
+  const dim3 grid = grid_for(B * (M / R / 2)), block(kThreads);
   const int rl = relu ? 1 : 0;
   switch (R) {
     case 2: hipLaunchKernelGGL(k_dit_unpack<2>, grid, block, 0, s, Z, dst, B, M, twM, rl); break;
@@ -429,13 +705,97 @@ hipError_t mid_bwd(const float2* Zh, float2* Zg, const float4* Mq, long long B, 
 }
 
 hipError_t unpack(const float2* Z, float* dst, long long B, long long N, bool relu, hipStream_t s) {
-  hipLaunchKernelGGL(k_unpack, grid_for(B * (N / 2)), dim3(kThreads), 0, s, Z, dst, B, N, relu ? 1 : 0);
+  hipLaunchKernelGGL(k_unpack, grid_for(B * (N / 4)), dim3(kThreads), 0, s, Z, dst, B, N, relu ? 1 : 0);
   return hipGetLastError();
 }
 
-hipError_t dA(const float* gh1, const float* u, const float* a, const int* perm, bool mask, float* imgA, float* gnext,
-              long long B, long long N, hipStream_t s) {
-  hipLaunchKernelGGL(k_dA, grid_for(B * N), dim3(kThreads), 0, s, gh1, u, a, perm, mask ? 1 : 0, imgA, gnext, B, N);
+hipError_t dA(const float* gh1, const float* u, const float* a, bool mask, float* imgA, float* gnext, long long B,
+              long long N, hipStream_t s) {
+  hipLaunchKernelGGL(k_dA, grid_for(B * N), dim3(kThreads), 0, s, gh1, u, a, mask ? 1 : 0, imgA, gnext, B, N);
+  return hipGetLastError();
+}
+
+PermGeo perm_geo(long long N) {
+  PermGeo p;
+  p.C = int(N < kPermChunk ? N : kPermChunk);
+  p.nC = int(N / p.C);
+  return p;
+}
+
+size_t perm_table_ints(long long N) {
+  const PermGeo p = perm_geo(N);
+  if (p.nC == 1) return 0;
+  return size_t(3 * N + 2 * (N / kThreads) * p.nC + 3LL * p.nC * p.nC);
+}
+
+PermTabs perm_tables_at(int* base, long long N) {
+  const PermGeo p = perm_geo(N);
+  PermTabs t;
+  if (p.nC == 1) return t;
+  const long long nb = N / kThreads, nn = (long long)p.nC * p.nC;
+  t.srcA = base;
+  t.gposB = t.srcA + N;
+  t.locB = t.gposB + N;
+  t.cntS = t.locB + N;
+  t.bpre = t.cntS + nb * p.nC;
+  t.cnt = t.bpre + nb * p.nC;
+  t.off = t.cnt + nn;
+  t.lst = t.off + nn;
+  return t;
+}
+
+hipError_t perm_build(const int* perm, long long N, const PermTabs& t, hipStream_t s) {
+  const PermGeo p = perm_geo(N);
+  if (p.nC == 1) return hipSuccess;
+  const unsigned nb = unsigned(N / kThreads), nn = unsigned(p.nC * p.nC);
+  hipLaunchKernelGGL(k_pt_count, dim3(nb), dim3(kThreads), 0, s, perm, N, p.C, p.nC, t.cntS);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pt_blocks, dim3((nn + kThreads - 1) / kThreads), dim3(kThreads), 0, s, t.cntS, p.C, p.nC,
+                     t.bpre, t.cnt);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pt_offsets, dim3(1), dim3(kThreads), 0, s, t.cnt, p.C, p.nC, t.off, t.lst);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pt_place, dim3(nb), dim3(kThreads), 0, s, perm, N, p.C, p.nC, t.bpre, t.off, t.lst, t.srcA,
+                     t.gposB, t.locB);
+  return hipGetLastError();
+}
+
+namespace {
+dim3 perm_grid(long long work) { return dim3(unsigned(work < 65536 ? (work < 1 ? 1 : work) : 65536)); }
+}  // namespace
+
+hipError_t permute(const float* in, float* out, float* tmp, const int* perm, const PermTabs& t, long long B,
+                   long long N, hipStream_t s) {
+  const PermGeo p = perm_geo(N);
+  const long long work = B * p.nC;
+  if (p.nC == 1) {
+    hipLaunchKernelGGL(k_pt_a, perm_grid(work), dim3(kPermThreads), 0, s, in, out, perm, N, p.C, p.nC, work);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(k_pt_a, perm_grid(work), dim3(kPermThreads), 0, s, in, tmp, t.srcA, N, p.C, p.nC, work);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pt_b, perm_grid(work), dim3(kPermThreads), 0, s, tmp, out, t.gposB, t.locB, N, p.C, p.nC,
+                     work);
+  return hipGetLastError();
+}
+
+hipError_t dA_permute(const float* gh1, const float* u, const float* a, bool mask, float* imgA, float* gnext,
+                      float* tmp, const int* perm, const PermTabs& t, long long B, long long N, hipStream_t s) {
+  const PermGeo p = perm_geo(N);
+  const long long work = B * p.nC;
+  const int mk = mask ? 1 : 0;
+  if (p.nC == 1) {
+    hipLaunchKernelGGL(k_pt_bt, perm_grid(work), dim3(kPermThreads), 0, s, gh1, u, a, mk, imgA, gnext,
+                       static_cast<const int*>(nullptr), perm, N, p.C, p.nC, work);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(k_pt_bt, perm_grid(work), dim3(kPermThreads), 0, s, gh1, u, a, mk, imgA, tmp, t.gposB, t.locB,
+                     N, p.C, p.nC, work);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pt_at, perm_grid(work), dim3(kPermThreads), 0, s, tmp, gnext, t.srcA, N, p.C, p.nC, work);
   return hipGetLastError();
 }
 

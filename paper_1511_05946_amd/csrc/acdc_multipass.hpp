@@ -4,15 +4,18 @@
 // the fused kernels' on-chip limit, or when ACDC_FLAG_MULTIPASS asks for it.
 //
 // Per layer and row, the steps of the fused kernels, one launch each:
-//   pack     u = z[perm] (stashed for the backward), h1 = u * a, Makhoul's
-//            even/odd-reversed packing into M complex values
+//   permute  u = z[perm] (into the stash slot for the backward), through LDS
+//            chunks, below
+//   pack     h1 = u * a, Makhoul's even/odd-reversed packing into M complex
+//            values (folded into the first DIF pass when there is one)
 //   DIF      zero, one or two radix-R passes (R <= 16) that split the M-point
 //            FFT into segments of L <= 8192 points, each with its twiddle
 //   segment  the L-point FFTs, one per workgroup, in registers and LDS
 //   middle   per quartet: real-FFT split, post-twiddle, * d (+ b), DCT-III
 //            pre-twiddle and inverse split (the fused kernels' quartet maps)
 //   inverse  segment IFFTs, then the DIT passes in reverse
-//   unpack   the inverse packing, ReLU, the layer output
+//   unpack   the inverse packing, ReLU, the layer output (folded into the
+//            last DIT pass when there is one)
 // The spectrum stays in the digit-reversed order the DIF passes leave it in;
 // the middle addresses it through pos() below.  The backward adds images of
 // dL/dd, dL/da (and dL/db) per row, summed over the batch by fixed-order
@@ -58,18 +61,17 @@ __host__ __device__ __forceinline__ void pack_idx(long long m, long long M, long
 
 // Launchers (acdc_multipass.hip).  All pointers are device pointers; every
 // launcher enqueues on `s` and returns the launch status.  Index arrays
-// (perm) are masked to [0, N), so a malformed permutation cannot address
-// outside its row.
-hipError_t pack(const float* src, const int* perm, const float* a, float* stash, float2* Z, long long B, long long N,
-                hipStream_t s);
+// (perm and the tables built from it) are masked into range, so a malformed
+// permutation cannot address outside its row.
+hipError_t pack(const float* src, const float* a, float* stash, float2* Z, long long B, long long N, hipStream_t s);
 hipError_t dif(float2* Z, long long B, const Geo& g, long long S, int R, const float2* twM, hipStream_t s);
 hipError_t dit(float2* Z, long long B, const Geo& g, long long S, int R, const float2* twM, hipStream_t s);
 hipError_t segments(float2* Z, long long nseg, int L, bool inverse, const char* seg_tab, hipStream_t s);
 // pack + the first DIF pass (radix R on whole rows), and the last DIT pass +
 // unpack (+ ReLU): the same results as the separate launches, two passes
 // over the batch fewer.
-hipError_t pack_dif(const float* src, const int* perm, const float* a, float* stash, float2* Z, long long B,
-                    long long M, int R, const float2* twM, hipStream_t s);
+hipError_t pack_dif(const float* src, const float* a, float* stash, float2* Z, long long B, long long M, int R,
+                    const float2* twM, hipStream_t s);
 hipError_t dit_unpack(const float2* Z, float* dst, long long B, long long M, int R, const float2* twM, bool relu,
                       hipStream_t s);
 hipError_t mq(const float* D, const float* Bias, float4* Mq, int K, long long NQ, const QuartetTabs& q,
@@ -78,8 +80,44 @@ hipError_t mid_fwd(float2* Z, const float4* Mq, long long B, const Geo& g, bool 
 hipError_t mid_bwd(const float2* Zh, float2* Zg, const float4* Mq, long long B, const Geo& g, float* imgD,
                    float* imgB, hipStream_t s);
 hipError_t unpack(const float2* Z, float* dst, long long B, long long N, bool relu, hipStream_t s);
-hipError_t dA(const float* gh1, const float* u, const float* a, const int* perm, bool mask, float* imgA, float* gnext,
-              long long B, long long N, hipStream_t s);
+hipError_t dA(const float* gh1, const float* u, const float* a, bool mask, float* imgA, float* gnext, long long B,
+              long long N, hipStream_t s);
+
+// Row permutations out[b][n] = in[b][perm[n]] for rows wider than one
+// workgroup's LDS.  A gather straight from HBM pulls a cache line per
+// element; here every access to HBM is contiguous, and the random accesses
+// hit LDS.  The row is cut into nC = N / C chunks of C floats:
+//   pass A  workgroup (b, c) loads source chunk c into LDS and writes the C
+//           values sourced from it to tmp[b][cC ...], ordered by destination
+//           chunk, then destination (nC runs, one per destination chunk)
+//   pass B  workgroup (b, d) reads the nC runs bound for chunk d into LDS,
+//           then writes chunk d of out in order
+// With one chunk (N <= kPermChunk) pass A alone is the permutation.  The
+// tables are built on the device from perm (perm_build, four small
+// launches), so a call needs no host copy of perm.  The backward applies the
+// adjoint (the inverse permutation) with the same tables, each pass's reads
+// and writes exchanged.
+constexpr int kPermChunk = 16384;                  // floats: 64 KB of LDS
+constexpr int kPermMaxChunks = (1 << 22) / kPermChunk;  // the widest row
+struct PermGeo {
+  int C, nC;
+};
+struct PermTabs {
+  int *srcA = nullptr, *gposB = nullptr, *locB = nullptr;  // [N] each
+  int *cntS = nullptr, *bpre = nullptr;                    // [N / 256][nC]
+  int *cnt = nullptr, *off = nullptr, *lst = nullptr;      // [nC][nC]
+};
+PermGeo perm_geo(long long N);
+size_t perm_table_ints(long long N);                  // 0 with one chunk
+PermTabs perm_tables_at(int* base, long long N);      // carve the tables from base
+hipError_t perm_build(const int* perm, long long N, const PermTabs& t, hipStream_t s);
+// out = in[perm] row by row; tmp is [B][N] scratch (unused with one chunk).
+hipError_t permute(const float* in, float* out, float* tmp, const int* perm, const PermTabs& t, long long B,
+                   long long N, hipStream_t s);
+// The backward's dL/da step with the adjoint permutation: gm = gh1 masked
+// (mask: where u <= 0), imgA = u gm, gnext[b][perm[n]] = gm[b][n] a[n].
+hipError_t dA_permute(const float* gh1, const float* u, const float* a, bool mask, float* imgA, float* gnext,
+                      float* tmp, const int* perm, const PermTabs& t, long long B, long long N, hipStream_t s);
 // out[w] (+)= sum over rows of img[b][w] in row order (blocks of kColRows
 // rows, then the block sums in block order); with q, column w = 4e + j is
 // the quartet value j of entry e, stored to its DCT index.
