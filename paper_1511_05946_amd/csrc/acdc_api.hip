@@ -526,8 +526,28 @@ int get_mp_tables(int N, MpTabs* out) {
 size_t mp_mq_bytes(long long N, int K) { return align256(size_t(K) * size_t(N / 4) * kMqRows * sizeof(float4)); }
 size_t mp_rows_bytes(int64_t batch, long long N) { return align256(size_t(batch) * size_t(N) * sizeof(float)); }
 
-size_t mp_perm_bytes(long long N, uint32_t flags) {
-  return (flags & kFlagPerm) ? align256(mp::perm_table_ints(N) * sizeof(int)) : 0;
+// Permutation tables: all K layers' built at once (four launches per call)
+// when they take at most 256 MB, else one layer's, rebuilt per layer.
+int mp_perm_layers(long long N, int K) {
+  const size_t per = mp::perm_table_ints(N) * sizeof(int);
+  return per * size_t(K) <= (size_t(256) << 20) ? K : 1;
+}
+size_t mp_perm_bytes(long long N, int K, uint32_t flags) {
+  if (!(flags & kFlagPerm)) return 0;
+  return align256(mp::perm_table_ints(N) * sizeof(int) * size_t(mp_perm_layers(N, K)));
+}
+// Layer k's tables, building them first when they are not all built.
+hipError_t mp_perm_tabs(const int32_t* perm, long long N, int K, int k, const mp::PermTabs& pt, mp::PermTabs* out,
+                        hipStream_t s) {
+  if (mp_perm_layers(N, K) == K) {
+    *out = mp::perm_layer(pt, k);
+    return hipSuccess;
+  }
+  *out = pt;
+  return mp::perm_build(perm + (long long)k * N, N, 1, pt, s);
+}
+hipError_t mp_perm_prebuild(const int32_t* perm, long long N, int K, const mp::PermTabs& pt, hipStream_t s) {
+  return mp_perm_layers(N, K) == K ? mp::perm_build(perm, N, K, pt, s) : hipSuccess;
 }
 
 // Forward workspace: quartet coefficients, the packed spectrum (also the
@@ -548,16 +568,17 @@ MpFwdWs mp_fwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
   w.z = take(mp_rows_bytes(batch, N));
   w.zbuf = take(mp_rows_bytes(batch, N));
   w.ubuf = take((flags & kFlagPerm) ? mp_rows_bytes(batch, N) : 0);
-  w.ptab = take(mp_perm_bytes(N, flags));
+  w.ptab = take(mp_perm_bytes(N, K, flags));
   w.total = off;
   return w;
 }
 
 // Backward workspace: quartet coefficients, the h and g spectra (contiguous,
 // transformed together), dL/dv of the current layer, the next layer's g,
-// the three images, the column-sum blocks, and the recompute stash.
+// the dL/da image, the row-block sums (dL/dd, then dL/da; dL/db), the
+// recompute stash and the permutation tables.
 struct MpBwdWs {
-  size_t mq = 0, zhg = 0, gh1 = 0, gbuf = 0, imgD = 0, imgA = 0, imgB = 0, part = 0, stash = 0, ptab = 0, total = 0;
+  size_t mq = 0, zhg = 0, gh1 = 0, gbuf = 0, imgA = 0, part = 0, partB = 0, stash = 0, ptab = 0, total = 0;
 };
 MpBwdWs mp_bwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved) {
   MpBwdWs w;
@@ -572,12 +593,12 @@ MpBwdWs mp_bwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have
   w.zhg = take(2 * rows);
   w.gh1 = take(rows);
   w.gbuf = take(rows);
-  w.imgD = take(rows);
   w.imgA = take(rows);
-  w.imgB = take((flags & kFlagBias) ? rows : 0);
-  w.part = take(size_t((batch + mp::kColRows - 1) / mp::kColRows) * size_t(N) * sizeof(float));
+  const size_t parts = size_t((batch + mp::kColRows - 1) / mp::kColRows) * size_t(N) * sizeof(float);
+  w.part = take(parts);
+  w.partB = take((flags & kFlagBias) ? parts : 0);
   w.stash = take(have_saved ? 0 : saved_floats(batch, N, K, flags) * sizeof(float));
-  w.ptab = take(mp_perm_bytes(N, flags));
+  w.ptab = take(mp_perm_bytes(N, K, flags));
   w.total = off;
   return w;
 }
@@ -628,9 +649,10 @@ float* mp_slot(float* saved, int k, int K, long long batch, long long N, bool pe
 // scratch; without, the packing stashes z itself.
 int mp_forward_layers(const float* x, float* y, const float* A, const float4* Mq, const int32_t* perm,
                       int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, float2* Z, float* zbuf,
-                      float* ubuf, const mp::PermTabs& pt, const MpTabs& t, hipStream_t s) {
+                      float* ubuf, const mp::PermTabs& pt, bool tables_built, const MpTabs& t, hipStream_t s) {
   const mp::Geo g = mp_geo(N);
   const bool perm_on = (flags & kFlagPerm) != 0, relu = (flags & kFlagRelu) != 0;
+  if (perm_on && !tables_built) MP_TRY(mp_perm_prebuild(perm, N, K, pt, s));
   for (int k = 0; k < K; ++k) {
     const float* src = k == 0 ? x : zbuf;
     float* slot = mp_slot(saved, k, K, batch, N, perm_on);
@@ -638,8 +660,9 @@ int mp_forward_layers(const float* x, float* y, const float* A, const float4* Mq
     if (perm_on) {
       const int32_t* pk = perm + (long long)k * N;
       float* udst = slot != nullptr ? slot : ubuf;
-      MP_TRY(mp::perm_build(pk, N, pt, s));
-      MP_TRY(mp::permute(src, udst, reinterpret_cast<float*>(Z), pk, pt, batch, N, s));
+      mp::PermTabs tk;
+      MP_TRY(mp_perm_tabs(perm, N, K, k, pt, &tk, s));
+      MP_TRY(mp::permute(src, udst, reinterpret_cast<float*>(Z), pk, tk, batch, N, s));
       u = udst;
       slot = nullptr;  // already stashed
     }
@@ -667,7 +690,7 @@ int mp_forward(const float* x, float* y, const float* A, const float* D, const f
   ProfScope prof(0, s);
   MP_TRY(mp::mq(D, bias, Mq, K, N / 4, t.q, s));
   if (batch == 0) return ACDC_OK;
-  return mp_forward_layers(x, y, A, Mq, perm, batch, N, K, flags, saved, Z, zbuf, ubuf, pt, t, s);
+  return mp_forward_layers(x, y, A, Mq, perm, batch, N, K, flags, saved, Z, zbuf, ubuf, pt, false, t, s);
 }
 
 int mp_backward(const float* x, const float* grad_y, const float* A, const float* D, const float* bias,
@@ -684,10 +707,9 @@ int mp_backward(const float* x, const float* grad_y, const float* A, const float
   float2* Zg = Zh + batch * (N / 2);  // the g spectra follow the h spectra
   float* gh1 = reinterpret_cast<float*>(ws + w.gh1);
   float* gbuf = reinterpret_cast<float*>(ws + w.gbuf);
-  float* imgD = reinterpret_cast<float*>(ws + w.imgD);
   float* imgA = reinterpret_cast<float*>(ws + w.imgA);
-  float* imgB = (flags & kFlagBias) ? reinterpret_cast<float*>(ws + w.imgB) : nullptr;
   float* part = reinterpret_cast<float*>(ws + w.part);
+  float* partB = (flags & kFlagBias) ? reinterpret_cast<float*>(ws + w.partB) : nullptr;
   float* stash = have_saved ? const_cast<float*>(saved) : reinterpret_cast<float*>(ws + w.stash);
   const mp::PermTabs pt = mp::perm_tables_at(reinterpret_cast<int*>(ws + w.ptab), N);
   const mp::Geo g = mp_geo(N);
@@ -696,9 +718,10 @@ int mp_backward(const float* x, const float* grad_y, const float* A, const float
   ProfScope prof(1, s);
   if (batch > 0) {
     MP_TRY(mp::mq(D, bias, Mq, K, N / 4, t.q, s));
+    if (perm_on) MP_TRY(mp_perm_prebuild(perm, N, K, pt, s));
     if (!have_saved) {
       // recompute the layer inputs into the workspace (Zh, gh1 are free until the layer loop)
-      rc = mp_forward_layers(x, nullptr, A, Mq, perm, batch, N, K, flags, stash, Zh, gh1, nullptr, pt, t, s);
+      rc = mp_forward_layers(x, nullptr, A, Mq, perm, batch, N, K, flags, stash, Zh, gh1, nullptr, pt, true, t, s);
       if (rc != ACDC_OK) return rc;
     }
   }
@@ -713,17 +736,18 @@ int mp_backward(const float* x, const float* grad_y, const float* A, const float
       if (rc != ACDC_OK) return rc;
       rc = mp_pack_fft(u, ak, nullptr, Zh, batch, N, g, t, s);
       if (rc != ACDC_OK) return rc;
-      MP_TRY(mp::mid_bwd(Zh, Zg, Mq + (long long)k * (N / 4) * kMqRows, batch, g, imgD, imgB, s));
-      MP_TRY(mp::colsum(imgD, batch, N, part, gD, &t.q, acc, s));
-      if (gB) MP_TRY(mp::colsum(imgB, batch, N, part, gB, &t.q, acc, s));
+      MP_TRY(mp::mid_bwd(Zh, Zg, Mq + (long long)k * (N / 4) * kMqRows, batch, g, part, partB, s));
+      MP_TRY(mp::colsum_parts(part, batch, N, gD, &t.q, acc, s));
+      if (gB) MP_TRY(mp::colsum_parts(partB, batch, N, gB, &t.q, acc, s));
       rc = mp_ifft_unpack(Zg, gh1, batch, N, false, g, t, s);
       if (rc != ACDC_OK) return rc;
       float* gnext = k == 0 ? grad_x : gbuf;
       if (perm_on) {
         // Zh and Zg are free again: the permutation's scratch
         const int32_t* pk = perm + (long long)k * N;
-        MP_TRY(mp::perm_build(pk, N, pt, s));
-        MP_TRY(mp::dA_permute(gh1, u, ak, relu && k > 0, imgA, gnext, reinterpret_cast<float*>(Zh), pk, pt, batch,
+        mp::PermTabs tk;
+        MP_TRY(mp_perm_tabs(perm, N, K, k, pt, &tk, s));
+        MP_TRY(mp::dA_permute(gh1, u, ak, relu && k > 0, imgA, gnext, reinterpret_cast<float*>(Zh), pk, tk, batch,
                               N, s));
       } else {
         MP_TRY(mp::dA(gh1, u, ak, relu && k > 0, imgA, gnext, batch, N, s));

@@ -240,53 +240,65 @@ __device__ __forceinline__ void pair_pos(const Geo& g, long long e, long long& p
   pb = pos(g, e == 0 ? g.M / 2 : g.M - e);
 }
 
+// Forward middle, kColRows rows per thread and quartet entry (the
+// coefficients loaded once for them).
 __global__ __launch_bounds__(kThreads) void k_mid_fwd(float2* __restrict__ Z, const float4* __restrict__ Mq,
                                                       long long B, Geo g, int bias) {
-  const long long NQ = g.M / 2, total = B * NQ;
+  const long long NQ = g.M / 2, P = (B + kColRows - 1) / kColRows, total = P * NQ;
   for (long long i = gindex(); i < total; i += gstride()) {
-    const long long b = i / NQ, e = i % NQ;
+    const long long p = i / NQ, e = i % NQ;
     long long pa, pb;
     pair_pos(g, e, pa, pb);
-    float2* row = Z + b * g.M;
-    float2 zk = row[pa], zm = row[pb];
     const float4 c0 = Mq[e * kMqRows], c1 = Mq[e * kMqRows + 1];
-    quartet_back(quartet_split(zk, zm, make_float2(c1.z, c1.w)), c0, c1, zk, zm);
-    if (bias) {
-      const float4 c3 = Mq[e * kMqRows + 3];
-      zk = make_float2(zk.x + c3.x, zk.y + c3.y);
-      zm = make_float2(zm.x + c3.z, zm.y + c3.w);
+    const float4 c3 = bias ? Mq[e * kMqRows + 3] : make_float4(0.f, 0.f, 0.f, 0.f);
+    const long long b0 = p * kColRows, b1 = b0 + kColRows < B ? b0 + kColRows : B;
+    for (long long b = b0; b < b1; ++b) {
+      float2* row = Z + b * g.M;
+      float2 zk = row[pa], zm = row[pb];
+      quartet_back(quartet_split(zk, zm, make_float2(c1.z, c1.w)), c0, c1, zk, zm);
+      if (bias) {
+        zk = make_float2(zk.x + c3.x, zk.y + c3.y);
+        zm = make_float2(zm.x + c3.z, zm.y + c3.w);
+      }
+      row[pa] = zk;
+      row[pb] = zm;
     }
-    row[pa] = zk;
-    row[pb] = zm;
   }
 }
 
-// Backward middle: images H*G (dL/dd) and, with a bias, G (dL/db) in
-// quartet order [b][4e + j]; g's spectrum is replaced by the DCT-III
-// pre-twiddle of G*d.
+// Backward middle over a block of kColRows rows (in row order) per thread
+// and quartet entry e: the images H*G (dL/dd) and, with a bias, G (dL/db),
+// summed over the block's rows into partD/partB[p][4e + j] (quartet order);
+// g's spectrum is replaced by the DCT-III pre-twiddle of G*d.  The
+// coefficients are loaded once per block.
 __global__ __launch_bounds__(kThreads) void k_mid_bwd(const float2* __restrict__ Zh, float2* __restrict__ Zg,
                                                       const float4* __restrict__ Mq, long long B, Geo g,
-                                                      float* __restrict__ imgD, float* __restrict__ imgB) {
-  const long long NQ = g.M / 2, total = B * NQ, W = 2 * g.M;
+                                                      float* __restrict__ partD, float* __restrict__ partB) {
+  const long long NQ = g.M / 2, P = (B + kColRows - 1) / kColRows, total = P * NQ, W = 2 * g.M;
   for (long long i = gindex(); i < total; i += gstride()) {
-    const long long b = i / NQ, e = i % NQ;
+    const long long p = i / NQ, e = i % NQ;
     long long pa, pb;
     pair_pos(g, e, pa, pb);
-    const float2* hrow = Zh + b * g.M;
-    float2* grow = Zg + b * g.M;
-    float2 gk = grow[pa], gm = grow[pb];
     const float4 c0 = Mq[e * kMqRows], c1 = Mq[e * kMqRows + 1], c2 = Mq[e * kMqRows + 2];
     const float2 w = make_float2(c1.z, c1.w), qa = make_float2(c2.x, c2.y), qbr = make_float2(c2.z, c2.w);
-    float H[4], G[4];
-    quartet_post(quartet_split(hrow[pa], hrow[pb], w), qa, qbr, H);
-    const Split sg = quartet_split(gk, gm, w);
-    quartet_post(sg, qa, qbr, G);
-    float4* d4 = reinterpret_cast<float4*>(imgD + b * W) + e;
-    *d4 = make_float4(H[0] * G[0], H[1] * G[1], H[2] * G[2], H[3] * G[3]);
-    if (imgB) *(reinterpret_cast<float4*>(imgB + b * W) + e) = make_float4(G[0], -G[1], G[2], G[3]);
-    quartet_back(sg, c0, c1, gk, gm);
-    grow[pa] = gk;
-    grow[pb] = gm;
+    float4 sD = make_float4(0.f, 0.f, 0.f, 0.f), sB = sD;
+    const long long b0 = p * kColRows, b1 = b0 + kColRows < B ? b0 + kColRows : B;
+    for (long long b = b0; b < b1; ++b) {
+      const float2* hrow = Zh + b * g.M;
+      float2* grow = Zg + b * g.M;
+      float2 gk = grow[pa], gm = grow[pb];
+      float H[4], G[4];
+      quartet_post(quartet_split(hrow[pa], hrow[pb], w), qa, qbr, H);
+      const Split sg = quartet_split(gk, gm, w);
+      quartet_post(sg, qa, qbr, G);
+      sD = make_float4(sD.x + H[0] * G[0], sD.y + H[1] * G[1], sD.z + H[2] * G[2], sD.w + H[3] * G[3]);
+      sB = make_float4(sB.x + G[0], sB.y - G[1], sB.z + G[2], sB.w + G[3]);
+      quartet_back(sg, c0, c1, gk, gm);
+      grow[pa] = gk;
+      grow[pb] = gm;
+    }
+    reinterpret_cast<float4*>(partD + p * W)[e] = sD;
+    if (partB) reinterpret_cast<float4*>(partB + p * W)[e] = sB;
   }
 }
 
@@ -331,8 +343,10 @@ __global__ __launch_bounds__(kThreads) void k_dA(const float* __restrict__ gh1, 
 // one chunk d, as C is a multiple of kThreads), the count of each source
 // chunk: cntS[blk][c].
 __global__ __launch_bounds__(kThreads) void k_pt_count(const int* __restrict__ src, long long N, int C, int nC,
-                                                       int* __restrict__ cntS) {
+                                                       int* __restrict__ cntS, long long stride) {
   __shared__ int h[kPermMaxChunks];
+  src += blockIdx.y * N;  // layer blockIdx.y
+  cntS += blockIdx.y * stride;
   for (int c = threadIdx.x; c < nC; c += kThreads) h[c] = 0;
   __syncthreads();
   const long long n = (long long)blockIdx.x * kThreads + threadIdx.x;
@@ -344,9 +358,13 @@ __global__ __launch_bounds__(kThreads) void k_pt_count(const int* __restrict__ s
 // Step 2, one thread per (d, c): the running count over chunk d's blocks
 // (bpre[blk][c], exclusive) and the total cnt[d][c].
 __global__ __launch_bounds__(kThreads) void k_pt_blocks(const int* __restrict__ cntS, int C, int nC,
-                                                        int* __restrict__ bpre, int* __restrict__ cnt) {
+                                                        int* __restrict__ bpre, int* __restrict__ cnt,
+                                                        long long stride) {
   const int i = blockIdx.x * kThreads + threadIdx.x;
   if (i >= nC * nC) return;
+  cntS += blockIdx.y * stride;
+  bpre += blockIdx.y * stride;
+  cnt += blockIdx.y * stride;
   const int d = i / nC, c = i % nC, per = C / kThreads;
   int run = 0;
   for (int j = 0; j < per; ++j) {
@@ -361,7 +379,11 @@ __global__ __launch_bounds__(kThreads) void k_pt_blocks(const int* __restrict__ 
 // (the tmp position of run (c, d)) and lst[d][c] = sum over c' < c of
 // cnt[d][c'] (its LDS position in pass B).
 __global__ __launch_bounds__(kThreads) void k_pt_offsets(const int* __restrict__ cnt, int C, int nC,
-                                                         int* __restrict__ off, int* __restrict__ lst) {
+                                                         int* __restrict__ off, int* __restrict__ lst,
+                                                         long long stride) {
+  cnt += blockIdx.x * stride;  // one workgroup per layer
+  off += blockIdx.x * stride;
+  lst += blockIdx.x * stride;
   for (int c = threadIdx.x; c < nC; c += kThreads) {
     long long run = (long long)c * C;
     for (int d = 0; d < nC; ++d) {
@@ -385,8 +407,17 @@ __global__ __launch_bounds__(kThreads) void k_pt_offsets(const int* __restrict__
 __global__ __launch_bounds__(kThreads) void k_pt_place(const int* __restrict__ src, long long N, int C, int nC,
                                                        const int* __restrict__ bpre, const int* __restrict__ off,
                                                        const int* __restrict__ lst, int* __restrict__ srcA,
-                                                       int* __restrict__ gposB, int* __restrict__ locB) {
+                                                       int* __restrict__ gposB, int* __restrict__ locB,
+                                                       long long stride) {
   __shared__ int h[kPermMaxChunks];
+  const long long ls = blockIdx.y * stride;
+  src += blockIdx.y * N;
+  bpre += ls;
+  off += ls;
+  lst += ls;
+  srcA += ls;
+  gposB += ls;
+  locB += ls;
   for (int c = threadIdx.x; c < nC; c += kThreads) h[c] = 0;
   __syncthreads();
   const long long n = (long long)blockIdx.x * kThreads + threadIdx.x;
@@ -572,17 +603,23 @@ __global__ __launch_bounds__(kPermThreads) void k_pt_at(const float* __restrict_
   }
 }
 
-// Column sums, stage 1: part[p][w] = sum of rows p*kColRows ... of img.
+// Column sums, stage 1: part[p][w] = sum of rows p*kColRows ... of img, in
+// row order, four columns per thread.
 __global__ __launch_bounds__(kThreads) void k_colsum1(const float* __restrict__ img, long long B, long long W,
                                                       float* __restrict__ part) {
-  const long long w = (long long)blockIdx.x * kThreads + threadIdx.x;
-  const long long p = blockIdx.y;
-  if (w >= W) return;
-  const long long b0 = p * kColRows;
-  const long long b1 = b0 + kColRows < B ? b0 + kColRows : B;
-  float s = 0.f;
-  for (long long b = b0; b < b1; ++b) s += img[b * W + w];
-  part[p * W + w] = s;
+  const long long W4 = W / 4, P = (B + kColRows - 1) / kColRows, total = P * W4;
+  for (long long i = gindex(); i < total; i += gstride()) {
+    const long long p = i / W4, w4 = i % W4;
+    const long long b0 = p * kColRows, b1 = b0 + kColRows < B ? b0 + kColRows : B;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    const float4* col = reinterpret_cast<const float4*>(img) + w4;
+#pragma unroll 4
+    for (long long b = b0; b < b1; ++b) {
+      const float4 v = col[b * W4];
+      s = make_float4(s.x + v.x, s.y + v.y, s.z + v.z, s.w + v.w);
+    }
+    reinterpret_cast<float4*>(part)[p * W4 + w4] = s;
+  }
 }
 
 // Stage 2: the block sums in block order, stored (or added) to the output.
@@ -694,13 +731,15 @@ hipError_t mq(const float* D, const float* Bias, float4* Mq, int K, long long NQ
 }
 
 hipError_t mid_fwd(float2* Z, const float4* Mq, long long B, const Geo& g, bool bias, hipStream_t s) {
-  hipLaunchKernelGGL(k_mid_fwd, grid_for(B * (g.M / 2)), dim3(kThreads), 0, s, Z, Mq, B, g, bias ? 1 : 0);
+  const long long P = (B + kColRows - 1) / kColRows;
+  hipLaunchKernelGGL(k_mid_fwd, grid_for(P * (g.M / 2)), dim3(kThreads), 0, s, Z, Mq, B, g, bias ? 1 : 0);
   return hipGetLastError();
 }
 
-hipError_t mid_bwd(const float2* Zh, float2* Zg, const float4* Mq, long long B, const Geo& g, float* imgD,
-                   float* imgB, hipStream_t s) {
-  hipLaunchKernelGGL(k_mid_bwd, grid_for(B * (g.M / 2)), dim3(kThreads), 0, s, Zh, Zg, Mq, B, g, imgD, imgB);
+hipError_t mid_bwd(const float2* Zh, float2* Zg, const float4* Mq, long long B, const Geo& g, float* partD,
+                   float* partB, hipStream_t s) {
+  const long long P = (B + kColRows - 1) / kColRows;
+  hipLaunchKernelGGL(k_mid_bwd, grid_for(P * (g.M / 2)), dim3(kThreads), 0, s, Zh, Zg, Mq, B, g, partD, partB);
   return hipGetLastError();
 }
 
@@ -732,6 +771,7 @@ PermTabs perm_tables_at(int* base, long long N) {
   const PermGeo p = perm_geo(N);
   PermTabs t;
   if (p.nC == 1) return t;
+  t.stride = (long long)perm_table_ints(N);
   const long long nb = N / kThreads, nn = (long long)p.nC * p.nC;
   t.srcA = base;
   t.gposB = t.srcA + N;
@@ -744,20 +784,35 @@ PermTabs perm_tables_at(int* base, long long N) {
   return t;
 }
 
-hipError_t perm_build(const int* perm, long long N, const PermTabs& t, hipStream_t s) {
+PermTabs perm_layer(const PermTabs& t, int l) {
+  if (t.srcA == nullptr) return t;
+  const long long o = l * t.stride;
+  PermTabs r = t;
+  r.srcA += o;
+  r.gposB += o;
+  r.locB += o;
+  r.cntS += o;
+  r.bpre += o;
+  r.cnt += o;
+  r.off += o;
+  r.lst += o;
+  return r;
+}
+
+hipError_t perm_build(const int* perm, long long N, int layers, const PermTabs& t, hipStream_t s) {
   const PermGeo p = perm_geo(N);
-  if (p.nC == 1) return hipSuccess;
-  const unsigned nb = unsigned(N / kThreads), nn = unsigned(p.nC * p.nC);
-  hipLaunchKernelGGL(k_pt_count, dim3(nb), dim3(kThreads), 0, s, perm, N, p.C, p.nC, t.cntS);
+  if (p.nC == 1 || layers <= 0) return hipSuccess;
+  const unsigned nb = unsigned(N / kThreads), nn = unsigned(p.nC * p.nC), L = unsigned(layers);
+  hipLaunchKernelGGL(k_pt_count, dim3(nb, L), dim3(kThreads), 0, s, perm, N, p.C, p.nC, t.cntS, t.stride);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_pt_blocks, dim3((nn + kThreads - 1) / kThreads), dim3(kThreads), 0, s, t.cntS, p.C, p.nC,
-                     t.bpre, t.cnt);
+  hipLaunchKernelGGL(k_pt_blocks, dim3((nn + kThreads - 1) / kThreads, L), dim3(kThreads), 0, s, t.cntS, p.C, p.nC,
+                     t.bpre, t.cnt, t.stride);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(k_pt_offsets, dim3(1), dim3(kThreads), 0, s, t.cnt, p.C, p.nC, t.off, t.lst);
+  hipLaunchKernelGGL(k_pt_offsets, dim3(L), dim3(kThreads), 0, s, t.cnt, p.C, p.nC, t.off, t.lst, t.stride);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(k_pt_place, dim3(nb), dim3(kThreads), 0, s, perm, N, p.C, p.nC, t.bpre, t.off, t.lst, t.srcA,
-                     t.gposB, t.locB);
+  hipLaunchKernelGGL(k_pt_place, dim3(nb, L), dim3(kThreads), 0, s, perm, N, p.C, p.nC, t.bpre, t.off, t.lst,
+                     t.srcA, t.gposB, t.locB, t.stride);
   return hipGetLastError();
 }
 
@@ -799,19 +854,24 @@ hipError_t dA_permute(const float* gh1, const float* u, const float* a, bool mas
   return hipGetLastError();
 }
 
-hipError_t colsum(const float* img, long long B, long long W, float* part, float* out, const QuartetTabs* q,
-                  bool accumulate, hipStream_t s) {
+hipError_t colsum_parts(const float* part, long long B, long long W, float* out, const QuartetTabs* q,
+                        bool accumulate, hipStream_t s) {
   const long long P = (B + kColRows - 1) / kColRows;
-  if (P > 0) {
-    hipLaunchKernelGGL(k_colsum1, dim3(unsigned((W + kThreads - 1) / kThreads), unsigned(P)), dim3(kThreads), 0, s,
-                       img, B, W, part);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
   const QuartetTabs qq = q ? *q : QuartetTabs{};
   hipLaunchKernelGGL(k_colsum2, grid_for(W), dim3(kThreads), 0, s, part, P, W, out, qq, q ? 1 : 0,
                      accumulate ? 1 : 0);
   return hipGetLastError();
+}
+
+hipError_t colsum(const float* img, long long B, long long W, float* part, float* out, const QuartetTabs* q,
+                  bool accumulate, hipStream_t s) {
+  const long long P = (B + kColRows - 1) / kColRows;
+  if (P > 0) {
+    hipLaunchKernelGGL(k_colsum1, grid_for(P * (W / 4)), dim3(kThreads), 0, s, img, B, W, part);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return colsum_parts(part, B, W, out, q, accumulate, s);
 }
 
 }  // namespace mp

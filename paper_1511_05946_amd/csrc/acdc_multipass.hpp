@@ -77,8 +77,11 @@ hipError_t dit_unpack(const float2* Z, float* dst, long long B, long long M, int
 hipError_t mq(const float* D, const float* Bias, float4* Mq, int K, long long NQ, const QuartetTabs& q,
               hipStream_t s);
 hipError_t mid_fwd(float2* Z, const float4* Mq, long long B, const Geo& g, bool bias, hipStream_t s);
-hipError_t mid_bwd(const float2* Zh, float2* Zg, const float4* Mq, long long B, const Geo& g, float* imgD,
-                   float* imgB, hipStream_t s);
+// The backward middle also sums the dL/dd (and dL/db) images over each
+// block of kColRows rows into partD/partB[P][N] (P = ceil(B / kColRows)),
+// for colsum_parts.
+hipError_t mid_bwd(const float2* Zh, float2* Zg, const float4* Mq, long long B, const Geo& g, float* partD,
+                   float* partB, hipStream_t s);
 hipError_t unpack(const float2* Z, float* dst, long long B, long long N, bool relu, hipStream_t s);
 hipError_t dA(const float* gh1, const float* u, const float* a, bool mask, float* imgA, float* gnext, long long B,
               long long N, hipStream_t s);
@@ -102,15 +105,19 @@ constexpr int kPermMaxChunks = (1 << 22) / kPermChunk;  // the widest row
 struct PermGeo {
   int C, nC;
 };
+// One layer's tables; layer l's sit stride ints further on.
 struct PermTabs {
   int *srcA = nullptr, *gposB = nullptr, *locB = nullptr;  // [N] each
   int *cntS = nullptr, *bpre = nullptr;                    // [N / 256][nC]
   int *cnt = nullptr, *off = nullptr, *lst = nullptr;      // [nC][nC]
+  long long stride = 0;
 };
 PermGeo perm_geo(long long N);
-size_t perm_table_ints(long long N);                  // 0 with one chunk
-PermTabs perm_tables_at(int* base, long long N);      // carve the tables from base
-hipError_t perm_build(const int* perm, long long N, const PermTabs& t, hipStream_t s);
+size_t perm_table_ints(long long N);                  // per layer; 0 with one chunk
+PermTabs perm_tables_at(int* base, long long N);      // carve layer 0's tables from base
+PermTabs perm_layer(const PermTabs& t, int l);        // layer l's tables
+// Tables of the permutations perm[0 .. layers-1][N] into layers 0 .. layers-1.
+hipError_t perm_build(const int* perm, long long N, int layers, const PermTabs& t, hipStream_t s);
 // out = in[perm] row by row; tmp is [B][N] scratch (unused with one chunk).
 hipError_t permute(const float* in, float* out, float* tmp, const int* perm, const PermTabs& t, long long B,
                    long long N, hipStream_t s);
@@ -120,10 +127,14 @@ hipError_t dA_permute(const float* gh1, const float* u, const float* a, bool mas
                       float* tmp, const int* perm, const PermTabs& t, long long B, long long N, hipStream_t s);
 // out[w] (+)= sum over rows of img[b][w] in row order (blocks of kColRows
 // rows, then the block sums in block order); with q, column w = 4e + j is
-// the quartet value j of entry e, stored to its DCT index.
-constexpr int kColRows = 64;
+// the quartet value j of entry e, stored to its DCT index.  W is a
+// multiple of 4; part holds [ceil(B / kColRows)][W].  colsum_parts runs the
+// second stage alone, on block sums made elsewhere (mid_bwd).
+constexpr int kColRows = 16;
 hipError_t colsum(const float* img, long long B, long long W, float* part, float* out, const QuartetTabs* q,
                   bool accumulate, hipStream_t s);
+hipError_t colsum_parts(const float* part, long long B, long long W, float* out, const QuartetTabs* q,
+                        bool accumulate, hipStream_t s);
 
 }  // namespace mp
 }  // namespace acdc
