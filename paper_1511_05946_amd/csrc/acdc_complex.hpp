@@ -79,6 +79,24 @@ struct CplxOps {
     });
   }
 
+  // The thread's perm entries (spatial layout), loaded ahead of the gather.
+  __host__ __device__ __forceinline__ static void load_idx(int (&idx)[P], GView perm, unsigned t) {
+#pragma unroll
+    for (int beta = 0; beta < B0; ++beta)
+#pragma unroll
+      for (int i = 0; i < R0; ++i) idx[beta * R0 + i] = perm.ldi1(t * 4u, unsigned(T * (beta + i * B0)) * 4u);
+  }
+  // u[n] = z[perm[n]] with the indices already in registers.
+  template <class Ctx>
+  __host__ __device__ __forceinline__ static void gather_idx(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
+                                                             const int (&idx)[P]) {
+    ctx.sync_row();
+    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { slab[l + c] = z; });
+    ctx.sync_row();
+#pragma unroll
+    for (int s = 0; s < P; ++s) v[s] = slab[idx[s]];
+  }
+
   template <class Ctx>
   __host__ __device__ __forceinline__ static void gather(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
                                                          GView perm) {
@@ -134,7 +152,12 @@ __host__ __device__ void cplx_forward_row(Ctx& ctx, const CplxArgs& a, unsigned 
   float2 v[P];
   O::load(GView::of(a.x + row0 * RS), roff, v, t, valid);
   for (int k = 0; k < a.K; ++k) {
-    if (a.flags & 1u) O::gather(ctx, v, t, slab2, GView::of(a.perm + (long long)k * N));
+    // the perm loads are issued before the gather's barriers
+    if (a.flags & 1u) {
+      int idx[P];
+      O::load_idx(idx, GView::of(a.perm + (long long)k * N), t);
+      O::gather_idx(ctx, v, t, slab2, idx);
+    }
     // stash u_k: u_1..u_{K-1} in slots 0..K-2, and with PERM u_0 in slot K-1
     if (a.saved != nullptr && (k > 0 || (a.flags & 1u)) && valid)
       O::store(GView::of(a.saved + ((long long)(k > 0 ? k - 1 : a.K - 1) * a.batch + row0) * RS), roff, v, t);
