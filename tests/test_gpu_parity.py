@@ -372,6 +372,12 @@ def test_multipass_wide_rows(acdc, N, K, B, flags):
     run_case(acdc, N, K, B, flags, seed=N + 7)
 
 
+def test_multipass_row_blocks(acdc):
+    # the backward sums images over blocks of 16 rows: 37 rows give two
+    # whole blocks and a ragged one; 4 permutation chunks per row
+    run_case(acdc, 65536, 2, 37, P | FLAG_BIAS, seed=76)
+
+
 @pytest.mark.parametrize("save", [True, False])
 def test_multipass_first_layer_permutation_and_recompute(acdc, save):
     run_case(acdc, 65536, 2, 3, P | R, seed=71, save=save, perm0=True)
