@@ -110,14 +110,18 @@ int acdc_prepare(int32_t N, uint32_t flags);
 size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
 
 /* Bytes of workspace acdc_forward needs (the per-layer quartet coefficients
- * built from D).  Host only. */
+ * built from D; on the multi-pass path also the packed spectra, a layer
+ * buffer and, with ACDC_FLAG_PERM, a buffer for the permuted layer input and
+ * the permutation tables that each call builds on the device from perm).
+ * Host only. */
 size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
 
 /* Bytes of workspace acdc_backward needs: per-workgroup partial sums of the
  * parameter gradients, the per-layer quartet coefficients, the batch sums
  * behind the bias gradient (ACDC_FLAG_BIAS), and -- when have_saved is 0 and
  * acdc_saved_bytes(...) is not 0 -- room to recompute the layer inputs (the
- * paper's recompute policy, Sec. 5.3). */
+ * paper's recompute policy, Sec. 5.3).  The multi-pass path adds its
+ * spectra, layer buffers, row-block sums and permutation tables. */
 size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags, int have_saved);
 
 /* Forward cascade: y = cascade(x).  `bias` is read with ACDC_FLAG_BIAS and
