@@ -364,11 +364,13 @@ def test_multipass_fused_widths(acdc, N):
 
 
 @pytest.mark.parametrize("N,K,B,flags", [(65536, 2, 3, P | R | FLAG_BIAS), (1 << 18, 2, 2, P | FLAG_BIAS),
-                                         (1 << 20, 2, 2, P | FLAG_BIAS)])
+                                         (1 << 20, 2, 2, P | FLAG_BIAS), (1 << 22, 4, 2, P | FLAG_BIAS)])
 def test_multipass_wide_rows(acdc, N, K, B, flags):
     # 65536: one radix-4 pass; 2^18: one radix-16 pass; 2^20: radix-16 then
-    # radix-4.  Rows of 2^18 and more nearly always hold a ReLU decision
-    # within 1e-5 rms of zero, so those run without ReLU.
+    # radix-4; 2^22: radix 16 twice, and permutation tables too large to
+    # build for all 4 layers at once (rebuilt per layer).  Rows of 2^18 and
+    # more nearly always hold a ReLU decision within 1e-5 rms of zero, so
+    # those run without ReLU.
     run_case(acdc, N, K, B, flags, seed=N + 7)
 
 
