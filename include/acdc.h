@@ -59,12 +59,13 @@
  *
  * Supported widths (acdc_supported): ACDC N in {8, 16, ..., 32768} and 9216
  * with the fused kernels (one row per workgroup or wave, all K layers in one
- * launch); AFDF N in {8, 16, ..., 16384}.  Real layers of power-of-two width
- * 256 ... 2^22 also run multi-pass (the multiple-call scheme of Sec. 5.2:
- * each layer's FFT goes through HBM in several launches, with hand-written
- * passes).  That path serves the widths past 32768, and any power-of-two
- * width with ACDC_FLAG_MULTIPASS; it needs more workspace (see the
- * *_workspace_bytes calls), and its permutation indices are read modulo N.
+ * launch); AFDF N in {8, 16, ..., 16384}.  Layers of power-of-two width also
+ * run multi-pass (the multiple-call scheme of Sec. 5.2: each layer's FFT
+ * goes through HBM in several launches, with hand-written passes): ACDC
+ * 256 ... 2^22, AFDF 256 ... 2^21.  That path serves the widths past the
+ * fused ones, and any such width with ACDC_FLAG_MULTIPASS; it needs more
+ * workspace (see the *_workspace_bytes calls), and its permutation indices
+ * are read modulo N.
  * Batch sizes from 0 upward; K >= 1.
  */
 #ifndef ACDC_H_

@@ -263,16 +263,16 @@ bool fused_supported(int N, unsigned flags) {
   return ok;
 }
 
-// Multi-pass path: real layers of power-of-two width 256 ... 2^22.
+// Multi-pass path: power-of-two rows, real ones of width 256 ... 2^22 and
+// complex ones of 256 ... 2^21 elements (the same M <= 2^21 point FFTs).
 bool mp_width(long long N) { return N >= 256 && N <= (1LL << 22) && (N & (N - 1)) == 0; }
+bool mp_width(long long N, unsigned flags) {
+  return (flags & kFlagComplex) ? N <= (1LL << 21) && mp_width(N) : mp_width(N);
+}
 bool use_multipass(int N, unsigned flags) {
-  if (flags & kFlagComplex) return false;
   return (flags & kFlagMultipass) != 0 || !fused_supported(N, flags);
 }
-bool supported(int N, unsigned flags) {
-  if (flags & kFlagComplex) return !(flags & kFlagMultipass) && fused_supported(N, flags);
-  return use_multipass(N, flags) ? mp_width(N) : true;
-}
+bool supported(int N, unsigned flags) { return use_multipass(N, flags) ? mp_width(N, flags) : true; }
 
 // Constant table of (N, complex) on the current device; built and uploaded
 // on first use.
@@ -526,28 +526,33 @@ int get_mp_tables(int N, MpTabs* out) {
 size_t mp_mq_bytes(long long N, int K) { return align256(size_t(K) * size_t(N / 4) * kMqRows * sizeof(float4)); }
 size_t mp_rows_bytes(int64_t batch, long long N) { return align256(size_t(batch) * size_t(N) * sizeof(float)); }
 
+// Floats per row element: 1, or 2 for complex (AFDF) rows.
+int mp_ew(uint32_t flags) { return (flags & kFlagComplex) ? 2 : 1; }
+
 // Permutation tables: all K layers' built at once (four launches per call)
 // when they take at most 256 MB, else one layer's, rebuilt per layer.
-int mp_perm_layers(long long N, int K) {
-  const size_t per = mp::perm_table_ints(N) * sizeof(int);
+int mp_perm_layers(long long N, int K, int ew) {
+  const size_t per = mp::perm_table_ints(N, ew) * sizeof(int);
   return per * size_t(K) <= (size_t(256) << 20) ? K : 1;
 }
 size_t mp_perm_bytes(long long N, int K, uint32_t flags) {
   if (!(flags & kFlagPerm)) return 0;
-  return align256(mp::perm_table_ints(N) * sizeof(int) * size_t(mp_perm_layers(N, K)));
+  const int ew = mp_ew(flags);
+  return align256(mp::perm_table_ints(N, ew) * sizeof(int) * size_t(mp_perm_layers(N, K, ew)));
 }
 // Layer k's tables, building them first when they are not all built.
 hipError_t mp_perm_tabs(const int32_t* perm, long long N, int K, int k, const mp::PermTabs& pt, mp::PermTabs* out,
-                        hipStream_t s) {
-  if (mp_perm_layers(N, K) == K) {
+                        hipStream_t s, int ew = 1) {
+  if (mp_perm_layers(N, K, ew) == K) {
     *out = mp::perm_layer(pt, k);
     return hipSuccess;
   }
   *out = pt;
-  return mp::perm_build(perm + (long long)k * N, N, 1, pt, s);
+  return mp::perm_build(perm + (long long)k * N, N, 1, pt, s, ew);
 }
-hipError_t mp_perm_prebuild(const int32_t* perm, long long N, int K, const mp::PermTabs& pt, hipStream_t s) {
-  return mp_perm_layers(N, K) == K ? mp::perm_build(perm, N, K, pt, s) : hipSuccess;
+hipError_t mp_perm_prebuild(const int32_t* perm, long long N, int K, const mp::PermTabs& pt, hipStream_t s,
+                            int ew = 1) {
+  return mp_perm_layers(N, K, ew) == K ? mp::perm_build(perm, N, K, pt, s, ew) : hipSuccess;
 }
 
 // Forward workspace: quartet coefficients, the packed spectrum (also the
@@ -564,10 +569,11 @@ MpFwdWs mp_fwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
     off += align256(bytes);
     return o;
   };
-  w.mq = take(mp_mq_bytes(N, K));
-  w.z = take(mp_rows_bytes(batch, N));
-  w.zbuf = take(mp_rows_bytes(batch, N));
-  w.ubuf = take((flags & kFlagPerm) ? mp_rows_bytes(batch, N) : 0);
+  const long long rowf = (long long)N * mp_ew(flags);  // floats per row
+  w.mq = take((flags & kFlagComplex) ? 0 : mp_mq_bytes(N, K));
+  w.z = take(mp_rows_bytes(batch, rowf));
+  w.zbuf = take(mp_rows_bytes(batch, rowf));
+  w.ubuf = take((flags & kFlagPerm) ? mp_rows_bytes(batch, rowf) : 0);
   w.ptab = take(mp_perm_bytes(N, K, flags));
   w.total = off;
   return w;
@@ -578,7 +584,7 @@ MpFwdWs mp_fwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
 // the dL/da image, the row-block sums (dL/dd, then dL/da; dL/db), the
 // recompute stash and the permutation tables.
 struct MpBwdWs {
-  size_t mq = 0, zhg = 0, gh1 = 0, gbuf = 0, imgA = 0, part = 0, partB = 0, stash = 0, ptab = 0, total = 0;
+  size_t mq = 0, zhg = 0, gh1 = 0, gbuf = 0, imgA = 0, gu = 0, part = 0, partB = 0, stash = 0, ptab = 0, total = 0;
 };
 MpBwdWs mp_bwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved) {
   MpBwdWs w;
@@ -588,13 +594,16 @@ MpBwdWs mp_bwd_ws(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have
     off += align256(bytes);
     return o;
   };
-  const size_t rows = size_t(batch) * size_t(N) * sizeof(float);
-  w.mq = take(mp_mq_bytes(N, K));
+  const bool cplx = (flags & kFlagComplex) != 0;
+  const size_t rowf = size_t(N) * size_t(mp_ew(flags));  // floats per row
+  const size_t rows = size_t(batch) * rowf * sizeof(float);
+  w.mq = take(cplx ? 0 : mp_mq_bytes(N, K));
   w.zhg = take(2 * rows);
   w.gh1 = take(rows);
   w.gbuf = take(rows);
   w.imgA = take(rows);
-  const size_t parts = size_t((batch + mp::kColRows - 1) / mp::kColRows) * size_t(N) * sizeof(float);
+  w.gu = take(cplx && (flags & kFlagPerm) ? rows : 0);  // complex dL/du before the adjoint permutation
+  const size_t parts = size_t((batch + mp::kColRows - 1) / mp::kColRows) * rowf * sizeof(float);
   w.part = take(parts);
   w.partB = take((flags & kFlagBias) ? parts : 0);
   w.stash = take(have_saved ? 0 : saved_floats(batch, N, K, flags) * sizeof(float));
@@ -675,8 +684,128 @@ int mp_forward_layers(const float* x, float* y, const float* A, const float4* Mq
   return ACDC_OK;
 }
 
+// ------------------------------------------------ complex (AFDF) multi-pass
+// Rows of N complex elements are their own N-point FFT inputs (M = N, the
+// geometry and twiddles of a real width 2N).  Per layer: u = z[perm] (into
+// the stash slot), Z = FFT(u * a), Z *= d / N, z' = unnormalised IFFT(Z).
+int mp_cplx_forward_layers(const float2* x, float2* y, const float2* A, const float2* D, const int32_t* perm,
+                           int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, float2* Z,
+                           float2* zbuf, float2* ubuf, const mp::PermTabs& pt, bool tables_built, const MpTabs& t,
+                           hipStream_t s) {
+  const mp::Geo g = mp_geo(2LL * N);
+  const bool perm_on = (flags & kFlagPerm) != 0;
+  const float invN = 1.0f / float(N);
+  if (perm_on && !tables_built) MP_TRY(mp_perm_prebuild(perm, N, K, pt, s, 2));
+  for (int k = 0; k < K; ++k) {
+    const float2* src = k == 0 ? x : zbuf;
+    float2* slot = reinterpret_cast<float2*>(mp_slot(saved, k, K, batch, 2LL * N, perm_on));
+    const float2* u = src;
+    if (perm_on) {
+      const int32_t* pk = perm + (long long)k * N;
+      float2* udst = slot != nullptr ? slot : ubuf;
+      mp::PermTabs tk;
+      MP_TRY(mp_perm_tabs(perm, N, K, k, pt, &tk, s, 2));
+      MP_TRY(mp::cpermute(src, udst, Z, pk, tk, batch, N, s));
+      u = udst;
+      slot = nullptr;  // already stashed
+    }
+    MP_TRY(mp::cfft_in(u, A + (long long)k * N, slot, Z, batch, g, t.tw, t.seg, s));
+    MP_TRY(mp::cmid_fwd(Z, D + (long long)k * N, batch, g, invN, s));
+    MP_TRY(mp::cifft_out(Z, (k == K - 1 && y != nullptr) ? y : zbuf, batch, g, t.tw, t.seg, s));
+  }
+  return ACDC_OK;
+}
+
+int mp_cplx_forward(const float* x, float* y, const float* A, const float* D, const int32_t* perm, int64_t batch,
+                    int32_t N, int32_t K, uint32_t flags, float* saved, void* workspace, hipStream_t s) {
+  MpTabs t;
+  int rc = get_mp_tables(2 * N, &t);
+  if (rc != ACDC_OK) return rc;
+  const MpFwdWs w = mp_fwd_ws(batch, N, K, flags);
+  char* ws = static_cast<char*>(workspace);
+  const mp::PermTabs pt = mp::perm_tables_at(reinterpret_cast<int*>(ws + w.ptab), N, 2);
+  ProfScope prof(0, s);
+  if (batch == 0) return ACDC_OK;
+  return mp_cplx_forward_layers(reinterpret_cast<const float2*>(x), reinterpret_cast<float2*>(y),
+                                reinterpret_cast<const float2*>(A), reinterpret_cast<const float2*>(D), perm, batch,
+                                N, K, flags, saved, reinterpret_cast<float2*>(ws + w.z),
+                                reinterpret_cast<float2*>(ws + w.zbuf), reinterpret_cast<float2*>(ws + w.ubuf), pt,
+                                false, t, s);
+}
+
+// Backward per layer (the fused complex kernels' steps): gh3 = FFT(g) / N,
+// h2 = FFT(u * a), dL/dd += gh3 conj(h2), gh1 = IFFT(gh3 conj(d)),
+// dL/da += gh1 conj(u), g_u = gh1 conj(a), scattered back through perm.
+int mp_cplx_backward(const float* x, const float* grad_y, const float* A, const float* D, const int32_t* perm,
+                     const float* saved, float* grad_x, float* grad_A, float* grad_D, int64_t batch, int32_t N,
+                     int32_t K, uint32_t flags, bool have_saved, void* workspace, hipStream_t s) {
+  MpTabs t;
+  int rc = get_mp_tables(2 * N, &t);
+  if (rc != ACDC_OK) return rc;
+  const MpBwdWs w = mp_bwd_ws(batch, N, K, flags, have_saved);
+  char* ws = static_cast<char*>(workspace);
+  float2* Zh = reinterpret_cast<float2*>(ws + w.zhg);
+  float2* Zg = Zh + batch * N;  // the g spectra follow the h spectra
+  float2* gh1 = reinterpret_cast<float2*>(ws + w.gh1);
+  float2* gbuf = reinterpret_cast<float2*>(ws + w.gbuf);
+  float2* imgA = reinterpret_cast<float2*>(ws + w.imgA);
+  float2* gu = reinterpret_cast<float2*>(ws + w.gu);
+  float* part = reinterpret_cast<float*>(ws + w.part);
+  float* stash = have_saved ? const_cast<float*>(saved) : reinterpret_cast<float*>(ws + w.stash);
+  const mp::PermTabs pt = mp::perm_tables_at(reinterpret_cast<int*>(ws + w.ptab), N, 2);
+  const mp::Geo g = mp_geo(2LL * N);
+  const bool perm_on = (flags & kFlagPerm) != 0, acc = (flags & kFlagAccumulate) != 0;
+  const float invN = 1.0f / float(N);
+  const long long W = 2LL * N;  // floats per row
+  const float2* x2 = reinterpret_cast<const float2*>(x);
+  const float2* A2 = reinterpret_cast<const float2*>(A);
+  const float2* D2 = reinterpret_cast<const float2*>(D);
+  ProfScope prof(1, s);
+  if (batch > 0) {
+    if (perm_on) MP_TRY(mp_perm_prebuild(perm, N, K, pt, s, 2));
+    if (!have_saved) {
+      // recompute the layer inputs into the workspace (Zh, gh1 are free until the layer loop)
+      rc = mp_cplx_forward_layers(x2, nullptr, A2, D2, perm, batch, N, K, flags, stash, Zh, gh1, nullptr, pt, true,
+                                  t, s);
+      if (rc != ACDC_OK) return rc;
+    }
+  }
+  for (int k = K - 1; k >= 0; --k) {
+    float* gA = grad_A + (long long)k * W;
+    float* gD = grad_D + (long long)k * W;
+    if (batch > 0) {
+      const float2* u = k > 0 || perm_on ? reinterpret_cast<const float2*>(mp_slot(stash, k, K, batch, W, perm_on))
+                                         : x2;
+      const float2* ak = A2 + (long long)k * N;
+      MP_TRY(mp::cfft_in(k == K - 1 ? reinterpret_cast<const float2*>(grad_y) : gbuf, nullptr, nullptr, Zg, batch, g,
+                         t.tw, t.seg, s));
+      MP_TRY(mp::cfft_in(u, ak, nullptr, Zh, batch, g, t.tw, t.seg, s));
+      MP_TRY(mp::cmid_bwd(Zh, Zg, D2 + (long long)k * N, batch, g, invN, reinterpret_cast<float2*>(part), s));
+      MP_TRY(mp::colsum_parts(part, batch, W, gD, nullptr, acc, s));
+      MP_TRY(mp::cifft_out(Zg, gh1, batch, g, t.tw, t.seg, s));
+      float2* gnext = reinterpret_cast<float2*>(k == 0 ? grad_x : reinterpret_cast<float*>(gbuf));
+      if (perm_on) {
+        const int32_t* pk = perm + (long long)k * N;
+        mp::PermTabs tk;
+        MP_TRY(mp_perm_tabs(perm, N, K, k, pt, &tk, s, 2));
+        MP_TRY(mp::cdA(gh1, u, ak, imgA, gu, batch, N, s));
+        MP_TRY(mp::cpermute_adjoint(gu, gnext, Zh, pk, tk, batch, N, s));  // Zh is free again
+      } else {
+        MP_TRY(mp::cdA(gh1, u, ak, imgA, gnext, batch, N, s));
+      }
+      MP_TRY(mp::colsum(reinterpret_cast<const float*>(imgA), batch, W, part, gA, nullptr, acc, s));
+    } else {
+      // no rows: zero (or unchanged, accumulating) parameter gradients
+      MP_TRY(mp::colsum(nullptr, 0, W, part, gD, nullptr, acc, s));
+      MP_TRY(mp::colsum(nullptr, 0, W, part, gA, nullptr, acc, s));
+    }
+  }
+  return ACDC_OK;
+}
+
 int mp_forward(const float* x, float* y, const float* A, const float* D, const float* bias, const int32_t* perm,
                int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, void* workspace, hipStream_t s) {
+  if (flags & kFlagComplex) return mp_cplx_forward(x, y, A, D, perm, batch, N, K, flags, saved, workspace, s);
   MpTabs t;
   int rc = get_mp_tables(N, &t);
   if (rc != ACDC_OK) return rc;
@@ -697,6 +826,9 @@ int mp_backward(const float* x, const float* grad_y, const float* A, const float
                 const int32_t* perm, const float* saved, float* grad_x, float* grad_A, float* grad_D,
                 float* grad_bias, int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved,
                 void* workspace, hipStream_t s) {
+  if (flags & kFlagComplex)
+    return mp_cplx_backward(x, grad_y, A, D, perm, saved, grad_x, grad_A, grad_D, batch, N, K, flags, have_saved,
+                            workspace, s);
   MpTabs t;
   int rc = get_mp_tables(N, &t);
   if (rc != ACDC_OK) return rc;
@@ -778,7 +910,7 @@ extern "C" int acdc_prepare(int32_t N, uint32_t flags) {
   if (!acdc_supported(N, flags)) return ACDC_ERR_UNSUPPORTED;
   if (use_multipass(N, flags)) {
     MpTabs t;
-    return get_mp_tables(N, &t);
+    return get_mp_tables((flags & kFlagComplex) ? 2 * N : N, &t);
   }
   const char* tab = nullptr;
   return get_table(N, (flags & kFlagComplex) != 0, &tab);

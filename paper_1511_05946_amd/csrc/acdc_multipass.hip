@@ -461,15 +461,18 @@ __device__ __forceinline__ void chunk_from_lds(float4* __restrict__ g4, const fl
 }
 
 // Forward pass A (or, with one chunk, the whole permutation with tab = perm):
-// out[b][cC + i] = in[b][cC + tab[cC + i]].
-__global__ __launch_bounds__(kPermThreads) void k_pt_a(const float* __restrict__ in, float* __restrict__ out,
+// out[b][cC + i] = in[b][cC + tab[cC + i]].  E is the element (float for
+// real rows, float2 for complex ones); N and C count elements.
+template <class E>
+__global__ __launch_bounds__(kPermThreads) void k_pt_a(const E* __restrict__ in, E* __restrict__ out,
                                                        const int* __restrict__ tab, long long N, int C, int nC,
                                                        long long work) {
+  constexpr int EW = int(sizeof(E) / sizeof(float));
   __shared__ float4 lds4[kPermChunk / 4];
-  const float* lds = reinterpret_cast<const float*>(lds4);
+  const E* lds = reinterpret_cast<const E*>(lds4);
   for (long long w = blockIdx.x; w < work; w += gridDim.x) {
     const long long b = w / nC, c = w % nC, base = b * N + c * C;
-    chunk_to_lds(lds4, reinterpret_cast<const float4*>(in + base), C);
+    chunk_to_lds(lds4, reinterpret_cast<const float4*>(in + base), C * EW);
     __syncthreads();
     const int* t = tab + c * C;
     if (C % kPermStep == 0) {
@@ -488,18 +491,20 @@ __global__ __launch_bounds__(kPermThreads) void k_pt_a(const float* __restrict__
 }
 
 // Forward pass B: out[b][dC + j] = L[locB[dC + j]], L[j] = tmp[b][gposB[dC + j]].
-__global__ __launch_bounds__(kPermThreads) void k_pt_b(const float* __restrict__ tmp, float* __restrict__ out,
+template <class E>
+__global__ __launch_bounds__(kPermThreads) void k_pt_b(const E* __restrict__ tmp, E* __restrict__ out,
                                                        const int* __restrict__ gposB, const int* __restrict__ locB,
                                                        long long N, int C, int nC, long long work) {
-  __shared__ float lds[kPermChunk];
+  __shared__ float4 lds4[kPermChunk / 4];
+  E* lds = reinterpret_cast<E*>(lds4);
   for (long long w = blockIdx.x; w < work; w += gridDim.x) {
     const long long b = w / nC, d = w % nC, base = b * N + d * C;
     const int* gp = gposB + d * C;
     const int* lc = locB + d * C;
-    const float* trow = tmp + b * N;
+    const E* trow = tmp + b * N;
     for (int j0 = threadIdx.x; j0 < C; j0 += kPermStep) {
       int id[kPermBatch];
-      float v[kPermBatch];
+      E v[kPermBatch];
 #pragma unroll
       for (int u = 0; u < kPermBatch; ++u) id[u] = gp[j0 + u * kPermThreads] & (N - 1);
 #pragma unroll
@@ -514,6 +519,52 @@ __global__ __launch_bounds__(kPermThreads) void k_pt_b(const float* __restrict__
       for (int u = 0; u < kPermBatch; ++u) id[u] = lc[j0 + u * kPermThreads] & (C - 1);
 #pragma unroll
       for (int u = 0; u < kPermBatch; ++u) out[base + j0 + u * kPermThreads] = lds[id[u]];
+    }
+    __syncthreads();
+  }
+}
+
+// The plain adjoint of pass B (or, with one chunk, of the whole
+// permutation: loc = perm, no gpos): L[loc[dC + j]] = in[b][dC + j], then
+// out[b][gpos[dC + j]] = L[j] (out[b][dC + j] without gpos).
+template <class E>
+__global__ __launch_bounds__(kPermThreads) void k_pt_btp(const E* __restrict__ in, E* __restrict__ out,
+                                                         const int* __restrict__ gpos, const int* __restrict__ loc,
+                                                         long long N, int C, int nC, long long work) {
+  constexpr int EW = int(sizeof(E) / sizeof(float));
+  __shared__ float4 lds4[kPermChunk / 4];
+  E* lds = reinterpret_cast<E*>(lds4);
+  for (long long w = blockIdx.x; w < work; w += gridDim.x) {
+    const long long b = w / nC, d = w % nC, base = b * N + d * C;
+    const int* lc = loc + d * C;
+    if (C % kPermStep == 0) {
+      for (int j0 = threadIdx.x; j0 < C; j0 += kPermStep) {
+        int id[kPermBatch];
+        E v[kPermBatch];
+#pragma unroll
+        for (int u = 0; u < kPermBatch; ++u) {
+          id[u] = lc[j0 + u * kPermThreads] & (C - 1);
+          v[u] = in[base + j0 + u * kPermThreads];
+        }
+#pragma unroll
+        for (int u = 0; u < kPermBatch; ++u) lds[id[u]] = v[u];
+      }
+    } else {
+      for (int j = threadIdx.x; j < C; j += kPermThreads) lds[lc[j] & (C - 1)] = in[base + j];
+    }
+    __syncthreads();
+    if (gpos) {
+      const int* gp = gpos + d * C;
+      E* orow = out + b * N;
+      for (int j0 = threadIdx.x; j0 < C; j0 += kPermStep) {
+        int id[kPermBatch];
+#pragma unroll
+        for (int u = 0; u < kPermBatch; ++u) id[u] = gp[j0 + u * kPermThreads] & (N - 1);
+#pragma unroll
+        for (int u = 0; u < kPermBatch; ++u) orow[id[u]] = lds[j0 + u * kPermThreads];
+      }
+    } else {
+      chunk_from_lds(reinterpret_cast<float4*>(out + base), lds4, C * EW);
     }
     __syncthreads();
   }
@@ -578,17 +629,19 @@ __global__ __launch_bounds__(kPermThreads) void k_pt_bt(const float* __restrict_
 
 // Backward, second pass (the adjoint of pass A): L[srcA[cC + i]] =
 // tmp[b][cC + i], then out[b][cC + i] = L[i].
-__global__ __launch_bounds__(kPermThreads) void k_pt_at(const float* __restrict__ tmp, float* __restrict__ out,
+template <class E>
+__global__ __launch_bounds__(kPermThreads) void k_pt_at(const E* __restrict__ tmp, E* __restrict__ out,
                                                         const int* __restrict__ srcA, long long N, int C, int nC,
                                                         long long work) {
+  constexpr int EW = int(sizeof(E) / sizeof(float));
   __shared__ float4 lds4[kPermChunk / 4];
-  float* lds = reinterpret_cast<float*>(lds4);
+  E* lds = reinterpret_cast<E*>(lds4);
   for (long long w = blockIdx.x; w < work; w += gridDim.x) {
     const long long b = w / nC, c = w % nC, base = b * N + c * C;
     const int* t = srcA + c * C;
     for (int i0 = threadIdx.x; i0 < C; i0 += kPermStep) {
       int id[kPermBatch];
-      float v[kPermBatch];
+      E v[kPermBatch];
 #pragma unroll
       for (int q = 0; q < kPermBatch; ++q) {
         id[q] = t[i0 + q * kPermThreads] & (C - 1);
@@ -598,8 +651,128 @@ __global__ __launch_bounds__(kPermThreads) void k_pt_at(const float* __restrict_
       for (int q = 0; q < kPermBatch; ++q) lds[id[q]] = v[q];
     }
     __syncthreads();
-    chunk_from_lds(reinterpret_cast<float4*>(out + base), lds4, C);
+    chunk_from_lds(reinterpret_cast<float4*>(out + base), lds4, C * EW);
     __syncthreads();
+  }
+}
+
+// ------------------------------------------------------- complex (AFDF) rows
+// A complex row is its own M = N point FFT input: no packing.  The steps
+// follow the fused complex kernels' arithmetic (u * a, X * d / N, the
+// unnormalised inverse; backward images g * conj(h) and gh1 * conj(u)).
+
+// First DIF pass (S = M) on u * a, read from the layer input out of place
+// (a may be null; with stash the input is stashed too).
+template <int R>
+__global__ __launch_bounds__(kThreads) void k_cdif_in(const float2* __restrict__ src, const float2* __restrict__ a,
+                                                      float2* __restrict__ stash, float2* __restrict__ Z, long long B,
+                                                      long long M, const float2* __restrict__ twM) {
+  const long long Q = M / R, total = B * Q;
+  for (long long i = gindex(); i < total; i += gstride()) {
+    const long long b = i / Q, n = i % Q;
+    float2 x[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const long long m = b * M + n + j * Q;
+      const float2 u = src[m];
+      if (stash) stash[m] = u;
+      x[j] = a ? cmul(u, a[n + j * Q]) : u;
+    }
+    Dft<R, false>::run(x);
+#pragma unroll
+    for (int r = 1; r < R; ++r) x[r] = cmul(x[r], twM[n * r]);
+#pragma unroll
+    for (int r = 0; r < R; ++r) Z[b * M + r * Q + n] = x[r];
+  }
+}
+
+// Last DIT pass (S = M), written out of place to the layer output.
+template <int R>
+__global__ __launch_bounds__(kThreads) void k_cdit_out(const float2* __restrict__ Z, float2* __restrict__ dst,
+                                                       long long B, long long M, const float2* __restrict__ twM) {
+  const long long Q = M / R, total = B * Q;
+  for (long long i = gindex(); i < total; i += gstride()) {
+    const long long b = i / Q, n = i % Q;
+    float2 y[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) y[r] = Z[b * M + r * Q + n];
+#pragma unroll
+    for (int r = 1; r < R; ++r) y[r] = cmulc(y[r], twM[n * r]);
+    Dft<R, true>::run(y);
+#pragma unroll
+    for (int j = 0; j < R; ++j) dst[b * M + n + j * Q] = y[j];
+  }
+}
+
+// Without DIF passes (one segment per row): Z = u * a (stashed), dst = Z.
+__global__ __launch_bounds__(kThreads) void k_cscale(const float2* __restrict__ src, const float2* __restrict__ a,
+                                                     float2* __restrict__ stash, float2* __restrict__ Z, long long B,
+                                                     long long M) {
+  const long long total = B * M;
+  for (long long i = gindex(); i < total; i += gstride()) {
+    const float2 u = src[i];
+    if (stash) stash[i] = u;
+    Z[i] = a ? cmul(u, a[i % M]) : u;
+  }
+}
+__global__ __launch_bounds__(kThreads) void k_ccopy(const float2* __restrict__ Z, float2* __restrict__ dst,
+                                                    long long total) {
+  for (long long i = gindex(); i < total; i += gstride()) dst[i] = Z[i];
+}
+
+// Spectrum index of storage position q (the inverse of pos()).
+__device__ __forceinline__ long long spec_index(const Geo& g, long long q) {
+  const long long S1 = g.M / g.R1;
+  const long long r1 = q / S1, rem = q % S1;
+  const long long r2 = rem / g.L, k2 = rem % g.L;
+  return r1 + (long long)g.R1 * (r2 + (long long)g.R2 * k2);
+}
+
+// Forward middle: X[k] *= d[k] / N, kColRows rows per thread and position.
+__global__ __launch_bounds__(kThreads) void k_cmid_fwd(float2* __restrict__ Z, const float2* __restrict__ d,
+                                                       long long B, Geo g, float invN) {
+  const long long M = g.M, P = (B + kColRows - 1) / kColRows, total = P * M;
+  for (long long i = gindex(); i < total; i += gstride()) {
+    const long long p = i / M, q = i % M;
+    const float2 dk = d[spec_index(g, q)];
+    const float2 w = make_float2(dk.x * invN, dk.y * invN);
+    const long long b0 = p * kColRows, b1 = b0 + kColRows < B ? b0 + kColRows : B;
+    for (long long b = b0; b < b1; ++b) Z[b * M + q] = cmul(Z[b * M + q], w);
+  }
+}
+
+// Backward middle: gh3 = FFT(g) / N, the dL/dd image gh3 * conj(h2) summed
+// over blocks of kColRows rows into part[p][k] (complex, spectrum order),
+// and g's spectrum replaced by gh3 * conj(d).
+__global__ __launch_bounds__(kThreads) void k_cmid_bwd(const float2* __restrict__ Zh, float2* __restrict__ Zg,
+                                                       const float2* __restrict__ d, long long B, Geo g, float invN,
+                                                       float2* __restrict__ part) {
+  const long long M = g.M, P = (B + kColRows - 1) / kColRows, total = P * M;
+  for (long long i = gindex(); i < total; i += gstride()) {
+    const long long p = i / M, q = i % M, k = spec_index(g, q);
+    const float2 dk = d[k];
+    float2 acc = make_float2(0.f, 0.f);
+    const long long b0 = p * kColRows, b1 = b0 + kColRows < B ? b0 + kColRows : B;
+    for (long long b = b0; b < b1; ++b) {
+      const float2 gz = Zg[b * M + q];
+      const float2 gh3 = make_float2(gz.x * invN, gz.y * invN);
+      const float2 img = cmulc(gh3, Zh[b * M + q]);
+      acc = make_float2(acc.x + img.x, acc.y + img.y);
+      Zg[b * M + q] = cmulc(gh3, dk);
+    }
+    part[p * M + k] = acc;
+  }
+}
+
+// The dL/da image gh1 * conj(u) and dL/du = gh1 * conj(a).
+__global__ __launch_bounds__(kThreads) void k_cdA(const float2* __restrict__ gh1, const float2* __restrict__ u,
+                                                  const float2* __restrict__ a, float2* __restrict__ imgA,
+                                                  float2* __restrict__ gu, long long B, long long N) {
+  const long long total = B * N;
+  for (long long i = gindex(); i < total; i += gstride()) {
+    const float2 gg = gh1[i];
+    imgA[i] = cmulc(gg, u[i]);
+    gu[i] = cmulc(gg, a[i % N]);
   }
 }
 
@@ -754,24 +927,25 @@ hipError_t dA(const float* gh1, const float* u, const float* a, bool mask, float
   return hipGetLastError();
 }
 
-PermGeo perm_geo(long long N) {
+PermGeo perm_geo(long long N, int ew) {
+  const long long cap = kPermChunk / ew;
   PermGeo p;
-  p.C = int(N < kPermChunk ? N : kPermChunk);
+  p.C = int(N < cap ? N : cap);
   p.nC = int(N / p.C);
   return p;
 }
 
-size_t perm_table_ints(long long N) {
-  const PermGeo p = perm_geo(N);
+size_t perm_table_ints(long long N, int ew) {
+  const PermGeo p = perm_geo(N, ew);
   if (p.nC == 1) return 0;
   return size_t(3 * N + 2 * (N / kThreads) * p.nC + 3LL * p.nC * p.nC);
 }
 
-PermTabs perm_tables_at(int* base, long long N) {
-  const PermGeo p = perm_geo(N);
+PermTabs perm_tables_at(int* base, long long N, int ew) {
+  const PermGeo p = perm_geo(N, ew);
   PermTabs t;
   if (p.nC == 1) return t;
-  t.stride = (long long)perm_table_ints(N);
+  t.stride = (long long)perm_table_ints(N, ew);
   const long long nb = N / kThreads, nn = (long long)p.nC * p.nC;
   t.srcA = base;
   t.gposB = t.srcA + N;
@@ -799,8 +973,8 @@ PermTabs perm_layer(const PermTabs& t, int l) {
   return r;
 }
 
-hipError_t perm_build(const int* perm, long long N, int layers, const PermTabs& t, hipStream_t s) {
-  const PermGeo p = perm_geo(N);
+hipError_t perm_build(const int* perm, long long N, int layers, const PermTabs& t, hipStream_t s, int ew) {
+  const PermGeo p = perm_geo(N, ew);
   if (p.nC == 1 || layers <= 0) return hipSuccess;
   const unsigned nb = unsigned(N / kThreads), nn = unsigned(p.nC * p.nC), L = unsigned(layers);
   hipLaunchKernelGGL(k_pt_count, dim3(nb, L), dim3(kThreads), 0, s, perm, N, p.C, p.nC, t.cntS, t.stride);
@@ -822,23 +996,23 @@ dim3 perm_grid(long long work) { return dim3(unsigned(work < 65536 ? (work < 1 ?
 
 hipError_t permute(const float* in, float* out, float* tmp, const int* perm, const PermTabs& t, long long B,
                    long long N, hipStream_t s) {
-  const PermGeo p = perm_geo(N);
+  const PermGeo p = perm_geo(N, 1);
   const long long work = B * p.nC;
   if (p.nC == 1) {
-    hipLaunchKernelGGL(k_pt_a, perm_grid(work), dim3(kPermThreads), 0, s, in, out, perm, N, p.C, p.nC, work);
+    hipLaunchKernelGGL(k_pt_a<float>, perm_grid(work), dim3(kPermThreads), 0, s, in, out, perm, N, p.C, p.nC, work);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(k_pt_a, perm_grid(work), dim3(kPermThreads), 0, s, in, tmp, t.srcA, N, p.C, p.nC, work);
+  hipLaunchKernelGGL(k_pt_a<float>, perm_grid(work), dim3(kPermThreads), 0, s, in, tmp, t.srcA, N, p.C, p.nC, work);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_pt_b, perm_grid(work), dim3(kPermThreads), 0, s, tmp, out, t.gposB, t.locB, N, p.C, p.nC,
+  hipLaunchKernelGGL(k_pt_b<float>, perm_grid(work), dim3(kPermThreads), 0, s, tmp, out, t.gposB, t.locB, N, p.C, p.nC,
                      work);
   return hipGetLastError();
 }
 
 hipError_t dA_permute(const float* gh1, const float* u, const float* a, bool mask, float* imgA, float* gnext,
                       float* tmp, const int* perm, const PermTabs& t, long long B, long long N, hipStream_t s) {
-  const PermGeo p = perm_geo(N);
+  const PermGeo p = perm_geo(N, 1);
   const long long work = B * p.nC;
   const int mk = mask ? 1 : 0;
   if (p.nC == 1) {
@@ -850,7 +1024,103 @@ hipError_t dA_permute(const float* gh1, const float* u, const float* a, bool mas
                      N, p.C, p.nC, work);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_pt_at, perm_grid(work), dim3(kPermThreads), 0, s, tmp, gnext, t.srcA, N, p.C, p.nC, work);
+  hipLaunchKernelGGL(k_pt_at<float>, perm_grid(work), dim3(kPermThreads), 0, s, tmp, gnext, t.srcA, N, p.C, p.nC, work);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------- complex launchers
+hipError_t cpermute(const float2* in, float2* out, float2* tmp, const int* perm, const PermTabs& t, long long B,
+                    long long N, hipStream_t s) {
+  const PermGeo p = perm_geo(N, 2);
+  const long long work = B * p.nC;
+  if (p.nC == 1) {
+    hipLaunchKernelGGL(k_pt_a<float2>, perm_grid(work), dim3(kPermThreads), 0, s, in, out, perm, N, p.C, p.nC, work);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(k_pt_a<float2>, perm_grid(work), dim3(kPermThreads), 0, s, in, tmp, t.srcA, N, p.C, p.nC, work);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pt_b<float2>, perm_grid(work), dim3(kPermThreads), 0, s, tmp, out, t.gposB, t.locB, N, p.C,
+                     p.nC, work);
+  return hipGetLastError();
+}
+
+hipError_t cpermute_adjoint(const float2* in, float2* out, float2* tmp, const int* perm, const PermTabs& t,
+                            long long B, long long N, hipStream_t s) {
+  const PermGeo p = perm_geo(N, 2);
+  const long long work = B * p.nC;
+  if (p.nC == 1) {
+    hipLaunchKernelGGL(k_pt_btp<float2>, perm_grid(work), dim3(kPermThreads), 0, s, in, out,
+                       static_cast<const int*>(nullptr), perm, N, p.C, p.nC, work);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(k_pt_btp<float2>, perm_grid(work), dim3(kPermThreads), 0, s, in, tmp, t.gposB, t.locB, N, p.C,
+                     p.nC, work);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pt_at<float2>, perm_grid(work), dim3(kPermThreads), 0, s, tmp, out, t.srcA, N, p.C, p.nC,
+                     work);
+  return hipGetLastError();
+}
+
+hipError_t cfft_in(const float2* src, const float2* a, float2* stash, float2* Z, long long B, const Geo& g,
+                   const float2* twM, const char* seg_tab, hipStream_t s) {
+  const dim3 block(kThreads);
+  if (g.R1 > 1) {
+    const dim3 grid = grid_for(B * (g.M / g.R1));
+    switch (g.R1) {
+      case 2: hipLaunchKernelGGL(k_cdif_in<2>, grid, block, 0, s, src, a, stash, Z, B, g.M, twM); break;
+      case 4: hipLaunchKernelGGL(k_cdif_in<4>, grid, block, 0, s, src, a, stash, Z, B, g.M, twM); break;
+      case 8: hipLaunchKernelGGL(k_cdif_in<8>, grid, block, 0, s, src, a, stash, Z, B, g.M, twM); break;
+      case 16: hipLaunchKernelGGL(k_cdif_in<16>, grid, block, 0, s, src, a, stash, Z, B, g.M, twM); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    hipLaunchKernelGGL(k_cscale, grid_for(B * g.M), block, 0, s, src, a, stash, Z, B, g.M);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (g.R2 > 1 && (e = dif(Z, B, g, g.M / g.R1, g.R2, twM, s)) != hipSuccess) return e;
+  return segments(Z, B * (g.M / g.L), g.L, false, seg_tab, s);
+}
+
+hipError_t cifft_out(float2* Z, float2* dst, long long B, const Geo& g, const float2* twM, const char* seg_tab,
+                     hipStream_t s) {
+  hipError_t e = segments(Z, B * (g.M / g.L), g.L, true, seg_tab, s);
+  if (e != hipSuccess) return e;
+  if (g.R2 > 1 && (e = dit(Z, B, g, g.M / g.R1, g.R2, twM, s)) != hipSuccess) return e;
+  const dim3 block(kThreads);
+  if (g.R1 > 1) {
+    const dim3 grid = grid_for(B * (g.M / g.R1));
+    switch (g.R1) {
+      case 2: hipLaunchKernelGGL(k_cdit_out<2>, grid, block, 0, s, Z, dst, B, g.M, twM); break;
+      case 4: hipLaunchKernelGGL(k_cdit_out<4>, grid, block, 0, s, Z, dst, B, g.M, twM); break;
+      case 8: hipLaunchKernelGGL(k_cdit_out<8>, grid, block, 0, s, Z, dst, B, g.M, twM); break;
+      case 16: hipLaunchKernelGGL(k_cdit_out<16>, grid, block, 0, s, Z, dst, B, g.M, twM); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    hipLaunchKernelGGL(k_ccopy, grid_for(B * g.M), block, 0, s, Z, dst, B * g.M);
+  }
+  return hipGetLastError();
+}
+
+hipError_t cmid_fwd(float2* Z, const float2* d, long long B, const Geo& g, float invN, hipStream_t s) {
+  const long long P = (B + kColRows - 1) / kColRows;
+  hipLaunchKernelGGL(k_cmid_fwd, grid_for(P * g.M), dim3(kThreads), 0, s, Z, d, B, g, invN);
+  return hipGetLastError();
+}
+
+hipError_t cmid_bwd(const float2* Zh, float2* Zg, const float2* d, long long B, const Geo& g, float invN,
+                    float2* part, hipStream_t s) {
+  const long long P = (B + kColRows - 1) / kColRows;
+  hipLaunchKernelGGL(k_cmid_bwd, grid_for(P * g.M), dim3(kThreads), 0, s, Zh, Zg, d, B, g, invN, part);
+  return hipGetLastError();
+}
+
+hipError_t cdA(const float2* gh1, const float2* u, const float2* a, float2* imgA, float2* gu, long long B,
+               long long N, hipStream_t s) {
+  hipLaunchKernelGGL(k_cdA, grid_for(B * N), dim3(kThreads), 0, s, gh1, u, a, imgA, gu, B, N);
   return hipGetLastError();
 }
 

@@ -112,12 +112,14 @@ struct PermTabs {
   int *cnt = nullptr, *off = nullptr, *lst = nullptr;      // [nC][nC]
   long long stride = 0;
 };
-PermGeo perm_geo(long long N);
-size_t perm_table_ints(long long N);                  // per layer; 0 with one chunk
-PermTabs perm_tables_at(int* base, long long N);      // carve layer 0's tables from base
-PermTabs perm_layer(const PermTabs& t, int l);        // layer l's tables
+// ew: floats per element (1 for real rows, 2 for complex ones); a chunk
+// holds kPermChunk / ew elements.
+PermGeo perm_geo(long long N, int ew = 1);
+size_t perm_table_ints(long long N, int ew = 1);              // per layer; 0 with one chunk
+PermTabs perm_tables_at(int* base, long long N, int ew = 1);  // carve layer 0's tables from base
+PermTabs perm_layer(const PermTabs& t, int l);                // layer l's tables
 // Tables of the permutations perm[0 .. layers-1][N] into layers 0 .. layers-1.
-hipError_t perm_build(const int* perm, long long N, int layers, const PermTabs& t, hipStream_t s);
+hipError_t perm_build(const int* perm, long long N, int layers, const PermTabs& t, hipStream_t s, int ew = 1);
 // out = in[perm] row by row; tmp is [B][N] scratch (unused with one chunk).
 hipError_t permute(const float* in, float* out, float* tmp, const int* perm, const PermTabs& t, long long B,
                    long long N, hipStream_t s);
@@ -125,6 +127,31 @@ hipError_t permute(const float* in, float* out, float* tmp, const int* perm, con
 // (mask: where u <= 0), imgA = u gm, gnext[b][perm[n]] = gm[b][n] a[n].
 hipError_t dA_permute(const float* gh1, const float* u, const float* a, bool mask, float* imgA, float* gnext,
                       float* tmp, const int* perm, const PermTabs& t, long long B, long long N, hipStream_t s);
+
+// Complex (AFDF) rows of N complex elements: M = N points per row, no
+// packing (acdc_multipass.hip).  The tables of cpermute come from
+// perm_build(..., ew = 2).
+hipError_t cpermute(const float2* in, float2* out, float2* tmp, const int* perm, const PermTabs& t, long long B,
+                    long long N, hipStream_t s);
+// out[b][perm[n]] = in[b][n] (the adjoint of cpermute, same tables)
+hipError_t cpermute_adjoint(const float2* in, float2* out, float2* tmp, const int* perm, const PermTabs& t,
+                            long long B, long long N, hipStream_t s);
+// Z = FFT(src * a) (spectrum in pos() order); src is stashed when stash is
+// set, a may be null.
+hipError_t cfft_in(const float2* src, const float2* a, float2* stash, float2* Z, long long B, const Geo& g,
+                   const float2* twM, const char* seg_tab, hipStream_t s);
+// dst = unnormalised inverse FFT of Z (Z is overwritten).
+hipError_t cifft_out(float2* Z, float2* dst, long long B, const Geo& g, const float2* twM, const char* seg_tab,
+                     hipStream_t s);
+// X[k] *= d[k] / N
+hipError_t cmid_fwd(float2* Z, const float2* d, long long B, const Geo& g, float invN, hipStream_t s);
+// gh3 = Zg / N; part[ceil(B / kColRows)][N] (complex) = row-block sums of
+// gh3 * conj(Zh); Zg = gh3 * conj(d)
+hipError_t cmid_bwd(const float2* Zh, float2* Zg, const float2* d, long long B, const Geo& g, float invN,
+                    float2* part, hipStream_t s);
+// imgA = gh1 * conj(u), gu = gh1 * conj(a)
+hipError_t cdA(const float2* gh1, const float2* u, const float2* a, float2* imgA, float2* gu, long long B,
+               long long N, hipStream_t s);
 // out[w] (+)= sum over rows of img[b][w] in row order (blocks of kColRows
 // rows, then the block sums in block order); with q, column w = 4e + j is
 // the quartet value j of entry e, stored to its DCT index.  W is a

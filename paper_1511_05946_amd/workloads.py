@@ -78,6 +78,9 @@ WORKLOADS = {
                                           FLAG_PERM | FLAG_RELU,
                                           "ACDC cascade N=65536 K=12 batch 512, fp32, permutations + ReLU "
                                           "(multi-pass)"),
+    "afdf_n65536_k8_perm": Workload("afdf_n65536_k8_perm", 65536, 8, 256, FLAG_PERM | FLAG_COMPLEX,
+                                    "complex AFDF cascade N=65536 K=8 batch 256, complex64, permutations "
+                                    "(multi-pass)"),
     # the headline cascade with the D-domain biases of Sec. 6.2
     "acdc_n4096_k12_perm_relu_bias": Workload("acdc_n4096_k12_perm_relu_bias", 4096, 12, 8192,
                                               FLAG_PERM | FLAG_RELU | FLAG_BIAS,

@@ -51,17 +51,21 @@ def test_supported_widths(L):
         assert L.acdc_supported(N, CX | PERM) == 1
     for N in (0, 2, 4, 6, 12, 100, 1000, 3072, 1 << 23):
         assert L.acdc_supported(N, 0) == 0
-    assert L.acdc_supported(32768, CX) == 0
-    # multi-pass: any power of two 256 ... 2^22, real layers only
+    # multi-pass: real rows of any power of two 256 ... 2^22, complex rows
+    # 256 ... 2^21 (the same FFT lengths)
     MP = 32
     for N in (65536, 1 << 19, 1 << 22):
         assert L.acdc_supported(N, PERM | RELU) == 1
-        assert L.acdc_supported(N, CX) == 0
+    for N in (32768, 65536, 1 << 21):
+        assert L.acdc_supported(N, CX | PERM) == 1
+    assert L.acdc_supported(1 << 22, CX) == 0
     for N in (256, 4096, 32768):
         assert L.acdc_supported(N, MP | PERM) == 1
+        assert L.acdc_supported(N, MP | CX | PERM) == 1
     for N in (128, 9216, 3072):
         assert L.acdc_supported(N, MP) == 0
-    assert L.acdc_supported(1024, MP | CX) == 0
+        assert L.acdc_supported(N, MP | CX) == 0
+    assert L.acdc_supported(65536, CX | RELU) == 0
     assert L.acdc_supported(9216, CX) == 0
     assert L.acdc_supported(4096, CX | RELU) == 0
     assert L.acdc_supported(4096, 8) == 1          # BIAS

@@ -140,7 +140,7 @@ def test_workloads_small_batch(acdc, name):
     w = WORKLOADS[name]
     B = {"acdc_n256_k1": 64, "acdc_n1024_k12_perm": 96, "acdc_n4096_k12_perm_relu": 48,
          "acdc_n9216_k16_perm_relu": 12, "afdf_n4096_k8_perm": 24, "acdc_n4096_k12_perm_relu_bias": 48,
-         "acdc_n65536_k12_perm_relu": 4}[name]
+         "acdc_n65536_k12_perm_relu": 4, "afdf_n65536_k8_perm": 4}[name]
     if name in ("acdc_n9216_k16_perm_relu", "acdc_n65536_k12_perm_relu"):
         # At N=9216, K=16 (and N=65536, K=12) nearly every row has some ReLU
         # decision within 1e-5 * rms of zero (the near-identity layers keep
@@ -419,6 +419,62 @@ def test_multipass_accumulate_and_determinism(acdc):
     acc = acdc.backward(xt, gyt, At, Dt, pt, flags | FLAG_ACCUMULATE, saved=s1, bias=bt, grads=grads)
     for g, p0, g0 in zip(acc[1:], pre, plain[1:]):
         assert np.array_equal(host(g), host(p0 + g0))
+
+
+# complex (AFDF) rows through the multi-pass path
+
+@pytest.mark.parametrize("N,K,B", [(32768, 2, 3), (65536, 2, 2), (1 << 20, 2, 2)])
+def test_multipass_complex_wide(acdc, N, K, B):
+    # past the fused complex cap (16384): 32768 (one radix-4 DIF pass, 4
+    # permutation chunks of 8192 complex), 65536 (radix 8), 2^20 (radix 16,
+    # then radix 8; 128 chunks)
+    run_case(acdc, N, K, B, CX | P, seed=N + 11)
+
+
+@pytest.mark.parametrize("N", [256, 4096, 16384])
+def test_multipass_complex_fused_widths(acdc, N):
+    # the fused complex widths forced through the multi-pass path (no DIF
+    # pass up to 8192)
+    run_case(acdc, N, 3, 21, CX | P | MP, seed=N + 13)
+
+
+@pytest.mark.parametrize("save", [True, False])
+def test_multipass_complex_first_layer_permutation_and_recompute(acdc, save):
+    run_case(acdc, 32768, 2, 3, CX | P, seed=77, save=save, perm0=True)
+    run_case(acdc, 32768, 1, 2, CX, seed=78, save=save)
+
+
+def test_multipass_complex_matches_fused_and_repeats(acdc):
+    import torch
+    N, K, B, flags = 4096, 4, 24, P
+    x, A, D, perm, gy = make_inputs(N, K, B, flags | CX, 79)
+    xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
+    yf, sf = acdc.forward(xt, At, Dt, pt, flags, save=True)
+    ym, sm = acdc.forward(xt, At, Dt, pt, flags | MP, save=True)
+    assert rel_err(host(ym), host(yf).astype(np.complex128)) < 1e-5
+    gf = acdc.backward(xt, gyt, At, Dt, pt, flags, saved=sf)
+    gm = acdc.backward(xt, gyt, At, Dt, pt, flags | MP, saved=sm)
+    for u, v in zip(gm[:3], gf[:3]):
+        assert rel_err(host(u), host(v).astype(np.complex128)) < 1e-5
+    again = acdc.backward(xt, gyt, At, Dt, pt, flags | MP, saved=None)
+    for u, v in zip(again[:3], gm[:3]):
+        assert np.array_equal(host(u), host(v))
+    pre = [torch.full_like(At, 0.25) for _ in range(2)]
+    grads = tuple(p.clone() for p in pre)
+    accd = acdc.backward(xt, gyt, At, Dt, pt, flags | MP | FLAG_ACCUMULATE, saved=sm, grads=grads)
+    for g, p0, g0 in zip(accd[1:3], pre, gm[1:3]):
+        assert np.array_equal(host(g), host(p0 + g0))
+
+
+def test_multipass_complex_empty_batch(acdc):
+    import torch
+    N, K = 32768, 2
+    A = torch.ones((K, N), dtype=torch.complex64, device="cuda")
+    x = torch.empty((0, N), dtype=torch.complex64, device="cuda")
+    y, _ = acdc.forward(x, A, A.clone(), None, 0)
+    assert y.shape == (0, N)
+    gx, gA, gD = acdc.backward(x, x.clone(), A, A.clone(), None, 0)
+    assert not host(gA).any() and not host(gD).any()
 
 
 def test_multipass_empty_batch(acdc):
