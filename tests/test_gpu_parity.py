@@ -352,6 +352,14 @@ def test_bias_autograd_wrapper(acdc):
     assert rel_err(host(bt.grad), rB) < TOL_REAL
 
 
+@pytest.mark.parametrize("N,K,flags", [(1024, 48, P), (512, 48, CX | P), (65536, 24, P | FLAG_MULTIPASS)])
+def test_deep_cascades(acdc, N, K, flags):
+    # K well past the workloads' 8-16 layers: stash slots, per-layer tables and
+    # the partial layout at depth (fused real and complex; multi-pass with all
+    # 24 layers' permutation tables built at once)
+    run_case(acdc, N, K, 5, flags, seed=N + K)
+
+
 # ------------------------------------------------------------ multi-pass path
 
 MP = FLAG_MULTIPASS
