@@ -181,6 +181,29 @@ def test_bias_workspace_sizes(L):
     assert L.acdc_supported(4096, CX | ACC) == 1
 
 
+def test_multipass_workspace_sizes(L):
+    MP = 32
+    B, N, K = 64, 65536, 4
+    rows_real, rows_cx = B * N * 4, B * N * 8  # bytes of one batch of rows
+    # forward: spectra and layer buffer, plus the permuted input with PERM
+    assert L.acdc_forward_workspace_bytes(B, N, K, PERM) >= 3 * rows_real
+    assert L.acdc_forward_workspace_bytes(B, N, K, CX | PERM) >= 3 * rows_cx
+    assert L.acdc_forward_workspace_bytes(B, N, K, CX) < L.acdc_forward_workspace_bytes(B, N, K, CX | PERM)
+    # backward: the h and g spectra (one batch each), dL/dv, the next g, the
+    # dL/da image (+ dL/du before the complex adjoint permutation), and the
+    # recompute stash when nothing is saved
+    assert L.acdc_backward_workspace_bytes(B, N, K, PERM, 1) >= 5 * rows_real
+    assert L.acdc_backward_workspace_bytes(B, N, K, CX | PERM, 1) >= 6 * rows_cx
+    saved = L.acdc_saved_bytes(B, N, K, CX | PERM)
+    assert saved == K * rows_cx
+    assert (L.acdc_backward_workspace_bytes(B, N, K, CX | PERM, 0)
+            >= L.acdc_backward_workspace_bytes(B, N, K, CX | PERM, 1) + saved)
+    # forcing the multi-pass path at a fused width needs more workspace
+    assert L.acdc_forward_workspace_bytes(B, 4096, K, CX | PERM | MP) > L.acdc_forward_workspace_bytes(B, 4096, K, CX | PERM)
+    # unsupported: complex rows past 2^21
+    assert L.acdc_forward_workspace_bytes(B, 1 << 22, K, CX) == 0
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
     monkeypatch.setattr(_lib, "_lib", None)
