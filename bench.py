@@ -79,6 +79,7 @@ def cpu_baseline(w, seed: int, budget_s: float = 12.0, max_rows: int = 512):
         rows = sl.stop
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     return {"value": rows * w.K / t_total, "unit": UNIT, "cores": int(threads), "kind": "oracle",
+            "blas_threads": int(threads), "affinity_cores": len(os.sched_getaffinity(0)),
             "sample": f"{rows} of {w.batch} rows, full N={w.N}, K={w.K}, fwd + bwd, fp64 oracle "
                       + ("(O(N^2) dense matrices" if w.N <= O.DENSE_MAX else "(library DCT/FFT above N=8192")
                       + f"), {t_total:.1f} s"}
@@ -96,6 +97,9 @@ def main():
                     help="run the layers through the multi-pass (HBM) path instead of the fused kernels")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--flush-mb", type=int, default=0,
+                    help="write this many MB between steps (evicts the 256 MB Infinity Cache); value and "
+                         "ms_per_step then come from per-step HIP events, without the flush")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 256 MiB device copy (known bytes) so that profiler "
                          "byte counters can be scaled against it")
@@ -134,8 +138,9 @@ def main():
     fl = w.flags & ~acdc.FLAG_COMPLEX
     if args.multipass:
         fl |= acdc.FLAG_MULTIPASS
-    # the fused kernels cover ACDC widths up to 32768; wider rows run multi-pass
-    multipass = not w.complex and (args.multipass or w.N > 32768)
+    # the fused kernels cover ACDC widths up to 32768 and AFDF up to 16384;
+    # wider rows run multi-pass
+    multipass = args.multipass or w.N > (16384 if w.complex else 32768)
     acdc.prepare(w.N, fl | (acdc.FLAG_COMPLEX if w.complex else 0))
     y = torch.empty_like(xt)
     saved = acdc.alloc_saved(xt, w.K, fl)
@@ -151,23 +156,31 @@ def main():
         step()
     torch.cuda.synchronize()
 
+    flush = torch.empty((args.flush_mb << 20) // 4, dtype=torch.float32, device=dev) if args.flush_mb > 0 else None
     L = lib()
     L.acdc_profile_enable(1)
     ms = (ctypes.c_double * 3)()
     cnt = (ctypes.c_int64 * 3)()
     L.acdc_profile_read(ms, cnt)  # clear
+    # per-step HIP events on the stream the library launches on (torch's current one)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
+        if flush is not None:
+            flush.fill_(float(i))
+        ev[i][0].record()
         step()
+        ev[i][1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     rc = L.acdc_profile_read(ms, cnt)
     L.acdc_profile_enable(0)
     if rc != 0:
         raise RuntimeError(f"acdc_profile_read failed: {rc}")
+    step_ms = sorted(a.elapsed_time(b) for a, b in ev)
 
-    ms_step = (t1 - t0) * 1e3 / args.steps
+    ms_step = sum(step_ms) / args.steps if flush is not None else (t1 - t0) * 1e3 / args.steps
     value = w.batch * w.K / (ms_step * 1e-3)
     kern = {name: {"avg_ms": ms[i] / max(cnt[i], 1), "launches": int(cnt[i])}
             for i, name in enumerate(("forward", "backward", "reduce"))}
@@ -203,6 +216,9 @@ def main():
         "step_roofline_frac": round(step_flops / (ms_step * 1e-3) / 1e12 / PEAK_FP32_TFLOPS, 4),
         "kernels": {k: {"avg_ms": round(v["avg_ms"], 4), "launches": v["launches"]} for k, v in kern.items()},
         "forward_tflops": round(fwd_achieved, 3),
+        "step_ms_median": round(step_ms[len(step_ms) // 2], 4),
+        "step_ms_min": round(step_ms[0], 4),
+        "flush_mb_between_steps": args.flush_mb,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.seed)
