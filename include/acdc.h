@@ -64,9 +64,17 @@
  * goes through HBM in several launches, with hand-written passes): ACDC
  * 256 ... 2^22, AFDF 256 ... 2^21.  That path serves the widths past the
  * fused ones, and any such width with ACDC_FLAG_MULTIPASS; it needs more
- * workspace (see the *_workspace_bytes calls), and its permutation indices
- * are read modulo N.
+ * workspace (see the *_workspace_size calls).
  * Batch sizes from 0 upward; K >= 1.
+ *
+ * Permutations.  Each row perm[k] must be a permutation of 0..N-1.  The
+ * library does not check this (it would cost a pass over perm and a host
+ * synchronisation per call); a row that is not a permutation gives
+ * unspecified values in y, grad_x and the parameter gradients but never an
+ * access outside the caller's buffers and the kernels' own LDS: the fused
+ * kernels use the entries only as LDS indices within the workgroup, and the
+ * multi-pass path reads every entry modulo N (the tables it builds from perm
+ * are masked into range).
  */
 #ifndef ACDC_H_
 #define ACDC_H_
@@ -115,7 +123,7 @@ size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
  * buffer and, with ACDC_FLAG_PERM, a buffer for the permuted layer input and
  * the permutation tables that each call builds on the device from perm).
  * Host only. */
-size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
+size_t acdc_forward_workspace_size(int64_t batch, int32_t N, int32_t K, uint32_t flags);
 
 /* Bytes of workspace acdc_backward needs: per-workgroup partial sums of the
  * parameter gradients, the per-layer quartet coefficients, the batch sums
@@ -123,7 +131,7 @@ size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_
  * acdc_saved_bytes(...) is not 0 -- room to recompute the layer inputs (the
  * paper's recompute policy, Sec. 5.3).  The multi-pass path adds its
  * spectra, layer buffers, row-block sums and permutation tables. */
-size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags, int have_saved);
+size_t acdc_backward_workspace_size(int64_t batch, int32_t N, int32_t K, uint32_t flags, int have_saved);
 
 /* Forward cascade: y = cascade(x).  `bias` is read with ACDC_FLAG_BIAS and
  * ignored (may be null) otherwise; `perm` likewise with ACDC_FLAG_PERM.  If

@@ -6,7 +6,8 @@ TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 tables or constants with that path.
 
 Everything is computed in float64 (complex128 for the AFDF variant) with dense
-O(N^2) matrices built directly from their definitions (up to N = DENSE_MAX;
+O(N^2) matrices built directly from their definitions (real rows up to
+N = DENSE_MAX_REAL = 16384, complex rows up to DENSE_MAX_COMPLEX = 8192;
 wider rows apply the same matrices through scipy's / numpy's transforms,
 which the pins equate with the dense matrices).  There is no blocking and no
 fusion: each function follows the paper's statement of the layer in the
@@ -36,6 +37,13 @@ Readings of the paper used here (each listed in the design doc):
 * Batch reduction of dL/da, dL/dd: sum over rows (Sec. 4 gives per-example
   derivatives).
 * ReLU derivative at 0 is 0 (strict v > 0).
+* ReLU decisions may be given as an input (``masks``): where a pre-ReLU value
+  lies within rounding of zero, an fp32 evaluation of the same cascade may
+  legitimately decide the other way, and every later value of that row then
+  follows that decision.  With ``masks`` the oracle takes those decisions and
+  computes everything else itself; callers check first that the decisions
+  they pass differ from the oracle's own only at such near-ties
+  (``mask_disagreements``).
 * AFDF: F[n, k] = exp(-2 pi i n k / N), F^{-1} its exact inverse conj(F)/N
   (Sec. 3); complex gradients follow the PyTorch convention
   grad = dL/dRe + i dL/dIm, i.e. g_x = g_y W^H.
@@ -48,6 +56,8 @@ torch autograd).
 
 from __future__ import annotations
 
+import functools
+
 import numpy as np
 
 FLAG_PERM = 1
@@ -57,35 +67,59 @@ FLAG_COMPLEX = 4
 _CHUNK = 512  # rows per dense product, only to bound memory
 
 
+def _frozen(a: np.ndarray) -> np.ndarray:
+    a.flags.writeable = False
+    return a
+
+
+@functools.lru_cache(maxsize=4)
 def dct_matrix(N: int) -> np.ndarray:
     """Orthonormal DCT-II matrix C[n, k] (Sec. 4, definition of c_nk).
 
     c_nk = sqrt(2/N) * eps_k * cos(pi (2n+1) k / (2N)),  n, k in [0, N),
     eps_0 = 1/sqrt(2), eps_k = 1 otherwise.  Row vector x maps to x @ C.
+    The integer argument (2n+1) k is kept reduced mod 4N (the cosine's
+    period), so the angle is exact for wide rows, and the cosine is taken
+    once for each of the 4N residues.  Row n + 1's arguments are row n's
+    plus 2k.  (Cached: the result is read-only.)
     """
-    n = np.arange(N, dtype=np.float64)[:, None]
-    k = np.arange(N, dtype=np.float64)[None, :]
+    k = np.arange(N, dtype=np.int64)
     eps = np.where(k == 0, 1.0 / np.sqrt(2.0), 1.0)
-    return np.sqrt(2.0 / N) * eps * np.cos(np.pi * (2.0 * n + 1.0) * k / (2.0 * N))
+    cos_of_residue = np.cos(np.pi * np.arange(4 * N, dtype=np.float64) / (2.0 * N))
+    C = np.empty((N, N))
+    arg = k.copy()                       # (2n+1) k mod 4N for n = 0
+    for n in range(N):
+        C[n] = cos_of_residue[arg]
+        arg += 2 * k                     # < 6N: one subtraction reduces it
+        np.subtract(arg, 4 * N, out=arg, where=arg >= 4 * N)
+    C *= np.sqrt(2.0 / N) * eps
+    return _frozen(C)
 
 
+@functools.lru_cache(maxsize=2)
 def dft_matrix(N: int) -> np.ndarray:
     """Unnormalised DFT matrix F[n, k] = exp(-2 pi i n k / N) (Sec. 3, AFDF).
 
     The exponent is reduced mod N in integers before scaling so the angle is
-    exact for large N.
+    exact for large N.  (Cached: the result is read-only.)
     """
     n = np.arange(N, dtype=np.int64)[:, None]
     k = np.arange(N, dtype=np.int64)[None, :]
-    return np.exp(-2j * np.pi * ((n * k) % N).astype(np.float64) / N)
+    return _frozen(np.exp(-2j * np.pi * ((n * k) % N).astype(np.float64) / N))
 
 
-# Widths up to this use the dense matrices above; wider rows apply the same
+# Widths up to these use the dense matrices above; wider rows apply the same
 # matrices through the library routines that tests/test_oracle.py equates
-# with them (scipy's orthonormal DCT-II / DCT-III, numpy's FFT), since an
-# N x N matrix no longer fits comfortably in memory (16384^2 complex doubles
-# take 4.3 GB).
-DENSE_MAX = 8192
+# with them (scipy's orthonormal DCT-II / DCT-III, numpy's FFT).  A real
+# 16384^2 matrix takes 2.1 GB in float64; a complex one of that width would
+# take 4.3 GB, so complex rows switch earlier.
+DENSE_MAX_REAL = 16384
+DENSE_MAX_COMPLEX = 8192
+
+
+def dense_limit(complex_: bool) -> int:
+    """Widest row the dense matrices serve (real or complex rows)."""
+    return DENSE_MAX_COMPLEX if complex_ else DENSE_MAX_REAL
 
 
 class _LibraryTransform:
@@ -109,14 +143,14 @@ def _transforms(N: int, complex_: bool):
     ACDC (Sec. 4): T = C, Tinv = C^T (C orthogonal), so Tinv_H = C, T_H = C^T.
     AFDF (Sec. 3): T = F, Tinv = conj(F) / N, so Tinv_H = F / N, T_H = conj(F).
     """
-    if N <= DENSE_MAX:
+    if N <= dense_limit(complex_):
         if complex_:
             F = dft_matrix(N)
             T, Tinv = F, np.conj(F) / N
-        else:
-            C = dct_matrix(N)
-            T, Tinv = C, C.T.copy()
-        return T, Tinv, np.conj(Tinv).T, np.conj(T).T
+            return T, Tinv, np.conj(Tinv).T, np.conj(T).T
+        # real: C^T is the exact inverse; views, no copies of a wide matrix
+        C = dct_matrix(N)
+        return C, C.T, C, C.T
     import scipy.fft
     if complex_:
         return (_LibraryTransform(lambda h: np.fft.fft(h, axis=-1)),
@@ -150,7 +184,19 @@ def _check(x, A, D, perm, flags, B=None):
     return x.astype(dt), A.astype(dt), D.astype(dt), perm, Bd
 
 
-def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False, B=None):
+def _check_masks(masks, flags, K, shape):
+    """ReLU decisions given as input: [K-1, B, N] bool (layer k's v_k > 0)."""
+    if masks is None:
+        return None
+    if not flags & FLAG_RELU:
+        raise ValueError("masks are ReLU decisions: they need FLAG_RELU")
+    m = np.asarray(masks)
+    if m.dtype != np.bool_ or m.shape != (K - 1,) + tuple(shape):
+        raise ValueError("masks must be bool [K-1, B, N]")
+    return m
+
+
+def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False, B=None, masks=None):
     """Cascade forward y = x prod_k [P_k] A_k T D_k T^{-1}  (eq. for AFDF_K in
     Sec. 3, made real in Sec. 4 as ACDC_K; permutations, ReLU and the D-domain
     biases as in Sec. 6.2).
@@ -163,11 +209,16 @@ def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False, B=None):
         v_k = h3 @ Tinv              (x A C D C^{-1})
         z   = max(v_k, 0)            (if RELU and k < K-1) else v_k
 
+    With ``masks`` ([K-1, B, N] bool) the ReLU of layer k keeps v_k where
+    masks[k] is true and zeroes it elsewhere, instead of deciding v_k > 0
+    itself (the decisions of another evaluation; see the module docstring).
+
     Returns y, or (y, cache) with cache = dict(u=[...], h2=[...], v=[...]) of
     per-layer float64 arrays when ``keep`` is true.
     """
     x, A, D, perm, Bd = _check(x, A, D, perm, flags, B)
     K, N = A.shape
+    masks = _check_masks(masks, flags, K, x.shape)
     T, Tinv, _, _ = _transforms(N, bool(flags & FLAG_COMPLEX))
     relu = bool(flags & FLAG_RELU)
     y = np.empty_like(x)
@@ -182,7 +233,10 @@ def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False, B=None):
             h2 = h1 @ T
             h3 = h2 * D[k] + Bd[k]
             v = h3 @ Tinv
-            z = np.maximum(v, 0.0) if (relu and k < K - 1) else v
+            if relu and k < K - 1:
+                z = np.maximum(v, 0.0) if masks is None else np.where(masks[k][r0:r0 + _CHUNK], v, 0.0)
+            else:
+                z = v
             if keep:
                 cache["u"][k][r0:r0 + _CHUNK] = u
                 cache["h2"][k][r0:r0 + _CHUNK] = h2
@@ -191,7 +245,7 @@ def forward(x, A, D, perm=None, flags: int = 0, keep: bool = False, B=None):
     return (y, cache) if keep else y
 
 
-def backward(x, grad_y, A, D, perm=None, flags: int = 0, B=None):
+def backward(x, grad_y, A, D, perm=None, flags: int = 0, B=None, masks=None):
     """Analytic backward of the cascade (Sec. 4 derivative block, applied
     layer by layer in reverse; ReLU and permutation steps of Sec. 6.2).
 
@@ -210,12 +264,16 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0, B=None):
         gh3 = g @ F / N, dd_k = sum conj(h2_k) gh3, gh1 = (gh3 conj(d_k)) @ conj(F),
         da_k = sum conj(u_k) gh1, gu = gh1 conj(a_k).
 
+    With ``masks`` the ReLU decisions (v_k > 0 above) are taken from masks[k]
+    instead, in the forward it recomputes and in the mask applied to g.
+
     Returns (grad_x [B,N], grad_A [K,N], grad_D [K,N]), and grad_B [K,N] as a
     fourth element when B is given; the parameter gradients are sums over the
     batch.  (B changes the stored h2 only through the forward values the
     backward recomputes: the ReLU masks of a biased cascade.)
     """
     x, A, D, perm, Bd = _check(x, A, D, perm, flags, B)
+    masks = _check_masks(masks, flags, A.shape[0] if np.ndim(A) == 2 else 0, x.shape)
     cplx = bool(flags & FLAG_COMPLEX)
     gy = np.asarray(grad_y).astype(np.complex128 if cplx else np.float64)
     if gy.shape != x.shape:
@@ -232,11 +290,12 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0, B=None):
     grad_B = np.zeros_like(D)
     for r0 in range(0, x.shape[0], _CHUNK):
         xs = x[r0:r0 + _CHUNK]
-        _, cache = forward(xs, A, D, perm, flags, keep=True, B=Bd)
+        ms = None if masks is None else masks[:, r0:r0 + _CHUNK]
+        _, cache = forward(xs, A, D, perm, flags, keep=True, B=Bd, masks=ms)
         g = gy[r0:r0 + _CHUNK]
         for k in range(K - 1, -1, -1):
             if relu and k < K - 1:
-                g = g * (cache["v"][k] > 0.0)
+                g = g * (cache["v"][k] > 0.0 if ms is None else ms[k])
             gh3 = g @ Tinv_H
             grad_B[k] += np.sum(gh3, axis=0)
             h2 = cache["h2"][k]
@@ -254,6 +313,27 @@ def backward(x, grad_y, A, D, perm=None, flags: int = 0, B=None):
     if B is not None:
         return grad_x, grad_A, grad_D, grad_B
     return grad_x, grad_A, grad_D
+
+
+def relu_decisions(cache, K: int) -> np.ndarray:
+    """The oracle's own ReLU decisions v_k > 0, k < K-1, from a forward
+    cache: [K-1, B, N] bool."""
+    B, N = cache["v"][0].shape
+    return np.array([cache["v"][k] > 0.0 for k in range(K - 1)], dtype=bool).reshape(K - 1, B, N)
+
+
+def mask_disagreements(masks, cache, K: int, band: float) -> int:
+    """Count the decisions in ``masks`` that differ from the oracle's own
+    (forward cache computed with those masks) at a pre-ReLU value outside the
+    near-tie band |v_k| < band * rms(v_k row).  Zero means every differing
+    decision is one that rounding may legitimately take either way."""
+    bad = 0
+    for k in range(K - 1):
+        v = cache["v"][k]
+        rms = np.sqrt(np.mean(v * v, axis=1, keepdims=True))
+        differ = np.asarray(masks[k]) != (v > 0.0)
+        bad += int(np.count_nonzero(differ & (np.abs(v) >= band * rms)))
+    return bad
 
 
 def layer_matrix(a, d, complex_: bool = False) -> np.ndarray:

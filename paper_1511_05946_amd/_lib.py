@@ -22,8 +22,8 @@ SIGNATURES = {
     "acdc_supported": (ctypes.c_int, [_I32, _U32]),
     "acdc_prepare": (ctypes.c_int, [_I32, _U32]),
     "acdc_saved_bytes": (_SZ, [_I64, _I32, _I32, _U32]),
-    "acdc_forward_workspace_bytes": (_SZ, [_I64, _I32, _I32, _U32]),
-    "acdc_backward_workspace_bytes": (_SZ, [_I64, _I32, _I32, _U32, ctypes.c_int]),
+    "acdc_forward_workspace_size": (_SZ, [_I64, _I32, _I32, _U32]),
+    "acdc_backward_workspace_size": (_SZ, [_I64, _I32, _I32, _U32, ctypes.c_int]),
     "acdc_forward": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _I64, _I32, _I32, _U32, _P, _SZ, _P, _SZ, _P]),
     "acdc_backward": (ctypes.c_int,
                       [_P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P, _P, _P, _I64, _I32, _I32, _U32, _P, _SZ, _P]),

@@ -921,13 +921,13 @@ extern "C" size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t
   return saved_floats(batch, N, K, flags) * sizeof(float);
 }
 
-extern "C" size_t acdc_forward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
+extern "C" size_t acdc_forward_workspace_size(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
   if (check_common(batch, N, K, flags) != ACDC_OK) return 0;
   if (use_multipass(N, flags)) return mp_fwd_ws(batch, N, K, flags).total;
   return fwd_ws(N, K, flags);
 }
 
-extern "C" size_t acdc_backward_workspace_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags,
+extern "C" size_t acdc_backward_workspace_size(int64_t batch, int32_t N, int32_t K, uint32_t flags,
                                                 int have_saved) {
   if (check_common(batch, N, K, flags) != ACDC_OK) return 0;
   const bool hs = have_saved != 0 || saved_layers(K, flags) == 0;

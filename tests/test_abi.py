@@ -32,7 +32,7 @@ def declared_functions():
 
 def test_header_declares_expected_entry_points():
     names = declared_functions()
-    for n in ("acdc_forward", "acdc_backward", "acdc_backward_workspace_bytes", "acdc_prepare",
+    for n in ("acdc_forward", "acdc_backward", "acdc_backward_workspace_size", "acdc_prepare",
               "acdc_status_string", "acdc_last_hip_error", "acdc_supported"):
         assert n in names
 
@@ -84,13 +84,13 @@ def test_sizes(L):
     assert L.acdc_saved_bytes(10, 64, 1, 0) == 0
     assert L.acdc_saved_bytes(10, 64, 1, PERM) == 10 * 64 * 4
     assert L.acdc_saved_bytes(10, 64, 3, CX) == 2 * 10 * 64 * 8
-    ws_saved = L.acdc_backward_workspace_bytes(8192, 4096, 12, PERM | RELU, 1)
-    ws_recompute = L.acdc_backward_workspace_bytes(8192, 4096, 12, PERM | RELU, 0)
+    ws_saved = L.acdc_backward_workspace_size(8192, 4096, 12, PERM | RELU, 1)
+    ws_recompute = L.acdc_backward_workspace_size(8192, 4096, 12, PERM | RELU, 0)
     assert ws_saved > 0 and ws_recompute >= ws_saved + 12 * 8192 * 4096 * 4
-    assert L.acdc_forward_workspace_bytes(8192, 4096, 12, 0) > 0
-    assert L.acdc_forward_workspace_bytes(10, 4096, 12, CX) == 0
+    assert L.acdc_forward_workspace_size(8192, 4096, 12, 0) > 0
+    assert L.acdc_forward_workspace_size(10, 4096, 12, CX) == 0
     # invalid combinations report 0
-    assert L.acdc_backward_workspace_bytes(8, 100, 2, 0, 1) == 0
+    assert L.acdc_backward_workspace_size(8, 100, 2, 0, 1) == 0
     assert L.acdc_saved_bytes(-1, 64, 2, 0) == 0
 
 
@@ -167,13 +167,13 @@ def test_backward_rejects_bad_arguments(L):
     need = L.acdc_saved_bytes(4, 64, 2, 0)
     assert bwd(saved=p(11), sb=need - 4) == EWS   # saved buffer smaller than its layout
     # the bias gradient needs workspace even for an empty batch
-    assert L.acdc_backward_workspace_bytes(0, 64, 2, BIAS, 1) > 0
+    assert L.acdc_backward_workspace_size(0, 64, 2, BIAS, 1) > 0
     assert bwd(B=0, flags=BIAS, b=b, gb=gb, ws=None) == EWS
 
 
 def test_bias_workspace_sizes(L):
-    plain = L.acdc_backward_workspace_bytes(8192, 4096, 12, PERM | RELU, 1)
-    biased = L.acdc_backward_workspace_bytes(8192, 4096, 12, PERM | RELU | BIAS, 1)
+    plain = L.acdc_backward_workspace_size(8192, 4096, 12, PERM | RELU, 1)
+    biased = L.acdc_backward_workspace_size(8192, 4096, 12, PERM | RELU | BIAS, 1)
     # one more N-float partial per tile and layer, plus the [K, N] batch sums
     assert biased >= plain + 12 * 4096 * 4
     assert L.acdc_supported(4096, PERM | RELU | BIAS | ACC) == 1
@@ -186,22 +186,22 @@ def test_multipass_workspace_sizes(L):
     B, N, K = 64, 65536, 4
     rows_real, rows_cx = B * N * 4, B * N * 8  # bytes of one batch of rows
     # forward: spectra and layer buffer, plus the permuted input with PERM
-    assert L.acdc_forward_workspace_bytes(B, N, K, PERM) >= 3 * rows_real
-    assert L.acdc_forward_workspace_bytes(B, N, K, CX | PERM) >= 3 * rows_cx
-    assert L.acdc_forward_workspace_bytes(B, N, K, CX) < L.acdc_forward_workspace_bytes(B, N, K, CX | PERM)
+    assert L.acdc_forward_workspace_size(B, N, K, PERM) >= 3 * rows_real
+    assert L.acdc_forward_workspace_size(B, N, K, CX | PERM) >= 3 * rows_cx
+    assert L.acdc_forward_workspace_size(B, N, K, CX) < L.acdc_forward_workspace_size(B, N, K, CX | PERM)
     # backward: the h and g spectra (one batch each), dL/dv, the next g, the
     # dL/da image (+ dL/du before the complex adjoint permutation), and the
     # recompute stash when nothing is saved
-    assert L.acdc_backward_workspace_bytes(B, N, K, PERM, 1) >= 5 * rows_real
-    assert L.acdc_backward_workspace_bytes(B, N, K, CX | PERM, 1) >= 6 * rows_cx
+    assert L.acdc_backward_workspace_size(B, N, K, PERM, 1) >= 5 * rows_real
+    assert L.acdc_backward_workspace_size(B, N, K, CX | PERM, 1) >= 6 * rows_cx
     saved = L.acdc_saved_bytes(B, N, K, CX | PERM)
     assert saved == K * rows_cx
-    assert (L.acdc_backward_workspace_bytes(B, N, K, CX | PERM, 0)
-            >= L.acdc_backward_workspace_bytes(B, N, K, CX | PERM, 1) + saved)
+    assert (L.acdc_backward_workspace_size(B, N, K, CX | PERM, 0)
+            >= L.acdc_backward_workspace_size(B, N, K, CX | PERM, 1) + saved)
     # forcing the multi-pass path at a fused width needs more workspace
-    assert L.acdc_forward_workspace_bytes(B, 4096, K, CX | PERM | MP) > L.acdc_forward_workspace_bytes(B, 4096, K, CX | PERM)
+    assert L.acdc_forward_workspace_size(B, 4096, K, CX | PERM | MP) > L.acdc_forward_workspace_size(B, 4096, K, CX | PERM)
     # unsupported: complex rows past 2^21
-    assert L.acdc_forward_workspace_bytes(B, 1 << 22, K, CX) == 0
+    assert L.acdc_forward_workspace_size(B, 1 << 22, K, CX) == 0
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
@@ -209,3 +209,42 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_lib, "_lib", None)
     with pytest.raises(_lib.LibraryMissing):
         _lib.lib()
+
+
+def test_binding_checks_shapes_before_any_library_call(L):
+    # The library takes raw pointers: a tensor of the wrong shape must be
+    # rejected by the binding (ValueError) before it reaches acdc_forward /
+    # acdc_backward.  CPU tensors suffice, since shapes are checked first.
+    torch = pytest.importorskip("torch")
+    import paper_1511_05946_amd.acdc as acdc
+    B, N, K = 3, 64, 2
+    x = torch.zeros(B, N)
+    A = torch.ones(K, N)
+    perm = torch.arange(N, dtype=torch.int32).repeat(K, 1)
+    bad = {
+        "A width": dict(A=torch.ones(K, N + 4)),
+        "D": dict(D=torch.ones(K + 1, N)),
+        "perm": dict(perm=torch.arange(N - 4, dtype=torch.int32).repeat(K, 1)),
+        "bias": dict(bias=torch.zeros(K, N - 4)),
+        "out": dict(out=torch.zeros(B + 1, N)),
+        "saved": dict(saved=torch.zeros(5)),
+    }
+    for what, kw in bad.items():
+        args = dict(x=x, A=A, D=A.clone(), perm=perm, flags=PERM)
+        args.update(kw)
+        with pytest.raises(ValueError):
+            acdc.forward(**args)
+    gbad = {
+        "grad_y": dict(grad_y=torch.zeros(B, N + 4)),
+        "grad_x": dict(out=torch.zeros(B - 1, N)),
+        "grad_A": dict(grads=(torch.zeros(K, N - 4), torch.zeros(K, N))),
+        "grad_D": dict(grads=(torch.zeros(K, N), torch.zeros(K - 1, N))),
+        "grads arity": dict(grads=(torch.zeros(K, N),)),
+        "grad_bias": dict(bias=torch.zeros(K, N), grads=(torch.zeros(K, N), torch.zeros(K, N), torch.zeros(K, 1))),
+        "perm": dict(perm=torch.zeros(K, N + 4, dtype=torch.int32)),
+    }
+    for what, kw in gbad.items():
+        args = dict(x=x, grad_y=torch.zeros(B, N), A=A, D=A.clone(), perm=perm, flags=PERM)
+        args.update(kw)
+        with pytest.raises(ValueError):
+            acdc.backward(**args)

@@ -325,11 +325,96 @@ def test_library_transform_path_equals_dense(monkeypatch, flags, N):
     x, A, D, perm, gy = rand_case(rng, 5, N, 3, flags, relu_input=True)
     b = rand_bias(rng, 3, N, bool(flags & CX))
     dense = O.forward(x, A, D, perm, flags, B=b), O.backward(x, gy, A, D, perm, flags, B=b)
-    monkeypatch.setattr(O, "DENSE_MAX", 4)
+    monkeypatch.setattr(O, "DENSE_MAX_REAL", 4)
+    monkeypatch.setattr(O, "DENSE_MAX_COMPLEX", 4)
     lib = O.forward(x, A, D, perm, flags, B=b), O.backward(x, gy, A, D, perm, flags, B=b)
     np.testing.assert_allclose(lib[0], dense[0], atol=1e-11)
     for a, c in zip(lib[1], dense[1]):
         np.testing.assert_allclose(a, c, atol=1e-10)
+
+
+def test_dense_path_serves_the_mixed_radix_width():
+    # N = 9216 = 2^10 * 3^2 (the Sec. 6.2 feature width) runs on the dense
+    # Sec. 4 matrix, which must agree with scipy's orthonormal DCT-II there
+    # too: a wrong angle reduction or index would show at this width first.
+    N = 9216
+    assert N <= O.dense_limit(False)
+    rng = np.random.default_rng(9216)
+    x = rng.standard_normal((3, N))
+    C = O.dct_matrix(N)
+    np.testing.assert_allclose(x @ C, scipy.fft.dct(x, type=2, norm="ortho", axis=1), rtol=0, atol=1e-11)
+    np.testing.assert_allclose(x @ C @ C.T, x, rtol=0, atol=1e-11)
+    # and a two-layer permuted ReLU cascade: dense oracle vs library transforms
+    x, A, D, perm, gy = rand_case(rng, 3, N, 2, P | R, relu_input=True)
+    np.testing.assert_allclose(O.forward(x, A, D, perm, P | R), lib_forward(x, A, D, perm, P | R),
+                               rtol=0, atol=1e-10)
+
+
+# ------------------------------------- ReLU decisions taken as an input
+
+@pytest.mark.parametrize("flags", [R, P | R])
+def test_own_decisions_reproduce_default(flags):
+    # Passing the oracle's own decisions changes nothing, bit for bit.
+    rng = np.random.default_rng(700 + flags)
+    x, A, D, perm, gy = rand_case(rng, 9, 32, 4, flags, relu_input=True)
+    b = rand_bias(rng, 4, 32, False)
+    y, c = O.forward(x, A, D, perm, flags, keep=True, B=b)
+    m = O.relu_decisions(c, 4)
+    assert m.shape == (3, 9, 32) and m.dtype == bool
+    assert np.array_equal(O.forward(x, A, D, perm, flags, B=b, masks=m), y)
+    for u, v in zip(O.backward(x, gy, A, D, perm, flags, B=b),
+                    O.backward(x, gy, A, D, perm, flags, B=b, masks=m)):
+        assert np.array_equal(u, v)
+    assert O.mask_disagreements(m, c, 4, 1e-4) == 0
+
+
+def test_given_decisions_are_used_consistently():
+    # With decisions fixed (here: random, not the oracle's), the cascade is
+    # linear in x, a and d separately, so the analytic backward must match
+    # finite differences of the forward under the same decisions.  This pins
+    # that forward and backward apply the given masks at the same places.
+    rng = np.random.default_rng(710)
+    N, K, flags = 8, 3, P | R
+    x, A, D, perm, gy = rand_case(rng, 2, N, K, flags)
+    m = rng.random((K - 1, 2, N)) < 0.5
+
+    def loss(x_, A_, D_):
+        return float(np.sum(gy * O.forward(x_, A_, D_, perm, flags, masks=m)))
+
+    gx, gA, gD = O.backward(x, gy, A, D, perm, flags, masks=m)
+    eps = 1e-6
+    for arr_id, got in enumerate((gx, gA, gD)):
+        arrs = [x, A, D]
+        for idx in np.ndindex(*got.shape):
+            p = [a.copy() for a in arrs]
+            q = [a.copy() for a in arrs]
+            p[arr_id][idx] += eps
+            q[arr_id][idx] -= eps
+            assert abs((loss(*p) - loss(*q)) / (2 * eps) - got[idx]) < 1e-7 + 1e-6 * abs(got[idx])
+    # and the decisions matter: the default ones give a different result
+    assert not np.allclose(O.backward(x, gy, A, D, perm, flags)[0], gx)
+
+
+def test_mask_disagreements_counts_only_clear_decisions():
+    # A decision flipped where |v| is far from zero is counted; one flipped
+    # inside the tie band is not.
+    v = np.array([[[3.0, -2.0, 1e-9, -1e-9]]])  # one layer, one row
+    cache = {"v": [v[0]]}
+    rms = np.sqrt(np.mean(v[0] ** 2))
+    own = v > 0
+    assert O.mask_disagreements(own, cache, 2, 1e-4) == 0
+    near = own.copy()
+    near[0, 0, 2] = ~near[0, 0, 2]
+    near[0, 0, 3] = ~near[0, 0, 3]
+    assert O.mask_disagreements(near, cache, 2, 1e-4) == 0
+    far = own.copy()
+    far[0, 0, 1] = ~far[0, 0, 1]
+    assert O.mask_disagreements(far, cache, 2, 1e-4) == 1
+    assert O.mask_disagreements(far, cache, 2, 2.0 / rms + 1e-9) == 0
+    with pytest.raises(ValueError):
+        O.forward(np.ones((1, 4)), np.ones((2, 4)), np.ones((2, 4)), None, 0, masks=own)  # no RELU flag
+    with pytest.raises(ValueError):
+        O.forward(np.ones((1, 4)), np.ones((3, 4)), np.ones((3, 4)), None, R, masks=own)  # wrong K
 
 
 # ------------------------------------------- D-domain bias (Sec. 6.2)
@@ -461,8 +546,20 @@ def test_cost_model_matches_paper_printed_numbers():
     assert abs(O.arithmetic_intensity(lo) - g["ai_range_printed"][0]) <= 0.05 + 1e-12
     assert abs(O.arithmetic_intensity(hi) - g["ai_range_printed"][1]) <= 0.05 + 1e-12
     assert round(g["titan_x_peak_gflops"] / g["titan_x_peak_gbps"]) == g["titan_x_ridge_flop_per_byte_approx"]
-    N = 4096
-    assert O.flops_per_row_layer(N) == 4 * N + 5 * N * 12
+
+
+def test_flop_counts_against_hand_computed_values():
+    # The roofline's numerator.  Values computed by hand from the Sec. 5
+    # count (4N + 5 N log2 N per real row-layer) and, for AFDF rows, two
+    # complex N-point FFTs in the same convention (5 N log2 N each) plus two
+    # complex diagonal products (6 flops per complex multiply, N each).
+    # Both the oracle's count and bench.py's own copy must reproduce them.
+    import bench
+    g = json.load(open(os.path.join(GOLDEN, "paper_cost_model.json")))
+    for case in g["flops_per_row_layer"]:
+        N, cplx, want = case["N"], case["complex"], case["flops"]
+        assert O.flops_per_row_layer(N, cplx) == pytest.approx(want, rel=1e-12)
+        assert bench.flops_row_layer(N, cplx) == pytest.approx(want, rel=1e-12)
 
 
 # ----------------------------------------- planted mistakes must be caught (CPU)
