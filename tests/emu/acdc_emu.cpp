@@ -238,3 +238,15 @@ extern "C" int acdc_emu_backward(const float* x, const float* gy, const float* A
   }
   return rc;
 }
+
+// The fixed-order batch reduction alone: out[e] (float4 e < n4) = the sum
+// over ntiles tiles of partial[t][e], in the kernels' order (tile phases,
+// groups of eight loads, phases added in order).
+extern "C" void acdc_emu_reduce4(const float* partial, long long ntiles, long long n4, float* out) {
+  for (long long e = 0; e < n4; ++e) {
+    float4 ph[kRedPhases];
+    for (int g = 0; g < kRedPhases; ++g)
+      ph[g] = tile_phase_sum4(reinterpret_cast<const float4*>(partial), ntiles, n4, e, g);
+    reinterpret_cast<float4*>(out)[e] = phases_total4(ph);
+  }
+}

@@ -138,3 +138,34 @@ def test_accumulate_adds_to_gradients(emu):
         outs.append(g)
     for plain, added in zip(*outs):
         np.testing.assert_allclose(added, plain + 0.5, rtol=1e-6, atol=1e-6)
+
+
+@pytest.mark.parametrize("ntiles", [1, 5, 28, 29, 32, 61, 256])
+def test_reduction_order_and_value(emu, ntiles):
+    # The batch reduction of the parameter-gradient partials: bit for bit the
+    # documented order (tiles split into 4 phases by t mod 4, each summed in
+    # increasing t, phase sums added in phase order), whichever branch of the
+    # grouped loads runs (groups of eight from 29 tiles on), and within fp32
+    # rounding of the exact fp64 sum.
+    emu.acdc_emu_reduce4.argtypes = [ctypes.c_void_p, ctypes.c_longlong, ctypes.c_longlong, ctypes.c_void_p]
+    rng = np.random.default_rng(ntiles)
+    n4 = 37
+    part = rng.standard_normal((ntiles, n4 * 4)).astype(np.float32)
+    out = np.zeros(n4 * 4, np.float32)
+    emu.acdc_emu_reduce4(part.ctypes.data, ntiles, n4, out.ctypes.data)
+    phases = []
+    for g in range(4):
+        s = np.zeros(n4 * 4, np.float32)
+        for t in range(g, ntiles, 4):
+            s = (s + part[t]).astype(np.float32)
+        phases.append(s)
+    want = (((phases[0] + phases[1]).astype(np.float32) + phases[2]).astype(np.float32) + phases[3]).astype(np.float32)
+    assert np.array_equal(out, want)
+    exact = part.astype(np.float64).sum(axis=0)
+    assert np.max(np.abs(out - exact)) <= 1e-6 * ntiles * np.max(np.abs(part)) + 1e-7
+
+
+def test_backward_over_many_tiles(emu):
+    # 61 backward tiles (N = 4096: 8 rows per tile) through the emulated
+    # kernels and their reduction, against the oracle
+    check(emu, 4096, 1, 61 * 8, 0, seed=61)
