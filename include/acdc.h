@@ -103,7 +103,8 @@ enum acdc_status {
   ACDC_ERR_INVALID_ARG = -1, /* null/misaligned/aliased pointer, bad size or flag */
   ACDC_ERR_UNSUPPORTED = -2, /* width N not built, or COMPLEX with RELU or BIAS */
   ACDC_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required */
-  ACDC_ERR_HIP = -4          /* a HIP runtime call failed */
+  ACDC_ERR_HIP = -4,         /* a HIP runtime call failed */
+  ACDC_ERR_NOT_PREPARED = -5 /* acdc_forward_noalloc: acdc_prepare(N, flags) not called on this device */
 };
 
 /* 1 if (N, flags) is supported by this build, else 0.  Host only. */
@@ -141,6 +142,27 @@ size_t acdc_backward_workspace_size(int64_t batch, int32_t N, int32_t K, uint32_
 int acdc_forward(const float* x, float* y, const float* A, const float* D, const float* bias,
                  const int32_t* perm, int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved,
                  size_t saved_bytes, void* workspace, size_t workspace_bytes, acdc_stream_t stream);
+
+/* Forward cascade that allocates nothing, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments and results as
+ * acdc_forward, bit for bit, without the workspace: the per-layer quartet
+ * coefficients go to a file-scope device array of the library (16 MiB per
+ * device, held until the process ends).
+ *  - acdc_prepare(N, flags) must have been called on the current device
+ *    first (it builds the constant table and finds that array's address);
+ *    otherwise ACDC_ERR_NOT_PREPARED, nothing launched.
+ *  - Fused widths only (ACDC_ERR_UNSUPPORTED for the multi-pass path, whose
+ *    workspace grows with the batch), and K * acdc_forward_workspace_size
+ *    per layer must fit the array: real rows need 16 N bytes per layer, so
+ *    K * N <= 2^20 (else ACDC_ERR_WORKSPACE).  Complex rows need no scratch.
+ *  - Every call on one device shares that device's array, and each call
+ *    rewrites the part it uses before reading it: calls that overlap on one
+ *    device (different streams or host threads without ordering) race.
+ * No hipMalloc, hipFree or other allocation happens in this call. */
+int acdc_forward_noalloc(const float* x, float* y, const float* A, const float* D, const float* bias,
+                         const int32_t* perm, int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved,
+                         size_t saved_bytes, acdc_stream_t stream);
 
 /* Backward cascade.  Given x and grad_y = dL/dy, writes grad_x = dL/dx and
  * grad_A, grad_D = dL/da_k, dL/dd_k summed over the batch, and with

@@ -25,6 +25,7 @@ SIGNATURES = {
     "acdc_forward_workspace_size": (_SZ, [_I64, _I32, _I32, _U32]),
     "acdc_backward_workspace_size": (_SZ, [_I64, _I32, _I32, _U32, ctypes.c_int]),
     "acdc_forward": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _I64, _I32, _I32, _U32, _P, _SZ, _P, _SZ, _P]),
+    "acdc_forward_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _I64, _I32, _I32, _U32, _P, _SZ, _P]),
     "acdc_backward": (ctypes.c_int,
                       [_P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P, _P, _P, _I64, _I32, _I32, _U32, _P, _SZ, _P]),
     "acdc_profile_enable": (ctypes.c_int, [ctypes.c_int]),

@@ -198,6 +198,13 @@ __global__ __launch_bounds__(256) void k_cplx_reduce(const float* __restrict__ p
   }
 }
 
+// Scratch of the no-allocation forward (acdc_forward_noalloc): the per-layer
+// quartet coefficients that acdc_forward keeps in the caller's workspace.
+// Each device holds its own copy until the process ends; host code reaches
+// it only through the address hipGetSymbolAddress returns on that device.
+constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
+static __device__ __align__(256) float4 scratch[kNoAllocScratchBytes / sizeof(float4)];
+
 // ------------------------------------------------------------------ host side
 
 namespace {
@@ -314,9 +321,11 @@ int get_table(int N, bool cplx, const char** out) {
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Workgroups of `kernel` (with `threads` threads) that fit on the current
-// device at once; the persistent kernels launch min(tiles, this).
+// device at once; the persistent kernels launch min(tiles, this).  With
+// `remember` false a value not yet cached is computed without caching it
+// (the no-allocation entry point inserts nothing).
 std::map<std::pair<const void*, int>, long long> g_resident;
-long long resident_workgroups(const void* kernel, int threads) {
+long long resident_workgroups(const void* kernel, int threads, bool remember = true) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   std::lock_guard<std::mutex> lock(g_mu);
@@ -328,13 +337,40 @@ long long resident_workgroups(const void* kernel, int threads) {
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) == hipSuccess &&
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
     n = (long long)per_cu * cus;
-  g_resident[key] = n;
+  if (remember) g_resident[key] = n;
   return n;
 }
 
-long long persistent_grid(const void* kernel, int threads, long long tiles) {
-  const long long n = resident_workgroups(kernel, threads);
+long long persistent_grid(const void* kernel, int threads, long long tiles, bool remember = true) {
+  const long long n = resident_workgroups(kernel, threads, remember);
   return (n > 0 && n < tiles) ? n : tiles;
+}
+
+// Per-device address of `scratch`, set by acdc_prepare (the library's set-up
+// call) with the device current; null until then.
+constexpr int kMaxDevices = 64;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_setup() {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e);
+  if (dev < 0 || dev >= kMaxDevices) return ACDC_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_mu);
+  if (g_scratch_ptr[dev] != nullptr) return ACDC_OK;
+  void* p = nullptr;
+  e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return hip_fail(e);
+  g_scratch_ptr[dev] = p;
+  return ACDC_OK;
+}
+
+// The constant table of (N, complex) on device `dev` if it exists (never
+// builds one).
+const char* find_table(int dev, int N, bool cplx) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  auto it = g_tables.find(std::make_tuple(dev, N, cplx ? 1 : 0));
+  return it == g_tables.end() ? nullptr : static_cast<const char*>(it->second);
 }
 
 constexpr uint32_t kAllFlags = kFlagPerm | kFlagRelu | kFlagComplex | kFlagBias | kFlagAccumulate | kFlagMultipass;
@@ -438,18 +474,18 @@ int launch_real_mq(const float* D, const float* Bias, float4* Mq, int K, const c
 }
 
 template <class PL, bool BIAS>
-void launch_real_fwd_k(const RealArgs& a, hipStream_t s) {
+void launch_real_fwd_k(const RealArgs& a, hipStream_t s, bool remember) {
   const long long tiles = fwd_blocks<PL>(a.batch);
   const long long grid = persistent_grid(reinterpret_cast<const void*>(&k_real_fwd<PL, BIAS>),
-                                         Launch<PL>::FWD_THREADS, tiles);
+                                         Launch<PL>::FWD_THREADS, tiles, remember);
   hipLaunchKernelGGL((k_real_fwd<PL, BIAS>), dim3(unsigned(grid)), dim3(Launch<PL>::FWD_THREADS), 0, s, a, tiles);
 }
 
 template <class PL>
-int launch_real_fwd(const RealArgs& a, hipStream_t s) {
+int launch_real_fwd(const RealArgs& a, hipStream_t s, bool remember = true) {
   ProfScope prof(0, s);
-  if (a.flags & kFlagBias) launch_real_fwd_k<PL, true>(a, s);
-  else launch_real_fwd_k<PL, false>(a, s);
+  if (a.flags & kFlagBias) launch_real_fwd_k<PL, true>(a, s, remember);
+  else launch_real_fwd_k<PL, false>(a, s, remember);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? ACDC_OK : hip_fail(e);
 }
@@ -895,6 +931,29 @@ int mp_backward(const float* x, const float* grad_y, const float* A, const float
   return ACDC_OK;
 }
 
+// The fused forward's launches (per-layer quartet coefficients into
+// `workspace`, then the cascade).  `remember` false: cache nothing on the host.
+int fused_forward(const float* x, float* y, const float* A, const float* D, const float* bias, const int32_t* perm,
+                  int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved, void* workspace,
+                  const char* tab, hipStream_t s, bool remember) {
+  int rc = ACDC_ERR_UNSUPPORTED;
+  if (flags & kFlagComplex) {
+    dispatch_complex(N, [&]<class PL>() {
+      CplxArgs a{x, y, A, D, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
+      rc = launch_cplx_fwd<PL>(a, s);
+    });
+  } else {
+    dispatch_real(N, [&]<class PL>() {
+      float4* Mq = static_cast<float4*>(workspace);
+      rc = launch_real_mq<PL>(D, bias, Mq, K, tab, s);
+      if (rc != ACDC_OK) return;
+      RealArgs a{x, y, A, Mq, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
+      rc = launch_real_fwd<PL>(a, s, remember);
+    });
+  }
+  return rc;
+}
+
 }  // namespace
 }  // namespace acdc
 
@@ -908,12 +967,21 @@ extern "C" int acdc_supported(int32_t N, uint32_t flags) {
 
 extern "C" int acdc_prepare(int32_t N, uint32_t flags) {
   if (!acdc_supported(N, flags)) return ACDC_ERR_UNSUPPORTED;
+  int rc = scratch_setup();
+  if (rc != ACDC_OK) return rc;
   if (use_multipass(N, flags)) {
     MpTabs t;
     return get_mp_tables((flags & kFlagComplex) ? 2 * N : N, &t);
   }
   const char* tab = nullptr;
-  return get_table(N, (flags & kFlagComplex) != 0, &tab);
+  rc = get_table(N, (flags & kFlagComplex) != 0, &tab);
+  if (rc != ACDC_OK || (flags & kFlagComplex)) return rc;
+  // cache the persistent forward grids, so that later calls look them up
+  dispatch_real(N, [&]<class PL>() {
+    (void)resident_workgroups(reinterpret_cast<const void*>(&k_real_fwd<PL, false>), Launch<PL>::FWD_THREADS);
+    (void)resident_workgroups(reinterpret_cast<const void*>(&k_real_fwd<PL, true>), Launch<PL>::FWD_THREADS);
+  });
+  return ACDC_OK;
 }
 
 extern "C" size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags) {
@@ -960,22 +1028,41 @@ extern "C" int acdc_forward(const float* x, float* y, const float* A, const floa
   const char* tab = nullptr;
   rc = get_table(N, cplx, &tab);
   if (rc != ACDC_OK) return rc;
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (cplx) {
-    dispatch_complex(N, [&]<class PL>() {
-      CplxArgs a{x, y, A, D, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
-      rc = launch_cplx_fwd<PL>(a, s);
-    });
-  } else {
-    dispatch_real(N, [&]<class PL>() {
-      float4* Mq = static_cast<float4*>(workspace);
-      rc = launch_real_mq<PL>(D, bias, Mq, K, tab, s);
-      if (rc != ACDC_OK) return;
-      RealArgs a{x, y, A, Mq, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
-      rc = launch_real_fwd<PL>(a, s);
-    });
+  return fused_forward(x, y, A, D, bias, perm, batch, N, K, flags, saved, workspace, tab,
+                       reinterpret_cast<hipStream_t>(stream), true);
+}
+
+extern "C" int acdc_forward_noalloc(const float* x, float* y, const float* A, const float* D, const float* bias,
+                                    const int32_t* perm, int64_t batch, int32_t N, int32_t K, uint32_t flags,
+                                    float* saved, size_t saved_bytes, acdc_stream_t stream) {
+  int rc = check_common(batch, N, K, flags);
+  if (rc != ACDC_OK) return rc;
+  if (use_multipass(N, flags)) return ACDC_ERR_UNSUPPORTED;  // its workspace grows with the batch
+  if (saved != nullptr && saved_bytes < saved_floats(batch, N, K, flags) * sizeof(float)) return ACDC_ERR_WORKSPACE;
+  const size_t need = fwd_ws(N, K, flags);
+  if (need > kNoAllocScratchBytes) return ACDC_ERR_WORKSPACE;
+  const bool perm_on = (flags & kFlagPerm) != 0;
+  const bool bias_on = (flags & kFlagBias) != 0;
+  if (batch == 0) return ACDC_OK;
+  rc = check_ptrs({x, y, A, D}, {perm_on ? (const void*)perm : nullptr, bias_on ? (const void*)bias : nullptr, saved});
+  if (rc != ACDC_OK) return rc;
+  if ((perm_on && perm == nullptr) || (bias_on && bias == nullptr)) return ACDC_ERR_INVALID_ARG;
+  if (!bias_on) bias = nullptr;
+  if (!distinct({y, saved}, {x, y, A, D, bias, perm, saved})) return ACDC_ERR_INVALID_ARG;
+  int dev = 0;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e);
+  if (dev < 0 || dev >= kMaxDevices) return ACDC_ERR_UNSUPPORTED;
+  const bool cplx = (flags & kFlagComplex) != 0;
+  const char* tab = find_table(dev, N, cplx);
+  void* ws = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_mu);
+    ws = g_scratch_ptr[dev];
   }
-  return rc;
+  if (tab == nullptr || ws == nullptr) return ACDC_ERR_NOT_PREPARED;
+  return fused_forward(x, y, A, D, bias, perm, batch, N, K, flags, saved, ws, tab,
+                       reinterpret_cast<hipStream_t>(stream), false);
 }
 
 extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A, const float* D,
@@ -1137,6 +1224,7 @@ extern "C" const char* acdc_status_string(int status) {
     case ACDC_ERR_UNSUPPORTED: return "unsupported width or flag combination";
     case ACDC_ERR_WORKSPACE: return "workspace missing or too small";
     case ACDC_ERR_HIP: return "HIP runtime error";
+    case ACDC_ERR_NOT_PREPARED: return "width not prepared on this device (call acdc_prepare first)";
     default: return "unknown status";
   }
 }

@@ -248,3 +248,18 @@ def test_binding_checks_shapes_before_any_library_call(L):
         args.update(kw)
         with pytest.raises(ValueError):
             acdc.backward(**args)
+
+
+def test_noalloc_forward_rejects_on_the_host(L):
+    # acdc_forward_noalloc refuses, before any HIP call, what its fixed
+    # scratch array cannot hold (more than 2^20 layer-elements of real rows)
+    # and the multi-pass path (workspace grows with the batch)
+    P = ctypes.c_void_p
+    x = P(0x1000)
+    y = P(0x2000)
+    A = P(0x3000)
+    D = P(0x4000)
+    assert L.acdc_forward_noalloc(x, y, A, D, None, None, 4, 4096, 300, 0, None, 0, None) == EWS
+    assert L.acdc_forward_noalloc(x, y, A, D, None, None, 4, 65536, 1, 0, None, 0, None) == EUNSUP
+    assert L.acdc_forward_noalloc(x, y, A, D, None, None, 4, 4096, 1, 1 << 20, None, 0, None) == EINVAL
+    assert L.acdc_status_string(-5).decode().startswith("width not prepared")
