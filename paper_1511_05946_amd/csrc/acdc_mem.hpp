@@ -81,16 +81,21 @@ struct GView {
   }
   // Stores go through a plain global pointer: buffer stores fed from the
   // register arrays defeat register promotion of those arrays in this
-  // compiler, so only loads use the buffer path.
+  // compiler (they end up in private scratch), so only loads use the buffer
+  // path.  The constant part of the offset goes to the uniform base first,
+  // so that every store is (SGPR base + one 32-bit lane offset): written as
+  // base + (voff + soff) the compiler forms a 64-bit address per store and
+  // hoists them out of the layer loop (2 VGPRs per row chunk, spilled at
+  // N = 9216).
   __host__ __device__ __forceinline__ void st4(float4 v, unsigned voff, unsigned soff) const {
-    *reinterpret_cast<float4*>(p + (voff + soff)) = v;
+    *reinterpret_cast<float4*>((p + soff) + voff) = v;
   }
   __host__ __device__ __forceinline__ void st4(float a, float b, float c, float d, unsigned voff,
                                                unsigned soff) const {
-    *reinterpret_cast<float4*>(p + (voff + soff)) = make_float4(a, b, c, d);
+    *reinterpret_cast<float4*>((p + soff) + voff) = make_float4(a, b, c, d);
   }
   __host__ __device__ __forceinline__ void st2(float2 v, unsigned voff, unsigned soff) const {
-    *reinterpret_cast<float2*>(p + (voff + soff)) = v;
+    *reinterpret_cast<float2*>((p + soff) + voff) = v;
   }
 };
 
