@@ -75,9 +75,13 @@ struct RealPlan {
   static constexpr int QF = NSL * T * 4;         // floats of one row's quartet image
   // FFT data in LDS: complex element a lives at a + (a >> PADSH), one pad
   // slot per 2^PADSH elements, so the stride-r writes of the first pass and
-  // the stride-1 reads of the next spread over all banks.
+  // the stride-1 reads of the next spread over all banks.  Plans whose first
+  // radix is not a power of two (N = 9216) go unpadded: there the padded
+  // write addresses of the mixed-radix passes are not affine in the lane,
+  // so each thread would hold one precomputed address per output (about 48
+  // VGPRs, spilled) instead of one base per butterfly.
   static constexpr int PADSH =
-      !ACDC_LDS_PAD ? 30 : (ilog2(R0_) >= 2 && (1 << ilog2(R0_)) == R0_ ? ilog2(R0_) : 4);
+      !ACDC_LDS_PAD ? 30 : (ilog2(R0_) >= 2 && (1 << ilog2(R0_)) == R0_ ? ilog2(R0_) : 30);
   static constexpr int FFT_FLOATS = 2 * (M + (M >> PADSH));
   static constexpr int SLAB = cmax(cmax(N, QF), FFT_FLOATS);  // LDS floats per row
   // twiddle table (float2) offsets: forward passes 1.., then inverse passes
@@ -151,7 +155,7 @@ struct ComplexPlan {
     return s;
   }
   static constexpr int PADSH =
-      !ACDC_LDS_PAD ? 30 : (ilog2(R0_) >= 2 && (1 << ilog2(R0_)) == R0_ ? ilog2(R0_) : 4);
+      !ACDC_LDS_PAD ? 30 : (ilog2(R0_) >= 2 && (1 << ilog2(R0_)) == R0_ ? ilog2(R0_) : 30);
   static constexpr int FFT_FLOATS = 2 * (N_ + (N_ >> PADSH));
   static constexpr int SLAB = FFT_FLOATS;  // LDS floats per row
   // Twiddles of a pass are stored in pairs (inputs i, i+1) so one 16-byte
