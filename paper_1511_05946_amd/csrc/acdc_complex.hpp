@@ -3,9 +3,12 @@
 //
 // A row of N complex values lives in the registers of T threads, P = N/T
 // each.  Spatial layout: v[beta*R0 + i] is element t + T*(beta + i*B0);
-// frequency layout: v[beta*RL + m] is element t + T*(beta + m*BL).  The
-// forward FFT maps the first to the second and the inverse FFT (radices
-// reversed) maps back, so D multiplies in place and nothing is reordered.
+// frequency layout: v[beta*RL + m] is element t + T*(beta + m*BL) -- or,
+// with adjacent butterfly pairs (CplxOps::PAIRS), 2t + (beta&1) +
+// 2T*(beta>>1) + i*T*B0 (resp. m*T*BL), so that each access moves two
+// neighbouring elements.  The forward FFT maps the spatial layout to the
+// frequency one and the inverse FFT (radices reversed) maps back, so D
+// multiplies in place and nothing is reordered.
 //
 // Backward (PyTorch convention, grad = dL/dRe + i dL/dIm, so g_x = g_y W^H):
 //   gh3 = FFT(g)/N, dd = sum conj(h2) gh3, gh1 = IFFT_unnorm(gh3 conj(d)),
@@ -24,29 +27,59 @@ struct CplxOps {
   static constexpr int N = PL::N, T = PL::T, P = PL::P;
   static constexpr int R0 = PL::rad(0), RL = PL::rad(PL::NPASS - 1);
   static constexpr int B0 = P / R0, BL = P / RL;
+  // Butterfly ownership of the first and last pass (acdc_stockham.hpp): the
+  // adjacent pairs (2p, 2p+1), p = t + T*(beta/2), when both passes give a
+  // thread an even number of butterflies, else plain (t + T*beta).
+  static constexpr bool PAIRS = ACDC_CPLX_PAIRS && B0 % 2 == 0 && BL % 2 == 0;
+  static constexpr int KIND = PAIRS ? 3 : 0;
 
-  // f(lane_part, const_part, v[s]) with element = t + const_part over the
-  // spatial (resp. frequency) layout.
+  // Element of v[beta*R0 + i] (spatial) or v[beta*RL + m] (frequency), as a
+  // lane part plus a compile-time part:
+  //   plain: t + T*(beta + i*B0)              (resp. t + T*(beta + m*BL))
+  //   pairs: 2t + (beta&1) + 2T*(beta>>1) + i*T*B0   (resp. ... + m*T*BL)
+  __host__ __device__ static constexpr unsigned lane_part(unsigned t) { return PAIRS ? 2u * t : t; }
+  __host__ __device__ static constexpr unsigned cpart(int beta, int i, int B) {
+    return PAIRS ? unsigned((beta & 1) + 2 * T * (beta >> 1) + i * T * B) : unsigned(T * (beta + i * B));
+  }
+
+  // f(lane_part, const_part, v[s]) with element = lane_part + const_part over
+  // the spatial (resp. frequency) layout.
   template <class F>
   __host__ __device__ __forceinline__ static void for_spatial(float2 (&v)[P], unsigned t, F&& f) {
 #pragma unroll
     for (int beta = 0; beta < B0; ++beta)
 #pragma unroll
-      for (int i = 0; i < R0; ++i) f(t, unsigned(T * (beta + i * B0)), v[beta * R0 + i]);
+      for (int i = 0; i < R0; ++i) f(lane_part(t), cpart(beta, i, B0), v[beta * R0 + i]);
   }
   template <class F>
   __host__ __device__ __forceinline__ static void for_spatial2(float2 (&v)[P], float2 (&w)[P], unsigned t, F&& f) {
 #pragma unroll
     for (int beta = 0; beta < B0; ++beta)
 #pragma unroll
-      for (int i = 0; i < R0; ++i) f(t, unsigned(T * (beta + i * B0)), v[beta * R0 + i], w[beta * R0 + i]);
+      for (int i = 0; i < R0; ++i) f(lane_part(t), cpart(beta, i, B0), v[beta * R0 + i], w[beta * R0 + i]);
   }
   template <class F>
   __host__ __device__ __forceinline__ static void for_freq(float2 (&v)[P], unsigned t, F&& f) {
 #pragma unroll
     for (int beta = 0; beta < BL; ++beta)
 #pragma unroll
-      for (int m = 0; m < RL; ++m) f(t, unsigned(T * (beta + m * BL)), v[beta * RL + m]);
+      for (int m = 0; m < RL; ++m) f(lane_part(t), cpart(beta, m, BL), v[beta * RL + m]);
+  }
+  // With PAIRS: f(lane_part, const_part, z0, z1) over the spatial (resp.
+  // frequency) layout's neighbouring elements (z1 = element + 1).
+  template <class F>
+  __host__ __device__ __forceinline__ static void for_spatial_pairs(float2 (&v)[P], unsigned t, F&& f) {
+#pragma unroll
+    for (int q = 0; q < B0 / 2; ++q)
+#pragma unroll
+      for (int i = 0; i < R0; ++i) f(lane_part(t), cpart(2 * q, i, B0), v[2 * q * R0 + i], v[(2 * q + 1) * R0 + i]);
+  }
+  template <class F>
+  __host__ __device__ __forceinline__ static void for_freq_pairs(float2 (&v)[P], unsigned t, F&& f) {
+#pragma unroll
+    for (int q = 0; q < BL / 2; ++q)
+#pragma unroll
+      for (int m = 0; m < RL; ++m) f(lane_part(t), cpart(2 * q, m, BL), v[2 * q * RL + m], v[(2 * q + 1) * RL + m]);
   }
 
   // g views the workgroup's first row; roff = this row's offset (complex elements)
@@ -55,36 +88,111 @@ struct CplxOps {
                                                        bool valid) {
     const unsigned ro = valid ? roff : 0u;
     const float zf = valid ? 1.0f : 0.0f;
-    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) {
-      const float2 h = g.ld2((l + ro) * 8u, c * 8u);
-      z = make_float2(h.x * zf, h.y * zf);
-    });
+    if constexpr (PAIRS) {
+      for_spatial_pairs(v, t, [&](unsigned l, unsigned c, float2& z0, float2& z1) {
+        const float4 h = g.ld4((l + ro) * 8u, c * 8u);
+        z0 = make_float2(h.x * zf, h.y * zf);
+        z1 = make_float2(h.z * zf, h.w * zf);
+      });
+    } else {
+      for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) {
+        const float2 h = g.ld2((l + ro) * 8u, c * 8u);
+        z = make_float2(h.x * zf, h.y * zf);
+      });
+    }
   }
   __host__ __device__ __forceinline__ static void store(GView g, unsigned roff, float2 (&v)[P], unsigned t) {
-    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { g.st2(z, (l + roff) * 8u, c * 8u); });
+    if constexpr (PAIRS) {
+      for_spatial_pairs(v, t, [&](unsigned l, unsigned c, float2& z0, float2& z1) {
+        g.st4(z0.x, z0.y, z1.x, z1.y, (l + roff) * 8u, c * 8u);
+      });
+    } else {
+      for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { g.st2(z, (l + roff) * 8u, c * 8u); });
+    }
   }
   template <bool CONJ>
   __host__ __device__ __forceinline__ static void scale(float2 (&v)[P], GView a, unsigned t) {
-    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) {
-      const float2 w = a.ld2(l * 8u, c * 8u);
-      z = CONJ ? cmulc(z, w) : cmul(z, w);
-    });
+    if constexpr (PAIRS) {
+      for_spatial_pairs(v, t, [&](unsigned l, unsigned c, float2& z0, float2& z1) {
+        const float4 w = a.ld4(l * 8u, c * 8u);
+        z0 = CONJ ? cmulc(z0, make_float2(w.x, w.y)) : cmul(z0, make_float2(w.x, w.y));
+        z1 = CONJ ? cmulc(z1, make_float2(w.z, w.w)) : cmul(z1, make_float2(w.z, w.w));
+      });
+    } else {
+      for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) {
+        const float2 w = a.ld2(l * 8u, c * 8u);
+        z = CONJ ? cmulc(z, w) : cmul(z, w);
+      });
+    }
   }
   template <bool CONJ>
   __host__ __device__ __forceinline__ static void scale_freq(float2 (&v)[P], GView d, float f, unsigned t) {
-    for_freq(v, t, [&](unsigned l, unsigned c, float2& z) {
-      const float2 dv = d.ld2(l * 8u, c * 8u);
-      const float2 w = make_float2(dv.x * f, dv.y * f);
-      z = CONJ ? cmulc(z, w) : cmul(z, w);
-    });
+    if constexpr (PAIRS) {
+      for_freq_pairs(v, t, [&](unsigned l, unsigned c, float2& z0, float2& z1) {
+        const float4 dv = d.ld4(l * 8u, c * 8u);
+        const float2 w0 = make_float2(dv.x * f, dv.y * f), w1 = make_float2(dv.z * f, dv.w * f);
+        z0 = CONJ ? cmulc(z0, w0) : cmul(z0, w0);
+        z1 = CONJ ? cmulc(z1, w1) : cmul(z1, w1);
+      });
+    } else {
+      for_freq(v, t, [&](unsigned l, unsigned c, float2& z) {
+        const float2 dv = d.ld2(l * 8u, c * 8u);
+        const float2 w = make_float2(dv.x * f, dv.y * f);
+        z = CONJ ? cmulc(z, w) : cmul(z, w);
+      });
+    }
+  }
+
+  // A row (segment) in the spatial or frequency layout, without the
+  // validity zeroing of load(): offsets as in load().
+  template <bool FREQ>
+  __host__ __device__ __forceinline__ static void ld_row(GView g, unsigned roff, float2 (&v)[P], unsigned t) {
+    if constexpr (PAIRS) {
+      auto f = [&](unsigned l, unsigned c, float2& z0, float2& z1) {
+        const float4 h = g.ld4((l + roff) * 8u, c * 8u);
+        z0 = make_float2(h.x, h.y);
+        z1 = make_float2(h.z, h.w);
+      };
+      if constexpr (FREQ) for_freq_pairs(v, t, f);
+      else for_spatial_pairs(v, t, f);
+    } else {
+      auto f = [&](unsigned l, unsigned c, float2& z) { z = g.ld2((l + roff) * 8u, c * 8u); };
+      if constexpr (FREQ) for_freq(v, t, f);
+      else for_spatial(v, t, f);
+    }
+  }
+  template <bool FREQ>
+  __host__ __device__ __forceinline__ static void st_row(GView g, unsigned roff, float2 (&v)[P], unsigned t) {
+    if constexpr (PAIRS) {
+      auto f = [&](unsigned l, unsigned c, float2& z0, float2& z1) {
+        g.st4(z0.x, z0.y, z1.x, z1.y, (l + roff) * 8u, c * 8u);
+      };
+      if constexpr (FREQ) for_freq_pairs(v, t, f);
+      else for_spatial_pairs(v, t, f);
+    } else {
+      auto f = [&](unsigned l, unsigned c, float2& z) { g.st2(z, (l + roff) * 8u, c * 8u); };
+      if constexpr (FREQ) for_freq(v, t, f);
+      else for_spatial(v, t, f);
+    }
   }
 
   // The thread's perm entries (spatial layout), loaded ahead of the gather.
   __host__ __device__ __forceinline__ static void load_idx(int (&idx)[P], GView perm, unsigned t) {
+    if constexpr (PAIRS) {
 #pragma unroll
-    for (int beta = 0; beta < B0; ++beta)
+      for (int q = 0; q < B0 / 2; ++q)
 #pragma unroll
-      for (int i = 0; i < R0; ++i) idx[beta * R0 + i] = perm.ldi1(t * 4u, unsigned(T * (beta + i * B0)) * 4u);
+        for (int i = 0; i < R0; ++i) {
+          const int2 p2 = perm.ldi2(lane_part(t) * 4u, cpart(2 * q, i, B0) * 4u);
+          idx[2 * q * R0 + i] = p2.x;
+          idx[(2 * q + 1) * R0 + i] = p2.y;
+        }
+    } else {
+#pragma unroll
+      for (int beta = 0; beta < B0; ++beta)
+#pragma unroll
+        for (int i = 0; i < R0; ++i) idx[beta * R0 + i] = perm.ldi1(t * 4u, cpart(beta, i, B0) * 4u);
+    }
   }
   // u[n] = z[perm[n]] with the indices already in registers.
   template <class Ctx>
@@ -108,8 +216,11 @@ struct CplxOps {
   template <class Ctx>
   __host__ __device__ __forceinline__ static void scatter(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
                                                           GView perm) {
+    int idx[P];
+    load_idx(idx, perm, t);
     ctx.sync_row();
-    for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { slab[perm.ldi1(l * 4u, c * 4u)] = z; });
+#pragma unroll
+    for (int s = 0; s < P; ++s) slab[idx[s]] = v[s];
     ctx.sync_row();
     for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { z = slab[l + c]; });
   }
@@ -117,7 +228,7 @@ struct CplxOps {
   template <bool INV, class Ctx>
   __host__ __device__ __forceinline__ static void fft(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
                                                       GView tw) {
-    stockham_fft<PL, INV, 0, 0>(ctx, v, t, slab, tw);
+    stockham_fft<PL, INV, KIND, KIND>(ctx, v, t, slab, tw);
   }
 };
 

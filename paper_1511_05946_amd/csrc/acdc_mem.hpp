@@ -70,6 +70,16 @@ struct GView {
     return v;
 #endif
   }
+  __host__ __device__ __forceinline__ int2 ldi2(unsigned voff, unsigned soff) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const u32x2 v = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+    return make_int2(int(v[0]), int(v[1]));
+#else
+    int2 v;
+    std::memcpy(&v, p + voff + soff, 8);
+    return v;
+#endif
+  }
   __host__ __device__ __forceinline__ int ldi1(unsigned voff, unsigned soff) const {
 #if defined(__HIP_DEVICE_COMPILE__)
     return (int)__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);

@@ -208,15 +208,9 @@ __global__ __launch_bounds__(Launch<CP>::FWD_THREADS) void k_seg(float2* __restr
   float2* slab = reinterpret_cast<float2*>(lds + r * L::FWD_SLAB);
   DevCtx<T> ctx;
   float2 v[P];
-  if constexpr (!INV) {
-    O::for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { z = g.ld2((l + roff) * 8u, c * 8u); });
-    O::template fft<false>(ctx, v, t, slab, GView::of(tab));
-    if (valid) O::for_freq(v, t, [&](unsigned l, unsigned c, float2& z) { g.st2(z, (l + roff) * 8u, c * 8u); });
-  } else {
-    O::for_freq(v, t, [&](unsigned l, unsigned c, float2& z) { z = g.ld2((l + roff) * 8u, c * 8u); });
-    O::template fft<true>(ctx, v, t, slab, GView::of(tab));
-    if (valid) O::for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { g.st2(z, (l + roff) * 8u, c * 8u); });
-  }
+  O::template ld_row<INV>(g, roff, v, t);
+  O::template fft<INV>(ctx, v, t, slab, GView::of(tab));
+  if (valid) O::template st_row<!INV>(g, roff, v, t);
 }
 
 // Per-layer quartet coefficients [K][NQ][kMqRows] (entry-major).

@@ -27,6 +27,9 @@
 #ifndef ACDC_FFT2
 #define ACDC_FFT2 1  // backward: the h- and g-path FFTs share twiddle loads
 #endif
+#ifndef ACDC_CPLX_PAIRS
+#define ACDC_CPLX_PAIRS 1  // complex rows: adjacent butterfly pairs where the plan allows
+#endif
 #ifndef ACDC_LDS_PAD
 #define ACDC_LDS_PAD 1
 #endif

@@ -35,7 +35,7 @@ using CP256 = ComplexPlan<256, 8, 16, 16>;
 using CP512 = ComplexPlan<512, 16, 32, 16>;
 using CP1024 = ComplexPlan<1024, 32, 32, 32>;
 using CP2048 = ComplexPlan<2048, 64, 32, 2, 32>;
-using CP4096 = ComplexPlan<4096, 128, 32, 4, 32>;
+using CP4096 = ComplexPlan<4096, 128, 16, 16, 16>;  // two butterflies per thread at both ends: adjacent pairs
 using CP8192 = ComplexPlan<8192, 256, 32, 8, 32>;
 using CP16384 = ComplexPlan<16384, 512, 32, 16, 32>;
 

@@ -10,8 +10,11 @@
 //
 // Which butterflies a thread owns in the first and last pass is a policy
 // (KIND): 0 plain (j = t + T*beta), 1 mirrored pairs (p, T*B-1-p), 2 negated
-// pairs (p, NB-p) with (0, NB/2) for p = 0.  The real path uses 1 and 2 so
-// that whole float4 chunks and Makhoul partners stay thread-local.
+// pairs (p, NB-p) with (0, NB/2) for p = 0, 3 adjacent pairs (2p, 2p+1),
+// p = t + T*(beta/2).  The real path uses 1 and 2 so that whole float4
+// chunks and Makhoul partners stay thread-local; the complex path uses 3
+// where its plan allows, so that neighbouring elements share a thread and
+// every row access is 16 bytes.
 #pragma once
 
 #include "acdc_dft.hpp"
@@ -26,9 +29,12 @@ __host__ __device__ __forceinline__ unsigned bfly(unsigned t, int beta) {
   } else if constexpr (KIND == 1) {
     const unsigned p = t + PL::T * (beta >> 1);
     return (beta & 1) ? PL::T * B - 1 - p : p;
-  } else {
+  } else if constexpr (KIND == 2) {
     const unsigned p = t + PL::T * (beta >> 1);
     return (beta & 1) ? (p == 0 ? PL::NB / 2 : PL::NB - p) : p;
+  } else {
+    static_assert(KIND == 3 && B % 2 == 0, "adjacent pairs need an even butterfly count");
+    return 2u * (t + PL::T * unsigned(beta >> 1)) + unsigned(beta & 1);
   }
 }
 
