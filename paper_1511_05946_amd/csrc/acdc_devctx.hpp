@@ -29,6 +29,23 @@ struct DevCtx {
     }
   }
   __device__ __forceinline__ void sync_all() { lds_barrier(); }
+
+  // gfx950 cross-lane swaps of the pair (a, b), in place, per group of 16
+  // lanes r0..r3 (lanes 0-15, 16-31, 32-47, 48-63 of the wave):
+  //   swap16: a <- (a.r0, b.r0, a.r2, b.r2), b <- (a.r1, b.r1, a.r3, b.r3)
+  //   swap32: a <- (a.lo, b.lo),             b <- (a.hi, b.hi)
+  // (lo, hi = lanes 0-31, 32-63), so a + b afterwards holds pair sums of
+  // a in one row (half) and of b in the other.
+  __device__ __forceinline__ static void swap16(float& a, float& b) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+  }
+  __device__ __forceinline__ static void swap32(float& a, float& b) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+  }
 };
 
 }  // namespace acdc

@@ -30,6 +30,9 @@
 #ifndef ACDC_CPLX_PAIRS
 #define ACDC_CPLX_PAIRS 1  // complex rows: adjacent butterfly pairs where the plan allows
 #endif
+#ifndef ACDC_XLANE_SUM
+#define ACDC_XLANE_SUM 0  // 1: rows of 16 lanes sum their images across the wave with lane swaps (measured slower)
+#endif
 #ifndef ACDC_LDS_PAD
 #define ACDC_LDS_PAD 1
 #endif

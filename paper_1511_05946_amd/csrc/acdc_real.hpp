@@ -310,6 +310,40 @@ struct RealOps {
         return false;
     return true;
   }(), "thread 0's permutation moves exactly the blocks v[RL/2..RL), v[3RL/2..2RL)");
+  // Rows of 16 lanes share a wave four at a time.  Their per-row images
+  // are summed across the wave's four rows before they reach LDS, with the
+  // gfx950 lane swaps (ctx.swap16 / swap32): for the float4 images f0..f3
+  // of four consecutive slots (or chunks) 4s .. 4s+3, stage 1 pairs f0 with
+  // f1 and f2 with f3 across rows (0,1), (2,3), stage 2 pairs the results
+  // across the halves, and row j of the wave ends with the 4-row sum of f_j
+  // (1.5 lane operations per float; the sum order is (r0 + r1) + (r2 + r3)).  Each row then writes one float4 in four,
+  // into the image of its wave (the slab of the wave's first row), and the
+  // cross-wave sum reads a quarter of the rows.
+  static constexpr bool XL = ACDC_XLANE_SUM && T == 16 && NSL % 4 == 0 && (P / 2) % 4 == 0;
+  // Stage 1 on (f0, f1) or (f2, f3): rows 0 / 2 get the first summed over
+  // their row pair, rows 1 / 3 the second.
+  template <class Ctx>
+  __host__ __device__ __forceinline__ static float4 xlane_pair16(Ctx& ctx, float4 f0, float4 f1) {
+    float a[4] = {f0.x, f0.y, f0.z, f0.w}, b[4] = {f1.x, f1.y, f1.z, f1.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      ctx.swap16(a[j], b[j]);
+      a[j] += b[j];
+    }
+    return make_float4(a[0], a[1], a[2], a[3]);
+  }
+  // Stage 2 on the two stage-1 results: row j ends with f_j summed over the
+  // wave's four rows.
+  template <class Ctx>
+  __host__ __device__ __forceinline__ static float4 xlane_pair32(Ctx& ctx, float4 h01, float4 h23) {
+    float a[4] = {h01.x, h01.y, h01.z, h01.w}, c[4] = {h23.x, h23.y, h23.z, h23.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      ctx.swap32(a[j], c[j]);
+      a[j] += c[j];
+    }
+    return make_float4(a[0], a[1], a[2], a[3]);
+  }
   // The DCT-III pre-twiddle of thread 0's slot 0 needs its own qb':
   // exp(i pi/8) / (2 sqrt(N)).
   static constexpr float kQbRe = float(0.9238795325112867561 / (2.0 * csqrt(double(N))));
@@ -392,31 +426,52 @@ struct RealOps {
   // H*G (the dL/dd term of this row, quartet layout) goes to the slab; then
   // g <- DCT-III pre-twiddle of G*d, from g's split (sym_back).  v is
   // consumed.
-  __host__ __device__ __forceinline__ static void mid_bwd(float2 (&v)[P], float2 (&g)[P], unsigned t, GView mq,
-                                                          MqTabs<3>& tb, float* slab) {
+  // One slot of the backward middle: returns the dL/dd image H*G and
+  // updates g's quartet in place.
+  __host__ __device__ __forceinline__ static float4 mid_bwd_slot(float2 (&v)[P], float2 (&g)[P], int slot,
+                                                                 const float4 (&c)[3]) {
+    const int q = slot / RL, i = slot % RL;
+    const float4 c0 = c[0], c1 = c[1], c2 = c[2];
+    const float2 w = make_float2(c1.z, c1.w), qa = make_float2(c2.x, c2.y), qbr = make_float2(c2.z, c2.w);
+    float2& gk = g[2 * q * RL + i];
+    float2& gm = g[2 * q * RL + 2 * RL - 1 - i];
+    float H[4], G[4];
+    post_x(split(v[2 * q * RL + i], v[2 * q * RL + 2 * RL - 1 - i], w), qa, qbr, H);
+    const Split sg = split(gk, gm, w);
+    post_x(sg, qa, qbr, G);
+    sym_back(sg, c0, c1, gk, gm);
+    return make_float4(H[0] * G[0], H[1] * G[1], H[2] * G[2], H[3] * G[3]);
+  }
+  // With XL each group of four consecutive slots' images is summed across
+  // the wave's rows (xlane_pair16 / xlane_pair32), and row rw writes slot
+  // 4s + rw of the sum into the wave image `wimg`.
+  template <class Ctx>
+  __host__ __device__ __forceinline__ static void mid_bwd(Ctx& ctx, float2 (&v)[P], float2 (&g)[P], unsigned t,
+                                                          GView mq, MqTabs<3>& tb, float* slab, float* wimg,
+                                                          unsigned rw) {
     constexpr int PFM = MqTabs<3>::PF;
     const bool sp = (t == 0);
     permute0(v, sp);
     permute0(g, sp);
+    float4 im0, h01;
 #pragma unroll
-    for (int q = 0; q < BL / 2; ++q)
-#pragma unroll
-      for (int i = 0; i < RL; ++i) {
-        const int slot = q * RL + i;
-        if (slot + PFM < NSL) load_mslot(tb, slot + PFM, t, mq);
-        ACDC_SCHED_FENCE();
-        const float4 c0 = tb.m[slot][0], c1 = tb.m[slot][1], c2 = tb.m[slot][2];
-        const float2 w = make_float2(c1.z, c1.w), qa = make_float2(c2.x, c2.y), qbr = make_float2(c2.z, c2.w);
-        float2& gk = g[2 * q * RL + i];
-        float2& gm = g[2 * q * RL + 2 * RL - 1 - i];
-        float H[4], G[4];
-        post_x(split(v[2 * q * RL + i], v[2 * q * RL + 2 * RL - 1 - i], w), qa, qbr, H);
-        const Split sg = split(gk, gm, w);
-        post_x(sg, qa, qbr, G);
-        reinterpret_cast<float4*>(slab)[slot * T + t] =
-            make_float4(H[0] * G[0], H[1] * G[1], H[2] * G[2], H[3] * G[3]);
-        sym_back(sg, c0, c1, gk, gm);
+    for (int n = 0; n < NSL; ++n) {
+      const int slot = n;
+      if (n + PFM < NSL) load_mslot(tb, n + PFM, t, mq);
+      ACDC_SCHED_FENCE();
+      const float4 c[3] = {tb.m[slot][0], tb.m[slot][1], tb.m[slot][2]};
+      const float4 im = mid_bwd_slot(v, g, slot, c);
+      if constexpr (!XL) {
+        reinterpret_cast<float4*>(slab)[slot * T + t] = im;
+      } else if (n % 2 == 0) {
+        im0 = im;
+      } else if (n % 4 == 1) {
+        h01 = xlane_pair16(ctx, im0, im);
+      } else {
+        const float4 sum = xlane_pair32(ctx, h01, xlane_pair16(ctx, im0, im));
+        reinterpret_cast<float4*>(wimg)[(unsigned(n - 3) + rw) * T + t] = sum;
       }
+    }
     unpermute0(g, sp);
   }
 };
@@ -496,6 +551,13 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
   const unsigned roff = rr * unsigned(N / 4);
   const typename O::Lane L = O::lane(t);
   float2* slab2 = reinterpret_cast<float2*>(slab);
+  // the images reach LDS one per row, or with XL one per wave (in the slab of
+  // the wave's first row), and the cross-row sums add SROWS of them
+  static_assert(!O::XL || ROWS % 4 == 0, "rows of 16 lanes fill whole waves");
+  constexpr int SROWS = O::XL ? ROWS / 4 : ROWS;
+  constexpr int SSTRIDE = O::XL ? 4 * PL::SLAB : PL::SLAB;
+  const unsigned rw = rr % 4u;  // row within its wave (XL)
+  float* const wimg = lds + (rr - rw) * PL::SLAB;
   // A row past the batch end reads the block's first row for u_k but starts
   // from g = 0, which every step keeps exactly zero (linear transforms,
   // diagonal scalings, masks); its images H * G and u * g therefore vanish
@@ -541,10 +603,10 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
       O::template fft<false>(ctx, g, t, slab2, tab, [&] { O::load_mhead(tb, t, mq); });
 #endif
       ctx.sync_row();
-      O::mid_bwd(v, g, t, mq, tb, slab);
+      O::mid_bwd(ctx, v, g, t, mq, tb, slab, wimg, rw);
     }
     ctx.sync_all();
-    sum_rows<ROWS, PL::SLAB, THREADS, QF>(lds, GView::of(part + N), tid);
+    sum_rows<SROWS, SSTRIDE, THREADS, QF>(lds, GView::of(part + N), tid);
     ctx.sync_all();
     // gh1 = DCT-III(gh3 * d); u_k is reloaded meanwhile
     O::template fft<true>(ctx, g, t, slab2, tab, [&] { O::load_raw(uv, u_view(k), roff, L, valid); });
@@ -554,21 +616,40 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
       // the dL/da image u * gh1 (spatial, natural order) goes to the slab.
       const bool mask = (a.flags & kFlagRelu) && k > 0;
       ctx.sync_row();
-      int n = 0;
-      O::for_chunks(g, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
+      auto chunk = [&](int n) {
+        float2& lo = g[O::ch_lo(n)];
+        float2& hi = g[O::ch_hi(n)];
         const float4 u = uv[n];
-        ++n;
         if (mask) {
           lo = make_float2(u.x > 0.f ? lo.x : 0.f, u.z > 0.f ? lo.y : 0.f);
           hi = make_float2(u.w > 0.f ? hi.x : 0.f, u.y > 0.f ? hi.y : 0.f);
         }
-        reinterpret_cast<float4*>(slab)[lc + cc] = make_float4(u.x * lo.x, u.y * hi.y, u.z * lo.y, u.w * hi.x);
-      });
+        return make_float4(u.x * lo.x, u.y * hi.y, u.z * lo.y, u.w * hi.x);
+      };
+      if constexpr (!O::XL) {
+#pragma unroll
+        for (int n = 0; n < NCH; ++n)
+          reinterpret_cast<float4*>(slab)[O::ch_lc(L, n) + O::ch_cc(n)] = chunk(n);
+      } else {
+        // chunks in groups of four, summed across the wave's rows; row rw
+        // writes the sum of chunk 4c + rw
+#pragma unroll
+        for (int c = 0; c < NCH / 4; ++c) {
+          const int n0 = 4 * c, n1 = n0 + 1, n2 = n0 + 2, n3 = n0 + 3;
+          const float4 h01 = O::xlane_pair16(ctx, chunk(n0), chunk(n1));
+          const float4 sum = O::xlane_pair32(ctx, h01, O::xlane_pair16(ctx, chunk(n2), chunk(n3)));
+          const unsigned p0 = O::ch_lc(L, n0) + O::ch_cc(n0), p1 = O::ch_lc(L, n1) + O::ch_cc(n1);
+          const unsigned p2 = O::ch_lc(L, n2) + O::ch_cc(n2), p3 = O::ch_lc(L, n3) + O::ch_cc(n3);
+          reinterpret_cast<float4*>(wimg)[rw == 0 ? p0 : rw == 1 ? p1 : rw == 2 ? p2 : p3] = sum;
+          ACDC_SCHED_FENCE();
+        }
+      }
     }
+    ACDC_SCHED_FENCE();  // the loads of a below stay behind the images (registers)
     O::load_vec(av, ak, L);
     ACDC_SCHED_FENCE();
     ctx.sync_all();
-    sum_rows<ROWS, PL::SLAB, THREADS, N>(lds, GView::of(part), tid);
+    sum_rows<SROWS, SSTRIDE, THREADS, N>(lds, GView::of(part), tid);
     ctx.sync_all();
     // dL/du = gh1 * a, then un-permute; the next layer's u loads meanwhile
     O::scale(g, av);

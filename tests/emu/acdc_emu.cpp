@@ -19,18 +19,40 @@ namespace {
 
 struct HostCtx {
   std::barrier<>* bar;
+  int tid;
+  float* xa;  // per-thread exchange slots of the cross-lane swaps
+  float* xb;
   void sync_row() { bar->arrive_and_wait(); }
   void sync_all() { bar->arrive_and_wait(); }
+  // The GPU's permlane16 / permlane32 swaps (acdc_devctx.hpp), through
+  // shared slots between two barriers.
+  template <int W>
+  void swap(float& a, float& b) {
+    xa[tid] = a;
+    xb[tid] = b;
+    bar->arrive_and_wait();
+    const int lane = tid % 64, base = tid - lane;
+    const bool upper = (lane / W) % 2 == 1;  // odd row (W = 16) or upper half (W = 32)
+    const int partner = base + (upper ? lane - W : lane + W);
+    const float na = upper ? xb[partner] : xa[tid];
+    const float nb = upper ? xb[tid] : xa[partner];
+    bar->arrive_and_wait();
+    a = na;
+    b = nb;
+  }
+  void swap16(float& a, float& b) { swap<16>(a, b); }
+  void swap32(float& a, float& b) { swap<32>(a, b); }
 };
 
 template <class F>
 void run_wg(int threads, F&& body) {
   std::barrier<> bar(threads);
+  std::vector<float> xa(threads), xb(threads);
   std::vector<std::thread> th;
   th.reserve(threads);
   for (int tid = 0; tid < threads; ++tid)
     th.emplace_back([&, tid] {
-      HostCtx ctx{&bar};
+      HostCtx ctx{&bar, tid, xa.data(), xb.data()};
       body(ctx, tid);
     });
   for (auto& x : th) x.join();
