@@ -16,8 +16,8 @@ using RP32 = RealPlan<32, 2, 4, 4>;
 using RP64 = RealPlan<64, 2, 4, 8>;
 using RP128 = RealPlan<128, 4, 8, 8>;
 using RP256 = RealPlan<256, 4, 16, 8>;
-using RP512 = RealPlan<512, 8, 16, 16>;
-using RP1024 = RealPlan<1024, 16, 16, 2, 16>;
+using RP512 = RealPlan<512, 16, 8, 4, 8>;  // 16 complex values per thread
+using RP1024 = RealPlan<1024, 32, 8, 8, 8>;  // 16 complex values per thread: 125 VGPRs forward, 4 waves per SIMD
 using RP2048 = RealPlan<2048, 32, 16, 4, 16>;
 using RP4096 = RealPlan<4096, 64, 16, 8, 16>;
 using RP8192 = RealPlan<8192, 128, 16, 16, 16>;
