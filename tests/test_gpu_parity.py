@@ -529,3 +529,25 @@ def test_multipass_empty_batch(acdc):
     assert y.shape == (0, N)
     gx, gA, gD, gB = acdc.backward(x, x.clone(), A, A.clone(), None, 0, bias=b)
     assert not host(gA).any() and not host(gD).any() and not host(gB).any()
+
+
+@pytest.mark.parametrize("N,K,flags", [(4096, 12, P | R), (1024, 6, P | R), (9216, 3, P | R), (2048, 3, CX | P)])
+def test_rows_independent_of_tiling(acdc, N, K, flags):
+    # Rows are independent in the forward and in grad_x: a row's results must
+    # not depend on how many rows share its launch, i.e. on the workgroup
+    # count, the persistent forward's tile assignment or the rows beside it
+    # in a tile.  Run the batch whole and in offset slices, bit for bit.
+    import torch
+    B = {4096: 1200, 1024: 900, 9216: 70, 2048: 130}[N]
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, 60 + N)
+    fl = flags & ~CX
+    xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
+    y, sv = acdc.forward(xt, At, Dt, pt, fl, save=True)
+    gx = acdc.backward(xt, gyt, At, Dt, pt, fl, saved=sv)[0]
+    yh, gxh = host(y), host(gx)
+    for lo, hi in ((0, 1), (3, B // 3), (B // 3, B - 5), (B - 7, B)):
+        xs, gs = xt[lo:hi].contiguous(), gyt[lo:hi].contiguous()
+        ys, ss = acdc.forward(xs, At, Dt, pt, fl, save=True)
+        assert np.array_equal(host(ys), yh[lo:hi]), (lo, hi)
+        assert np.array_equal(host(acdc.backward(xs, gs, At, Dt, pt, fl, saved=ss)[0]), gxh[lo:hi]), (lo, hi)
+    torch.cuda.synchronize()
