@@ -5,7 +5,9 @@
 //   k_real_fwd     forward cascade, ROWS rows per workgroup, all K layers
 //                  fused, rows kept in registers + one LDS slab per row
 //   k_real_bwd     backward cascade with the reduction of dL/da, dL/dd over
-//                  the workgroup's rows into one partial per workgroup
+//                  the workgroup's rows into one partial per tile, or (wide
+//                  unbiased rows) persistent workgroups that add their tiles
+//                  into one partial each
 //   k_real_reduce  fixed-order sum of the partials over workgroups
 //   k_real_dct     DCT-II of the batch sums of g (bias gradient, tiny)
 // The multi-pass path (acdc_multipass.hip) serves widths beyond the fused
@@ -84,20 +86,32 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::FWD_WPE))) void k_real_fwd(RealAr
 
 template <class PL, bool BIAS>
 __global__ __launch_bounds__(Launch<PL>::BWD_THREADS)
-__attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealArgs a) {
+__attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealArgs a, long long ntiles) {
   using L = Launch<PL>;
-  __shared__ float lds[L::BWD_LDS_FLOATS];
+  constexpr bool ACC = L::BWD_ACC && !BIAS;
+  __shared__ float lds[L::BWD_LDS_FLOATS + (ACC ? L::ACC_FLOATS : 0)];
   DevCtx<PL::T> ctx;
   const int tid = threadIdx.x;
   const unsigned t = unsigned(tid) % PL::T;
   int r = tid / PL::T;
   if constexpr (PL::T >= 64) r = __builtin_amdgcn_readfirstlane(r);  // one row per whole wave
-  // LDS: [twiddle copy (TW_FLOATS)][row slabs]; the table sits at offset 0
-  // so that its loads address it through the instruction's immediate offset
+  // LDS: [twiddle copy (TW_FLOATS)][row slabs][previous partial values (ACC)];
+  // the table sits at offset 0 so that its loads address it through the
+  // instruction's immediate offset
   float* const rows = lds + L::BWD_TW_FLOATS;
   float* slab = rows + r * L::BWD_SLAB;
-  // one tile per workgroup (a loop over tiles here would keep its
-  // invariants live across the whole layer loop)
+  if constexpr (ACC) {
+    // persistent: workgroup w runs tiles w, w + G, ... (G = gridDim.x) and
+    // adds them, in that order, into partial slot w
+    static_assert(!L::BWD_TW_LDS, "persistent backward reads its twiddles from global memory");
+    float* const old = lds + L::BWD_LDS_FLOATS;
+    const unsigned w = blockIdx.x, nt = unsigned(ntiles);  // tiles < 2^31: batch <= 2^40 / N rows and N >= 1024
+    for (unsigned tile = w; tile < nt; tile += gridDim.x)
+      real_backward_row<PL, L::BWD_ROWS, BIAS, true>(ctx, a, t, (long long)tile * L::BWD_ROWS, unsigned(r), tid, w,
+                                                     rows, slab, GView::of(a.tab), tile == w ? nullptr : old);
+    return;
+  }
+  // one tile per workgroup, one partial slot per tile
   const long long tile = blockIdx.x;
   if constexpr (L::BWD_TW_LDS) {
     float* twl = lds;
@@ -976,10 +990,12 @@ extern "C" int acdc_prepare(int32_t N, uint32_t flags) {
   const char* tab = nullptr;
   rc = get_table(N, (flags & kFlagComplex) != 0, &tab);
   if (rc != ACDC_OK || (flags & kFlagComplex)) return rc;
-  // cache the persistent forward grids, so that later calls look them up
+  // cache the persistent grids, so that later calls look them up
   dispatch_real(N, [&]<class PL>() {
     (void)resident_workgroups(reinterpret_cast<const void*>(&k_real_fwd<PL, false>), Launch<PL>::FWD_THREADS);
     (void)resident_workgroups(reinterpret_cast<const void*>(&k_real_fwd<PL, true>), Launch<PL>::FWD_THREADS);
+    if constexpr (Launch<PL>::BWD_ACC)
+      (void)resident_workgroups(reinterpret_cast<const void*>(&k_real_bwd<PL, false>), Launch<PL>::BWD_THREADS);
   });
   return ACDC_OK;
 }
@@ -1145,6 +1161,12 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
     dispatch_real(N, [&]<class PL>() {
       using L = Launch<PL>;
       const long long tiles = bwd_tiles<PL>(batch);
+      // partial slots: one per tile, or one per resident workgroup of the
+      // persistent (accumulating) unbiased backward
+      const long long slots =
+          (L::BWD_ACC && !bias_on)
+              ? persistent_grid(reinterpret_cast<const void*>(&k_real_bwd<PL, false>), L::BWD_THREADS, tiles)
+              : tiles;
       float4* Mq = reinterpret_cast<float4*>(ws + w.off_mq);
       float* gS = bias_on ? reinterpret_cast<float*>(ws + w.off_gs) : nullptr;
       if (batch > 0 || bias_on) {
@@ -1161,8 +1183,10 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
         hipError_t e;
         {
           ProfScope prof(1, s);
-          if (bias_on) hipLaunchKernelGGL((k_real_bwd<PL, true>), dim3(unsigned(tiles)), dim3(L::BWD_THREADS), 0, s, a);
-          else hipLaunchKernelGGL((k_real_bwd<PL, false>), dim3(unsigned(tiles)), dim3(L::BWD_THREADS), 0, s, a);
+          if (bias_on)
+            hipLaunchKernelGGL((k_real_bwd<PL, true>), dim3(unsigned(tiles)), dim3(L::BWD_THREADS), 0, s, a, tiles);
+          else
+            hipLaunchKernelGGL((k_real_bwd<PL, false>), dim3(unsigned(slots)), dim3(L::BWD_THREADS), 0, s, a, tiles);
           e = hipGetLastError();
         }
         if (e != hipSuccess) {
@@ -1175,7 +1199,7 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
       {
         ProfScope prof(2, s);
         hipLaunchKernelGGL(k_real_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(256), 0, s,
-                           partial, tiles, K, grad_A, grad_D, gS, tab, bias_on ? 1 : 0, accumulate);
+                           partial, slots, K, grad_A, grad_D, gS, tab, bias_on ? 1 : 0, accumulate);
         e = hipGetLastError();
         if (e == hipSuccess && bias_on) {
           hipLaunchKernelGGL(k_real_dct<PL>, dim3(unsigned(K)), dim3(PL::T), 0, s, gS, grad_bias, Mq, tab,

@@ -89,6 +89,20 @@ struct GView {
     return v;
 #endif
   }
+  // 16 bytes per lane straight into LDS (buffer_load_dwordx4 ... lds): lane
+  // l's bytes land at lds + 16 l, with lds the same for the whole wave.  No
+  // register holds the data; the wave's vmcnt covers the copy.  The load is
+  // device-coherent (sc1: it misses the L1), so it reads what this workgroup
+  // stored earlier.
+  __host__ __device__ __forceinline__ void ld_lds16(float* lds, unsigned lane, unsigned voff, unsigned soff) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    (void)lane;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, soff, 0,
+                                             16 /* sc1 */);
+#else
+    std::memcpy(lds + 4 * lane, p + voff + soff, 16);
+#endif
+  }
   // Stores go through a plain global pointer: buffer stores fed from the
   // register arrays defeat register promotion of those arrays in this
   // compiler (they end up in private scratch), so only loads use the buffer

@@ -40,6 +40,7 @@
 namespace acdc {
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
+constexpr int cmin(int a, int b) { return a < b ? a : b; }
 constexpr double csqrt(double x) {
   double r = x > 1 ? x : 1.0;
   for (int i = 0; i < 64; ++i) r = 0.5 * (r + x / r);

@@ -489,7 +489,7 @@ struct RealArgs {
                        // PERM u_0 in slot K-1 (may be null)
   const float* gy;     // backward: upstream gradient
   float* gx;           // backward: input gradient
-  float* partial;      // backward: [tiles][K][N + QF] per-tile sums
+  float* partial;      // backward: [slots][K][N + QF] sums, one slot per tile or per persistent workgroup
   const char* tab;     // plan tables
   long long batch;
   int K;
@@ -537,9 +537,17 @@ __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned 
   if (a.y != nullptr && valid) O::store(GView::of(a.y + row0 * N), roff, v, L);
 }
 
-template <class PL, int ROWS, bool BIAS, class Ctx, class TW>
+// Backward of one row of a tile (ROWS rows, one workgroup).  The tile's
+// dL/da and dL/dd images go to partial slot `slot`.  With ACC the
+// workgroup runs several tiles in turn and adds each one's images to the
+// slot: `old` (LDS, max(N, QF) floats) is null on its first tile, and on
+// the others receives the slot's previous values ahead of each sum
+// (direct-to-LDS loads issued one phase early).
+template <class PL, int ROWS, bool BIAS, bool ACC = false, class Ctx, class TW>
 __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned t, long long row0, unsigned rr,
-                                           int tid, long long tile, float* lds, float* slab, TW tab) {
+                                           int tid, long long slot, float* lds, float* slab, TW tab,
+                                           float* old = nullptr) {
+  static_assert(!(ACC && BIAS), "the biased backward writes one partial per tile");
   using O = RealOps<PL>;
   constexpr int N = PL::N, P = PL::P, NSL = PL::NSL, T = PL::T, QF = PL::QF, NCH = O::NCH;
   constexpr int THREADS = ROWS * T;
@@ -576,7 +584,10 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
   for (int k = a.K - 1; k >= 0; --k) {
     const GView ak = GView::of(a.A + (long long)k * N);
     const GView mq = GView::of(a.Mq + (long long)k * NSL * kMqRows * T);
-    float* part = a.partial + (tile * a.K + k) * PS;
+    float* part = a.partial + (slot * a.K + k) * PS;
+    // the slot's dL/dd values from earlier tiles, for the sum after the middle
+    if constexpr (ACC)
+      if (old != nullptr) lds_fetch<QF, THREADS>(old, GView::of(part + N), tid);
     if constexpr (BIAS) {
       // dL/db_k = sum over rows of DCT(g) = DCT(sum over rows of g): the
       // tile sums g here (spatial, natural order); one DCT per layer of the
@@ -605,9 +616,14 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
       ctx.sync_row();
       O::mid_bwd(ctx, v, g, t, mq, tb, slab, wimg, rw);
     }
+    if constexpr (ACC)
+      if (old != nullptr) lds_fetch_wait();
     ctx.sync_all();
-    sum_rows<SROWS, SSTRIDE, THREADS, QF>(lds, GView::of(part + N), tid);
+    sum_rows<SROWS, SSTRIDE, THREADS, QF>(lds, GView::of(part + N), tid, ACC ? old : nullptr);
     ctx.sync_all();
+    // and its dL/da values, for the sum after the inverse transform
+    if constexpr (ACC)
+      if (old != nullptr) lds_fetch<N, THREADS>(old, GView::of(part), tid);
     // gh1 = DCT-III(gh3 * d); u_k is reloaded meanwhile
     O::template fft<true>(ctx, g, t, slab2, tab, [&] { O::load_raw(uv, u_view(k), roff, L, valid); });
     {
@@ -646,10 +662,12 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
       }
     }
     ACDC_SCHED_FENCE();  // the loads of a below stay behind the images (registers)
+    if constexpr (ACC)
+      if (old != nullptr) lds_fetch_wait();  // only the fetch is still outstanding here
     O::load_vec(av, ak, L);
     ACDC_SCHED_FENCE();
     ctx.sync_all();
-    sum_rows<SROWS, SSTRIDE, THREADS, N>(lds, GView::of(part), tid);
+    sum_rows<SROWS, SSTRIDE, THREADS, N>(lds, GView::of(part), tid, ACC ? old : nullptr);
     ctx.sync_all();
     // dL/du = gh1 * a, then un-permute; the next layer's u loads meanwhile
     O::scale(g, av);

@@ -81,6 +81,19 @@ using CP16384 = ComplexPlan<16384, 512, 32, 16, 32>;
 #ifndef ACDC_TW_LDS_BWD
 #define ACDC_TW_LDS_BWD 0
 #endif
+// Persistent backward workgroups that add their tiles into one partial each
+// (unbiased real rows, tiles of at most ACDC_BWD_ACC_MAX_ROWS rows): 0 turns
+// them off.  Each added tile first fetches the slot's previous values, and
+// the vector-memory counter completes in order, so every later load waits
+// for that fetch too: at N = 4096 (8-row tiles) the backward lost more
+// (0.087 ms) than the smaller reduction saved (0.059 ms); at N = 9216
+// (2-row tiles, twice the partial bytes per row) the step gained 2.5 %.
+#ifndef ACDC_BWD_ACC
+#define ACDC_BWD_ACC 1
+#endif
+#ifndef ACDC_BWD_ACC_MAX_ROWS
+#define ACDC_BWD_ACC_MAX_ROWS 2
+#endif
 constexpr int kLdsBytes = 160 * 1024;
 template <class PL>
 struct Launch {
@@ -107,6 +120,18 @@ struct Launch {
   // Occupancy the register allocator must reach (512 / WPE registers per lane).
   static constexpr int FWD_WPE = 2;
   static constexpr int BWD_WPE = 2;
+  // Persistent accumulation keeps the previous partial values of one sum
+  // (max(N, QF) floats) in LDS after the row slabs.  It is used where that
+  // fits and does not cost a resident workgroup: the count that the LDS
+  // allows stays at least the count that BWD_WPE waves per SIMD allow.
+  static constexpr int ACC_FLOATS = cmax(PL::N, PL::QF);
+  static constexpr int BWD_WAVE_WGS = (4 * BWD_WPE * 64) / BWD_THREADS;
+  static constexpr int BWD_ACC_LDS_BYTES = BWD_LDS_BYTES + ACC_FLOATS * 4;
+  static constexpr bool BWD_ACC = ACDC_BWD_ACC && !PL::kComplex && PL::N >= 1024 &&
+                                  BWD_ROWS <= ACDC_BWD_ACC_MAX_ROWS && (PL::N / 4) % 64 == 0 &&
+                                  (PL::QF / 4) % 64 == 0 && BWD_THREADS % 64 == 0 &&
+                                  BWD_ACC_LDS_BYTES <= kLdsBytes &&
+                                  kLdsBytes / BWD_ACC_LDS_BYTES >= cmin(kLdsBytes / BWD_LDS_BYTES, BWD_WAVE_WGS);
   static_assert(FWD_LDS_BYTES <= kLdsBytes && BWD_LDS_BYTES <= kLdsBytes, "LDS budget");
   static_assert(BWD_THREADS <= 1024 && FWD_THREADS <= 1024, "workgroup size");
 };

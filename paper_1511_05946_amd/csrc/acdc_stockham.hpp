@@ -285,10 +285,12 @@ __host__ __device__ __forceinline__ void stockham_fft2(Ctx& ctx, float2 (&v)[PL:
 }
 
 // Sum the per-row images [rows][SLAB] of a workgroup in fixed row order and
-// write the first NFL floats to out (float4 granularity).  Called by every
-// thread; the trip count is a compile-time constant.
+// write the first NFL floats to out (float4 granularity).  With `old` (LDS,
+// NFL floats) the sum is added to it afterwards: old + (row 0 + ... ).
+// Called by every thread; the trip count is a compile-time constant.
 template <int ROWS, int SLAB, int THREADS, int NFL>
-__host__ __device__ __forceinline__ void sum_rows(const float* lds, GView out, int tid) {
+__host__ __device__ __forceinline__ void sum_rows(const float* lds, GView out, int tid,
+                                                  const float* old = nullptr) {
   constexpr int N4 = NFL / 4;
 #pragma unroll
   for (int e0 = 0; e0 < N4; e0 += THREADS) {
@@ -303,9 +305,44 @@ __host__ __device__ __forceinline__ void sum_rows(const float* lds, GView out, i
         s.z += u.z;
         s.w += u.w;
       }
+      if (old != nullptr) {
+        const float4 o = reinterpret_cast<const float4*>(old)[e];
+        s = make_float4(o.x + s.x, o.y + s.y, o.z + s.z, o.w + s.w);
+      }
       out.st4(s, e * 16u, 0u);
     }
   }
+}
+
+// Copy NFL floats of global memory (view src, from its base) into LDS at
+// dst, the workgroup's THREADS threads together, each wave 1 KiB blocks.  On
+// the GPU these are direct-to-LDS loads that complete in the background;
+// lds_fetch_wait() then the workgroup barrier publish them.
+template <int NFL, int THREADS>
+__host__ __device__ __forceinline__ void lds_fetch(float* dst, GView src, int tid) {
+  constexpr int N4 = NFL / 4;
+  static_assert(NFL % 4 == 0 && THREADS % 64 == 0, "whole waves of float4");
+  const unsigned lane = unsigned(tid) % 64u;
+#if defined(__HIP_DEVICE_COMPILE__)
+  const unsigned w = __builtin_amdgcn_readfirstlane(unsigned(tid) / 64u);
+#else
+  const unsigned w = unsigned(tid) / 64u;
+#endif
+#pragma unroll
+  for (int i = 0; i < (N4 + THREADS - 1) / THREADS; ++i) {
+    const unsigned e0 = w * 64u + unsigned(i * THREADS);  // this wave's first float4
+    if (N4 % THREADS == 0 || e0 < unsigned(N4)) {
+      static_assert(N4 % 64 == 0, "blocks of 64 float4");
+      src.ld_lds16(dst + e0 * 4u, lane, lane * 16u, e0 * 16u);
+    }
+  }
+}
+// Wait for this wave's outstanding vector-memory operations, the
+// direct-to-LDS loads included (vmcnt(0); expcnt and lgkmcnt left open).
+__host__ __device__ __forceinline__ void lds_fetch_wait() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+#endif
 }
 
 }  // namespace acdc

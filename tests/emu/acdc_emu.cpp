@@ -115,16 +115,41 @@ void real_fwd(const float* x, float* y, const float* A, const float* D, const fl
   else real_fwd_k<PL, false>(a, tab);
 }
 
+// Persistent backward workgroups to emulate (0: one workgroup per tile, as
+// the GPU runs plans without persistent accumulation or with at least as
+// many resident workgroups as tiles).
+long long g_bwd_slots = 0;
+
 template <class PL, bool BIAS>
-void real_bwd_k(const RealArgs& a, long long ntiles, float* lds_rows, const std::vector<unsigned char>& tab) {
+constexpr bool emu_acc() {
+  return Launch<PL>::BWD_ACC && !BIAS;
+}
+
+// Partial slots of a backward over ntiles tiles.
+template <class PL, bool BIAS>
+long long bwd_slots(long long ntiles) {
+  return (emu_acc<PL, BIAS>() && g_bwd_slots > 0 && g_bwd_slots < ntiles) ? g_bwd_slots : ntiles;
+}
+
+template <class PL, bool BIAS>
+void real_bwd_k(const RealArgs& a, long long ntiles, float* lds, const std::vector<unsigned char>& tab) {
   using L = Launch<PL>;
-  for (long long wg = 0; wg < ntiles; ++wg)
-    run_wg(L::BWD_THREADS, [&](HostCtx& ctx, int tid) {
-      const int r = tid / PL::T, t = tid % PL::T;
-      float* slab = lds_rows + (size_t)r * L::BWD_SLAB;
-      real_backward_row<PL, L::BWD_ROWS, BIAS>(ctx, a, unsigned(t), wg * L::BWD_ROWS, unsigned(r), tid, wg, lds_rows,
-                                               slab, GView::of(tab.data()));
-    });
+  const long long slots = bwd_slots<PL, BIAS>(ntiles);
+  // workgroup w runs tiles w, w + slots, ... in turn, as the persistent
+  // kernel does, adding them into slot w (its LDS kept across its tiles)
+  for (long long w = 0; w < slots; ++w)
+    for (long long tile = w; tile < ntiles; tile += slots)
+      run_wg(L::BWD_THREADS, [&](HostCtx& ctx, int tid) {
+        const int r = tid / PL::T, t = tid % PL::T;
+        float* slab = lds + (size_t)r * L::BWD_SLAB;
+        if constexpr (emu_acc<PL, BIAS>())
+          real_backward_row<PL, L::BWD_ROWS, BIAS, true>(ctx, a, unsigned(t), tile * L::BWD_ROWS, unsigned(r), tid, w,
+                                                         lds, slab, GView::of(tab.data()),
+                                                         tile == w ? nullptr : lds + L::BWD_LDS_FLOATS);
+        else
+          real_backward_row<PL, L::BWD_ROWS, BIAS>(ctx, a, unsigned(t), tile * L::BWD_ROWS, unsigned(r), tid, w, lds,
+                                                   slab, GView::of(tab.data()));
+      });
 }
 
 template <class PL>
@@ -145,15 +170,16 @@ void real_bwd(const float* x, const float* gy, const float* A, const float* D, c
   }
   const std::vector<float4> mq = quartet_coefficients<PL>(D, bias ? B : nullptr, K, tab);
   const long long ntiles = (batch + L::BWD_ROWS - 1) / L::BWD_ROWS;
+  const long long slots = bias ? bwd_slots<PL, true>(ntiles) : bwd_slots<PL, false>(ntiles);
   const long long PS4 = partial_entries4<PL>(bias);
-  std::vector<float> partial((size_t)ntiles * K * PS4 * 4);
+  std::vector<float> partial((size_t)slots * K * PS4 * 4);
   RealArgs a{x, nullptr, A, mq.data(), perm, const_cast<float*>(saved), gy, gx, partial.data(),
              (const char*)tab.data(), batch, K, flags};
-  std::vector<float> lds((size_t)L::BWD_LDS_FLOATS);
+  std::vector<float> lds((size_t)L::BWD_LDS_FLOATS + L::ACC_FLOATS);
   if (bias) real_bwd_k<PL, true>(a, ntiles, lds.data(), tab);
   else real_bwd_k<PL, false>(a, ntiles, lds.data(), tab);
   std::vector<float> gS(bias ? (size_t)K * PL::N : 0);
-  reduce_all<PL>(partial.data(), ntiles, K, PS4, [&](float4 s, int k, int e4) {
+  reduce_all<PL>(partial.data(), slots, K, PS4, [&](float4 s, int k, int e4) {
     real_reduce_store4<PL>(s, k, e4, gA, gD, gS.data(), (const char*)tab.data(), acc);
   });
   if (bias) {
@@ -259,6 +285,16 @@ extern "C" int acdc_emu_backward(const float* x, const float* gy, const float* A
     });
   }
   return rc;
+}
+
+// Emulate `slots` persistent backward workgroups where the plan accumulates
+// (0: one per tile).  Returns whether the unbiased backward of real rows of
+// width N accumulates in this build.
+extern "C" int acdc_emu_set_backward_slots(long long slots, int N) {
+  g_bwd_slots = slots;
+  int acc = 0;
+  dispatch_real(N, [&]<class PL>() { acc = Launch<PL>::BWD_ACC ? 1 : 0; });
+  return acc;
 }
 
 // The fixed-order batch reduction alone: out[e] (float4 e < n4) = the sum

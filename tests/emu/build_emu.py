@@ -18,8 +18,10 @@ def build() -> str:
     hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     os.makedirs(os.path.dirname(OUT), exist_ok=True)
     tmp = OUT + ".tmp"
+    # every plan from 1024 up may run as persistent accumulating workgroups
+    # here (acdc_emu_set_backward_slots), not only those that do on the GPU
     subprocess.run([hipcc, "-std=c++20", "-x", "hip", "--offload-host-only", "-O1", "-fPIC", "-shared",
-                    SRC, "-o", tmp, "-lpthread"], check=True, capture_output=True)
+                    "-DACDC_BWD_ACC_MAX_ROWS=16", SRC, "-o", tmp, "-lpthread"], check=True, capture_output=True)
     os.replace(tmp, OUT)
     return OUT
 

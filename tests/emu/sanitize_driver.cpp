@@ -4,8 +4,9 @@
 // tests/emu/build_sanitize.py, it runs
 //   1. the kernels' __host__ __device__ row bodies in the CPU emulation
 //      (acdc_emu.cpp) on small cascades of every flag combination, ragged
-//      last workgroups included, and checks determinism and that the saved
-//      and recompute backwards agree bit for bit;
+//      last workgroups included (and persistent backward workgroups that
+//      add several tiles into one partial), and checks determinism and that
+//      the saved and recompute backwards agree bit for bit;
 //   2. the C ABI's host-side argument validation and size arithmetic
 //      (acdc_api.hip, compiled for the host only) on bad, extreme and
 //      boundary arguments, which must return the documented status codes.
@@ -155,6 +156,10 @@ int main() {
       {4096, 1, 3, kFlagComplex},
   };
   for (const Case& c : cases) run_case(c);
+  // the persistent accumulating backward: 3 tiles of 2 rows over 2 slots
+  CHECK(acdc_emu_set_backward_slots(2, 9216) == 1);
+  run_case({9216, 2, 5, kFlagPerm});
+  acdc_emu_set_backward_slots(0, 9216);
   abi_checks();
   if (g_fail) {
     std::fprintf(stderr, "%d checks failed\n", g_fail);

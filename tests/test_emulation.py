@@ -32,6 +32,8 @@ def emu():
                                    ctypes.c_uint, P]
     L.acdc_emu_backward.argtypes = [P, P, P, P, P, P, P, P, P, P, P, ctypes.c_longlong, ctypes.c_int,
                                     ctypes.c_int, ctypes.c_uint]
+    L.acdc_emu_set_backward_slots.argtypes = [ctypes.c_longlong, ctypes.c_int]
+    L.acdc_emu_set_backward_slots.restype = ctypes.c_int
     return L
 
 
@@ -169,3 +171,31 @@ def test_backward_over_many_tiles(emu):
     # 61 backward tiles (N = 4096: 8 rows per tile) through the emulated
     # kernels and their reduction, against the oracle
     check(emu, 4096, 1, 61 * 8, 0, seed=61)
+
+
+@pytest.mark.parametrize("N,B,slots", [(1024, 83, 3), (9216, 7, 2)])
+def test_persistent_workgroups_accumulate(emu, N, B, slots):
+    # Persistent backward workgroups run several tiles each and add them into
+    # one partial slot, fetching the slot's earlier values into LDS before
+    # each sum.  With fewer slots than tiles (ragged last tile included),
+    # grad_x is bitwise that of one workgroup per tile and every gradient
+    # matches the oracle.
+    K, flags = 3 if N == 1024 else 2, O.FLAG_PERM
+    x, A, D, perm, gy = make_inputs(N, K, B, flags, 40 + slots)
+    runs = []
+    for s in (0, slots):
+        assert emu.acdc_emu_set_backward_slots(s, N) == 1
+        g = [np.zeros_like(x), np.zeros_like(A), np.zeros_like(D)]
+        try:
+            assert emu.acdc_emu_backward(_p(x), _p(gy), _p(A), _p(D), None, _p(perm), None, _p(g[0]), _p(g[1]),
+                                         _p(g[2]), None, B, N, K, flags) == 0
+        finally:
+            emu.acdc_emu_set_backward_slots(0, N)
+        runs.append(g)
+    np.testing.assert_array_equal(runs[1][0], runs[0][0])
+    ref = O.backward(x, gy, A, D, perm, flags)
+    for got, want in zip(runs[1], ref):
+        assert rel_err(got, want) < TOL_REAL
+    # the sums really were split over slots (tiles w, w + slots, ...: not the
+    # reduction's own tile phases): same values, another rounding order
+    assert not np.array_equal(runs[1][1], runs[0][1])

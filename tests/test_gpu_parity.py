@@ -200,6 +200,8 @@ def test_workloads_full_size_sampled(acdc, name):
     (4096, 8, 64, CX | P, 32),                   # afdf_n4096_k8_perm's width and depth (2 rows per tile)
     (9216, 16, 64, P | R, 32),                   # acdc_n9216_k16_perm_relu's width and depth (2 rows per tile)
     (9216, 16, 64, P, 32),                       # ... without ReLU: every stash slot, the K = 16 partials
+    (9216, 2, 1100, P, 550),                     # more tiles than resident workgroups (256 on MI355X): the
+                                                 # persistent backward adds 2 or 3 tiles into each partial
 ])
 def test_reduction_many_tiles(acdc, N, K, B, flags, tiles):
     print(f"[case] reduction over {tiles} tiles", flush=True)
