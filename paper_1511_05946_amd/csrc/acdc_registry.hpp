@@ -136,14 +136,17 @@ struct Launch {
   static_assert(BWD_THREADS <= 1024 && FWD_THREADS <= 1024, "workgroup size");
 };
 
-// ACDC_ONLY_N=<width> instantiates a single real plan (quick development
-// builds); ACDC_PLAN_SUBSET instantiates real plans 8, 64, 1024, 4096, 9216
-// and complex plans 16, 256, 4096 (the sanitizer build of the tests).  Every
-// other width then reports unsupported.
+// ACDC_ONLY_N=<width> instantiates a single real plan and ACDC_ONLY_CN a
+// single complex plan (quick development builds); ACDC_PLAN_SUBSET
+// instantiates real plans 8, 64, 1024, 4096, 9216 and complex plans 16, 256,
+// 4096 (the sanitizer build of the tests).  Every other width then reports
+// unsupported.
 template <class PLn>
 constexpr bool plan_built() {
 #if defined(ACDC_ONLY_N)
   return PLn::N == ACDC_ONLY_N && !PLn::kComplex;
+#elif defined(ACDC_ONLY_CN)
+  return PLn::N == ACDC_ONLY_CN && PLn::kComplex;
 #elif defined(ACDC_PLAN_SUBSET)
   return PLn::kComplex ? (PLn::N == 16 || PLn::N == 256 || PLn::N == 4096)
                        : (PLn::N == 8 || PLn::N == 64 || PLn::N == 1024 || PLn::N == 4096 || PLn::N == 9216);
