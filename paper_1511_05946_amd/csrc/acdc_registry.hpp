@@ -67,6 +67,12 @@ using CP16384 = ComplexPlan<16384, 512, 32, 16, 32>;
 #ifndef ACDC_TW_LDS_T
 #define ACDC_TW_LDS_T 0
 #endif
+// Rows per backward workgroup for real rows of 32 threads (N = 1024, 2048):
+// 8 (four waves, three workgroups per CU at 3 waves per SIMD) ran the
+// backward 6-8 % faster than 16, more than the doubled partials cost.
+#ifndef ACDC_BWD_ROWS_T32
+#define ACDC_BWD_ROWS_T32 8
+#endif
 // Rows per backward workgroup for the three-wave rows of N = 9216.
 #ifndef ACDC_BWD_ROWS_T192
 #define ACDC_BWD_ROWS_T192 2
@@ -105,8 +111,9 @@ struct Launch {
   static constexpr int FWD_ROWS =
       TW_LDS ? WIDE_ROWS : (PL::T >= ACDC_FWD_THREADS ? 1 : ACDC_FWD_THREADS / PL::T);
   static constexpr int BWD_ROWS =
-      PL::T == 192                      ? ACDC_BWD_ROWS_T192
-      : (PL::kComplex && PL::T == 128) ? ACDC_BWD_ROWS_CPLX_T128
+      (PL::T == 32 && !PL::kComplex)    ? ACDC_BWD_ROWS_T32
+      : PL::T == 192                    ? ACDC_BWD_ROWS_T192
+      : (PL::kComplex && PL::T == 128)  ? ACDC_BWD_ROWS_CPLX_T128
                                         : (TW_LDS ? WIDE_ROWS : (PL::T >= ACDC_BWD_THREADS ? 1 : ACDC_BWD_THREADS / PL::T));
   static constexpr bool BWD_TW_LDS = TW_LDS && ACDC_TW_LDS_BWD;
   static constexpr int FWD_THREADS = FWD_ROWS * PL::T;

@@ -193,7 +193,7 @@ def test_workloads_full_size_sampled(acdc, name):
 # as every benchmark batch does (128 to 1024 tiles); these cases compare the
 # batch-summed dL/da, dL/dd (and dL/db) with the oracle at such tile counts.
 @pytest.mark.parametrize("N,K,B,flags,tiles", [
-    (1024, 12, 4096, P, 256),                    # acdc_n1024_k12_perm at its full batch (16 rows per tile)
+    (1024, 12, 4096, P, 512),                    # acdc_n1024_k12_perm at its full batch (8 rows per tile)
     (4096, 12, 256, P, 32),                      # the headline width and depth, 8 rows per tile
     (4096, 12, 256, P | R, 32),                  # ... with ReLU (GPU decisions)
     (4096, 12, 256, P | R | FLAG_BIAS, 32),      # ... with the D-domain bias
