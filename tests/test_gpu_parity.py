@@ -208,8 +208,12 @@ def test_reduction_many_tiles(acdc, N, K, B, flags, tiles):
     run_case(acdc, N, K, B, flags, seed=500 + N + K + flags)
 
 
-def test_determinism_and_saved_equals_recompute(acdc):
-    N, K, B, flags = 1024, 6, 300, P | R
+@pytest.mark.parametrize("N,K,B", [(1024, 6, 300), (9216, 2, 1100)])
+def test_determinism_and_saved_equals_recompute(acdc, N, K, B):
+    # N = 9216 at 1100 rows runs the persistent backward (550 tiles added
+    # into one partial per resident workgroup): its fixed tile order keeps
+    # the gradients bitwise reproducible, with and without the stash
+    flags = P | R
     x, A, D, perm, gy = make_inputs(N, K, B, flags, 3)
     xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
     y1, s1 = acdc.forward(xt, At, Dt, pt, flags, save=True)
