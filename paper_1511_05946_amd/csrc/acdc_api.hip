@@ -5,9 +5,9 @@
 //   k_real_fwd     forward cascade, ROWS rows per workgroup, all K layers
 //                  fused, rows kept in registers + one LDS slab per row
 //   k_real_bwd     backward cascade with the reduction of dL/da, dL/dd over
-//                  the workgroup's rows into one partial per tile, or (wide
-//                  unbiased rows) persistent workgroups that add their tiles
-//                  into one partial each
+//                  the workgroup's rows into one partial per tile, or
+//                  (unbiased rows in tiles of at most two rows) persistent
+//                  workgroups that add their tiles into one partial each
 //   k_real_reduce  fixed-order sum of the partials over workgroups
 //   k_real_dct     DCT-II of the batch sums of g (bias gradient, tiny)
 // The multi-pass path (acdc_multipass.hip) serves widths beyond the fused

@@ -663,7 +663,7 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
     }
     ACDC_SCHED_FENCE();  // the loads of a below stay behind the images (registers)
     if constexpr (ACC)
-      if (old != nullptr) lds_fetch_wait();  // only the fetch is still outstanding here
+      if (old != nullptr) lds_fetch_wait();  // the fetch landed during the inverse transform
     O::load_vec(av, ak, L);
     ACDC_SCHED_FENCE();
     ctx.sync_all();
