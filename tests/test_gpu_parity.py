@@ -202,6 +202,8 @@ def test_workloads_full_size_sampled(acdc, name):
     (9216, 16, 64, P, 32),                       # ... without ReLU: every stash slot, the K = 16 partials
     (9216, 2, 1100, P, 550),                     # more tiles than resident workgroups (256 on MI355X): the
                                                  # persistent backward adds 2 or 3 tiles into each partial
+    (9216, 1, 513, P, 257),                      # one tile more than the resident workgroups, a ragged last
+                                                 # tile, a single layer: one workgroup adds a second tile
 ])
 def test_reduction_many_tiles(acdc, N, K, B, flags, tiles):
     print(f"[case] reduction over {tiles} tiles", flush=True)
