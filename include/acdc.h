@@ -164,8 +164,13 @@ int acdc_forward_noalloc(const float* x, float* y, const float* A, const float* 
                          const int32_t* perm, int64_t batch, int32_t N, int32_t K, uint32_t flags, float* saved,
                          size_t saved_bytes, acdc_stream_t stream);
 
-/* Backward cascade.  Given x and grad_y = dL/dy, writes grad_x = dL/dx and
- * grad_A, grad_D = dL/da_k, dL/dd_k summed over the batch, and with
+/* Backward cascade (Sec. 4, the derivatives of a layer with respect to x,
+ * a and d, chained through the cascade).  Given x and grad_y = dL/dy, writes
+ * grad_x = dL/dx and grad_A, grad_D = dL/da_k, dL/dd_k summed over the
+ * batch, in a fixed order that depends only on the batch size and the
+ * device (workgroups sum their rows, and the partials are then added in
+ * fixed phases; at N = 9216 each resident workgroup first adds its tiles
+ * into one partial), and with
  * ACDC_FLAG_BIAS grad_bias = dL/db_k (bias and grad_bias are then required,
  * and ignored otherwise).  The parameter gradients are overwritten, or with
  * ACDC_FLAG_ACCUMULATE added to what the arrays hold.  `saved` is the buffer
