@@ -90,7 +90,6 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealAr
   using L = Launch<PL>;
   constexpr bool ACC = L::BWD_ACC && !BIAS;
   __shared__ float lds[L::BWD_LDS_FLOATS + (ACC ? L::ACC_FLOATS : 0)];
-  DevCtx<PL::T> ctx;
   const int tid = threadIdx.x;
   const unsigned t = unsigned(tid) % PL::T;
   int r = tid / PL::T;
@@ -100,28 +99,40 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealAr
   // instruction's immediate offset
   float* const rows = lds + L::BWD_TW_FLOATS;
   float* slab = rows + r * L::BWD_SLAB;
-  if constexpr (ACC) {
-    // persistent: workgroup w runs tiles w, w + G, ... (G = gridDim.x) and
-    // adds them, in that order, into partial slot w
-    static_assert(!L::BWD_TW_LDS, "persistent backward reads its twiddles from global memory");
-    float* const old = lds + L::BWD_LDS_FLOATS;
-    const unsigned w = blockIdx.x, nt = unsigned(ntiles);  // tiles < 2^31: batch <= 2^40 / N rows and N >= 1024
-    for (unsigned tile = w; tile < nt; tile += gridDim.x)
-      real_backward_row<PL, L::BWD_ROWS, BIAS, true>(ctx, a, t, (long long)tile * L::BWD_ROWS, unsigned(r), tid, w,
-                                                     rows, slab, GView::of(a.tab), tile == w ? nullptr : old);
-    return;
-  }
-  // one tile per workgroup, one partial slot per tile
-  const long long tile = blockIdx.x;
-  if constexpr (L::BWD_TW_LDS) {
-    float* twl = lds;
-    copy_twiddles<PL>(twl, a.tab, tid, L::BWD_THREADS);
-    ctx.sync_all();
-    real_backward_row<PL, L::BWD_ROWS, BIAS>(ctx, a, t, tile * L::BWD_ROWS, unsigned(r), tid, tile, rows, slab,
-                                       LdsView::of(twl));
+  auto body = [&](auto& ctx) {
+    if constexpr (ACC) {
+      // persistent: workgroup w runs tiles w, w + G, ... (G = gridDim.x) and
+      // adds them, in that order, into partial slot w
+      static_assert(!L::BWD_TW_LDS, "persistent backward reads its twiddles from global memory");
+      float* const old = lds + L::BWD_LDS_FLOATS;
+      const unsigned w = blockIdx.x, nt = unsigned(ntiles);  // tiles < 2^31: batch <= 2^40 / N rows and N >= 1024
+      for (unsigned tile = w; tile < nt; tile += gridDim.x)
+        real_backward_row<PL, L::BWD_ROWS, BIAS, true>(ctx, a, t, (long long)tile * L::BWD_ROWS, unsigned(r), tid,
+                                                       w, rows, slab, GView::of(a.tab), tile == w ? nullptr : old);
+    } else if constexpr (L::BWD_TW_LDS) {
+      // one tile per workgroup, one partial slot per tile
+      const long long tile = blockIdx.x;
+      float* twl = lds;
+      copy_twiddles<PL>(twl, a.tab, tid, L::BWD_THREADS);
+      ctx.sync_all();
+      real_backward_row<PL, L::BWD_ROWS, BIAS>(ctx, a, t, tile * L::BWD_ROWS, unsigned(r), tid, tile, rows, slab,
+                                               LdsView::of(twl));
+    } else {
+      const long long tile = blockIdx.x;
+      real_backward_row<PL, L::BWD_ROWS, BIAS>(ctx, a, t, tile * L::BWD_ROWS, unsigned(r), tid, tile, rows, slab,
+                                               GView::of(a.tab));
+    }
+  };
+  if constexpr (L::BWD_GROUP_SYNC) {
+    // rows of several waves meet at their own LDS counter (GroupCtx)
+    __shared__ unsigned arrivals[L::BWD_ROWS];
+    if (tid < L::BWD_ROWS) arrivals[tid] = 0u;
+    DevCtx<PL::T>::lds_barrier();
+    GroupCtx<PL::T> ctx(&arrivals[r]);
+    body(ctx);
   } else {
-    real_backward_row<PL, L::BWD_ROWS, BIAS>(ctx, a, t, tile * L::BWD_ROWS, unsigned(r), tid, tile, rows, slab,
-                                       GView::of(a.tab));
+    DevCtx<PL::T> ctx;
+    body(ctx);
   }
 }
 
@@ -183,13 +194,22 @@ __global__ __launch_bounds__(Launch<PL>::BWD_THREADS)
 __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_cplx_bwd(CplxArgs a) {
   using L = Launch<PL>;
   __shared__ float lds[L::BWD_ROWS * L::BWD_SLAB];
-  DevCtx<PL::T> ctx;
   const int tid = threadIdx.x;
   const unsigned t = unsigned(tid) % PL::T;
   int r = tid / PL::T;
   if constexpr (PL::T >= 64) r = __builtin_amdgcn_readfirstlane(r);  // one row per whole wave
-  cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS, unsigned(r), tid,
-                                     (long long)blockIdx.x, lds, lds + r * L::BWD_SLAB);
+  if constexpr (L::BWD_GROUP_SYNC) {
+    __shared__ unsigned arrivals[L::BWD_ROWS];
+    if (tid < L::BWD_ROWS) arrivals[tid] = 0u;
+    DevCtx<PL::T>::lds_barrier();
+    GroupCtx<PL::T> ctx(&arrivals[r]);
+    cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS, unsigned(r), tid,
+                                       (long long)blockIdx.x, lds, lds + r * L::BWD_SLAB);
+  } else {
+    DevCtx<PL::T> ctx;
+    cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS, unsigned(r), tid,
+                                       (long long)blockIdx.x, lds, lds + r * L::BWD_SLAB);
+  }
 }
 
 template <class PL>

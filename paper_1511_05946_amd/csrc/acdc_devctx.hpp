@@ -4,6 +4,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstdint>
+
 namespace acdc {
 
 // LDS synchronisation for a row spread over T threads.  A row that fits in
@@ -46,6 +48,62 @@ struct DevCtx {
     a = __uint_as_float(r[0]);
     b = __uint_as_float(r[1]);
   }
+};
+
+// LDS synchronisation for rows of W = T/64 > 1 waves that meet only each
+// other, not the whole workgroup: the row's waves count arrivals in an LDS
+// word.  A wave adds 1 once its LDS accesses have completed and leaves when
+// the count reaches W times its own arrivals (the count only grows, so a
+// partner already at its next sync keeps it there).  The waves of a row make
+// the same sequence of sync_row calls, so the count always gets there; the
+// polling is also bounded, so every wave ends whatever happens.  sync_all
+// stays the workgroup barrier.  `cnt` must be zero, and seen as zero by the
+// whole workgroup, before the first sync_row.
+template <int T>
+struct GroupCtx {
+  static_assert(T > 64 && T % 64 == 0, "rows of whole waves");
+  static constexpr unsigned W = T / 64;
+  unsigned addr;  // LDS byte address of this row's arrival count
+  unsigned gen;   // W times this wave's arrivals so far
+  __device__ explicit GroupCtx(unsigned* c)
+      : addr(unsigned(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned*)c))), gen(0) {}
+  // One asm block (a single instruction to the register allocator, so the
+  // polling loop adds no control flow around the row code).  The wave's LDS
+  // accesses complete first (release), one lane adds 1 with the rest of the
+  // exec mask saved and restored, then the wave polls until the count
+  // reaches gen or the poll budget runs out.  The "memory" clobber keeps the
+  // compiler's LDS accesses on their side of it (acquire).
+  __device__ __forceinline__ void sync_row() {
+    gen += W;
+    unsigned long long save;
+    unsigned tmp, seen, g, it;
+    // Only VGPR inputs (they need not be known uniform, also at -O0); the
+    // uniform copies live in SGPRs the block declares as outputs.
+    asm volatile(
+        "s_waitcnt lgkmcnt(0)\n"
+        "v_readfirstlane_b32 %[g], %[genv]\n"
+        "s_mov_b32 %[it], 0x10000\n"  // poll budget (about 2 ms)
+        "s_mov_b64 %[save], exec\n"
+        "s_mov_b64 exec, 1\n"
+        "ds_add_u32 %[addr], %[one]\n"
+        "s_mov_b64 exec, %[save]\n"
+        "1:\n"
+        "ds_read_b32 %[tmp], %[addr]\n"
+        "s_waitcnt lgkmcnt(0)\n"
+        "v_readfirstlane_b32 %[seen], %[tmp]\n"
+        "s_cmp_ge_u32 %[seen], %[g]\n"
+        "s_cbranch_scc1 2f\n"
+        "s_sleep 1\n"
+        "s_sub_u32 %[it], %[it], 1\n"
+        "s_cbranch_scc0 1b\n"
+        "2:\n"
+        : [save] "=&s"(save), [tmp] "=&v"(tmp), [seen] "=&s"(seen), [g] "=&s"(g), [it] "=&s"(it)
+        : [addr] "v"(addr), [one] "v"(1u), [genv] "v"(gen)
+        : "scc", "memory");
+  }
+  __device__ __forceinline__ void sync_all() { DevCtx<T>::lds_barrier(); }
+  __device__ __forceinline__ static void swap16(float& a, float& b) { DevCtx<T>::swap16(a, b); }
+  __device__ __forceinline__ static void swap32(float& a, float& b) { DevCtx<T>::swap32(a, b); }
 };
 
 }  // namespace acdc

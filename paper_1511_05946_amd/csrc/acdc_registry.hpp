@@ -77,15 +77,24 @@ using CP16384 = ComplexPlan<16384, 512, 32, 16, 32>;
 #ifndef ACDC_BWD_ROWS_T192
 #define ACDC_BWD_ROWS_T192 2
 #endif
-// Rows per backward workgroup for the two-wave complex rows of N = 4096:
-// two 256-thread workgroups per CU instead of one of 512 threads keep one
-// workgroup's barriers off the other's path (backward 12 % faster, at the
-// cost of twice the partials; 2.5 % off the AFDF step).
+// Rows per backward workgroup for the two-wave complex rows of N = 4096.
+// With the workgroup barrier for every FFT exchange, two 256-thread
+// workgroups per CU beat one of 512 threads (backward 12 % faster, at twice
+// the partials).  With each row's waves meeting only each other
+// (GroupCtx), four rows per workgroup cost the backward 2 % and halve the
+// partials: step 0.803 -> 0.765 ms.
 #ifndef ACDC_BWD_ROWS_CPLX_T128
-#define ACDC_BWD_ROWS_CPLX_T128 2
+#define ACDC_BWD_ROWS_CPLX_T128 4
 #endif
 #ifndef ACDC_TW_LDS_BWD
 #define ACDC_TW_LDS_BWD 0
+#endif
+// Rows of several waves in multi-row backward workgroups meet at an LDS
+// counter of their own (GroupCtx) instead of the workgroup barrier at every
+// FFT exchange: 0 turns that off.  Measured (same results bit for bit):
+// backward 0.846 -> 0.774 ms at N = 9216, 0.775 -> 0.663 ms at N = 8192.
+#ifndef ACDC_GROUP_SYNC
+#define ACDC_GROUP_SYNC 1
 #endif
 // Persistent backward workgroups that add their tiles into one partial each
 // (unbiased real rows, tiles of at most ACDC_BWD_ACC_MAX_ROWS rows): 0 turns
@@ -116,6 +125,7 @@ struct Launch {
       : (PL::kComplex && PL::T == 128)  ? ACDC_BWD_ROWS_CPLX_T128
                                         : (TW_LDS ? WIDE_ROWS : (PL::T >= ACDC_BWD_THREADS ? 1 : ACDC_BWD_THREADS / PL::T));
   static constexpr bool BWD_TW_LDS = TW_LDS && ACDC_TW_LDS_BWD;
+  static constexpr bool BWD_GROUP_SYNC = ACDC_GROUP_SYNC && PL::T > 64 && PL::T % 64 == 0 && BWD_ROWS > 1;
   static constexpr int FWD_THREADS = FWD_ROWS * PL::T;
   static constexpr int BWD_THREADS = BWD_ROWS * PL::T;
   static constexpr int TW_FLOATS = TW_LDS ? PL::TW_FLOAT2 * 2 : 0;  // LDS copy of the twiddles

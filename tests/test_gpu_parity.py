@@ -197,7 +197,7 @@ def test_workloads_full_size_sampled(acdc, name):
     (4096, 12, 256, P, 32),                      # the headline width and depth, 8 rows per tile
     (4096, 12, 256, P | R, 32),                  # ... with ReLU (GPU decisions)
     (4096, 12, 256, P | R | FLAG_BIAS, 32),      # ... with the D-domain bias
-    (4096, 8, 64, CX | P, 32),                   # afdf_n4096_k8_perm's width and depth (2 rows per tile)
+    (4096, 8, 128, CX | P, 32),                  # afdf_n4096_k8_perm's width and depth (4 rows per tile)
     (9216, 16, 64, P | R, 32),                   # acdc_n9216_k16_perm_relu's width and depth (2 rows per tile)
     (9216, 16, 64, P, 32),                       # ... without ReLU: every stash slot, the K = 16 partials
     (9216, 2, 1100, P, 550),                     # more tiles than resident workgroups (256 on MI355X): the
