@@ -55,10 +55,12 @@ struct DevCtx {
 // word.  A wave adds 1 once its LDS accesses have completed and leaves when
 // the count reaches W times its own arrivals (the count only grows, so a
 // partner already at its next sync keeps it there).  The waves of a row make
-// the same sequence of sync_row calls, so the count always gets there; the
-// polling is also bounded, so every wave ends whatever happens.  sync_all
-// stays the workgroup barrier.  `cnt` must be zero, and seen as zero by the
-// whole workgroup, before the first sync_row.
+// the same sequence of sync_row calls and share a workgroup (resident, and
+// saved and restored together), so the count always gets there within the
+// time the slowest partner needs for the same work; the polling is also
+// bounded (2^20 polls, tens of milliseconds), so every wave ends whatever
+// happens.  sync_all stays the workgroup barrier.  `cnt` must be zero, and
+// seen as zero by the whole workgroup, before the first sync_row.
 template <int T>
 struct GroupCtx {
   static_assert(T > 64 && T % 64 == 0, "rows of whole waves");
@@ -82,7 +84,7 @@ struct GroupCtx {
     asm volatile(
         "s_waitcnt lgkmcnt(0)\n"
         "v_readfirstlane_b32 %[g], %[genv]\n"
-        "s_mov_b32 %[it], 0x10000\n"  // poll budget (about 2 ms)
+        "s_mov_b32 %[it], 0x100000\n"  // poll budget (2^20 polls, tens of ms)
         "s_mov_b64 %[save], exec\n"
         "s_mov_b64 exec, 1\n"
         "ds_add_u32 %[addr], %[one]\n"
