@@ -198,6 +198,19 @@ const char* acdc_status_string(int status);
 /* hipError_t behind the calling thread's most recent ACDC_ERR_HIP (0 if none). */
 int acdc_last_hip_error(void);
 
+/* Health check of the backward kernels' row synchronisation.  Where one
+ * batch row of the backward cascade (Sec. 4's gradients) spans several
+ * wavefronts, those waves meet at a counter of their own instead of the
+ * workgroup barrier, and each wait polls a bounded number of times (tens of
+ * milliseconds) so that a wave can never spin forever.  A wait that runs out
+ * of polls is counted on the device; its workgroup's results are then not
+ * to be trusted.  acdc_sync_timeouts writes the count of the current device
+ * (accumulated since the last clear) to *count and, when clear != 0, resets
+ * it.  It copies synchronously on the null stream: synchronise the streams
+ * that ran acdc_backward first.  Returns ACDC_ERR_INVALID_ARG for a null
+ * count, ACDC_ERR_HIP when a copy fails (then *count is 0). */
+int acdc_sync_timeouts(int64_t* count, int clear);
+
 #ifdef __cplusplus
 }
 #endif

@@ -32,6 +32,7 @@ SIGNATURES = {
     "acdc_profile_read": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     "acdc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "acdc_last_hip_error": (ctypes.c_int, []),
+    "acdc_sync_timeouts": (ctypes.c_int, [ctypes.POINTER(ctypes.c_int64), ctypes.c_int]),
 }
 
 

@@ -13,6 +13,8 @@ y = (x A C D + b) C^{-1}.
 
 from __future__ import annotations
 
+import ctypes
+
 import torch
 
 from ._lib import lib, status_string
@@ -106,6 +108,17 @@ def supported(N: int, flags: int = 0) -> bool:
 def prepare(N: int, flags: int = 0, device=None):
     with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
         _check(lib().acdc_prepare(int(N), int(flags)), "acdc_prepare")
+
+
+def sync_timeouts(device=None, clear: bool = False) -> int:
+    """Backward row syncs on `device` whose bounded wait ran out (0 when healthy).
+
+    Synchronises the device first; with clear=True the count restarts at 0."""
+    with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
+        torch.cuda.synchronize()
+        n = ctypes.c_int64(0)
+        _check(lib().acdc_sync_timeouts(ctypes.byref(n), int(bool(clear))), "acdc_sync_timeouts")
+        return int(n.value)
 
 
 def saved_numel(x: torch.Tensor, K: int, flags: int = 0) -> int:

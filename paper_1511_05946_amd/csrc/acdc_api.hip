@@ -28,6 +28,11 @@
 
 namespace acdc {
 
+// Number of row syncs (GroupCtx) on this device whose polling budget ran out
+// before the row's waves had all arrived; nonzero would mean wrong results.
+// acdc_sync_timeouts reads and clears it.
+static __device__ unsigned long long sync_timeouts;
+
 template <class PL>
 __global__ __launch_bounds__(256) void k_real_mq(const float* __restrict__ D, const float* __restrict__ Bias,
                                                  float4* __restrict__ Mq, int K, const char* __restrict__ tab) {
@@ -125,11 +130,13 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealAr
   };
   if constexpr (L::BWD_GROUP_SYNC) {
     // rows of several waves meet at their own LDS counter (GroupCtx)
-    __shared__ unsigned arrivals[L::BWD_ROWS];
-    if (tid < L::BWD_ROWS) arrivals[tid] = 0u;
+    using G = GroupCtx<PL::T>;
+    __shared__ unsigned words[G::kWords * L::BWD_ROWS];
+    if (tid < G::kWords * L::BWD_ROWS) words[tid] = 0u;
     DevCtx<PL::T>::lds_barrier();
-    GroupCtx<PL::T> ctx(&arrivals[r]);
+    G ctx(&words[G::kWords * r]);
     body(ctx);
+    G::report(words, L::BWD_ROWS, tid, &sync_timeouts);
   } else {
     DevCtx<PL::T> ctx;
     body(ctx);
@@ -199,12 +206,14 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_cplx_bwd(CplxAr
   int r = tid / PL::T;
   if constexpr (PL::T >= 64) r = __builtin_amdgcn_readfirstlane(r);  // one row per whole wave
   if constexpr (L::BWD_GROUP_SYNC) {
-    __shared__ unsigned arrivals[L::BWD_ROWS];
-    if (tid < L::BWD_ROWS) arrivals[tid] = 0u;
+    using G = GroupCtx<PL::T>;
+    __shared__ unsigned words[G::kWords * L::BWD_ROWS];
+    if (tid < G::kWords * L::BWD_ROWS) words[tid] = 0u;
     DevCtx<PL::T>::lds_barrier();
-    GroupCtx<PL::T> ctx(&arrivals[r]);
+    G ctx(&words[G::kWords * r]);
     cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS, unsigned(r), tid,
                                        (long long)blockIdx.x, lds, lds + r * L::BWD_SLAB);
+    G::report(words, L::BWD_ROWS, tid, &sync_timeouts);
   } else {
     DevCtx<PL::T> ctx;
     cplx_backward_row<PL, L::BWD_ROWS>(ctx, a, t, (long long)blockIdx.x * L::BWD_ROWS, unsigned(r), tid,
@@ -1274,3 +1283,18 @@ extern "C" const char* acdc_status_string(int status) {
 }
 
 extern "C" int acdc_last_hip_error(void) { return g_last_hip; }
+
+extern "C" int acdc_sync_timeouts(int64_t* count, int clear) {
+  if (count == nullptr) return ACDC_ERR_INVALID_ARG;
+  *count = 0;
+  unsigned long long n = 0;
+  hipError_t e = hipMemcpyFromSymbol(&n, HIP_SYMBOL(sync_timeouts), sizeof(n), 0, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e);
+  *count = (int64_t)n;
+  if (clear != 0 && n != 0) {
+    const unsigned long long zero = 0;
+    e = hipMemcpyToSymbol(HIP_SYMBOL(sync_timeouts), &zero, sizeof(zero), 0, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  return ACDC_OK;
+}

@@ -65,7 +65,11 @@ template <int T>
 struct GroupCtx {
   static_assert(T > 64 && T % 64 == 0, "rows of whole waves");
   static constexpr unsigned W = T / 64;
-  unsigned addr;  // LDS byte address of this row's arrival count
+  // Each row owns two LDS words: [0] its arrival count, [1] the number of
+  // its waits whose polling ran out (zero unless something is badly wrong;
+  // report() adds those to a global count after the row work).
+  static constexpr int kWords = 2;
+  unsigned addr;  // LDS byte address of this row's two words
   unsigned gen;   // W times this wave's arrivals so far
   __device__ explicit GroupCtx(unsigned* c)
       : addr(unsigned(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned*)c))), gen(0) {}
@@ -73,8 +77,10 @@ struct GroupCtx {
   // polling loop adds no control flow around the row code).  The wave's LDS
   // accesses complete first (release), one lane adds 1 with the rest of the
   // exec mask saved and restored, then the wave polls until the count
-  // reaches gen or the poll budget runs out.  The "memory" clobber keeps the
-  // compiler's LDS accesses on their side of it (acquire).
+  // reaches gen or the poll budget runs out; a run-out adds 1 to the row's
+  // second word (on the fall-through path only, so the normal path is
+  // unchanged).  The "memory" clobber keeps the compiler's LDS accesses on
+  // their side of it (acquire).
   __device__ __forceinline__ void sync_row() {
     gen += W;
     unsigned long long save;
@@ -98,10 +104,22 @@ struct GroupCtx {
         "s_sleep 1\n"
         "s_sub_u32 %[it], %[it], 1\n"
         "s_cbranch_scc0 1b\n"
+        "s_mov_b64 exec, 1\n"
+        "ds_add_u32 %[addr], %[one] offset:4\n"
+        "s_mov_b64 exec, %[save]\n"
         "2:\n"
         : [save] "=&s"(save), [tmp] "=&v"(tmp), [seen] "=&s"(seen), [g] "=&s"(g), [it] "=&s"(it)
         : [addr] "v"(addr), [one] "v"(1u), [genv] "v"(gen)
         : "scc", "memory");
+  }
+  // After the workgroup's last row sync: adds the run-outs of its `rows`
+  // rows (words laid out as above from `words`) to *count.
+  __device__ static void report(const unsigned* words, int rows, int tid, unsigned long long* count) {
+    DevCtx<T>::lds_barrier();
+    if (tid < rows) {
+      const unsigned n = words[kWords * tid + 1];
+      if (n != 0u) __hip_atomic_fetch_add(count, (unsigned long long)n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
   __device__ __forceinline__ void sync_all() { DevCtx<T>::lds_barrier(); }
   __device__ __forceinline__ static void swap16(float& a, float& b) { DevCtx<T>::swap16(a, b); }

@@ -33,7 +33,7 @@ def declared_functions():
 def test_header_declares_expected_entry_points():
     names = declared_functions()
     for n in ("acdc_forward", "acdc_backward", "acdc_backward_workspace_size", "acdc_prepare",
-              "acdc_status_string", "acdc_last_hip_error", "acdc_supported"):
+              "acdc_status_string", "acdc_last_hip_error", "acdc_supported", "acdc_sync_timeouts"):
         assert n in names
 
 

@@ -559,3 +559,24 @@ def test_rows_independent_of_tiling(acdc, N, K, flags):
         assert np.array_equal(host(ys), yh[lo:hi]), (lo, hi)
         assert np.array_equal(host(acdc.backward(xs, gs, At, Dt, pt, fl, saved=ss)[0]), gxh[lo:hi]), (lo, hi)
     torch.cuda.synchronize()
+
+
+def test_row_syncs_never_time_out(acdc):
+    # Backward rows that span several wavefronts meet at LDS counters with a
+    # bounded wait; a wait that ran out would leave wrong results behind.
+    # The device count covers every backward this process ran (the tests
+    # before this one included) plus a set of busy launches of those widths.
+    import torch
+    for N, K, B, flags in ((8192, 2, 96, P | R), (9216, 3, 1100, P | R), (9216, 2, 300, P | R | FLAG_BIAS),
+                           (16384, 2, 40, P), (32768, 2, 12, P), (4096, 4, 300, CX | P), (8192, 2, 96, CX | P),
+                           (16384, 2, 24, CX | P)):
+        print(f"[case] N={N} K={K} B={B} flags={flags}", flush=True)
+        x, A, D, perm, gy = make_inputs(N, K, B, flags, 70 + N)
+        bias = dev(make_bias(N, K, 70 + N)) if flags & FLAG_BIAS else None
+        xt, At, Dt, pt, gyt = dev(x), dev(A), dev(D), dev(perm), dev(gy)
+        fl = flags & ~CX
+        _, sv = acdc.forward(xt, At, Dt, pt, fl, save=True, bias=bias)
+        for _ in range(3):
+            acdc.backward(xt, gyt, At, Dt, pt, fl, saved=sv, bias=bias)
+        torch.cuda.synchronize()
+    assert acdc.sync_timeouts() == 0
