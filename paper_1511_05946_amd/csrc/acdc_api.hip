@@ -33,12 +33,25 @@ namespace acdc {
 // acdc_sync_timeouts reads and clears it.
 static __device__ unsigned long long sync_timeouts;
 
+// Threads past the K * NSL * T table entries repack perm for the row
+// kernels (RealOps::pack_perm_entry), when P16 is given.
 template <class PL>
 __global__ __launch_bounds__(256) void k_real_mq(const float* __restrict__ D, const float* __restrict__ Bias,
-                                                 float4* __restrict__ Mq, int K, const char* __restrict__ tab) {
+                                                 float4* __restrict__ Mq, int K, const char* __restrict__ tab,
+                                                 const int* __restrict__ perm, int4* __restrict__ P16) {
   constexpr int E = PL::NSL * PL::T;
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (long long)K * E) return;
+  if (i >= (long long)K * E) {
+    using O = RealOps<PL>;
+    if constexpr (O::kPackedPerm) {
+      constexpr int W = O::NIW * PL::T;
+      const long long q = i - (long long)K * E;
+      if (P16 == nullptr || q >= (long long)K * W) return;
+      const int k = int(q / W), r = int(q % W);
+      P16[q] = O::pack_perm_entry(perm + (long long)k * PL::N, r / PL::T, unsigned(r % PL::T));
+    }
+    return;
+  }
   const int k = int(i / E), e = int(i % E);
   float4 row[kMqRows];
   real_mq_entry<PL>(D + (long long)k * PL::N, Bias != nullptr ? Bias + (long long)k * PL::N : nullptr, tab, e, row);
@@ -473,9 +486,22 @@ struct WsLayout {
   size_t off_mq = 0, off_partial = 0, off_gs = 0, off_stash = 0;
 };
 
+// The quartet table, then for the backward (with PERM, where the plan packs
+// it) the packed perm of every layer.
 template <class PL>
-size_t mq_bytes(int32_t K) {
+size_t mq_table_bytes(int32_t K) {
   return align256(size_t(K) * PL::NSL * kMqRows * PL::T * sizeof(float4));
+}
+template <class PL>
+size_t mq_bytes(int32_t K, uint32_t flags, bool backward) {
+  using O = RealOps<PL>;
+  const bool packed = backward && O::kPackedPerm && (flags & kFlagPerm) != 0;
+  return mq_table_bytes<PL>(K) + (packed ? align256(size_t(K) * O::NIW * PL::T * sizeof(int4)) : 0);
+}
+template <class PL>
+int4* perm16_of(float4* Mq, int32_t K, uint32_t flags) {
+  if (!RealOps<PL>::kPackedPerm || !(flags & kFlagPerm)) return nullptr;
+  return reinterpret_cast<int4*>(reinterpret_cast<char*>(Mq) + mq_table_bytes<PL>(K));
 }
 
 WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool have_saved) {
@@ -486,7 +512,7 @@ WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool ha
     w.partial = align256(size_t(tiles) * K * partial_entries4<PL>(bias) * sizeof(float4));
     if constexpr (!PL::kComplex) {
       // the bias gradient's DCT reads w, qa, qb' from the quartet table
-      if (batch > 0 || bias) w.mq = mq_bytes<PL>(K);
+      if (batch > 0 || bias) w.mq = mq_bytes<PL>(K, flags, true);
       if (bias) w.gs = align256(size_t(K) * PL::N * sizeof(float));
     }
   };
@@ -504,14 +530,17 @@ WsLayout bwd_layout(int64_t batch, int32_t N, int32_t K, uint32_t flags, bool ha
 size_t fwd_ws(int32_t N, int32_t K, uint32_t flags) {
   size_t b = 0;
   if (!(flags & kFlagComplex))
-    dispatch_real(N, [&]<class PL>() { b = mq_bytes<PL>(K); });
+    dispatch_real(N, [&]<class PL>() { b = mq_bytes<PL>(K, flags, false); });
   return b;
 }
 
+// The quartet table into Mq, and the packed perm into P16 (if not null).
 template <class PL>
-int launch_real_mq(const float* D, const float* Bias, float4* Mq, int K, const char* tab, hipStream_t s) {
-  const long long n = (long long)K * PL::NSL * PL::T;
-  hipLaunchKernelGGL(k_real_mq<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, D, Bias, Mq, K, tab);
+int launch_real_mq(const float* D, const float* Bias, float4* Mq, int K, const char* tab, const int* perm,
+                   int4* P16, hipStream_t s) {
+  const long long n = (long long)K * PL::NSL * PL::T + (P16 != nullptr ? (long long)K * RealOps<PL>::NIW * PL::T : 0);
+  hipLaunchKernelGGL(k_real_mq<PL>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, D, Bias, Mq, K, tab, perm,
+                     P16);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? ACDC_OK : hip_fail(e);
 }
@@ -988,7 +1017,7 @@ int fused_forward(const float* x, float* y, const float* A, const float* D, cons
   } else {
     dispatch_real(N, [&]<class PL>() {
       float4* Mq = static_cast<float4*>(workspace);
-      rc = launch_real_mq<PL>(D, bias, Mq, K, tab, s);
+      rc = launch_real_mq<PL>(D, bias, Mq, K, tab, perm, nullptr, s);
       if (rc != ACDC_OK) return;
       RealArgs a{x, y, A, Mq, perm, saved, nullptr, nullptr, nullptr, tab, batch, K, flags};
       rc = launch_real_fwd<PL>(a, s, remember);
@@ -1197,9 +1226,10 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
               ? persistent_grid(reinterpret_cast<const void*>(&k_real_bwd<PL, false>), L::BWD_THREADS, tiles)
               : tiles;
       float4* Mq = reinterpret_cast<float4*>(ws + w.off_mq);
+      int4* P16 = batch > 0 ? perm16_of<PL>(Mq, K, flags) : nullptr;
       float* gS = bias_on ? reinterpret_cast<float*>(ws + w.off_gs) : nullptr;
       if (batch > 0 || bias_on) {
-        rc = launch_real_mq<PL>(D, bias, Mq, K, tab, s);
+        rc = launch_real_mq<PL>(D, bias, Mq, K, tab, perm, P16, s);
         if (rc != ACDC_OK) return;
       }
       if (batch > 0) {
@@ -1209,6 +1239,7 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
           if (rc != ACDC_OK) return;
         }
         RealArgs a{x, nullptr, A, Mq, perm, stash, grad_y, grad_x, partial, tab, batch, K, flags};
+        a.perm16 = P16;
         hipError_t e;
         {
           ProfScope prof(1, s);

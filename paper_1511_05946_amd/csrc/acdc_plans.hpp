@@ -24,6 +24,9 @@
 #ifndef ACDC_MQ_PF_BWD
 #define ACDC_MQ_PF_BWD 2  // the same in the backward middle (three float4 per slot)
 #endif
+#ifndef ACDC_PACKED_PERM
+#define ACDC_PACKED_PERM 1  // fused real rows: perm as packed 16-bit slab offsets (N <= 16384)
+#endif
 #ifndef ACDC_FFT2
 #define ACDC_FFT2 1  // backward: the h- and g-path FFTs share twiddle loads
 #endif

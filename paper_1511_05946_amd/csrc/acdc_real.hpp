@@ -174,9 +174,53 @@ struct RealOps {
 #pragma unroll
     for (int n = 0; n < NCH; ++n) s[n] = g.ld4(ch_lc(L, n) * 16u, ch_cc(n) * 16u);
   }
-  __host__ __device__ __forceinline__ static void load_idx(int4 (&s)[NCH], GView g, Lane L) {
+  // Permutation indices.  Where a row's byte offsets fit 16 bits (N <=
+  // 16384), k_real_mq repacks perm[k] per thread for the backward: for chunk
+  // pair (2j, 2j+1) of lane t one int4 at [j][t] holds the eight slab byte
+  // offsets 4 perm[.] of the two chunks, two per int (low half first), so a
+  // thread loads NCH/2 int4 instead of NCH, and a 16-bit half feeds the LDS
+  // address add directly.  Otherwise (and in the forward, where the packed
+  // form measured slower) a thread loads its int4 chunks of perm[k].
+  static constexpr bool kPackedPerm = ACDC_PACKED_PERM && N <= 16384 && NCH % 2 == 0;
+  static constexpr int NIW = kPackedPerm ? NCH / 2 : NCH;  // int4 words per thread, packed table
+  template <bool PK>
+  static constexpr int niw() {
+    return PK ? NIW : NCH;
+  }
+  // g: perm[k] (plain) or layer k of the packed table (PK)
+  template <bool PK>
+  __host__ __device__ __forceinline__ static void load_idx(int4 (&s)[niw<PK>()], GView g, Lane L, unsigned t) {
 #pragma unroll
-    for (int n = 0; n < NCH; ++n) s[n] = g.ldi4(ch_lc(L, n) * 16u, ch_cc(n) * 16u);
+    for (int n = 0; n < niw<PK>(); ++n)
+      s[n] = PK ? g.ldi4(t * 16u, unsigned(n * T * 16)) : g.ldi4(ch_lc(L, n) * 16u, ch_cc(n) * 16u);
+  }
+  // Slab byte offset of index c (0..3: perm of chunk element c) of chunk n.
+  template <bool PK>
+  __host__ __device__ __forceinline__ static unsigned idx_off(const int4 (&s)[niw<PK>()], int n, int c) {
+    if constexpr (PK) {
+      const int4 w = s[n >> 1];
+      const unsigned u = unsigned((n & 1) ? (c < 2 ? w.z : w.w) : (c < 2 ? w.x : w.y));
+      return (c & 1) ? (u >> 16) : (u & 0xffffu);
+    } else {
+      const int4 w = s[n];
+      return 4u * unsigned(c == 0 ? w.x : c == 1 ? w.y : c == 2 ? w.z : w.w);
+    }
+  }
+  // The packed int4 of lane t, chunk pair j, from layer k's perm (host or
+  // device).  Indices outside [0, N) become 0.
+  __host__ __device__ static int4 pack_perm_entry(const int* pk, int j, unsigned t) {
+    const Lane L = lane(t);
+    unsigned o[8];
+    for (int h = 0; h < 2; ++h) {
+      const int n = 2 * j + h;
+      const unsigned base = (ch_lc(L, n) + ch_cc(n)) * 4u;
+      for (int c = 0; c < 4; ++c) {
+        const int p = pk[base + c];
+        o[4 * h + c] = (p >= 0 && p < N) ? 4u * unsigned(p) : 0u;
+      }
+    }
+    return make_int4(int(o[0] | (o[1] << 16)), int(o[2] | (o[3] << 16)), int(o[4] | (o[5] << 16)),
+                     int(o[6] | (o[7] << 16)));
   }
   // v *= a (spatial diagonal of one layer, chunks from load_vec)
   __host__ __device__ __forceinline__ static void scale(float2 (&v)[P], const float4 (&s)[NCH]) {
@@ -195,9 +239,9 @@ struct RealOps {
   // u[n] = z[perm[n]]: write z to LDS in natural order, read it back gathered
   // through the thread's index chunks (from load_idx).  `hook` runs between
   // the LDS write and the gathered reads.
-  template <class Ctx, class Hook>
+  template <bool PK, class Ctx, class Hook>
   __host__ __device__ __forceinline__ static void gather(Ctx& ctx, float2 (&v)[P], Lane L, float* slab,
-                                                         const int4 (&idx)[NCH], Hook&& hook) {
+                                                         const int4 (&idx)[niw<PK>()], Hook&& hook) {
     ctx.sync_row();
     for_chunks(v, L, [&](unsigned lc, unsigned cc, float2& lo, float2& hi) {
       reinterpret_cast<float4*>(slab)[lc + cc] = make_float4(lo.x, hi.y, lo.y, hi.x);
@@ -205,25 +249,29 @@ struct RealOps {
     ctx.sync_row();
     hook();
     ACDC_SCHED_FENCE();
+    const char* sb = reinterpret_cast<const char*>(slab);
+    auto at = [&](unsigned off) { return *reinterpret_cast<const float*>(sb + off); };
     int n = 0;
     for_chunks(v, L, [&](unsigned, unsigned, float2& lo, float2& hi) {
-      const int4 pi = idx[n++];
-      lo = make_float2(slab[pi.x], slab[pi.z]);
-      hi = make_float2(slab[pi.w], slab[pi.y]);
+      lo = make_float2(at(idx_off<PK>(idx, n, 0)), at(idx_off<PK>(idx, n, 2)));
+      hi = make_float2(at(idx_off<PK>(idx, n, 3)), at(idx_off<PK>(idx, n, 1)));
+      ++n;
     });
   }
   // g_z[perm[n]] = g_u[n]: the adjoint of gather.
-  template <class Ctx, class Hook>
+  template <bool PK, class Ctx, class Hook>
   __host__ __device__ __forceinline__ static void scatter(Ctx& ctx, float2 (&v)[P], Lane L, float* slab,
-                                                          const int4 (&idx)[NCH], Hook&& hook) {
+                                                          const int4 (&idx)[niw<PK>()], Hook&& hook) {
     ctx.sync_row();
+    char* sb = reinterpret_cast<char*>(slab);
+    auto at = [&](unsigned off) -> float& { return *reinterpret_cast<float*>(sb + off); };
     int n = 0;
     for_chunks(v, L, [&](unsigned, unsigned, float2& lo, float2& hi) {
-      const int4 pi = idx[n++];
-      slab[pi.x] = lo.x;
-      slab[pi.y] = hi.y;
-      slab[pi.z] = lo.y;
-      slab[pi.w] = hi.x;
+      at(idx_off<PK>(idx, n, 0)) = lo.x;
+      at(idx_off<PK>(idx, n, 1)) = hi.y;
+      at(idx_off<PK>(idx, n, 2)) = lo.y;
+      at(idx_off<PK>(idx, n, 3)) = hi.x;
+      ++n;
     });
     ctx.sync_row();
     hook();
@@ -483,7 +531,7 @@ struct RealArgs {
   const float* x;
   float* y;            // forward output (may be null: stash-only forward)
   const float* A;
-  const float4* Mq;    // [K][NSL][3][T] quartet coefficients (real_mq_entry)
+  const float4* Mq;    // [K][NSL][kMqRows][T] quartet coefficients (real_mq_entry)
   const int* perm;     // [K][N] (PERM only)
   float* saved;        // layer inputs [slots][batch][N]: u_1..u_{K-1} in slots 0..K-2, and with
                        // PERM u_0 in slot K-1 (may be null)
@@ -494,6 +542,7 @@ struct RealArgs {
   long long batch;
   int K;
   unsigned flags;
+  const int4* perm16 = nullptr;  // backward: [K][NCH/2][T] packed perm (PERM with RealOps::kPackedPerm)
 };
 
 // BIAS: the layers add the D-domain bias (Sec. 6.2), carried by row c3 of
@@ -517,8 +566,8 @@ __host__ __device__ void real_forward_row(Ctx& ctx, const RealArgs& a, unsigned 
     const GView ak = GView::of(a.A + (long long)k * N);
     const GView mq = GView::of(a.Mq + (long long)k * NSL * kMqRows * T);
     if (permute) {
-      O::load_idx(idx, GView::of(a.perm + (long long)k * N), L);
-      O::gather(ctx, v, L, slab, idx, [&] { O::load_vec(av, ak, L); });
+      O::template load_idx<false>(idx, GView::of(a.perm + (long long)k * N), L, t);
+      O::template gather<false>(ctx, v, L, slab, idx, [&] { O::load_vec(av, ak, L); });
     } else {
       O::load_vec(av, ak, L);
     }
@@ -578,7 +627,7 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
   auto u_view = [&](int k) { return GView::of(k == 0 ? u0 : s0 + (long long)k * a.batch * N); };
   float2 g[P];
   float4 uv[NCH], av[NCH];
-  int4 idx[NCH];
+  int4 idx[O::NIW];
   O::load(GView::of(a.gy + row0 * N), roff, g, L, valid);
   O::load_raw(uv, u_view(a.K - 1), roff, L, valid);
   for (int k = a.K - 1; k >= 0; --k) {
@@ -674,8 +723,10 @@ __host__ __device__ void real_backward_row(Ctx& ctx, const RealArgs& a, unsigned
     const int kn = k > 0 ? k - 1 : 0;
     auto next = [&] { O::load_raw(uv, u_view(kn), roff, L, valid); };
     if (permute) {
-      O::load_idx(idx, GView::of(a.perm + (long long)k * N), L);
-      O::scatter(ctx, g, L, slab, idx, next);
+      constexpr bool PK = O::kPackedPerm;
+      O::template load_idx<PK>(idx, PK ? GView::of(a.perm16 + (long long)k * O::NIW * T)
+                                       : GView::of(a.perm + (long long)k * N), L, t);
+      O::template scatter<PK>(ctx, g, L, slab, idx, next);
     } else {
       next();
     }

@@ -87,6 +87,21 @@ std::vector<float4> quartet_coefficients(const float* D, const float* B, int K, 
   return mq;
 }
 
+// The packed perm the backward reads where the plan packs it (k_real_mq's
+// extra threads on the GPU); empty otherwise.
+template <class PL>
+std::vector<int4> packed_perm(const int* perm, int K, unsigned flags) {
+  using O = RealOps<PL>;
+  std::vector<int4> p;
+  if (!O::kPackedPerm || !(flags & kFlagPerm) || perm == nullptr) return p;
+  p.resize((size_t)K * O::NIW * PL::T);
+  for (int k = 0; k < K; ++k)
+    for (int j = 0; j < O::NIW; ++j)
+      for (int t = 0; t < PL::T; ++t)
+        p[((size_t)k * O::NIW + j) * PL::T + t] = O::pack_perm_entry(perm + (size_t)k * PL::N, j, unsigned(t));
+  return p;
+}
+
 template <class PL, bool BIAS>
 void real_fwd_k(const RealArgs& a, const std::vector<unsigned char>& tab) {
   using L = Launch<PL>;
@@ -173,8 +188,10 @@ void real_bwd(const float* x, const float* gy, const float* A, const float* D, c
   const long long slots = bias ? bwd_slots<PL, true>(ntiles) : bwd_slots<PL, false>(ntiles);
   const long long PS4 = partial_entries4<PL>(bias);
   std::vector<float> partial((size_t)slots * K * PS4 * 4);
+  const std::vector<int4> p16 = packed_perm<PL>(perm, K, flags);
   RealArgs a{x, nullptr, A, mq.data(), perm, const_cast<float*>(saved), gy, gx, partial.data(),
              (const char*)tab.data(), batch, K, flags};
+  a.perm16 = p16.empty() ? nullptr : p16.data();
   std::vector<float> lds((size_t)L::BWD_LDS_FLOATS + L::ACC_FLOATS);
   if (bias) real_bwd_k<PL, true>(a, ntiles, lds.data(), tab);
   else real_bwd_k<PL, false>(a, ntiles, lds.data(), tab);
