@@ -127,7 +127,8 @@ size_t acdc_saved_bytes(int64_t batch, int32_t N, int32_t K, uint32_t flags);
 size_t acdc_forward_workspace_size(int64_t batch, int32_t N, int32_t K, uint32_t flags);
 
 /* Bytes of workspace acdc_backward needs: per-workgroup partial sums of the
- * parameter gradients, the per-layer quartet coefficients, the batch sums
+ * parameter gradients, the per-layer quartet coefficients (with
+ * ACDC_FLAG_PERM followed by perm repacked as 16-bit offsets), the batch sums
  * behind the bias gradient (ACDC_FLAG_BIAS), and -- when have_saved is 0 and
  * acdc_saved_bytes(...) is not 0 -- room to recompute the layer inputs (the
  * paper's recompute policy, Sec. 5.3).  The multi-pass path adds its
