@@ -42,9 +42,7 @@ __device__ __forceinline__ float4 chunk_of(float2 even, float2 odd) { return mak
 __device__ __forceinline__ float4 scale4(float4 h, float4 a) {
   return make_float4(h.x * a.x, h.y * a.y, h.z * a.z, h.w * a.w);
 }
-__device__ __forceinline__ float4 relu4(float4 h) {
-  return make_float4(h.x > 0.f ? h.x : 0.f, h.y > 0.f ? h.y : 0.f, h.z > 0.f ? h.z : 0.f, h.w > 0.f ? h.w : 0.f);
-}
+__device__ __forceinline__ float4 relu4(float4 h) { return make_float4(relu1(h.x), relu1(h.y), relu1(h.z), relu1(h.w)); }
 
 // Chunk q (q < M/2) of row b: Z[q] and Z[M-1-q], scaled by a, stashed.
 __global__ __launch_bounds__(kThreads) void k_pack(const float* __restrict__ src, const float* __restrict__ a,

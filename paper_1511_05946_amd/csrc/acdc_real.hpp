@@ -44,6 +44,15 @@ enum : unsigned {
 // Rows of the per-layer quartet-coefficient table (real_mq_entry).
 constexpr int kMqRows = 4;
 
+// max(x, 0) as one integer max over the bit pattern: a float with the sign
+// bit set is a negative int32, so -0 and every negative value become +0.
+// (The float forms, max or compare-and-select, cost a second instruction
+// that quiets NaNs first.)  A NaN keeps its sign's side: NaN or +0.
+__host__ __device__ __forceinline__ float relu1(float x) {
+  const int b = __builtin_bit_cast(int, x);
+  return __builtin_bit_cast(float, b > 0 ? b : 0);
+}
+
 __host__ __device__ __forceinline__ float2 sel2(bool c, float2 a, float2 b) {
   return make_float2(c ? a.x : b.x, c ? a.y : b.y);
 }
@@ -233,7 +242,7 @@ struct RealOps {
   }
   __host__ __device__ __forceinline__ static void relu(float2 (&v)[P]) {
 #pragma unroll
-    for (int s = 0; s < P; ++s) v[s] = make_float2(v[s].x > 0.f ? v[s].x : 0.f, v[s].y > 0.f ? v[s].y : 0.f);
+    for (int s = 0; s < P; ++s) v[s] = make_float2(relu1(v[s].x), relu1(v[s].y));
   }
 
   // u[n] = z[perm[n]]: write z to LDS in natural order, read it back gathered
