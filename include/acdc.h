@@ -71,10 +71,12 @@
  * library does not check this (it would cost a pass over perm and a host
  * synchronisation per call); a row that is not a permutation gives
  * unspecified values in y, grad_x and the parameter gradients but never an
- * access outside the caller's buffers and the kernels' own LDS: the fused
- * kernels use the entries only as LDS indices within the workgroup, and the
- * multi-pass path reads every entry modulo N (the tables it builds from perm
- * are masked into range).
+ * access outside the caller's buffers: the fused kernels use the entries
+ * only as LDS indices within the workgroup (the backward's repacked copy
+ * maps entries outside [0, N) to 0; in the forward an index past the
+ * workgroup's LDS allocation reads 0, by the hardware's LDS bounds check),
+ * and the multi-pass path reads every entry modulo N (the tables it builds
+ * from perm are masked into range).
  */
 #ifndef ACDC_H_
 #define ACDC_H_
