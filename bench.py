@@ -118,7 +118,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: the library runs on one GPU only (asked for --gpus {args.gpus}); "
               "the cascade shards over rows with one all-reduce of dL/da, dL/dd, "
               "which is not built here.", file=sys.stderr)
         sys.exit(2)

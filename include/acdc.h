@@ -109,7 +109,7 @@ enum acdc_status {
   ACDC_ERR_NOT_PREPARED = -5 /* acdc_forward_noalloc: acdc_prepare(N, flags) not called on this device */
 };
 
-/* 1 if (N, flags) is supported by this build, else 0.  Host only. */
+/* 1 if (N, flags) is supported by the compiled library, else 0.  Host only. */
 int acdc_supported(int32_t N, uint32_t flags);
 
 /* Build and upload the constant table for (N, flags) on the current device,

@@ -27,7 +27,7 @@ Conventions (row vectors throughout, as in the paper's Sec. 1 eq. (1) y = xW):
                    D matrices, none on A)
 * ``flags``        bit 0 PERM, bit 1 RELU (after layers 0..K-2), bit 2 COMPLEX
 
-Readings of the paper used here (each listed in the design doc):
+Readings of the paper used here:
 
 * DCT index range: n, k in [0, N) and eps_0 = 1/sqrt(2) only (Sec. 4, the
   c_nk definition; the "k = N" clause is a DCT-I leftover -- only this reading

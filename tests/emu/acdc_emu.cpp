@@ -306,7 +306,7 @@ extern "C" int acdc_emu_backward(const float* x, const float* gy, const float* A
 
 // Emulate `slots` persistent backward workgroups where the plan accumulates
 // (0: one per tile).  Returns whether the unbiased backward of real rows of
-// width N accumulates in this build.
+// width N accumulates with the compiled launch settings.
 extern "C" int acdc_emu_set_backward_slots(long long slots, int N) {
   g_bwd_slots = slots;
   int acc = 0;
