@@ -195,12 +195,14 @@ struct CplxOps {
     }
   }
   // u[n] = z[perm[n]] with the indices already in registers.
-  template <class Ctx>
+  template <class Ctx, class Hook>
   __host__ __device__ __forceinline__ static void gather_idx(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
-                                                             const int (&idx)[P]) {
+                                                             const int (&idx)[P], Hook&& hook) {
     ctx.sync_row();
     for_spatial(v, t, [&](unsigned l, unsigned c, float2& z) { slab[l + c] = z; });
     ctx.sync_row();
+    hook();
+    ACDC_SCHED_FENCE();
 #pragma unroll
     for (int s = 0; s < P; ++s) v[s] = slab[idx[s]];
   }
@@ -229,6 +231,39 @@ struct CplxOps {
   __host__ __device__ __forceinline__ static void fft(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
                                                       GView tw) {
     stockham_fft<PL, INV, KIND, KIND>(ctx, v, t, slab, tw);
+  }
+  // `tail` runs in the last pass right after its twiddle multiplies.
+  template <bool INV, class Ctx, class Tail>
+  __host__ __device__ __forceinline__ static void fft(Ctx& ctx, float2 (&v)[P], unsigned t, float2* slab,
+                                                      GView tw, Tail&& tail) {
+    stockham_fft<PL, INV, KIND, KIND>(ctx, v, t, slab, tw, tail);
+  }
+
+  // A layer diagonal loaded ahead of its use (pairs layout: each float4 is
+  // the two neighbouring elements of one pair), spatial or frequency order.
+  static constexpr int NQ = P / 2;
+  template <bool FREQ>
+  __host__ __device__ __forceinline__ static void ld_diag(float4 (&r)[NQ], GView g, unsigned t) {
+    static_assert(PAIRS, "pairs layout");
+    int n = 0;
+    auto f = [&](unsigned l, unsigned c, float2&, float2&) { r[n++] = g.ld4(l * 8u, c * 8u); };
+    float2 dummy[P];
+    if constexpr (FREQ) for_freq_pairs(dummy, t, f);
+    else for_spatial_pairs(dummy, t, f);
+  }
+  // v *= diag (spatial) or v *= diag * f (frequency), diag from ld_diag
+  template <bool FREQ, bool CONJ>
+  __host__ __device__ __forceinline__ static void mul_diag(float2 (&v)[P], const float4 (&r)[NQ], float f, unsigned t) {
+    int n = 0;
+    auto g = [&](unsigned, unsigned, float2& z0, float2& z1) {
+      const float4 w = r[n++];
+      const float2 w0 = FREQ ? make_float2(w.x * f, w.y * f) : make_float2(w.x, w.y);
+      const float2 w1 = FREQ ? make_float2(w.z * f, w.w * f) : make_float2(w.z, w.w);
+      z0 = CONJ ? cmulc(z0, w0) : cmul(z0, w0);
+      z1 = CONJ ? cmulc(z1, w1) : cmul(z1, w1);
+    };
+    if constexpr (FREQ) for_freq_pairs(v, t, g);
+    else for_spatial_pairs(v, t, g);
   }
 };
 
@@ -262,19 +297,36 @@ __host__ __device__ void cplx_forward_row(Ctx& ctx, const CplxArgs& a, unsigned 
   const float invN = 1.0f / float(N);
   float2 v[P];
   O::load(GView::of(a.x + row0 * RS), roff, v, t, valid);
+  // With adjacent pairs on rows of two or more waves, a is loaded during
+  // the gather and d in the forward FFT's last pass, one step ahead of their
+  // use (smaller rows would lose a wave per SIMD to the 64 extra registers).
+  constexpr bool AHEAD = ACDC_CPLX_FWD_PF && O::PAIRS && PL::T >= 128;
   for (int k = 0; k < a.K; ++k) {
+    const GView ak = GView::of(a.A + k * RS), dk = GView::of(a.D + k * RS);
+    float4 dg[O::NQ];
+    auto load_a = [&] {
+      if constexpr (AHEAD) O::template ld_diag<false>(dg, ak, t);
+    };
     // the perm loads are issued before the gather's barriers
     if (a.flags & 1u) {
       int idx[P];
       O::load_idx(idx, GView::of(a.perm + (long long)k * N), t);
-      O::gather_idx(ctx, v, t, slab2, idx);
+      O::gather_idx(ctx, v, t, slab2, idx, load_a);
+    } else {
+      load_a();
     }
     // stash u_k: u_1..u_{K-1} in slots 0..K-2, and with PERM u_0 in slot K-1
     if (a.saved != nullptr && (k > 0 || (a.flags & 1u)) && valid)
       O::store(GView::of(a.saved + ((long long)(k > 0 ? k - 1 : a.K - 1) * a.batch + row0) * RS), roff, v, t);
-    O::template scale<false>(v, GView::of(a.A + k * RS), t);
-    O::template fft<false>(ctx, v, t, slab2, tab);
-    O::template scale_freq<false>(v, GView::of(a.D + k * RS), invN, t);
+    if constexpr (AHEAD) {
+      O::template mul_diag<false, false>(v, dg, 1.0f, t);
+      O::template fft<false>(ctx, v, t, slab2, tab, [&] { O::template ld_diag<true>(dg, dk, t); });
+      O::template mul_diag<true, false>(v, dg, invN, t);
+    } else {
+      O::template scale<false>(v, ak, t);
+      O::template fft<false>(ctx, v, t, slab2, tab);
+      O::template scale_freq<false>(v, dk, invN, t);
+    }
     O::template fft<true>(ctx, v, t, slab2, tab);
   }
   if (a.y != nullptr && valid) O::store(GView::of(a.y + row0 * RS), roff, v, t);

@@ -24,6 +24,9 @@
 #ifndef ACDC_MQ_PF_BWD
 #define ACDC_MQ_PF_BWD 2  // the same in the backward middle (three float4 per slot)
 #endif
+#ifndef ACDC_CPLX_FWD_PF
+#define ACDC_CPLX_FWD_PF 1  // complex forward: A and D loaded one step ahead of their use
+#endif
 #ifndef ACDC_PACKED_PERM
 #define ACDC_PACKED_PERM 1  // fused real rows: perm as packed 16-bit slab offsets (N <= 16384)
 #endif
