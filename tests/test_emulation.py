@@ -85,6 +85,13 @@ def test_complex_small(emu, N):
     check(emu, N, 2, 5, O.FLAG_COMPLEX | O.FLAG_PERM, seed=N)
 
 
+@pytest.mark.parametrize("flags", [O.FLAG_COMPLEX, O.FLAG_COMPLEX | O.FLAG_PERM])
+def test_complex_4096_loads_ahead(emu, flags):
+    # N = 4096 rows (adjacent pairs, 128 threads) load a and d ahead of use
+    # in the forward, with and without the gather
+    check(emu, 4096, 1, 1, flags, seed=41)
+
+
 @pytest.mark.parametrize("flags", [O.FLAG_PERM | O.FLAG_RELU, O.FLAG_COMPLEX | O.FLAG_PERM])
 @pytest.mark.parametrize("K", [1, 3])
 def test_first_layer_permutation(emu, flags, K):

@@ -132,6 +132,13 @@ def test_complex_widths(acdc, N):
     run_case(acdc, N, 3, 11, CX | P, seed=N)
 
 
+@pytest.mark.parametrize("N", [64, 4096, 8192])
+def test_complex_without_perm(acdc, N):
+    # the forward's diagonal loads run ahead of the gather with PERM and on
+    # their own without it (N = 4096)
+    run_case(acdc, N, 3, 9, CX, seed=N + 5)
+
+
 @pytest.mark.parametrize("save", [True, False])
 @pytest.mark.parametrize("N,flags", [(1024, P | R), (4096, P | R | FLAG_BIAS), (9216, P | R), (2048, CX | P)])
 def test_first_layer_permutation(acdc, N, flags, save):
