@@ -160,11 +160,14 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealAr
 // gradient (over all layers, entry index k * PS4 + e4) and sums them over the
 // tiles with one thread per (entry, phase); phase sums meet in LDS and are
 // added in phase order (tile_phase_sum4 / phases_total4).
-constexpr int kRedEntries = 64;
-static_assert(kRedEntries * kRedPhases == 256, "one thread per (entry, phase)");
+#ifndef ACDC_RED_ENTRIES
+#define ACDC_RED_ENTRIES 32  // 128-thread blocks: beat 256 (and 64) threads at N = 4096
+#endif
+constexpr int kRedEntries = ACDC_RED_ENTRIES;
+constexpr int kRedThreads = kRedEntries * kRedPhases;  // one thread per (entry, phase)
 
 template <class PL>
-__global__ __launch_bounds__(256) void k_real_reduce(const float* __restrict__ partial, long long ntiles, int K,
+__global__ __launch_bounds__(kRedThreads) void k_real_reduce(const float* __restrict__ partial, long long ntiles, int K,
                                                      float* __restrict__ gA, float* __restrict__ gD,
                                                      float* __restrict__ gS, const char* __restrict__ tab,
                                                      int bias, int accumulate) {
@@ -235,7 +238,7 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_cplx_bwd(CplxAr
 }
 
 template <class PL>
-__global__ __launch_bounds__(256) void k_cplx_reduce(const float* __restrict__ partial, long long ntiles, int K,
+__global__ __launch_bounds__(kRedThreads) void k_cplx_reduce(const float* __restrict__ partial, long long ntiles, int K,
                                                      float* __restrict__ gA, float* __restrict__ gD,
                                                      int accumulate) {
   constexpr long long PS4 = partial_entries4<PL>();
@@ -1209,7 +1212,7 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
       hipError_t e;
       {
         ProfScope prof(2, s);
-        hipLaunchKernelGGL(k_cplx_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(256), 0, s,
+        hipLaunchKernelGGL(k_cplx_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(kRedThreads), 0, s,
                            partial, tiles, K, grad_A, grad_D, accumulate);
         e = hipGetLastError();
       }
@@ -1258,7 +1261,7 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
       hipError_t e;
       {
         ProfScope prof(2, s);
-        hipLaunchKernelGGL(k_real_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(256), 0, s,
+        hipLaunchKernelGGL(k_real_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(kRedThreads), 0, s,
                            partial, slots, K, grad_A, grad_D, gS, tab, bias_on ? 1 : 0, accumulate);
         e = hipGetLastError();
         if (e == hipSuccess && bias_on) {

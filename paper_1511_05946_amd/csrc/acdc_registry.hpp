@@ -339,6 +339,11 @@ __host__ __device__ inline void real_mq_entry(const float* Dk, const float* Bk, 
 // kernel runs the phases on separate threads and combines them in LDS; the
 // CPU emulation calls the same functions in the same order.
 constexpr int kRedPhases = 4;
+#ifndef ACDC_RED_GROUP
+#define ACDC_RED_GROUP 4
+#endif
+// loads each thread issues ahead of their adds (at N = 4096, 4 beat 8 and 16)
+constexpr int kRedGroup = ACDC_RED_GROUP;
 
 __host__ __device__ __forceinline__ float4 add4(float4 a, float4 b) {
   return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
@@ -348,13 +353,13 @@ __host__ __device__ __forceinline__ float4 tile_phase_sum4(const float4* partial
                                                            long long stride, long long e, int phase) {
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
   long long t = phase;
-  // loads in groups of 8 ahead of their (in-order) adds
-  for (; t + 7 * kRedPhases < ntiles; t += 8 * kRedPhases) {
-    float4 u[8];
+  // loads in groups of kRedGroup ahead of their (in-order) adds
+  for (; t + (kRedGroup - 1) * kRedPhases < ntiles; t += kRedGroup * kRedPhases) {
+    float4 u[kRedGroup];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) u[j] = partial[(t + j * kRedPhases) * stride + e];
+    for (int j = 0; j < kRedGroup; ++j) u[j] = partial[(t + j * kRedPhases) * stride + e];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s = add4(s, u[j]);
+    for (int j = 0; j < kRedGroup; ++j) s = add4(s, u[j]);
   }
   for (; t < ntiles; t += kRedPhases) s = add4(s, partial[t * stride + e]);
   return s;

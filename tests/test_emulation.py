@@ -149,12 +149,13 @@ def test_accumulate_adds_to_gradients(emu):
         np.testing.assert_allclose(added, plain + 0.5, rtol=1e-6, atol=1e-6)
 
 
-@pytest.mark.parametrize("ntiles", [1, 5, 28, 29, 32, 61, 256])
+@pytest.mark.parametrize("ntiles", [1, 5, 12, 13, 16, 28, 29, 32, 61, 256])
 def test_reduction_order_and_value(emu, ntiles):
     # The batch reduction of the parameter-gradient partials: bit for bit the
     # documented order (tiles split into 4 phases by t mod 4, each summed in
     # increasing t, phase sums added in phase order), whichever branch of the
-    # grouped loads runs (groups of eight from 29 tiles on), and within fp32
+    # grouped loads runs (groups of four: phase 0 from 13 tiles on, every
+    # phase from 16), and within fp32
     # rounding of the exact fp64 sum.
     emu.acdc_emu_reduce4.argtypes = [ctypes.c_void_p, ctypes.c_longlong, ctypes.c_longlong, ctypes.c_void_p]
     rng = np.random.default_rng(ntiles)
