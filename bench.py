@@ -56,13 +56,13 @@ def recorded_traffic(workload: str, kernel: str):
     return (k["fetch_kib"] * rec["fetch_scale"] + k["write_kib"] * rec["write_scale"]) * 1024.0
 
 
-def cpu_baseline(w, seed: int, budget_s: float = 20.0, max_rows: int = 512):
+def cpu_baseline(w, seed: int, budget_s: float = 20.0, max_rows: int = 2048):
     """Time the oracle (forward + analytic backward, fp64, as it stands) on the
-    first rows of the workload: the first 512 rows (the whole batch when it
-    is smaller), or fewer when those would take much more than budget_s.
-    The sample grows from 8 rows until one call fills half the budget; the
-    last call is the one reported.  The dense matrix is built before timing
-    starts."""
+    first rows of the workload.  The sample grows from 8 rows until one call
+    fills half of budget_s (so the reported call takes about 10-20 s), up to
+    max_rows rows or the whole batch; at the widths up to 9216 that is at
+    least the first 512 rows.  The last call is the one reported.  The dense
+    matrix is built before timing starts."""
     import numpy as np  # noqa: F401
     from threadpoolctl import threadpool_info
 
