@@ -156,34 +156,33 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_real_bwd(RealAr
   }
 }
 
-// Batch reduction: a block owns kRedEntries float4 entries of the reduced
-// gradient (over all layers, entry index k * PS4 + e4) and sums them over the
-// tiles with one thread per (entry, phase); phase sums meet in LDS and are
-// added in phase order (tile_phase_sum4 / phases_total4).
-#ifndef ACDC_RED_ENTRIES
-#define ACDC_RED_ENTRIES 32  // 128-thread blocks: beat 256 (and 64) threads at N = 4096
-#endif
-constexpr int kRedEntries = ACDC_RED_ENTRIES;
-constexpr int kRedThreads = kRedEntries * kRedPhases;  // one thread per (entry, phase)
+// Batch reduction: a block of kRedThreads threads owns kRedThreads / PH
+// float4 entries of the reduced gradient (over all layers, entry index
+// k * PS4 + e4) and sums them over the tiles with one thread per (entry,
+// phase); phase sums meet in LDS and are added in phase order
+// (tile_phase_sum4 / phases_total4).  128-thread blocks beat 256 and 64
+// threads at N = 4096.
+constexpr int kRedThreads = 128;
 
-template <class PL>
+template <class PL, int PH>
 __global__ __launch_bounds__(kRedThreads) void k_real_reduce(const float* __restrict__ partial, long long ntiles, int K,
                                                      float* __restrict__ gA, float* __restrict__ gD,
                                                      float* __restrict__ gS, const char* __restrict__ tab,
                                                      int bias, int accumulate) {
   const long long PS4 = partial_entries4<PL>(bias != 0);
-  __shared__ float4 ph[kRedPhases][kRedEntries];
-  const int lane = threadIdx.x % kRedEntries, g = threadIdx.x / kRedEntries;
-  const long long i = (long long)blockIdx.x * kRedEntries + lane;
+  constexpr int E = kRedThreads / PH;
+  __shared__ float4 ph[PH][E];
+  const int lane = threadIdx.x % E, g = threadIdx.x / E;
+  const long long i = (long long)blockIdx.x * E + lane;
   const long long n = (long long)K * PS4;
-  ph[g][lane] = i < n ? tile_phase_sum4(reinterpret_cast<const float4*>(partial), ntiles, n, i, g)
+  ph[g][lane] = i < n ? tile_phase_sum4<PH>(reinterpret_cast<const float4*>(partial), ntiles, n, i, g)
                       : make_float4(0.f, 0.f, 0.f, 0.f);
   __syncthreads();
   if (g == 0 && i < n) {
-    float4 all[kRedPhases];
+    float4 all[PH];
 #pragma unroll
-    for (int q = 0; q < kRedPhases; ++q) all[q] = ph[q][lane];
-    real_reduce_store4<PL>(phases_total4(all), int(i / PS4), int(i % PS4), gA, gD, gS, tab, accumulate != 0);
+    for (int q = 0; q < PH; ++q) all[q] = ph[q][lane];
+    real_reduce_store4<PL>(phases_total4<PH>(all), int(i / PS4), int(i % PS4), gA, gD, gS, tab, accumulate != 0);
   }
 }
 
@@ -237,23 +236,24 @@ __attribute__((amdgpu_waves_per_eu(Launch<PL>::BWD_WPE))) void k_cplx_bwd(CplxAr
   }
 }
 
-template <class PL>
+template <class PL, int PH>
 __global__ __launch_bounds__(kRedThreads) void k_cplx_reduce(const float* __restrict__ partial, long long ntiles, int K,
                                                      float* __restrict__ gA, float* __restrict__ gD,
                                                      int accumulate) {
   constexpr long long PS4 = partial_entries4<PL>();
-  __shared__ float4 ph[kRedPhases][kRedEntries];
-  const int lane = threadIdx.x % kRedEntries, g = threadIdx.x / kRedEntries;
-  const long long i = (long long)blockIdx.x * kRedEntries + lane;
+  constexpr int E = kRedThreads / PH;
+  __shared__ float4 ph[PH][E];
+  const int lane = threadIdx.x % E, g = threadIdx.x / E;
+  const long long i = (long long)blockIdx.x * E + lane;
   const long long n = (long long)K * PS4;
-  ph[g][lane] = i < n ? tile_phase_sum4(reinterpret_cast<const float4*>(partial), ntiles, n, i, g)
+  ph[g][lane] = i < n ? tile_phase_sum4<PH>(reinterpret_cast<const float4*>(partial), ntiles, n, i, g)
                       : make_float4(0.f, 0.f, 0.f, 0.f);
   __syncthreads();
   if (g == 0 && i < n) {
-    float4 all[kRedPhases];
+    float4 all[PH];
 #pragma unroll
-    for (int q = 0; q < kRedPhases; ++q) all[q] = ph[q][lane];
-    cplx_reduce_store4<PL>(phases_total4(all), int(i / PS4), int(i % PS4), gA, gD, accumulate != 0);
+    for (int q = 0; q < PH; ++q) all[q] = ph[q][lane];
+    cplx_reduce_store4<PL>(phases_total4<PH>(all), int(i / PS4), int(i % PS4), gA, gD, accumulate != 0);
   }
 }
 
@@ -1212,8 +1212,13 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
       hipError_t e;
       {
         ProfScope prof(2, s);
-        hipLaunchKernelGGL(k_cplx_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(kRedThreads), 0, s,
-                           partial, tiles, K, grad_A, grad_D, accumulate);
+        auto reduce = [&]<int PH>() {
+          constexpr int E = kRedThreads / PH;
+          hipLaunchKernelGGL((k_cplx_reduce<PL, PH>), dim3(unsigned((n + E - 1) / E)), dim3(kRedThreads), 0, s,
+                             partial, tiles, K, grad_A, grad_D, accumulate);
+        };
+        if (red_phases(n) == 8) reduce.template operator()<8>();
+        else reduce.template operator()<4>();
         e = hipGetLastError();
       }
       rc = e == hipSuccess ? ACDC_OK : hip_fail(e);
@@ -1261,8 +1266,13 @@ extern "C" int acdc_backward(const float* x, const float* grad_y, const float* A
       hipError_t e;
       {
         ProfScope prof(2, s);
-        hipLaunchKernelGGL(k_real_reduce<PL>, dim3(unsigned((n + kRedEntries - 1) / kRedEntries)), dim3(kRedThreads), 0, s,
-                           partial, slots, K, grad_A, grad_D, gS, tab, bias_on ? 1 : 0, accumulate);
+        auto reduce = [&]<int PH>() {
+          constexpr int E = kRedThreads / PH;
+          hipLaunchKernelGGL((k_real_reduce<PL, PH>), dim3(unsigned((n + E - 1) / E)), dim3(kRedThreads), 0, s,
+                             partial, slots, K, grad_A, grad_D, gS, tab, bias_on ? 1 : 0, accumulate);
+        };
+        if (red_phases(n) == 8) reduce.template operator()<8>();
+        else reduce.template operator()<4>();
         e = hipGetLastError();
         if (e == hipSuccess && bias_on) {
           hipLaunchKernelGGL(k_real_dct<PL>, dim3(unsigned(K)), dim3(PL::T), 0, s, gS, grad_bias, Mq, tab,

@@ -63,12 +63,16 @@ void run_wg(int threads, F&& body) {
 template <class PL, class Store>
 void reduce_all(const float* partial, long long ntiles, int K, long long PS4, Store&& store) {
   const long long n = (long long)K * PS4;
-  for (long long i = 0; i < n; ++i) {
-    float4 ph[kRedPhases];
-    for (int g = 0; g < kRedPhases; ++g)
-      ph[g] = tile_phase_sum4(reinterpret_cast<const float4*>(partial), ntiles, n, i, g);
-    store(phases_total4(ph), int(i / PS4), int(i % PS4));
-  }
+  auto run = [&]<int PH>() {
+    for (long long i = 0; i < n; ++i) {
+      float4 ph[PH];
+      for (int g = 0; g < PH; ++g)
+        ph[g] = tile_phase_sum4<PH>(reinterpret_cast<const float4*>(partial), ntiles, n, i, g);
+      store(phases_total4<PH>(ph), int(i / PS4), int(i % PS4));
+    }
+  };
+  if (red_phases(n) == 8) run.template operator()<8>();
+  else run.template operator()<4>();
 }
 
 // Per-layer quartet coefficients in the kernel's [k][slot][kMqRows][T] layout.
@@ -315,13 +319,18 @@ extern "C" int acdc_emu_set_backward_slots(long long slots, int N) {
 }
 
 // The fixed-order batch reduction alone: out[e] (float4 e < n4) = the sum
-// over ntiles tiles of partial[t][e], in the kernels' order (tile phases,
-// groups of eight loads, phases added in order).
-extern "C" void acdc_emu_reduce4(const float* partial, long long ntiles, long long n4, float* out) {
-  for (long long e = 0; e < n4; ++e) {
-    float4 ph[kRedPhases];
-    for (int g = 0; g < kRedPhases; ++g)
-      ph[g] = tile_phase_sum4(reinterpret_cast<const float4*>(partial), ntiles, n4, e, g);
-    reinterpret_cast<float4*>(out)[e] = phases_total4(ph);
-  }
+// over ntiles tiles of partial[t][e], in the kernels' order (red_phases(n4)
+// tile phases, grouped loads, phases added in order).  Returns the number of
+// phases used.
+extern "C" int acdc_emu_reduce4(const float* partial, long long ntiles, long long n4, float* out) {
+  auto run = [&]<int PH>() {
+    for (long long e = 0; e < n4; ++e) {
+      float4 ph[PH];
+      for (int g = 0; g < PH; ++g)
+        ph[g] = tile_phase_sum4<PH>(reinterpret_cast<const float4*>(partial), ntiles, n4, e, g);
+      reinterpret_cast<float4*>(out)[e] = phases_total4<PH>(ph);
+    }
+    return PH;
+  };
+  return red_phases(n4) == 8 ? run.template operator()<8>() : run.template operator()<4>();
 }

@@ -149,27 +149,31 @@ def test_accumulate_adds_to_gradients(emu):
         np.testing.assert_allclose(added, plain + 0.5, rtol=1e-6, atol=1e-6)
 
 
-@pytest.mark.parametrize("ntiles", [1, 5, 12, 13, 16, 28, 29, 32, 61, 256])
-def test_reduction_order_and_value(emu, ntiles):
+@pytest.mark.parametrize("n4,ntiles", [(37, t) for t in (1, 5, 24, 25, 32, 33, 61, 256)]
+                         + [(16384, t) for t in (1, 12, 13, 16, 29)])
+def test_reduction_order_and_value(emu, n4, ntiles):
     # The batch reduction of the parameter-gradient partials: bit for bit the
-    # documented order (tiles split into 4 phases by t mod 4, each summed in
-    # increasing t, phase sums added in phase order), whichever branch of the
-    # grouped loads runs (groups of four: phase 0 from 13 tiles on, every
-    # phase from 16), and within fp32
-    # rounding of the exact fp64 sum.
+    # documented order (tiles split into P phases by t mod P, each summed in
+    # increasing t, phase sums added in phase order; P = 8 below 16384 float4
+    # entries, else 4), whichever branch of the grouped loads runs (groups of
+    # four: phase 0 from 3P + 1 tiles on, every phase from 4P), and within
+    # fp32 rounding of the exact fp64 sum.
     emu.acdc_emu_reduce4.argtypes = [ctypes.c_void_p, ctypes.c_longlong, ctypes.c_longlong, ctypes.c_void_p]
-    rng = np.random.default_rng(ntiles)
-    n4 = 37
+    emu.acdc_emu_reduce4.restype = ctypes.c_int
+    rng = np.random.default_rng(ntiles + n4)
     part = rng.standard_normal((ntiles, n4 * 4)).astype(np.float32)
     out = np.zeros(n4 * 4, np.float32)
-    emu.acdc_emu_reduce4(part.ctypes.data, ntiles, n4, out.ctypes.data)
+    P = emu.acdc_emu_reduce4(part.ctypes.data, ntiles, n4, out.ctypes.data)
+    assert P == (8 if n4 < 16384 else 4)
     phases = []
-    for g in range(4):
+    for g in range(P):
         s = np.zeros(n4 * 4, np.float32)
-        for t in range(g, ntiles, 4):
+        for t in range(g, ntiles, P):
             s = (s + part[t]).astype(np.float32)
         phases.append(s)
-    want = (((phases[0] + phases[1]).astype(np.float32) + phases[2]).astype(np.float32) + phases[3]).astype(np.float32)
+    want = phases[0]
+    for g in range(1, P):
+        want = (want + phases[g]).astype(np.float32)
     assert np.array_equal(out, want)
     exact = part.astype(np.float64).sum(axis=0)
     assert np.max(np.abs(out - exact)) <= 1e-6 * ntiles * np.max(np.abs(part)) + 1e-7

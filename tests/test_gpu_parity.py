@@ -196,8 +196,9 @@ def test_workloads_full_size_sampled(acdc, name):
 
 # Backward tiles (rows per workgroup) of each case below, and the tile count
 # its batch gives.  The fixed-order reduction sums the tiles of each phase
-# (tile mod 4) in groups of four loads, which runs for every phase at 16 tiles
-# or more, as every benchmark batch has (128 to 1024 tiles); these cases compare the
+# (tile mod P, P = 4 or 8) in groups of four loads, which runs for every phase
+# at 4P tiles or more, as every benchmark batch has (128 to 1024 tiles); these
+# cases compare the
 # batch-summed dL/da, dL/dd (and dL/db) with the oracle at such tile counts.
 @pytest.mark.parametrize("N,K,B,flags,tiles", [
     (1024, 12, 4096, P, 512),                    # acdc_n1024_k12_perm at its full batch (8 rows per tile)
