@@ -170,10 +170,11 @@ int acdc_forward_noalloc(const float* x, float* y, const float* A, const float* 
 /* Backward cascade (Sec. 4, the derivatives of a layer with respect to x,
  * a and d, chained through the cascade).  Given x and grad_y = dL/dy, writes
  * grad_x = dL/dx and grad_A, grad_D = dL/da_k, dL/dd_k summed over the
- * batch, in a fixed order that depends only on the batch size and the
- * device (workgroups sum their rows, and the partials are then added in
- * fixed phases; at N = 9216 each resident workgroup first adds its tiles
- * into one partial), and with
+ * batch, in a fixed order that depends only on the call's shapes (batch,
+ * N, K, flags) and the device (workgroups sum their rows, and the partials
+ * are then added in 4 or 8 fixed tile phases, 8 for the smaller gradients;
+ * at N = 9216 each resident workgroup first adds its tiles into one
+ * partial), and with
  * ACDC_FLAG_BIAS grad_bias = dL/db_k (bias and grad_bias are then required,
  * and ignored otherwise).  The parameter gradients are overwritten, or with
  * ACDC_FLAG_ACCUMULATE added to what the arrays hold.  `saved` is the buffer
